@@ -1,0 +1,417 @@
+"""Pins for the CPU oracle: checks against what the paper and mathematics fix.
+
+Nothing here retypes the oracle's own formulas.  Masks are checked against
+the bin counts printed in Appendix A, against the special cases of Sec. 3.2
+(all-zero pattern = StreamingLLM's sink + recent, head-level pattern, all-keep)
+and against a brute-force construction that paints whole bins instead of
+looking up each position.  Packing is checked against a pure-Python loop and
+its invariants (order kept, rows bit-identical).  Attention is checked
+against torch's scaled_dot_product_attention (a library routine, with and
+without a boolean mask, with its own GQA grouping) and against closed forms
+(one row, two rows, equal logits).
+"""
+
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as o
+import dkv_inputs as di
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _golden(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+# ---------------------------------------------------------------------------
+# helpers that are independent of the oracle
+# ---------------------------------------------------------------------------
+
+def paint_masks(pattern, T, S, R, edges, n_kv):
+    """Brute force: paint sink, recent and then whole bins, in pure Python."""
+    n_units, n_q, D = pattern.shape
+    G = n_q // n_kv
+    qm = np.zeros((n_units, n_q, T), dtype=np.uint8)
+    for n in range(n_units):
+        for h in range(n_q):
+            for j in range(min(S, T)):
+                qm[n, h, j] = 1
+            for j in range(max(0, T - R), T):
+                qm[n, h, j] = 1
+            for k in range(D):
+                for u in range(edges[k], edges[k + 1]):
+                    j = T - 1 - R - u          # u counts back from the recent window
+                    if S <= j <= T - 1 - R:
+                        qm[n, h, j] = pattern[n, h, k]
+    km = np.zeros((n_units, n_kv, T), dtype=np.uint8)
+    for n in range(n_units):
+        for g in range(n_kv):
+            for h in range(g * G, g * G + G):
+                for j in range(T):
+                    if qm[n, h, j]:
+                        km[n, g, j] = 1
+    return qm, km
+
+
+def sdpa(q, k, v, scale, mask=None):
+    """torch SDPA in float64 on [B][H][1][d] queries with GQA grouping."""
+    qt = torch.from_numpy(q)[:, :, None, :]
+    kt = torch.from_numpy(k)
+    vt = torch.from_numpy(v)
+    out = torch.nn.functional.scaled_dot_product_attention(
+        qt, kt, vt, attn_mask=mask, scale=scale, enable_gqa=True)
+    return out[:, :, 0, :].numpy()
+
+
+def random_layout(rng):
+    T = int(rng.integers(0, 70))
+    S = int(rng.integers(0, 5))
+    R = int(rng.integers(0, 5))
+    D = int(rng.integers(1, 9))
+    steps = rng.integers(1, 6, size=D)
+    edges = [0] + list(np.cumsum(steps))
+    n_kv = int(rng.integers(1, 4))
+    G = int(rng.integers(1, 4))
+    n_units = int(rng.integers(1, 3))
+    pattern = (rng.uniform(size=(n_units, n_kv * G, D)) < rng.uniform()).astype(np.uint8)
+    return T, S, R, [int(e) for e in edges], n_kv, pattern
+
+
+# ---------------------------------------------------------------------------
+# bf16 widening
+# ---------------------------------------------------------------------------
+
+def test_widen_bf16_known_bits():
+    bits = np.array([0x3F80, 0xC000, 0x3F81, 0x0000, 0x8000, 0x7F7F, 0x0001], dtype=np.uint16)
+    want = [1.0, -2.0, 1.0 + 2.0 ** -7, 0.0, -0.0, (2 - 2.0 ** -7) * 2.0 ** 127, 2.0 ** -133]
+    got = o.widen(bits, o.BF16)
+    assert got.dtype == np.float64
+    assert list(got) == want
+
+
+def test_widen_matches_torch_bf16():
+    x = torch.randn(1000, generator=torch.Generator().manual_seed(3)).to(torch.bfloat16)
+    bits = x.view(torch.int16).numpy().view(np.uint16)
+    np.testing.assert_array_equal(o.widen(bits, o.BF16), x.double().numpy())
+
+
+# ---------------------------------------------------------------------------
+# Eq. (4) / Eq. (5): the paper's printed bin layouts
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("idx", [0, 1])
+def test_paper_bin_count(idx):
+    g = _golden("paper_layout.json")
+    lay = g["layouts"][idx]
+    T, S, R, W = lay["context_len"], g["sink"], g["recent"], g["bin_width"]
+    D_print = lay["num_bins"]
+    D_big = D_print + 40  # more bins than the context can instantiate
+    edges = di.uniform_bin_edges(W, D_big)
+    # one query head that keeps only the odd bins
+    pat = np.zeros((1, 1, D_big), dtype=np.uint8)
+    pat[0, 0, 1::2] = 1
+    qm = o.q_keep_mask(pat, T, S, R, edges)[0, 0]
+    # which bins were instantiated: every bin that covers at least one position
+    j = np.arange(S, T - R)
+    ks = o.bin_index(T - 1 - j - R, edges)
+    assert sorted(set(ks.tolist())) == list(range(D_print))
+    # the kept compressible count is 128 per odd instantiated bin
+    assert int(qm[S:T - R].sum()) == W * len(range(1, D_print, 2))
+    assert int(qm.sum()) == S + R + W * len(range(1, D_print, 2))
+
+
+@pytest.mark.parametrize("idx", [0, 1])
+def test_paper_bin_endpoints(idx):
+    g = _golden("paper_layout.json")
+    lay = g["layouts"][idx]
+    T, S, R, W = lay["context_len"], g["sink"], g["recent"], g["bin_width"]
+    D = lay["num_bins"]
+    edges = di.uniform_bin_edges(W, D)
+    # 1-indexed i = 129 is the first compressible position, in the farthest bin
+    j_first = g["first_compressible_position_1idx"] - 1
+    j_last = T - g["last_compressible_offset_from_end"] - 1   # i = T_c - 1024
+    k_first = o.bin_index(T - 1 - j_first - R, edges)
+    k_last = o.bin_index(T - 1 - j_last - R, edges)
+    assert int(k_first) == D - 1
+    assert int(k_last) == 0
+    # their neighbours are sink and recent: kept even by an all-zero pattern
+    qm = o.q_keep_mask(np.zeros((1, 1, D), np.uint8), T, S, R, edges)[0, 0]
+    assert qm[j_first - 1] == 1 and qm[j_first] == 0
+    assert qm[j_last] == 0 and qm[j_last + 1] == 1
+
+
+def test_streaming_llm_special_case():
+    g = _golden("paper_layout.json")
+    lay = g["layouts"][0]
+    T, S, R, W, D = lay["context_len"], g["sink"], g["recent"], g["bin_width"], lay["num_bins"]
+    sl = g["streaming_llm"]
+    pat = np.zeros((2, 8, D), dtype=np.uint8)
+    _, km, kv_len = o.map_pattern(pat, T, S, R, di.uniform_bin_edges(W, D), 2)
+    assert (kv_len == sl["sink"] + sl["recent"]).all()
+    assert km[:, :, :sl["sink"]].all() and km[:, :, T - sl["recent"]:].all()
+    assert not km[:, :, sl["sink"]:T - sl["recent"]].any()
+    cf = o.closed_form_lengths(pat, T, S, R, di.uniform_bin_edges(W, D), 2)
+    assert (cf == 1152).all()
+
+
+def test_all_keep_pattern_keeps_every_position():
+    T, S, R = 5000, 128, 1024
+    edges = di.log_bin_edges(T - S - R, 12)
+    pat = np.ones((1, 4, 12), dtype=np.uint8)
+    _, km, kv_len = o.map_pattern(pat, T, S, R, edges, 2)
+    assert km.all() and (kv_len == T).all()
+
+
+def test_head_level_pattern():
+    """Sec. 3.2: M[l,h,d] = z_h for all d recovers a head-level policy."""
+    T, S, R, W, D = 9000, 128, 1024, 128, (9000 - 1152) // 128 + 1
+    rng = np.random.default_rng(0)
+    z = (rng.uniform(size=16) < 0.3).astype(np.uint8)
+    pat = np.repeat(z[None, :, None], D, axis=2)
+    _, _, kv_len = o.map_pattern(pat, T, S, R, di.uniform_bin_edges(W, D), 4)
+    for g in range(4):
+        want = T if z[4 * g:4 * g + 4].any() else S + R
+        assert kv_len[0, g] == want
+
+
+def test_map_matches_bruteforce_paint():
+    rng = np.random.default_rng(1234)
+    for _ in range(250):
+        T, S, R, edges, n_kv, pat = random_layout(rng)
+        qm, km, kv_len = o.map_pattern(pat, T, S, R, edges, n_kv)
+        pq, pk = paint_masks(pat, T, S, R, edges, n_kv)
+        np.testing.assert_array_equal(qm, pq)
+        np.testing.assert_array_equal(km, pk)
+        np.testing.assert_array_equal(kv_len, pk.sum(axis=2))
+        cf = o.closed_form_lengths(pat, T, S, R, edges, n_kv)
+        np.testing.assert_array_equal(cf, kv_len)
+
+
+def test_sink_recent_overlap_keeps_all():
+    for T in range(0, 20):
+        pat = np.zeros((1, 2, 3), dtype=np.uint8)
+        _, km, kv_len = o.map_pattern(pat, T, 8, 12, [0, 4, 8, 16], 1)
+        assert km.all() and kv_len[0, 0] == T
+
+
+def test_log_bins_with_recent_equal_forced_first_bin():
+    """R = 128 with D-1 bins == R = 0 with D bins whose bin 0 is [0,128) kept."""
+    T = 3000
+    e = di.log_bin_edges(T, 10)                 # E[1] = 128
+    rng = np.random.default_rng(5)
+    pat = (rng.uniform(size=(1, 6, 10)) < 0.4).astype(np.uint8)
+    pat_a = pat.copy()
+    pat_a[:, :, 0] = 1
+    _, km_a, _ = o.map_pattern(pat_a, T, 0, 0, e, 3)
+    e_b = [x - 128 for x in e[1:]]
+    _, km_b, _ = o.map_pattern(pat[:, :, 1:], T, 0, 128, e_b, 3)
+    np.testing.assert_array_equal(km_a, km_b)
+
+
+def test_position_beyond_last_bin_is_pruned():
+    T, S, R = 400, 4, 8
+    edges = [0, 10, 30]                          # covers u < 30 only
+    pat = np.ones((1, 1, 2), dtype=np.uint8)
+    qm = o.q_keep_mask(pat, T, S, R, edges)[0, 0]
+    assert int(qm.sum()) == S + R + 30
+
+
+# ---------------------------------------------------------------------------
+# packing and append
+# ---------------------------------------------------------------------------
+
+def _rand_bits(rng, shape):
+    return rng.integers(0, 1 << 16, size=shape, dtype=np.uint16)
+
+
+def test_compact_all_keep_is_dense_bytes():
+    rng = np.random.default_rng(2)
+    k = _rand_bits(rng, (2, 3, 37, 8))
+    v = _rand_bits(rng, (2, 3, 37, 8))
+    r = o.compact(k, v, np.ones((2, 3, 37), np.uint8), 0)
+    np.testing.assert_array_equal(r["k_c"], k.reshape(-1, 8))
+    np.testing.assert_array_equal(r["v_c"], v.reshape(-1, 8))
+    assert (r["seg_len"] == 37).all()
+    np.testing.assert_array_equal(r["seg_off"], 37 * np.arange(6))
+
+
+def test_compact_matches_python_loop():
+    rng = np.random.default_rng(3)
+    for _ in range(40):
+        N, H, T, d = rng.integers(1, 3), rng.integers(1, 4), rng.integers(0, 50), 4
+        cap = int(rng.integers(0, 4))
+        k = rng.standard_normal((N, H, T, d)).astype(np.float32)
+        v = rng.standard_normal((N, H, T, d)).astype(np.float32)
+        m = (rng.uniform(size=(N, H, T)) < rng.uniform()).astype(np.uint8)
+        r = o.compact(k, v, m, cap)
+        row = 0
+        for n in range(N):
+            for g in range(H):
+                s = n * H + g
+                assert r["seg_off"][s] == row
+                cnt = 0
+                for j in range(T):
+                    if m[n, g, j]:
+                        assert (r["k_c"][row + cnt] == k[n, g, j]).all()
+                        assert (r["v_c"][row + cnt] == v[n, g, j]).all()
+                        assert r["src_pos"][row + cnt] == j
+                        cnt += 1
+                assert r["seg_len"][s] == cnt
+                row += cnt + cap
+        assert r["rows"] == row
+
+
+def test_compact_invariants():
+    rng = np.random.default_rng(4)
+    k = _rand_bits(rng, (3, 2, 300, 16))
+    v = _rand_bits(rng, (3, 2, 300, 16))
+    m = (rng.uniform(size=(3, 2, 300)) < 0.3).astype(np.uint8)
+    r = o.compact(k, v, m, 5)
+    assert int(r["seg_len"].sum()) == int(m.sum())
+    for s in range(6):
+        n, g = divmod(s, 2)
+        lo, ln = int(r["seg_off"][s]), int(r["seg_len"][s])
+        sp = r["src_pos"][lo:lo + ln]
+        assert (np.diff(sp) > 0).all()
+        np.testing.assert_array_equal(r["k_c"][lo:lo + ln], k[n, g, sp])
+        assert (r["src_pos"][lo + ln:lo + ln + 5] == -1).all()
+
+
+def test_append_positions():
+    rng = np.random.default_rng(5)
+    k = rng.standard_normal((2, 2, 20, 4)).astype(np.float32)
+    m = (rng.uniform(size=(2, 2, 20)) < 0.5).astype(np.uint8)
+    r = o.compact(k, k, m, 3)
+    kn = rng.standard_normal((2, 2, 2, 4)).astype(np.float32)
+    kc, _ = o.append(r["k_c"], r["v_c"], r["seg_off"], r["seg_len"], kn, kn, 1)
+    want = r["k_c"].copy()
+    for s in range(4):
+        n, g = divmod(s, 2)
+        base = int(r["seg_off"][s]) + int(r["seg_len"][s])
+        # slot n_tail = 0 stays free; tokens land in slots 1 and 2
+        want[base + 1] = kn[n, g, 0]
+        want[base + 2] = kn[n, g, 1]
+    np.testing.assert_array_equal(kc, want)
+
+
+# ---------------------------------------------------------------------------
+# attention
+# ---------------------------------------------------------------------------
+
+def _attn_case(rng, B=2, n_kv=2, G=3, T=40, d=8):
+    q = rng.standard_normal((B, n_kv * G, d)).astype(np.float32)
+    k = rng.standard_normal((B, n_kv, T, d)).astype(np.float32)
+    v = rng.standard_normal((B, n_kv, T, d)).astype(np.float32)
+    return q, k, v
+
+
+def test_decode_all_keep_matches_sdpa():
+    rng = np.random.default_rng(6)
+    q, k, v = _attn_case(rng)
+    r = o.compact(k, v, np.ones(k.shape[:3], np.uint8), 0)
+    out = o.decode_attn(q, r["k_c"], r["v_c"], r["seg_off"], r["seg_len"], 0, 0.37, 2, o.F32)
+    ref = sdpa(q.astype(np.float64), k.astype(np.float64), v.astype(np.float64), 0.37)
+    np.testing.assert_allclose(out, ref, rtol=1e-12, atol=1e-13)
+
+
+def test_dense_decode_matches_sdpa():
+    rng = np.random.default_rng(7)
+    q, k, v = _attn_case(rng, T=50)
+    out = o.dense_decode_attn(q, k, v, 31, 0.5, o.F32)
+    ref = sdpa(q.astype(np.float64), k[:, :, :31].astype(np.float64),
+               v[:, :, :31].astype(np.float64), 0.5)
+    np.testing.assert_allclose(out, ref, rtol=1e-12, atol=1e-13)
+
+
+def test_masked_dense_matches_sdpa_with_bool_mask():
+    rng = np.random.default_rng(8)
+    B, n_kv, G, T, d = 2, 2, 4, 33, 8
+    q, k, v = _attn_case(rng, B, n_kv, G, T, d)
+    m = (rng.uniform(size=(B, n_kv, T)) < 0.4).astype(np.uint8)
+    m[:, :, 0] = 1
+    kt = np.zeros((B, n_kv, 0, d), np.float32)
+    out = o.masked_dense_attn(q, k, v, m, kt, kt, 0.3, o.F32)
+    mask = torch.from_numpy(np.repeat(m, G, axis=1).astype(bool))[:, :, None, :]
+    ref = sdpa(q.astype(np.float64), k.astype(np.float64), v.astype(np.float64), 0.3, mask)
+    np.testing.assert_allclose(out, ref, rtol=1e-12, atol=1e-13)
+
+
+def test_packed_decode_equals_masked_dense_with_tail():
+    rng = np.random.default_rng(9)
+    for trial in range(10):
+        B, n_kv, G, T, d = 2, 3, 2, 64, 16
+        q, k, v = _attn_case(rng, B, n_kv, G, T, d)
+        m = (rng.uniform(size=(B, n_kv, T)) < 0.35).astype(np.uint8)
+        n_tail = int(rng.integers(0, 4))
+        kn = rng.standard_normal((B, n_kv, n_tail, d)).astype(np.float32)
+        vn = rng.standard_normal((B, n_kv, n_tail, d)).astype(np.float32)
+        r = o.compact(k, v, m, 4)
+        kc, vc = o.append(r["k_c"], r["v_c"], r["seg_off"], r["seg_len"], kn, vn, 0)
+        out = o.decode_attn(q, kc, vc, r["seg_off"], r["seg_len"], n_tail, 0.25, n_kv, o.F32)
+        ref = o.masked_dense_attn(q, k, v, m, kn, vn, 0.25, o.F32)
+        np.testing.assert_allclose(out, ref, rtol=1e-12, atol=1e-13)
+
+
+def test_decode_single_row_returns_that_value_row():
+    rng = np.random.default_rng(10)
+    q, k, v = _attn_case(rng, 1, 1, 2, 10, 8)
+    m = np.zeros((1, 1, 10), np.uint8)
+    m[0, 0, 6] = 1
+    r = o.compact(k, v, m, 0)
+    out = o.decode_attn(q, r["k_c"], r["v_c"], r["seg_off"], r["seg_len"], 0, 1.0, 1, o.F32)
+    for h in range(2):
+        np.testing.assert_array_equal(out[0, h], v[0, 0, 6].astype(np.float64))
+
+
+def test_decode_zero_query_is_mean_of_retained_values():
+    rng = np.random.default_rng(11)
+    _, k, v = _attn_case(rng, 1, 2, 2, 30, 8)
+    q = np.zeros((1, 4, 8), np.float32)
+    m = (rng.uniform(size=(1, 2, 30)) < 0.5).astype(np.uint8)
+    r = o.compact(k, v, m, 0)
+    out = o.decode_attn(q, r["k_c"], r["v_c"], r["seg_off"], r["seg_len"], 0, 1.0, 2, o.F32)
+    for h in range(4):
+        g = h // 2
+        np.testing.assert_allclose(out[0, h], v[0, g][m[0, g] == 1].astype(np.float64).mean(0),
+                                   rtol=1e-13, atol=1e-14)
+
+
+def test_decode_two_rows_is_logistic_mix():
+    q = np.array([[[0.5, -1.0]]], np.float32)
+    k = np.array([[[[1.0, 2.0], [3.0, -1.0]]]], np.float32)
+    v = np.array([[[[10.0, 0.0], [0.0, 10.0]]]], np.float32)
+    r = o.compact(k, v, np.ones((1, 1, 2), np.uint8), 0)
+    out = o.decode_attn(q, r["k_c"], r["v_c"], r["seg_off"], r["seg_len"], 0, 0.7, 1, o.F32)
+    s1, s2 = 0.7 * (0.5 - 2.0), 0.7 * (1.5 + 1.0)
+    w1 = 1.0 / (1.0 + np.exp(s2 - s1))
+    np.testing.assert_allclose(out[0, 0], [10 * w1, 10 * (1 - w1)], rtol=1e-14)
+
+
+def test_decode_empty_segment_is_zero():
+    q = np.ones((1, 2, 4), np.float32)
+    k = np.ones((1, 1, 5, 4), np.float32)
+    r = o.compact(k, k, np.zeros((1, 1, 5), np.uint8), 2)
+    out = o.decode_attn(q, r["k_c"], r["v_c"], r["seg_off"], r["seg_len"], 0, 1.0, 1, o.F32)
+    assert (out == 0).all()
+    out2 = o.masked_dense_attn(q, k, k, np.zeros((1, 1, 5), np.uint8),
+                               np.zeros((1, 1, 0, 4), np.float32),
+                               np.zeros((1, 1, 0, 4), np.float32), 1.0, o.F32)
+    assert (out2 == 0).all()
+
+
+def test_decode_bf16_matches_sdpa_on_widened_values():
+    rng = np.random.default_rng(12)
+    x = rng.standard_normal((1, 2, 25, 8)).astype(np.float32)
+    kb = di.f32_to_bf16_bits(x)
+    vb = di.f32_to_bf16_bits(x[:, :, ::-1])
+    qb = di.f32_to_bf16_bits(rng.standard_normal((1, 4, 8)).astype(np.float32))
+    r = o.compact(kb, vb, np.ones((1, 2, 25), np.uint8), 0)
+    out = o.decode_attn(qb, r["k_c"], r["v_c"], r["seg_off"], r["seg_len"], 0, 0.5, 2, o.BF16)
+    ref = sdpa(o.widen(qb, o.BF16), o.widen(kb, o.BF16), o.widen(vb, o.BF16), 0.5)
+    np.testing.assert_allclose(out, ref, rtol=1e-12, atol=1e-13)
