@@ -1,0 +1,212 @@
+/*
+ * dkv.h -- C ABI of the Distance-KV inference hot path on MI355X (gfx950).
+ *
+ * Distance-KV keeps a static binary pattern M[layer][query head][distance bin]
+ * (Sec. 3.2).  At inference the pattern is mapped to token positions measured
+ * from the end of the context (Sec. 3.4, Eq. (4) and Eq. (5)), query heads that
+ * share a KV head are combined by union (last paragraph of Sec. 3.4), the KV
+ * cache is pruned and packed once in original token order, new tokens are
+ * appended and always kept, and decode attends to the packed cache (Sec. 3.4).
+ * This library runs those four steps on one GPU:
+ *
+ *   dkv_map_pattern   pattern -> per-KV-head keep masks and retained lengths
+ *   dkv_compact       dense K/V + keep mask -> packed K/V, offsets, lengths
+ *   dkv_append        new tokens -> free rows after each packed segment
+ *   dkv_decode_attn   one decode step of attention over the packed segments
+ *
+ * plus dkv_dense_decode_attn, the same attention kernel over an uncompressed
+ * cache (the "Dense" comparator of Sec. 4.3).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Pointers are DEVICE pointers unless marked (host).  The caller allocates
+ *   and owns every buffer, including workspaces; the library allocates and
+ *   frees nothing and keeps no state between calls.
+ * - Every call only enqueues work on `stream` (a hipStream_t; NULL is the
+ *   default stream) and returns without synchronising.  Buffers must stay
+ *   alive until the stream has executed the work.  Calls are re-entrant;
+ *   two calls that share an output or a workspace must be ordered by the
+ *   caller.
+ * - Arguments are checked on the host before anything is enqueued; on any
+ *   error nothing is enqueued and the status says why.  DKV_ERR_HIP means the
+ *   HIP runtime refused a launch.  Faults inside a kernel surface at the
+ *   caller's next synchronisation.
+ * - Positions are 0-indexed: position j of a context of length T has
+ *   distance delta = T - 1 - j from the last context token.  (Eq. (4) is
+ *   written for 1-indexed i = j + 1; with S = 128, R = 1024 and 128-token
+ *   bins both give the paper's D = 1013 bins at T = 130,816.)
+ * - Query head h belongs to KV head h / G, G = num_q_heads / num_kv_heads.
+ * - Element types: DKV_BF16 (K, V, q as bfloat16) or DKV_F32.  Attention
+ *   accumulates in fp32 and writes fp32.  head_dim is 64 or 128.  Row and
+ *   base pointers of K, V, q, out and packed buffers must be 16-byte aligned.
+ * - Sizes: N = num_units (independent (layer, sequence) units),
+ *   Hq / Hkv heads, d = head_dim, T = context_len, D = num_bins.
+ */
+#ifndef DKV_H
+#define DKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum dkv_status {
+  DKV_OK = 0,
+  DKV_ERR_INVALID_ARG = 1, /* null pointer, negative or inconsistent size, bad bin edges */
+  DKV_ERR_UNSUPPORTED = 2, /* head_dim, group size, bin count or segment count beyond limits */
+  DKV_ERR_MISALIGNED = 3,  /* a K/V/q/out/packed pointer is not 16-byte aligned */
+  DKV_ERR_CAPACITY = 4,    /* n_tail + n_new exceeds the free rows reserved per segment */
+  DKV_ERR_WORKSPACE = 5,   /* workspace missing or smaller than the query function says */
+  DKV_ERR_HIP = 6          /* the HIP runtime refused to launch a kernel */
+} dkv_status;
+
+typedef enum dkv_dtype { DKV_BF16 = 0, DKV_F32 = 1 } dkv_dtype;
+
+/* Limits (checked; larger values return DKV_ERR_UNSUPPORTED). */
+#define DKV_MAX_GROUP 16            /* Hq / Hkv */
+#define DKV_MAX_GENERAL_BINS 512    /* bins with arbitrary edges */
+#define DKV_MAX_UNIFORM_BINS 16384  /* bins with edges E[k] = W k */
+#define DKV_MAX_SEGMENTS 2048       /* batch * num_kv_heads in one decode call */
+
+/*
+ * Shape of a pattern-mapping / compaction call (host struct).
+ *
+ * bin_edges (host) holds D + 1 offsets E[0] = 0 < E[1] < ... < E[D].  A
+ * position that is neither sink (j < sink) nor recent (delta < recent) has
+ * offset u = delta - recent past the recent window and lies in bin k when
+ * E[k] <= u < E[k+1] (Eq. (4); the paper's layout is sink = 128,
+ * recent = 1024, E[k] = 128 k).  Positions with u >= E[D] lie in no bin and
+ * are pruned: only bins the context covers are instantiated (Sec. 3.4).
+ */
+typedef struct dkv_layout {
+  int32_t num_units;
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  int32_t context_len;
+  int32_t sink;
+  int32_t recent;
+  int32_t num_bins;
+  const int32_t *bin_edges;
+} dkv_layout;
+
+/*
+ * dkv_map_pattern -- Eq. (5) of Sec. 3.4, then the GQA union.
+ *
+ * pattern  uint8 [N][Hq][D]; nonzero = bin retained for that query head.
+ * kv_mask  out, uint8 [N][Hkv][T]; 1 where any query head of the group keeps
+ *          the position (sink and recent positions are always 1), else 0.
+ * kv_len   out, int32 [N][Hkv]; number of ones in each kv_mask row.
+ * q_mask   out, optional (NULL to skip), uint8 [N][Hq][T]: the per-query-head
+ *          logical decision m[l,h,j] of Eq. (5).
+ * Limits: D <= DKV_MAX_GENERAL_BINS, or D <= DKV_MAX_UNIFORM_BINS when the
+ * edges are uniform.  kv_mask and q_mask must be 16-byte aligned; with
+ * context_len = 0 they are not written and may be NULL.
+ */
+dkv_status dkv_map_pattern(const dkv_layout *layout, const uint8_t *pattern,
+                           uint8_t *kv_mask, int32_t *kv_len, uint8_t *q_mask,
+                           void *stream);
+
+/* Workspace bytes dkv_compact needs for this layout (host, no GPU call). */
+size_t dkv_compact_workspace_bytes(const dkv_layout *layout);
+
+/*
+ * dkv_compact -- the one-time prune and pack of Sec. 3.4 / Fig. 2(b).
+ *
+ * k, v       dense cache, [N][Hkv][T][d] rows of d elements of `dtype`.
+ * kv_mask    uint8 [N][Hkv][T] (nonzero = retained), e.g. from dkv_map_pattern.
+ * append_cap free rows reserved after every segment for dkv_append (>= 0).
+ * k_out, v_out  packed output, out_rows rows of d elements.  Segment
+ *            s = n * Hkv + g starts at seg_off[s] and holds its retained rows
+ *            in original token order, followed by append_cap free rows that
+ *            this call does not touch.
+ * out_rows   capacity of k_out / v_out in rows.  The layout needs
+ *            sum_s (kv_len[s] + append_cap) rows; rows that would fall at or
+ *            beyond out_rows are not written (their segments are then
+ *            incomplete), and the true requirement is reported in
+ *            *rows_needed so that the caller can check it.
+ * seg_off    out, int64 [N*Hkv], row offset of each segment (unit-major).
+ * seg_len    out, int32 [N*Hkv], retained rows of each segment.
+ * src_pos    out, optional int32 [out_rows]: original position j of every
+ *            packed row (free rows untouched).
+ * rows_needed out, optional int64 [1]: sum_s (seg_len[s] + append_cap).
+ * workspace  at least dkv_compact_workspace_bytes(layout) bytes, no
+ *            initial contents required.
+ * The dense cache may be freed once the stream has executed this call: that
+ * is what realises the memory reduction.
+ */
+dkv_status dkv_compact(const dkv_layout *layout, dkv_dtype dtype, const void *k,
+                       const void *v, const uint8_t *kv_mask, int32_t append_cap,
+                       void *k_out, void *v_out, int64_t out_rows, int64_t *seg_off,
+                       int32_t *seg_len, int32_t *src_pos, int64_t *rows_needed,
+                       void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * dkv_append -- appended tokens are retained in full (Sec. 3.4).
+ *
+ * k_new, v_new  [num_segments][n_new][d]; token t of segment s is written to
+ *               packed row seg_off[s] + seg_len[s] + n_tail + t.
+ * n_tail        (host) tokens already appended to every segment.
+ * append_cap    (host) free rows reserved per segment; n_tail + n_new must not
+ *               exceed it (DKV_ERR_CAPACITY otherwise).
+ * seg_off, seg_len  as returned by dkv_compact; pass seg_off + first segment
+ *               to address a subset (e.g. one layer's B * Hkv segments).
+ * K is stored already rotated (RoPE at the token's absolute position is the
+ * caller's job); the library never re-rotates.
+ */
+dkv_status dkv_append(dkv_dtype dtype, int32_t num_segments, int32_t head_dim,
+                      const void *k_new, const void *v_new, int32_t n_new, int32_t n_tail,
+                      int32_t append_cap, void *k_c, void *v_c, const int64_t *seg_off,
+                      const int32_t *seg_len, void *stream);
+
+/* Workspace bytes for dkv_decode_attn / dkv_dense_decode_attn (host, no GPU call). */
+size_t dkv_decode_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                  int32_t head_dim);
+
+/*
+ * dkv_decode_attn -- one decode step over the packed cache (Sec. 3.4).
+ *
+ * q        [B][Hq][d] queries of this step.
+ * k_c, v_c packed cache (shared base pointers of a whole-stack compaction).
+ * seg_off, seg_len  the B * Hkv segments of this call, batch-major
+ *          (s = b * Hkv + g); for layer l of a stack compacted with units
+ *          l * B + b, pass seg_off + l * B * Hkv and seg_len + l * B * Hkv.
+ * n_tail   (host) appended tokens per segment; segment s attends rows
+ *          [seg_off[s], seg_off[s] + seg_len[s] + n_tail).
+ * Every query head of group g attends to all rows of segment (b, g): the
+ * union of its group (Sec. 3.4).  out[b][h][:] = softmax(sm_scale * K q) V
+ * over those rows, fp32 [B][Hq][d]; a segment with no rows gives zeros.
+ * rows_hint (host) expected total rows of the call (0 = unknown); it only
+ * sizes the grid, never the result's correctness.
+ * workspace  at least dkv_decode_workspace_bytes(...) bytes, ZERO-FILLED
+ *          before its first use; every completed call leaves it reusable
+ *          without clearing again.  One workspace serves one call at a time.
+ */
+dkv_status dkv_decode_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_heads,
+                           int32_t num_kv_heads, int32_t head_dim, const void *q,
+                           const void *k_c, const void *v_c, const int64_t *seg_off,
+                           const int32_t *seg_len, int32_t n_tail, float sm_scale,
+                           int64_t rows_hint, float *out, void *workspace,
+                           size_t workspace_bytes, void *stream);
+
+/*
+ * dkv_dense_decode_attn -- the same attention over an uncompressed cache
+ * k, v [B][Hkv][t_cap][d]; every segment attends rows [0, n_valid),
+ * n_valid <= t_cap.  Same workspace rules as dkv_decode_attn.
+ */
+dkv_status dkv_dense_decode_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_heads,
+                                 int32_t num_kv_heads, int32_t head_dim, const void *q,
+                                 const void *k, const void *v, int64_t t_cap,
+                                 int32_t n_valid, float sm_scale, float *out,
+                                 void *workspace, size_t workspace_bytes, void *stream);
+
+/* Static description of a status code. */
+const char *dkv_status_string(dkv_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DKV_H */

@@ -285,13 +285,14 @@ def decode_attn(q, k_c, v_c, seg_off, seg_len, n_tail, sm_scale, num_kv_heads, d
     G = Hq // num_kv_heads
     out = np.zeros((B, Hq, d), dtype=np.float64)
     for b in range(B):
-        for h in range(Hq):
-            s = b * num_kv_heads + h // G
+        for g in range(num_kv_heads):
+            s = b * num_kv_heads + g
             lo = int(seg_off[s])
             hi = lo + int(seg_len[s]) + int(n_tail)
             kr = widen(k_c[lo:hi], dtype)
             vr = widen(v_c[lo:hi], dtype)
-            out[b, h] = _softmax_attend(qf[b, h], kr, vr, sm_scale)
+            for h in range(g * G, (g + 1) * G):
+                out[b, h] = _softmax_attend(qf[b, h], kr, vr, sm_scale)
     return out
 
 
@@ -306,11 +307,11 @@ def dense_decode_attn(q, k, v, n_valid, sm_scale, dtype):
     G = Hq // n_kv
     out = np.zeros((B, Hq, d), dtype=np.float64)
     for b in range(B):
-        for h in range(Hq):
-            g = h // G
+        for g in range(n_kv):
             kr = widen(k[b, g, :n_valid], dtype)
             vr = widen(v[b, g, :n_valid], dtype)
-            out[b, h] = _softmax_attend(qf[b, h], kr, vr, sm_scale)
+            for h in range(g * G, (g + 1) * G):
+                out[b, h] = _softmax_attend(qf[b, h], kr, vr, sm_scale)
     return out
 
 

@@ -1,0 +1,194 @@
+"""ctypes binding of libdkv.so: argument marshalling only.
+
+Each function has the name and argument order of its C entry point in
+include/dkv.h.  Tensors are passed as device pointers (torch is used for
+device memory and streams only); every step of the hot path runs in the HIP
+kernels of libdkv.so.  There is no fallback: if the library is missing or a
+call fails, an exception is raised.
+"""
+
+import ctypes
+import os
+
+import torch
+
+__all__ = [
+    "DKV_OK", "DKV_ERR_INVALID_ARG", "DKV_ERR_UNSUPPORTED", "DKV_ERR_MISALIGNED",
+    "DKV_ERR_CAPACITY", "DKV_ERR_WORKSPACE", "DKV_ERR_HIP", "DKV_BF16", "DKV_F32",
+    "DkvError", "Layout", "make_layout", "library", "library_path", "dtype_code",
+    "dkv_map_pattern", "dkv_compact_workspace_bytes", "dkv_compact", "dkv_append",
+    "dkv_decode_workspace_bytes", "dkv_decode_attn", "dkv_dense_decode_attn",
+    "dkv_status_string",
+]
+
+(DKV_OK, DKV_ERR_INVALID_ARG, DKV_ERR_UNSUPPORTED, DKV_ERR_MISALIGNED, DKV_ERR_CAPACITY,
+ DKV_ERR_WORKSPACE, DKV_ERR_HIP) = range(7)
+DKV_BF16, DKV_F32 = 0, 1
+
+library_path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdkv.so")
+
+
+class DkvError(RuntimeError):
+    """A libdkv call returned a status other than DKV_OK."""
+
+    def __init__(self, fn, status):
+        self.status = status
+        super().__init__(f"{fn} failed: {dkv_status_string(status)} (status {status})")
+
+
+class Layout(ctypes.Structure):
+    _fields_ = [
+        ("num_units", ctypes.c_int32),
+        ("num_q_heads", ctypes.c_int32),
+        ("num_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("context_len", ctypes.c_int32),
+        ("sink", ctypes.c_int32),
+        ("recent", ctypes.c_int32),
+        ("num_bins", ctypes.c_int32),
+        ("bin_edges", ctypes.POINTER(ctypes.c_int32)),
+    ]
+
+
+def make_layout(num_units, num_q_heads, num_kv_heads, head_dim, context_len, sink, recent,
+                bin_edges):
+    """A dkv_layout; the host edge array is kept alive on the returned object."""
+    edges = (ctypes.c_int32 * len(bin_edges))(*[int(e) for e in bin_edges])
+    lay = Layout(int(num_units), int(num_q_heads), int(num_kv_heads), int(head_dim),
+                 int(context_len), int(sink), int(recent), len(bin_edges) - 1,
+                 ctypes.cast(edges, ctypes.POINTER(ctypes.c_int32)))
+    lay._edges = edges
+    return lay
+
+
+_lib = None
+
+
+def library():
+    """The loaded libdkv.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(library_path):
+        raise ImportError(
+            f"{library_path} is missing: build it with `python -m paper_2609_32663_amd.build` "
+            "(the Distance-KV path has no fallback)")
+    lib = ctypes.CDLL(library_path)
+    P, I32, I64, SZ, F32, VP = (ctypes.POINTER(Layout), ctypes.c_int32, ctypes.c_int64,
+                                ctypes.c_size_t, ctypes.c_float, ctypes.c_void_p)
+    sigs = {
+        "dkv_map_pattern": (I32, [P, VP, VP, VP, VP, VP]),
+        "dkv_compact_workspace_bytes": (SZ, [P]),
+        "dkv_compact": (I32, [P, I32, VP, VP, VP, I32, VP, VP, I64, VP, VP, VP, VP, VP, SZ, VP]),
+        "dkv_append": (I32, [I32, I32, I32, VP, VP, I32, I32, I32, VP, VP, VP, VP, VP]),
+        "dkv_decode_workspace_bytes": (SZ, [I32, I32, I32, I32]),
+        "dkv_decode_attn": (I32, [I32, I32, I32, I32, I32, VP, VP, VP, VP, VP, I32, F32, I64, VP,
+                                  VP, SZ, VP]),
+        "dkv_dense_decode_attn": (I32, [I32, I32, I32, I32, I32, VP, VP, VP, I64, I32, F32, VP, VP,
+                                        SZ, VP]),
+        "dkv_status_string": (ctypes.c_char_p, [I32]),
+    }
+    for name, (res, args) in sigs.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = lib
+    return lib
+
+
+# ---------------------------------------------------------------------------
+# marshalling helpers
+# ---------------------------------------------------------------------------
+
+def dtype_code(t):
+    if t == torch.bfloat16:
+        return DKV_BF16
+    if t == torch.float32:
+        return DKV_F32
+    raise TypeError(f"unsupported element type {t}")
+
+
+def _dev(t, name, optional=False):
+    if t is None:
+        if optional:
+            return None
+        raise ValueError(f"{name} is required")
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+def _check(fn, status):
+    if status != DKV_OK:
+        raise DkvError(fn, status)
+
+
+# ---------------------------------------------------------------------------
+# entry points
+# ---------------------------------------------------------------------------
+
+def dkv_status_string(status):
+    return library().dkv_status_string(int(status)).decode()
+
+
+def dkv_map_pattern(layout, pattern, kv_mask, kv_len, q_mask=None, stream=None):
+    _check("dkv_map_pattern", library().dkv_map_pattern(
+        ctypes.byref(layout), _dev(pattern, "pattern"), _dev(kv_mask, "kv_mask"),
+        _dev(kv_len, "kv_len"), _dev(q_mask, "q_mask", True), _stream(stream)))
+
+
+def dkv_compact_workspace_bytes(layout):
+    return int(library().dkv_compact_workspace_bytes(ctypes.byref(layout)))
+
+
+def dkv_compact(layout, k, v, kv_mask, append_cap, k_out, v_out, seg_off, seg_len, workspace,
+                src_pos=None, rows_needed=None, stream=None):
+    _check("dkv_compact", library().dkv_compact(
+        ctypes.byref(layout), dtype_code(k.dtype), _dev(k, "k"), _dev(v, "v"),
+        _dev(kv_mask, "kv_mask"), int(append_cap), _dev(k_out, "k_out"), _dev(v_out, "v_out"),
+        k_out.shape[0], _dev(seg_off, "seg_off"), _dev(seg_len, "seg_len"),
+        _dev(src_pos, "src_pos", True), _dev(rows_needed, "rows_needed", True),
+        _dev(workspace, "workspace"), workspace.numel() * workspace.element_size(),
+        _stream(stream)))
+
+
+def dkv_append(k_new, v_new, n_tail, append_cap, k_c, v_c, seg_off, seg_len, stream=None):
+    """k_new, v_new: [num_segments][n_new][d]."""
+    nseg, n_new, d = k_new.shape
+    _check("dkv_append", library().dkv_append(
+        dtype_code(k_new.dtype), nseg, d, _dev(k_new, "k_new"), _dev(v_new, "v_new"), n_new,
+        int(n_tail), int(append_cap), _dev(k_c, "k_c"), _dev(v_c, "v_c"),
+        _dev(seg_off, "seg_off"), _dev(seg_len, "seg_len"), _stream(stream)))
+
+
+def dkv_decode_workspace_bytes(batch, num_q_heads, num_kv_heads, head_dim):
+    return int(library().dkv_decode_workspace_bytes(batch, num_q_heads, num_kv_heads, head_dim))
+
+
+def dkv_decode_attn(q, k_c, v_c, seg_off, seg_len, n_tail, sm_scale, out, workspace,
+                    num_kv_heads, rows_hint=0, stream=None):
+    """q: [B][Hq][d]; seg_off/seg_len: the B*Hkv segments of this call."""
+    B, Hq, d = q.shape
+    _check("dkv_decode_attn", library().dkv_decode_attn(
+        dtype_code(q.dtype), B, Hq, int(num_kv_heads), d, _dev(q, "q"), _dev(k_c, "k_c"),
+        _dev(v_c, "v_c"), _dev(seg_off, "seg_off"), _dev(seg_len, "seg_len"), int(n_tail),
+        float(sm_scale), int(rows_hint), _dev(out, "out"), _dev(workspace, "workspace"),
+        workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def dkv_dense_decode_attn(q, k, v, n_valid, sm_scale, out, workspace, stream=None):
+    """q: [B][Hq][d]; k, v: [B][Hkv][t_cap][d]."""
+    B, Hq, d = q.shape
+    _, Hkv, t_cap, _ = k.shape
+    _check("dkv_dense_decode_attn", library().dkv_dense_decode_attn(
+        dtype_code(q.dtype), B, Hq, Hkv, d, _dev(q, "q"), _dev(k, "k"), _dev(v, "v"), t_cap,
+        int(n_valid), float(sm_scale), _dev(out, "out"), _dev(workspace, "workspace"),
+        workspace.numel() * workspace.element_size(), _stream(stream)))

@@ -1,0 +1,80 @@
+// Launch interface between the C-ABI layer (argument checks) and the kernels.
+// Every launcher assumes its arguments were validated by the caller.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/dkv.h"
+
+namespace dkv {
+
+// --------------------------------------------------------------- map pattern
+struct MapParams {
+  const uint8_t* pattern;  // [N][Hq][D]
+  uint8_t* kv_mask;        // [N][Hkv][T]
+  int32_t* kv_len;         // [N*Hkv]
+  uint8_t* q_mask;         // [N][Hq][T] or null
+  int32_t T, S, R, D, Hq, Hkv, G;
+  int32_t uniform_width;   // > 0: edges are E[k] = uniform_width * k
+  int32_t edges[DKV_MAX_GENERAL_BINS + 1];
+};
+hipError_t launch_map_pattern(const MapParams& p, int num_segments, hipStream_t stream);
+
+// ---------------------------------------------------------------- compaction
+constexpr int kCompactTile = 4096;  // positions per compaction tile
+
+struct CompactParams {
+  const uint8_t* mask;     // [nseg][T]
+  const void* k;           // [nseg][T][d]
+  const void* v;
+  void* k_out;             // [out_rows][d]
+  void* v_out;
+  int32_t* tile_cnt;       // [nseg][ntiles] (workspace)
+  int32_t* tile_base;      // [nseg][ntiles] (workspace)
+  int64_t* seg_off;        // [nseg]
+  int32_t* seg_len;        // [nseg]
+  int32_t* src_pos;        // [out_rows] or null
+  int64_t* rows_needed;    // [1] or null
+  int64_t out_rows;
+  int32_t T, nseg, ntiles, cap, row_bytes;
+};
+size_t compact_workspace_bytes(int64_t nseg, int64_t T);
+hipError_t launch_compact(const CompactParams& p, hipStream_t stream);
+
+struct AppendParams {
+  const void* k_new;  // [nseg][n_new][d]
+  const void* v_new;
+  void* k_c;
+  void* v_c;
+  const int64_t* seg_off;
+  const int32_t* seg_len;
+  int32_t nseg, n_new, n_tail, row_bytes;
+};
+hipError_t launch_append(const AppendParams& p, hipStream_t stream);
+
+// ------------------------------------------------------------ decode attention
+constexpr int kDecodeMaxWG = 1024;  // upper bound on the split count
+
+struct DecodeParams {
+  const void* q;           // [B][Hq][d]
+  const void* k;           // packed (or dense) K rows
+  const void* v;
+  const int64_t* seg_off;  // null: dense addressing
+  const int32_t* seg_len;  // null: dense addressing
+  int64_t dense_stride;    // rows between dense segments (t_cap)
+  int32_t dense_len;       // rows attended per dense segment (n_valid)
+  int32_t n_tail;
+  int32_t nseg, Hkv, Hq, G;
+  float scale_log2;        // sm_scale * log2(e)
+  float* out;              // [B][Hq][d] fp32
+  int32_t* counters;       // [DKV_MAX_SEGMENTS], zero between calls
+  float* partials;         // [(P + nseg)][GP][d + 2]
+  int32_t P;               // workgroups launched
+};
+int decode_group_pad(int G);
+size_t decode_partials_bytes(int nseg, int G, int head_dim);  // partial records only
+hipError_t launch_decode(const DecodeParams& p, dkv_dtype dtype, int head_dim, hipStream_t stream);
+
+}  // namespace dkv

@@ -1,0 +1,133 @@
+// Pattern -> per-KV-head keep mask (Distance-KV, Sec. 3.4, Eq. (4)-(5) and the
+// GQA union).
+//
+// One workgroup per (unit, KV head) segment.  The group's G pattern rows are
+// folded into one G-bit word per bin in LDS (bit h = query head g*G+h keeps
+// the bin), so the union over the group is "word != 0" and the per-head
+// decision is one bit.  Each thread then owns 16 consecutive positions per
+// sweep: it classifies each as sink / recent / binned / uncovered, looks the
+// bin up (a division for uniform edges, a binary search over the edges in LDS
+// otherwise), and writes 16 mask bytes with one 16-byte store when the row
+// is 16-byte aligned.  The retained count is reduced in the block and written
+// once, so kv_len needs no atomics and no pre-clearing.
+
+#include "dkv_device.hpp"
+#include "dkv_launch.hpp"
+
+namespace dkv {
+
+namespace {
+
+constexpr int kMapThreads = 256;
+constexpr int kMapPerThread = 16;
+
+__device__ __forceinline__ int find_bin(int32_t u, const int32_t* edges, int D, int uniform_w) {
+  if (uniform_w > 0) {
+    const int32_t k = u / uniform_w;
+    return k < D ? k : -1;
+  }
+  if (u >= edges[D]) return -1;
+  int lo = 0, hi = D;  // edges[lo] <= u < edges[hi]
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (edges[mid] <= u) lo = mid; else hi = mid;
+  }
+  return lo;
+}
+
+__global__ __launch_bounds__(kMapThreads) void map_pattern_kernel(MapParams p) {
+  extern __shared__ __align__(16) uint8_t smem[];
+  __shared__ int64_t red[kMapThreads / kWave + 1];
+
+  const int seg = blockIdx.x;
+  const int unit = seg / p.Hkv;
+  const int g = seg - unit * p.Hkv;
+  const int tid = threadIdx.x;
+  const int D = p.D, T = p.T, G = p.G;
+
+  uint16_t* qbits = reinterpret_cast<uint16_t*>(smem);
+  int32_t* edges = reinterpret_cast<int32_t*>(smem + ((D * 2 + 15) & ~15));
+
+  const uint8_t* prow = p.pattern + ((int64_t)unit * p.Hq + (int64_t)g * G) * D;
+  for (int k = tid; k < D; k += kMapThreads) {
+    uint32_t bits = 0;
+    for (int h = 0; h < G; ++h) bits |= (prow[(int64_t)h * D + k] != 0 ? 1u : 0u) << h;
+    qbits[k] = (uint16_t)bits;
+  }
+  if (p.uniform_width == 0)
+    for (int k = tid; k <= D; k += kMapThreads) edges[k] = p.edges[k];
+  __syncthreads();
+
+  const uint32_t all_heads = (1u << G) - 1u;
+  const bool aligned_rows = (T & 15) == 0;
+  uint8_t* kv_row = p.kv_mask + (int64_t)seg * T;
+  int64_t count = 0;
+
+  for (int64_t j0 = (int64_t)tid * kMapPerThread; j0 < T; j0 += (int64_t)kMapThreads * kMapPerThread) {
+    uint32_t hb[kMapPerThread];
+#pragma unroll
+    for (int e = 0; e < kMapPerThread; ++e) {
+      const int64_t j = j0 + e;
+      uint32_t bits = 0;
+      if (j < T) {
+        const int32_t delta = T - 1 - (int32_t)j;
+        if (j < p.S || delta < p.R) {
+          bits = all_heads;
+        } else {
+          const int k = find_bin(delta - p.R, edges, D, p.uniform_width);
+          if (k >= 0) bits = qbits[k];
+        }
+      }
+      hb[e] = bits;
+      count += bits != 0u ? 1 : 0;
+    }
+    if (aligned_rows) {
+      u32x4 w;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        w[q] = (hb[4 * q] != 0u ? 1u : 0u) | (hb[4 * q + 1] != 0u ? 1u : 0u) << 8 |
+               (hb[4 * q + 2] != 0u ? 1u : 0u) << 16 | (hb[4 * q + 3] != 0u ? 1u : 0u) << 24;
+      }
+      *reinterpret_cast<u32x4*>(kv_row + j0) = w;
+    } else {
+#pragma unroll
+      for (int e = 0; e < kMapPerThread; ++e)
+        if (j0 + e < T) kv_row[j0 + e] = hb[e] != 0u ? 1 : 0;
+    }
+    if (p.q_mask != nullptr) {
+      for (int h = 0; h < G; ++h) {
+        uint8_t* q_row = p.q_mask + ((int64_t)unit * p.Hq + (int64_t)g * G + h) * T;
+        if (aligned_rows) {
+          u32x4 w;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            uint32_t x = 0;
+#pragma unroll
+            for (int b = 0; b < 4; ++b) x |= ((hb[4 * q + b] >> h) & 1u) << (8 * b);
+            w[q] = x;
+          }
+          *reinterpret_cast<u32x4*>(q_row + j0) = w;
+        } else {
+#pragma unroll
+          for (int e = 0; e < kMapPerThread; ++e)
+            if (j0 + e < T) q_row[j0 + e] = (uint8_t)((hb[e] >> h) & 1u);
+        }
+      }
+    }
+  }
+
+  int64_t total;
+  block_exclusive_scan<kMapThreads>(count, red, &total);
+  if (tid == 0) p.kv_len[seg] = (int32_t)total;
+}
+
+}  // namespace
+
+hipError_t launch_map_pattern(const MapParams& p, int num_segments, hipStream_t stream) {
+  size_t lds = ((size_t)p.D * 2 + 15) & ~(size_t)15;
+  if (p.uniform_width == 0) lds += (size_t)(p.D + 1) * 4;
+  hipLaunchKernelGGL(map_pattern_kernel, dim3(num_segments), dim3(kMapThreads), lds, stream, p);
+  return hipGetLastError();
+}
+
+}  // namespace dkv

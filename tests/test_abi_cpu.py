@@ -1,0 +1,169 @@
+"""Host-only checks of the C ABI: the library loads, exports every entry point
+declared in include/dkv.h, and rejects bad arguments on the host with the
+documented status before anything reaches the GPU.
+
+No call here passes validation, so no kernel is launched and no GPU is
+needed; fake device addresses are never dereferenced on the host.
+"""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_32663_amd as d
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dkv.h")
+
+A = ctypes.c_void_p(0x10000)      # fake 16-byte-aligned device address
+MIS = ctypes.c_void_p(0x10008)    # fake misaligned address
+NUL = None
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dkv_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_hot_path_calls():
+    names = declared_functions()
+    for n in ("dkv_map_pattern", "dkv_compact", "dkv_append", "dkv_decode_attn",
+              "dkv_dense_decode_attn", "dkv_compact_workspace_bytes",
+              "dkv_decode_workspace_bytes", "dkv_status_string"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(d.library_path)
+    for n in declared_functions():
+        assert hasattr(lib, n), n
+
+
+def test_status_strings():
+    for s in range(7):
+        assert d.dkv_status_string(s)
+    assert d.dkv_status_string(99) == "unknown status"
+
+
+def _lay(N=1, Hq=8, Hkv=2, dim=128, T=1024, S=4, R=8, edges=(0, 100, 300, 1012)):
+    return d.make_layout(N, Hq, Hkv, dim, T, S, R, list(edges))
+
+
+def _map(lay, pattern=A, kv_mask=A, kv_len=A, q_mask=NUL):
+    return d.library().dkv_map_pattern(ctypes.byref(lay) if lay is not None else None,
+                                       pattern, kv_mask, kv_len, q_mask, NUL)
+
+
+def test_map_validation():
+    assert _map(None) == d.DKV_ERR_INVALID_ARG
+    assert _map(_lay(Hq=6, Hkv=4)) == d.DKV_ERR_INVALID_ARG
+    assert _map(_lay(Hq=34, Hkv=2)) == d.DKV_ERR_UNSUPPORTED
+    assert _map(_lay(T=-1)) == d.DKV_ERR_INVALID_ARG
+    assert _map(_lay(edges=(1, 5, 9))) == d.DKV_ERR_INVALID_ARG
+    assert _map(_lay(edges=(0, 5, 5))) == d.DKV_ERR_INVALID_ARG
+    assert _map(_lay(edges=(0, 9, 5))) == d.DKV_ERR_INVALID_ARG
+    assert _map(_lay(edges=[0] + [k * k + 1 for k in range(1, 514)])) == d.DKV_ERR_UNSUPPORTED
+    assert _map(_lay(edges=[3 * k for k in range(16386)])) == d.DKV_ERR_UNSUPPORTED
+    assert _map(_lay(), pattern=NUL) == d.DKV_ERR_INVALID_ARG
+    assert _map(_lay(), kv_len=NUL) == d.DKV_ERR_INVALID_ARG
+    assert _map(_lay(), kv_mask=NUL) == d.DKV_ERR_INVALID_ARG
+    assert _map(_lay(), kv_mask=MIS) == d.DKV_ERR_MISALIGNED
+    assert _map(_lay(), q_mask=MIS) == d.DKV_ERR_MISALIGNED
+    # nothing to do: no launch, success
+    assert _map(_lay(N=0), pattern=NUL, kv_mask=NUL, kv_len=NUL) == d.DKV_OK
+
+
+def _compact(lay, dtype=d.DKV_BF16, k=A, v=A, mask=A, cap=4, k_out=A, v_out=A, out_rows=100,
+             seg_off=A, seg_len=A, ws=A, ws_bytes=None):
+    if ws_bytes is None:
+        ws_bytes = d.dkv_compact_workspace_bytes(lay)
+    return d.library().dkv_compact(ctypes.byref(lay), dtype, k, v, mask, cap, k_out, v_out,
+                                   out_rows, seg_off, seg_len, NUL, NUL, ws, ws_bytes, NUL)
+
+
+def test_compact_validation():
+    assert d.dkv_compact_workspace_bytes(_lay()) > 0
+    assert _compact(_lay(dim=96)) == d.DKV_ERR_UNSUPPORTED
+    assert _compact(_lay(), dtype=7) == d.DKV_ERR_INVALID_ARG
+    assert _compact(_lay(), cap=-1) == d.DKV_ERR_INVALID_ARG
+    assert _compact(_lay(), out_rows=-1) == d.DKV_ERR_INVALID_ARG
+    assert _compact(_lay(), k=NUL) == d.DKV_ERR_INVALID_ARG
+    assert _compact(_lay(), seg_off=NUL) == d.DKV_ERR_INVALID_ARG
+    assert _compact(_lay(), v=MIS) == d.DKV_ERR_MISALIGNED
+    assert _compact(_lay(), k_out=MIS) == d.DKV_ERR_MISALIGNED
+    assert _compact(_lay(), mask=MIS) == d.DKV_ERR_MISALIGNED
+    assert _compact(_lay(), ws=NUL) == d.DKV_ERR_WORKSPACE
+    assert _compact(_lay(), ws_bytes=d.dkv_compact_workspace_bytes(_lay()) - 1) == d.DKV_ERR_WORKSPACE
+    assert _compact(_lay(N=40000, Hq=2, Hkv=2)) == d.DKV_ERR_UNSUPPORTED
+    assert _compact(_lay(N=0), k=NUL) == d.DKV_OK
+
+
+def _append(dtype=d.DKV_BF16, nseg=4, dim=128, kn=A, vn=A, n_new=1, n_tail=0, cap=2, kc=A, vc=A,
+            so=A, sl=A):
+    return d.library().dkv_append(dtype, nseg, dim, kn, vn, n_new, n_tail, cap, kc, vc, so, sl, NUL)
+
+
+def test_append_validation():
+    assert _append(n_tail=2, n_new=1, cap=2) == d.DKV_ERR_CAPACITY
+    assert _append(n_tail=-1) == d.DKV_ERR_INVALID_ARG
+    assert _append(dim=32) == d.DKV_ERR_UNSUPPORTED
+    assert _append(kn=NUL) == d.DKV_ERR_INVALID_ARG
+    assert _append(so=NUL) == d.DKV_ERR_INVALID_ARG
+    assert _append(vc=MIS) == d.DKV_ERR_MISALIGNED
+    assert _append(n_new=0, kn=NUL) == d.DKV_OK
+
+
+def _decode(dtype=d.DKV_BF16, B=1, Hq=32, Hkv=8, dim=128, q=A, kc=A, vc=A, so=A, sl=A, n_tail=0,
+            scale=1.0, out=A, ws=A, ws_bytes=None):
+    if ws_bytes is None:
+        ws_bytes = d.dkv_decode_workspace_bytes(max(B, 0), Hq, Hkv, dim) if Hq % Hkv == 0 else 0
+    return d.library().dkv_decode_attn(dtype, B, Hq, Hkv, dim, q, kc, vc, so, sl, n_tail, scale,
+                                       0, out, ws, ws_bytes, NUL)
+
+
+def test_decode_validation():
+    assert d.dkv_decode_workspace_bytes(1, 32, 8, 128) > 0
+    assert d.dkv_decode_workspace_bytes(1, 34, 2, 128) == 0
+    assert d.dkv_decode_workspace_bytes(1, 32, 8, 80) == 0
+    assert _decode(Hq=30, Hkv=8) == d.DKV_ERR_INVALID_ARG
+    assert _decode(Hq=34, Hkv=2) == d.DKV_ERR_UNSUPPORTED
+    assert _decode(dim=256) == d.DKV_ERR_UNSUPPORTED
+    assert _decode(B=300, Hkv=8, Hq=8) == d.DKV_ERR_UNSUPPORTED
+    assert _decode(scale=float("nan")) == d.DKV_ERR_INVALID_ARG
+    assert _decode(scale=float("inf")) == d.DKV_ERR_INVALID_ARG
+    assert _decode(dtype=5) == d.DKV_ERR_INVALID_ARG
+    assert _decode(q=NUL) == d.DKV_ERR_INVALID_ARG
+    assert _decode(so=NUL) == d.DKV_ERR_INVALID_ARG
+    assert _decode(sl=NUL) == d.DKV_ERR_INVALID_ARG
+    assert _decode(n_tail=-1) == d.DKV_ERR_INVALID_ARG
+    assert _decode(out=MIS) == d.DKV_ERR_MISALIGNED
+    assert _decode(kc=MIS) == d.DKV_ERR_MISALIGNED
+    assert _decode(ws=NUL) == d.DKV_ERR_WORKSPACE
+    assert _decode(ws=MIS) == d.DKV_ERR_WORKSPACE
+    assert _decode(ws_bytes=d.dkv_decode_workspace_bytes(1, 32, 8, 128) - 1) == d.DKV_ERR_WORKSPACE
+    assert _decode(B=0, q=NUL, out=NUL) == d.DKV_OK
+
+
+def test_dense_decode_validation():
+    lib = d.library()
+    ws = d.dkv_decode_workspace_bytes(1, 8, 2, 64)
+    assert lib.dkv_dense_decode_attn(d.DKV_F32, 1, 8, 2, 64, A, A, A, 100, 101, 1.0, A, A, ws,
+                                     NUL) == d.DKV_ERR_INVALID_ARG
+    assert lib.dkv_dense_decode_attn(d.DKV_F32, 1, 8, 2, 64, A, A, A, 100, -1, 1.0, A, A, ws,
+                                     NUL) == d.DKV_ERR_INVALID_ARG
+    assert lib.dkv_dense_decode_attn(d.DKV_F32, 1, 8, 2, 64, A, MIS, A, 100, 10, 1.0, A, A, ws,
+                                     NUL) == d.DKV_ERR_MISALIGNED
+    assert lib.dkv_dense_decode_attn(d.DKV_F32, 1, 8, 2, 64, A, A, A, 100, 10, 1.0, A, A, ws - 4,
+                                     NUL) == d.DKV_ERR_WORKSPACE
+
+
+def test_binding_rejects_host_tensors():
+    import torch
+    lay = _lay()
+    with pytest.raises(ValueError):
+        d.dkv_map_pattern(lay, torch.zeros(1, 8, 3, dtype=torch.uint8),
+                          torch.zeros(1, 2, 1024, dtype=torch.uint8),
+                          torch.zeros(1, 2, dtype=torch.int32))

@@ -1,0 +1,446 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Masks, lengths, offsets, packed rows and source positions must match
+bit-for-bit; attention rows must match within ATTN_TOL (max relative error of
+each (batch, head) output row, bf16 in / fp32 accumulate / fp32 out).  Inputs
+are seeded; the oracle computes everything it compares from the same inputs
+on its own.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import dkv_inputs as di
+import oracle as o
+from _helpers import ATTN_TOL, GpuPack, bits, odt, row_rel_err
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+@pytest.fixture(scope="module")
+def d():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2609_32663_amd as lib
+    return lib
+
+
+def _layout(d, N, Hq, Hkv, dim, T, S, R, edges):
+    return d.make_layout(N, Hq, Hkv, dim, T, S, R, edges)
+
+
+def _rand_edges(rng, uniform):
+    D = int(rng.integers(1, 40))
+    if uniform:
+        W = int(rng.integers(1, 200))
+        return [W * k for k in range(D + 1)]
+    steps = rng.integers(1, 300, size=D)
+    return [0] + [int(x) for x in np.cumsum(steps)]
+
+
+def _check_map(d, N, Hq, Hkv, T, S, R, edges, pattern):
+    lay = _layout(d, N, Hq, Hkv, 128, T, S, R, edges)
+    pat = torch.from_numpy(pattern).to(DEV)
+    # flat buffers with slack so that a zero-length context still has a pointer
+    km = torch.full((N * Hkv * T + 16,), 9, dtype=torch.uint8, device=DEV)[:N * Hkv * T].view(N, Hkv, T)
+    kl = torch.full((N, Hkv), -1, dtype=torch.int32, device=DEV)
+    qm = torch.full((N * Hq * T + 16,), 9, dtype=torch.uint8, device=DEV)[:N * Hq * T].view(N, Hq, T)
+    d.dkv_map_pattern(lay, pat, km, kl, qm)
+    torch.cuda.synchronize()
+    oq, okm, okl = o.map_pattern(pattern, T, S, R, edges, Hkv)
+    np.testing.assert_array_equal(km.cpu().numpy(), okm)
+    np.testing.assert_array_equal(kl.cpu().numpy(), okl)
+    np.testing.assert_array_equal(qm.cpu().numpy(), oq)
+
+
+# ---------------------------------------------------------------------------
+# dkv_map_pattern
+# ---------------------------------------------------------------------------
+
+def test_map_random_layouts(d):
+    rng = np.random.default_rng(100)
+    for trial in range(60):
+        N = int(rng.integers(1, 4))
+        Hkv = int(rng.integers(1, 4))
+        G = int(rng.choice([1, 2, 3, 4, 7, 8, 16]))
+        T = int(rng.choice([0, 1, 15, 16, 17, 100, 1000, 4096, 4097, 5000]))
+        S = int(rng.integers(0, 300))
+        R = int(rng.integers(0, 300))
+        edges = _rand_edges(rng, uniform=bool(trial % 2))
+        pattern = (rng.uniform(size=(N, Hkv * G, len(edges) - 1)) < rng.uniform()).astype(np.uint8)
+        _check_map(d, N, Hkv * G, Hkv, T, S, R, edges, pattern)
+
+
+def test_map_paper_layout(d):
+    """Sink 128, recent 1024, 1013 uniform 128-token bins at T = 130,816."""
+    rng = np.random.default_rng(101)
+    pattern = (rng.uniform(size=(2, 8, 1013)) < 0.2).astype(np.uint8)
+    _check_map(d, 2, 8, 2, 130816, 128, 1024, di.uniform_bin_edges(128, 1013), pattern)
+
+
+def test_map_nonzero_pattern_values_count_as_keep(d):
+    rng = np.random.default_rng(102)
+    pattern = rng.integers(0, 4, size=(1, 4, 10)).astype(np.uint8)
+    lay = _layout(d, 1, 4, 2, 128, 800, 3, 5, [0, 7, 20, 50, 90, 150, 230, 330, 460, 600, 792])
+    km = torch.empty((1, 2, 800), dtype=torch.uint8, device=DEV)
+    kl = torch.empty((1, 2), dtype=torch.int32, device=DEV)
+    d.dkv_map_pattern(lay, torch.from_numpy(pattern).to(DEV), km, kl, None)
+    _, okm, okl = o.map_pattern((pattern != 0).astype(np.uint8), 800, 3, 5, lay._edges[:], 2)
+    np.testing.assert_array_equal(km.cpu().numpy(), okm)
+    np.testing.assert_array_equal(kl.cpu().numpy(), okl)
+
+
+@pytest.mark.parametrize("name,units", [
+    ("tiny", None), ("llama8b_layer_32k", None), ("llama70b_layer_bs16_32k", None),
+    ("llama8b_stack_128k", 4), ("qwen7b_stack_bs4_128k", 8)])
+def test_map_workloads(d, name, units):
+    w = di.workload(name)
+    for b in (w.budgets or (None,)):
+        pattern, _ = di.make_pattern(w, budget=b)
+        if units is not None:
+            pattern = pattern[:units]
+        _check_map(d, pattern.shape[0], w.num_q_heads, w.num_kv_heads, w.context_len, w.sink,
+                   w.recent, list(w.bin_edges), np.ascontiguousarray(pattern))
+
+
+# ---------------------------------------------------------------------------
+# dkv_compact / dkv_append
+# ---------------------------------------------------------------------------
+
+def _rand_kv(rng, shape, dtype):
+    x = torch.from_numpy(rng.standard_normal(shape).astype(np.float32))
+    return x.to(dtype).to(DEV)
+
+
+def _check_pack(pack, ref, rows_written=None):
+    seg_off = pack.seg_off.cpu().numpy()
+    seg_len = pack.seg_len.cpu().numpy()
+    np.testing.assert_array_equal(seg_off, ref["seg_off"])
+    np.testing.assert_array_equal(seg_len, ref["seg_len"])
+    assert int(pack.rows_needed.item()) == ref["rows"]
+    kc, vc, sp = bits(pack.k_c), bits(pack.v_c), pack.src_pos.cpu().numpy()
+    for s in range(len(seg_off)):
+        lo, ln = int(seg_off[s]), int(seg_len[s])
+        np.testing.assert_array_equal(kc[lo:lo + ln], ref["k_c"][lo:lo + ln])
+        np.testing.assert_array_equal(vc[lo:lo + ln], ref["v_c"][lo:lo + ln])
+        np.testing.assert_array_equal(sp[lo:lo + ln], ref["src_pos"][lo:lo + ln])
+        assert (sp[lo + ln:lo + ln + pack.cap] == -7).all()  # free rows untouched
+
+
+def test_compact_random(d):
+    rng = np.random.default_rng(200)
+    for trial in range(24):
+        dtype = torch.bfloat16 if trial % 3 else torch.float32
+        dim = 128 if trial % 2 else 64
+        N, Hkv, G = int(rng.integers(1, 3)), int(rng.integers(1, 4)), int(rng.choice([1, 2, 4, 8]))
+        T = int(rng.choice([1, 33, 1000, 4096, 4100, 9000]))
+        S, R = int(rng.integers(0, 64)), int(rng.integers(0, 64))
+        edges = _rand_edges(rng, uniform=bool(trial % 2))
+        cap = int(rng.integers(0, 5))
+        pattern = (rng.uniform(size=(N, Hkv * G, len(edges) - 1)) < rng.uniform()).astype(np.uint8)
+        k = _rand_kv(rng, (N, Hkv, T, dim), dtype)
+        v = _rand_kv(rng, (N, Hkv, T, dim), dtype)
+        lay = _layout(d, N, Hkv * G, Hkv, dim, T, S, R, edges)
+        pack = GpuPack(d, lay, pattern, k, v, cap)
+        torch.cuda.synchronize()
+        _, okm, _ = o.map_pattern(pattern, T, S, R, edges, Hkv)
+        ref = o.compact(bits(k), bits(v), okm, cap)
+        _check_pack(pack, ref)
+
+
+def test_compact_zero_and_full_segments(d):
+    rng = np.random.default_rng(201)
+    N, Hkv, T, dim = 1, 4, 5000, 128
+    pattern = np.zeros((N, 4, 5), np.uint8)
+    pattern[0, 1] = 1          # head 1 keeps every bin
+    pattern[0, 3, 2] = 1
+    edges = [0, 100, 700, 1500, 3000, 5000]
+    k = _rand_kv(rng, (N, Hkv, T, dim), torch.bfloat16)
+    v = _rand_kv(rng, (N, Hkv, T, dim), torch.bfloat16)
+    lay = _layout(d, N, 4, Hkv, dim, T, 0, 0, edges)
+    pack = GpuPack(d, lay, pattern, k, v, 3)
+    torch.cuda.synchronize()
+    _, okm, okl = o.map_pattern(pattern, T, 0, 0, edges, Hkv)
+    assert okl[0, 0] == 0 and okl[0, 1] == T
+    _check_pack(pack, o.compact(bits(k), bits(v), okm, 3))
+
+
+def test_compact_all_keep_is_dense(d):
+    rng = np.random.default_rng(202)
+    k = _rand_kv(rng, (2, 2, 3000, 128), torch.bfloat16)
+    v = _rand_kv(rng, (2, 2, 3000, 128), torch.bfloat16)
+    lay = _layout(d, 2, 4, 2, 128, 3000, 0, 0, [0, 3000])
+    pack = GpuPack(d, lay, np.ones((2, 4, 1), np.uint8), k, v, 0)
+    torch.cuda.synchronize()
+    assert torch.equal(pack.k_c, k.reshape(-1, 128)) and torch.equal(pack.v_c, v.reshape(-1, 128))
+
+
+def test_compact_respects_out_rows(d):
+    """Rows at or beyond out_rows are never written; rows_needed reports the need."""
+    rng = np.random.default_rng(203)
+    N, Hkv, T, dim, cap = 1, 2, 2000, 64, 2
+    mask = torch.from_numpy((rng.uniform(size=(N, Hkv, T)) < 0.5).astype(np.uint8)).to(DEV)
+    k = _rand_kv(rng, (N, Hkv, T, dim), torch.bfloat16)
+    need = int(mask.sum().item()) + Hkv * cap
+    out_rows = need - 300
+    big_k = torch.full((need + 64, dim), 3.0, dtype=torch.bfloat16, device=DEV)
+    big_v = torch.full((need + 64, dim), 3.0, dtype=torch.bfloat16, device=DEV)
+    lay = _layout(d, N, 2, Hkv, dim, T, 0, 0, [0, T])
+    seg_off = torch.empty(Hkv, dtype=torch.int64, device=DEV)
+    seg_len = torch.empty(Hkv, dtype=torch.int32, device=DEV)
+    rn = torch.empty(1, dtype=torch.int64, device=DEV)
+    ws = torch.empty(d.dkv_compact_workspace_bytes(lay), dtype=torch.uint8, device=DEV)
+    d.dkv_compact(lay, k, k, mask, cap, big_k[:out_rows], big_v[:out_rows], seg_off, seg_len, ws,
+                  rows_needed=rn)
+    torch.cuda.synchronize()
+    assert int(rn.item()) == need
+    assert (big_k[out_rows:].float() == 3.0).all() and (big_v[out_rows:].float() == 3.0).all()
+    ref = o.compact(bits(k), bits(k), mask.cpu().numpy(), cap)
+    np.testing.assert_array_equal(bits(big_k[:out_rows])[:ref["seg_len"][0]],
+                                  ref["k_c"][:ref["seg_len"][0]])
+
+
+def test_append_matches_oracle(d):
+    rng = np.random.default_rng(204)
+    for dtype, dim in ((torch.bfloat16, 128), (torch.float32, 64), (torch.bfloat16, 64)):
+        N, Hkv, G, T, cap = 2, 3, 2, 700, 6
+        edges = [0, 100, 250, 700]
+        pattern = (rng.uniform(size=(N, Hkv * G, 3)) < 0.4).astype(np.uint8)
+        k = _rand_kv(rng, (N, Hkv, T, dim), dtype)
+        v = _rand_kv(rng, (N, Hkv, T, dim), dtype)
+        lay = _layout(d, N, Hkv * G, Hkv, dim, T, 4, 8, edges)
+        pack = GpuPack(d, lay, pattern, k, v, cap)
+        _, okm, _ = o.map_pattern(pattern, T, 4, 8, edges, Hkv)
+        ref = o.compact(bits(k), bits(v), okm, cap)
+        kc_ref, vc_ref = ref["k_c"], ref["v_c"]
+        n_tail = 0
+        for n_new in (2, 1, 3):
+            kn = _rand_kv(rng, (N * Hkv, n_new, dim), dtype)
+            vn = _rand_kv(rng, (N * Hkv, n_new, dim), dtype)
+            d.dkv_append(kn, vn, n_tail, cap, pack.k_c, pack.v_c, pack.seg_off, pack.seg_len)
+            kc_ref, vc_ref = o.append(kc_ref, vc_ref, ref["seg_off"], ref["seg_len"],
+                                      bits(kn).reshape(N, Hkv, n_new, dim),
+                                      bits(vn).reshape(N, Hkv, n_new, dim), n_tail)
+            n_tail += n_new
+        torch.cuda.synchronize()
+        kc, vc = bits(pack.k_c), bits(pack.v_c)
+        for s in range(N * Hkv):
+            lo = int(ref["seg_off"][s])
+            hi = lo + int(ref["seg_len"][s]) + n_tail
+            np.testing.assert_array_equal(kc[lo:hi], kc_ref[lo:hi])
+            np.testing.assert_array_equal(vc[lo:hi], vc_ref[lo:hi])
+        with pytest.raises(d.DkvError) as e:
+            d.dkv_append(kn, vn, n_tail, cap, pack.k_c, pack.v_c, pack.seg_off, pack.seg_len)
+        assert e.value.status == d.DKV_ERR_CAPACITY
+
+
+# ---------------------------------------------------------------------------
+# dkv_decode_attn / dkv_dense_decode_attn
+# ---------------------------------------------------------------------------
+
+def _decode_case(d, rng, B, Hkv, G, T, dim, dtype, density, n_tail, cap=8, rows_hint=0,
+                 zero_seg=False, sm_scale=None):
+    Hq = Hkv * G
+    mask = (rng.uniform(size=(B, Hkv, T)) < density).astype(np.uint8)
+    if zero_seg:
+        mask[0, 0] = 0
+    k = _rand_kv(rng, (B, Hkv, T, dim), dtype)
+    v = _rand_kv(rng, (B, Hkv, T, dim), dtype)
+    q = _rand_kv(rng, (B, Hq, dim), dtype)
+    lay = _layout(d, B, Hq, Hkv, dim, T, 0, 0, [0, max(T, 1)])
+    mask_d = torch.from_numpy(mask).to(DEV)
+    rows = int(mask.sum()) + B * Hkv * cap
+    k_c = torch.empty((max(rows, 1), dim), dtype=dtype, device=DEV)
+    v_c = torch.empty_like(k_c)
+    seg_off = torch.empty(B * Hkv, dtype=torch.int64, device=DEV)
+    seg_len = torch.empty(B * Hkv, dtype=torch.int32, device=DEV)
+    ws = torch.empty(d.dkv_compact_workspace_bytes(lay), dtype=torch.uint8, device=DEV)
+    d.dkv_compact(lay, k, v, mask_d, cap, k_c, v_c, seg_off, seg_len, ws)
+    ref = o.compact(bits(k), bits(v), mask, cap)
+    kc_ref, vc_ref = ref["k_c"], ref["v_c"]
+    if n_tail:
+        kn = _rand_kv(rng, (B * Hkv, n_tail, dim), dtype)
+        vn = _rand_kv(rng, (B * Hkv, n_tail, dim), dtype)
+        d.dkv_append(kn, vn, 0, cap, k_c, v_c, seg_off, seg_len)
+        kc_ref, vc_ref = o.append(kc_ref, vc_ref, ref["seg_off"], ref["seg_len"],
+                                  bits(kn).reshape(B, Hkv, n_tail, dim),
+                                  bits(vn).reshape(B, Hkv, n_tail, dim), 0)
+    scale = 1.0 / np.sqrt(dim) if sm_scale is None else sm_scale
+    out = torch.full((B, Hq, dim), float("nan"), dtype=torch.float32, device=DEV)
+    dws = torch.zeros(d.dkv_decode_workspace_bytes(B, Hq, Hkv, dim), dtype=torch.uint8, device=DEV)
+    d.dkv_decode_attn(q, k_c, v_c, seg_off, seg_len, n_tail, scale, out, dws, Hkv, rows_hint=rows_hint)
+    torch.cuda.synchronize()
+    want = o.decode_attn(bits(q), kc_ref, vc_ref, ref["seg_off"], ref["seg_len"], n_tail, scale,
+                         Hkv, odt(q))
+    return out.cpu().numpy(), want, (q, k_c, v_c, seg_off, seg_len, out, dws, scale)
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+@pytest.mark.parametrize("dim", [64, 128])
+def test_decode_random_shapes(d, dtype, dim):
+    rng = np.random.default_rng(300 + dim + (dtype == torch.float32))
+    for trial, G in enumerate([1, 2, 3, 4, 5, 7, 8, 16]):
+        B, Hkv = int(rng.integers(1, 3)), int(rng.integers(1, 4))
+        T = int(rng.choice([5, 31, 33, 200, 1000, 3001]))
+        density = float(rng.choice([0.02, 0.3, 0.9]))
+        n_tail = int(rng.choice([0, 1, 5]))
+        rows_hint = int(rng.choice([0, 1, 10 ** 9]))
+        got, want, _ = _decode_case(d, rng, B, Hkv, G, T, dim, dtype, density, n_tail,
+                                    rows_hint=rows_hint, zero_seg=trial % 3 == 0)
+        assert np.isfinite(got).all()
+        err = row_rel_err(got, want)
+        assert err <= ATTN_TOL, (G, B, Hkv, T, density, n_tail, rows_hint, err)
+
+
+def test_decode_empty_segment_gives_zeros(d):
+    rng = np.random.default_rng(310)
+    got, want, _ = _decode_case(d, rng, 2, 2, 4, 600, 128, torch.bfloat16, 0.4, 0, zero_seg=True)
+    assert (got[0, :4] == 0).all() and (want[0, :4] == 0).all()
+    assert row_rel_err(got[1], want[1]) <= ATTN_TOL
+
+
+def test_decode_tail_only_segment(d):
+    rng = np.random.default_rng(311)
+    got, want, _ = _decode_case(d, rng, 1, 2, 2, 300, 128, torch.bfloat16, 0.5, 3, zero_seg=True)
+    assert row_rel_err(got, want) <= ATTN_TOL
+
+
+@pytest.mark.parametrize("rows_hint", [0, 100, 5000])
+def test_decode_many_pieces_and_determinism(d, rows_hint):
+    rng = np.random.default_rng(320)
+    got, want, args = _decode_case(d, rng, 2, 4, 4, 20000, 128, torch.bfloat16, 0.35, 2,
+                                   rows_hint=rows_hint)
+    assert row_rel_err(got, want) <= ATTN_TOL
+    q, k_c, v_c, seg_off, seg_len, out, dws, scale = args
+    for _ in range(3):
+        out2 = torch.empty_like(out)
+        d.dkv_decode_attn(q, k_c, v_c, seg_off, seg_len, 2, scale, out2, dws, 4, rows_hint=rows_hint)
+        torch.cuda.synchronize()
+        assert torch.equal(out, out2)  # fixed merge order: bitwise reproducible
+
+
+def test_decode_large_logits_are_stable(d):
+    rng = np.random.default_rng(321)
+    got, want, _ = _decode_case(d, rng, 1, 2, 4, 5000, 128, torch.bfloat16, 0.5, 1, sm_scale=8.0)
+    assert np.isfinite(got).all()
+    assert row_rel_err(got, want) <= ATTN_TOL
+
+
+@pytest.mark.parametrize("dtype,dim", [(torch.bfloat16, 128), (torch.float32, 64),
+                                       (torch.bfloat16, 64)])
+def test_dense_decode_matches_oracle(d, dtype, dim):
+    rng = np.random.default_rng(330)
+    for B, Hkv, G, t_cap, n_valid in ((1, 8, 4, 4096, 4000), (3, 2, 8, 900, 900), (2, 1, 7, 50, 17),
+                                      (1, 2, 1, 64, 0)):
+        k = _rand_kv(rng, (B, Hkv, t_cap, dim), dtype)
+        v = _rand_kv(rng, (B, Hkv, t_cap, dim), dtype)
+        q = _rand_kv(rng, (B, Hkv * G, dim), dtype)
+        out = torch.empty((B, Hkv * G, dim), dtype=torch.float32, device=DEV)
+        ws = torch.zeros(d.dkv_decode_workspace_bytes(B, Hkv * G, Hkv, dim), dtype=torch.uint8,
+                         device=DEV)
+        d.dkv_dense_decode_attn(q, k, v, n_valid, 0.125, out, ws)
+        torch.cuda.synchronize()
+        want = o.dense_decode_attn(bits(q), bits(k), bits(v), n_valid, 0.125, odt(q))
+        assert row_rel_err(out.cpu().numpy(), want) <= ATTN_TOL
+
+
+def test_all_keep_packed_decode_equals_dense_kernel(d):
+    """With every position kept the packed cache is the dense cache, the two
+    calls see the same rows and the same split, so they agree bit for bit."""
+    rng = np.random.default_rng(340)
+    B, Hkv, G, T, dim = 1, 8, 4, 8192, 128
+    k = _rand_kv(rng, (B, Hkv, T, dim), torch.bfloat16)
+    v = _rand_kv(rng, (B, Hkv, T, dim), torch.bfloat16)
+    q = _rand_kv(rng, (B, Hkv * G, dim), torch.bfloat16)
+    lay = _layout(d, B, Hkv * G, Hkv, dim, T, 0, 0, [0, T])
+    pack = GpuPack(d, lay, np.ones((B, Hkv * G, 1), np.uint8), k, v, 0)
+    ws = torch.zeros(d.dkv_decode_workspace_bytes(B, Hkv * G, Hkv, dim), dtype=torch.uint8, device=DEV)
+    o1 = torch.empty((B, Hkv * G, dim), dtype=torch.float32, device=DEV)
+    o2 = torch.empty_like(o1)
+    d.dkv_decode_attn(q, pack.k_c, pack.v_c, pack.seg_off, pack.seg_len, 0, 0.1, o1, ws, Hkv,
+                      rows_hint=B * Hkv * T)
+    d.dkv_dense_decode_attn(q, k, v, T, 0.1, o2, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2)
+    want = o.dense_decode_attn(bits(q), bits(k), bits(v), T, 0.1, o.BF16)
+    assert row_rel_err(o1.cpu().numpy(), want) <= ATTN_TOL
+
+
+# ---------------------------------------------------------------------------
+# whole path on the workloads (map -> compact -> append -> decode)
+# ---------------------------------------------------------------------------
+
+def _workload_path(d, w, pattern, units, gen_device, steps=1):
+    """Run the path for the given unit indices of a workload (one sequence each)."""
+    for unit in units:
+        k, v = di.kv_unit(w, unit, device=gen_device)
+        k, v = k.to(DEV)[None], v.to(DEV)[None]
+        pat = np.ascontiguousarray(pattern[unit:unit + 1])
+        lay = d.make_layout(1, w.num_q_heads, w.num_kv_heads, w.head_dim, w.context_len, w.sink,
+                            w.recent, list(w.bin_edges))
+        pack = GpuPack(d, lay, pat, k, v, w.append_cap)
+        torch.cuda.synchronize()
+        _, okm, _ = o.map_pattern(pat, w.context_len, w.sink, w.recent, w.bin_edges, w.num_kv_heads)
+        ref = o.compact(bits(k), bits(v), okm, w.append_cap)
+        _check_pack(pack, ref)
+        kc_ref, vc_ref = ref["k_c"], ref["v_c"]
+        ws = torch.zeros(d.dkv_decode_workspace_bytes(1, w.num_q_heads, w.num_kv_heads, w.head_dim),
+                         dtype=torch.uint8, device=DEV)
+        for step in range(steps):
+            kn, vn = di.kv_new_step(w, unit, step, device=gen_device)
+            kn = kn.to(DEV)[0].contiguous()
+            vn = vn.to(DEV)[0].contiguous()
+            d.dkv_append(kn, vn, step, w.append_cap, pack.k_c, pack.v_c, pack.seg_off, pack.seg_len)
+            kc_ref, vc_ref = o.append(kc_ref, vc_ref, ref["seg_off"], ref["seg_len"],
+                                      bits(kn)[None], bits(vn)[None], step)
+            q = di.q_step(w, unit, step, device=gen_device).to(DEV)[:1].contiguous()
+            out = torch.empty((1, w.num_q_heads, w.head_dim), dtype=torch.float32, device=DEV)
+            d.dkv_decode_attn(q, pack.k_c, pack.v_c, pack.seg_off, pack.seg_len, step + 1,
+                              w.sm_scale, out, ws, w.num_kv_heads, rows_hint=pack.rows)
+            torch.cuda.synchronize()
+            want = o.decode_attn(bits(q), kc_ref, vc_ref, ref["seg_off"], ref["seg_len"], step + 1,
+                                 w.sm_scale, w.num_kv_heads, odt(q))
+            err = row_rel_err(out.cpu().numpy(), want)
+            assert err <= ATTN_TOL, (w.name, unit, step, err)
+
+
+def test_path_tiny(d):
+    w = di.workload("tiny")
+    pattern, _ = di.make_pattern(w)
+    _workload_path(d, w, pattern, [0], "cpu", steps=3)
+
+
+def test_path_llama8b_layer_32k(d):
+    w = di.workload("llama8b_layer_32k")
+    pattern, _ = di.make_pattern(w)
+    _workload_path(d, w, pattern, [0], DEV, steps=2)
+
+
+@pytest.mark.parametrize("budget", [0.10, 0.20, 0.50])
+def test_path_llama70b_batched_budgets(d, budget):
+    """Batched 70B-shaped layer: decode all 16 sequences in one call."""
+    w = di.workload("llama70b_layer_bs16_32k")
+    pattern, _ = di.make_pattern(w, budget=budget)
+    B = w.batch
+    ks, vs = zip(*(di.kv_unit(w, b, device=DEV) for b in range(B)))
+    k, v = torch.stack(ks), torch.stack(vs)
+    lay = d.make_layout(B, w.num_q_heads, w.num_kv_heads, w.head_dim, w.context_len, w.sink,
+                        w.recent, list(w.bin_edges))
+    pack = GpuPack(d, lay, pattern, k, v, w.append_cap)
+    torch.cuda.synchronize()
+    _, okm, okl = o.map_pattern(pattern, w.context_len, w.sink, w.recent, w.bin_edges, w.num_kv_heads)
+    np.testing.assert_array_equal(pack.kv_len.cpu().numpy(), okl)
+    ref = o.compact(bits(k), bits(v), okm, w.append_cap)
+    _check_pack(pack, ref)
+    q = di.q_step(w, 0, 0, device=DEV)
+    out = torch.empty((B, w.num_q_heads, w.head_dim), dtype=torch.float32, device=DEV)
+    ws = torch.zeros(d.dkv_decode_workspace_bytes(B, w.num_q_heads, w.num_kv_heads, w.head_dim),
+                     dtype=torch.uint8, device=DEV)
+    d.dkv_decode_attn(q, pack.k_c, pack.v_c, pack.seg_off, pack.seg_len, 0, w.sm_scale, out, ws,
+                      w.num_kv_heads, rows_hint=pack.rows)
+    torch.cuda.synchronize()
+    want = o.decode_attn(bits(q), ref["k_c"], ref["v_c"], ref["seg_off"], ref["seg_len"], 0,
+                         w.sm_scale, w.num_kv_heads, o.BF16)
+    assert row_rel_err(out.cpu().numpy(), want) <= ATTN_TOL
