@@ -179,10 +179,13 @@ size_t dkv_decode_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t nu
  * union of its group (Sec. 3.4).  out[b][h][:] = softmax(sm_scale * K q) V
  * over those rows, fp32 [B][Hq][d]; a segment with no rows gives zeros.
  * rows_hint (host) expected total rows of the call (0 = unknown); it only
- * sizes the grid, never the result's correctness.
- * workspace  at least dkv_decode_workspace_bytes(...) bytes, ZERO-FILLED
- *          before its first use; every completed call leaves it reusable
- *          without clearing again.  One workspace serves one call at a time.
+ * sizes the split, never the result's correctness.
+ * workspace  at least dkv_decode_workspace_bytes(...) bytes of scratch for
+ *          the split partial results; no initial contents are required.  One
+ *          workspace serves one call at a time (calls on one stream are
+ *          ordered, so reusing it across a stream's calls is safe).
+ * The call enqueues the split attention kernel and, when a segment is split
+ * over several workgroups, a combine kernel.
  */
 dkv_status dkv_decode_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_heads,
                            int32_t num_kv_heads, int32_t head_dim, const void *q,

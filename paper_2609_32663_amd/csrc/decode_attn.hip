@@ -10,12 +10,16 @@
 // crosses segment boundaries yields one piece per segment.  Piece (w, s) of
 // workgroup w in segment s writes its online-softmax state (max m, sum l and
 // unnormalised accumulator per query head) to slot w + s of the workspace;
-// these slots are unique and a segment's slots are contiguous.  The last
-// workgroup to finish a segment (device-scope counter) merges its slots in
-// slot order, so the result does not depend on arrival order, and resets the
-// counter.  A segment covered by one workgroup skips the workspace.
+// these slots are unique and a segment's slots are contiguous.  A second,
+// wide kernel (one workgroup per segment and query head) merges each
+// segment's slots in slot order, so the result does not depend on timing.  A
+// segment covered by one workgroup is written directly and skips the merge.
+// Publishing the partials through the kernel boundary instead of a
+// last-workgroup-merges scheme avoids device-scope fences, which on this part
+// are whole-L2 write-backs and cost more than the merge itself.
 //
-// Inside a workgroup the 4 waves take 32-key tiles round-robin.  Per tile:
+// Inside a workgroup the 4 waves take 32-key tiles round-robin, with the next
+// tile's loads in flight while the current one is computed.  Per tile:
 //   * K rows go straight from HBM into MFMA operands: lane (j, kg) of a wave
 //     loads 16-byte chunks kg, kg+4, ... of key j (j = lane % 16), which is
 //     exactly the B-operand layout of v_mfma_f32_16x16x32_bf16 (8 bf16 per
@@ -54,6 +58,8 @@ struct DecodeCfg {
   static constexpr int kRPT = kTK / kRP;           // V rows per lane per tile
   static constexpr int kKG = kTK / 16;             // 16-key groups per tile
   static constexpr int kRec = GP * (D + 2);        // floats per partial record
+  static constexpr int kMergeChunk = kWaves * D;   // pieces per merge pass (weights fit in wacc)
+  static constexpr int64_t kSubRows = (1LL << 30) / kRowBytes;  // rows per buffer descriptor
   static_assert(kTK % kRP == 0, "tile must cover whole row phases");
 };
 
@@ -89,8 +95,185 @@ __device__ __forceinline__ int64_t owner_of(int64_t x, int64_t total, int64_t P)
   return w < P - 1 ? w : P - 1;
 }
 
+template <int W>
+__device__ __forceinline__ float group_max(float x) {
+#pragma unroll
+  for (int o = W / 2; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, W));
+  return x;
+}
+
+template <int W>
+__device__ __forceinline__ float group_sum(float x) {
+#pragma unroll
+  for (int o = W / 2; o > 0; o >>= 1) x += __shfl_xor(x, o, W);
+  return x;
+}
+
+// K and V registers of one wave tile.
 template <bool BF16, int D, int GP>
-__global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
+struct Tile {
+  using C = DecodeCfg<BF16, D, GP>;
+  u32x4 k[C::kKG][C::kChunks];
+  u32x4 v[C::kRPT];
+};
+
+// Buffer descriptor over `bytes` bytes at `base` (raw buffer, stride 0).  A
+// load whose offset lies past the range returns zeros instead of touching
+// memory, which is what the ragged end of a piece relies on.
+// Every argument must be wave-uniform; readfirstlane makes that explicit so
+// the descriptor lives in SGPRs (otherwise each load becomes a loop).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const char* base, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+  char* ub = reinterpret_cast<char*>(((uint64_t)hi << 32) | lo);
+  return __builtin_amdgcn_make_buffer_rsrc(ub, (short)0, (int)__builtin_amdgcn_readfirstlane(bytes), 0x00020000);
+}
+
+__device__ __forceinline__ int64_t uniform64(int64_t x) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)x >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// Loads the K and V rows [row, row + kTK) of a piece.  k_lane / v_lane are
+// the lane-constant byte offsets (key j16 chunk kg, and row phase rp column
+// chunk cc).  The whole offset stays in the vector offset, which is what the
+// descriptor's range check covers.
+template <bool BF16, int D, int GP>
+__device__ __forceinline__ void load_tile(Tile<BF16, D, GP>& t, __amdgpu_buffer_rsrc_t kr, __amdgpu_buffer_rsrc_t vr,
+                                          uint32_t row, uint32_t k_lane, uint32_t v_lane) {
+  using C = DecodeCfg<BF16, D, GP>;
+#pragma unroll
+  for (int kk = 0; kk < C::kKG; ++kk) {
+    const uint32_t vo = k_lane + (row + 16 * kk) * C::kRowBytes;
+#pragma unroll
+    for (int u = 0; u < C::kChunks; ++u)
+      t.k[kk][u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(kr, vo + 64 * u, 0, 0));
+  }
+#pragma unroll
+  for (int i = 0; i < C::kRPT; ++i) {
+    const uint32_t vo = v_lane + (row + C::kRP * i) * C::kRowBytes;
+    t.v[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(vr, vo, 0, 0));
+  }
+}
+
+// Online-softmax state of one wave.
+template <bool BF16, int D, int GP>
+struct WaveState {
+  using C = DecodeCfg<BF16, D, GP>;
+  float m[4];                 // running max of heads 4*kg + v (uniform over the 16 key lanes)
+  float l[4];                 // this lane's share of the running sum
+  float acc[GP][C::kCPL];     // unnormalised output, columns cc*CPL.., rows of phase rp
+};
+
+template <bool BF16, int D, int GP>
+__device__ __forceinline__ void compute_tile(WaveState<BF16, D, GP>& st, const Tile<BF16, D, GP>& t,
+                                             const u32x4* qa, uint32_t row, uint32_t nrows, float scale_log2,
+                                             float (*pb)[GP], float* ab, int j16, int kg, int rp) {
+  using C = DecodeCfg<BF16, D, GP>;
+  float sc[C::kKG][4];
+#pragma unroll
+  for (int kk = 0; kk < C::kKG; ++kk) {
+    f32x4 c = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int u = 0; u < C::kChunks; ++u) c = qk_mfma(qa[u], t.k[kk][u], c, BF16);
+    const bool valid = row + 16 * kk + j16 < nrows;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) sc[kk][v] = valid ? c[v] * scale_log2 : -INFINITY;
+  }
+
+  float alpha[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    float mt = sc[0][v];
+#pragma unroll
+    for (int kk = 1; kk < C::kKG; ++kk) mt = fmaxf(mt, sc[kk][v]);
+    mt = row16_max(mt);
+    const float m_new = fmaxf(st.m[v], mt);
+    const float m_use = m_new == -INFINITY ? 0.f : m_new;
+    alpha[v] = fast_exp2(st.m[v] - m_use);
+    float psum = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < C::kKG; ++kk) {
+      sc[kk][v] = fast_exp2(sc[kk][v] - m_use);
+      psum += sc[kk][v];
+    }
+    st.l[v] = st.l[v] * alpha[v] + psum;
+    st.m[v] = m_new;
+  }
+
+  if (4 * kg < GP) {
+#pragma unroll
+    for (int kk = 0; kk < C::kKG; ++kk) {
+      f32x4 pv = {sc[kk][0], sc[kk][1], sc[kk][2], sc[kk][3]};
+      *reinterpret_cast<f32x4*>(&pb[16 * kk + j16][4 * kg]) = pv;
+    }
+    if (j16 == 0) {
+      f32x4 av = {alpha[0], alpha[1], alpha[2], alpha[3]};
+      *reinterpret_cast<f32x4*>(&ab[4 * kg]) = av;
+    }
+  }
+  wave_lds_fence();
+
+#pragma unroll
+  for (int h4 = 0; h4 < GP / 4; ++h4) {
+    const f32x4 al = *reinterpret_cast<const f32x4*>(&ab[4 * h4]);
+#pragma unroll
+    for (int v = 0; v < 4; ++v)
+#pragma unroll
+      for (int c = 0; c < C::kCPL; ++c) st.acc[4 * h4 + v][c] *= al[v];
+  }
+#pragma unroll
+  for (int i = 0; i < C::kRPT; ++i) {
+    float vv[C::kCPL];
+    widen16<BF16>(t.v[i], vv);
+    const int r = C::kRP * i + rp;
+#pragma unroll
+    for (int h4 = 0; h4 < GP / 4; ++h4) {
+      const f32x4 pr = *reinterpret_cast<const f32x4*>(&pb[r][4 * h4]);
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+#pragma unroll
+        for (int c = 0; c < C::kCPL; ++c) st.acc[4 * h4 + v][c] = fmaf(pr[v], vv[c], st.acc[4 * h4 + v][c]);
+    }
+  }
+  wave_lds_fence();
+}
+
+// Flat row prefix over the call's segments: pre[s] = rows of segments < s,
+// pre[nseg] = total.  Called by every thread of a workgroup; `red` holds
+// kWaves + 1 int64 of LDS.
+__device__ __forceinline__ void build_row_prefix(const DecodeParams& p, int64_t* pre, int64_t* red) {
+  const int tid = threadIdx.x;
+  const int nseg = p.nseg;
+  const bool dense = p.seg_len == nullptr;
+  const int per = (nseg + kThreads - 1) / kThreads;
+  const int s_lo = tid * per;
+  const int s_hi = min(nseg, s_lo + per);
+  int64_t sum = 0;
+  for (int s = s_lo; s < s_hi; ++s) sum += dense ? p.dense_len : (int64_t)p.seg_len[s] + p.n_tail;
+  int64_t total_unused;
+  int64_t run = block_exclusive_scan<kThreads>(sum, red, &total_unused);
+  for (int s = s_lo; s < s_hi; ++s) {
+    pre[s] = run;
+    run += dense ? p.dense_len : (int64_t)p.seg_len[s] + p.n_tail;
+  }
+  if (s_hi == nseg && s_lo <= nseg) pre[nseg] = run;
+  if (nseg == 0 && tid == 0) pre[0] = 0;
+  __syncthreads();
+}
+
+// Two waves per SIMD where the double-buffered tiles and the accumulators fit
+// in 256 VGPRs without spilling; one otherwise.
+template <bool BF16, int D, int GP>
+constexpr int decode_waves_per_eu() {
+  return (GP == 4 && (BF16 || D == 64)) ? 2 : 1;
+}
+
+template <bool BF16, int D, int GP>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(decode_waves_per_eu<BF16, D, GP>())))
+void decode_kernel(DecodeParams p) {
   using C = DecodeCfg<BF16, D, GP>;
   extern __shared__ __align__(16) int64_t pre[];          // [nseg + 1] row prefix
   __shared__ __align__(16) float pbuf[kWaves][kTK][GP];   // probabilities per wave tile
@@ -99,33 +282,16 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
   __shared__ float wm[kWaves][GP];
   __shared__ float wl[kWaves][GP];
   __shared__ int64_t red[kWaves + 1];
-  __shared__ int last_flag;
 
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
-  const int wave = tid / kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int w = blockIdx.x;
   const int nseg = p.nseg;
   const bool dense = p.seg_len == nullptr;
 
-  // ---- flat row prefix over the call's segments ------------------------
-  {
-    const int per = (nseg + kThreads - 1) / kThreads;
-    const int s_lo = tid * per;
-    const int s_hi = min(nseg, s_lo + per);
-    int64_t sum = 0;
-    for (int s = s_lo; s < s_hi; ++s) sum += dense ? p.dense_len : (int64_t)p.seg_len[s] + p.n_tail;
-    int64_t total_unused;
-    int64_t run = block_exclusive_scan<kThreads>(sum, red, &total_unused);
-    for (int s = s_lo; s < s_hi; ++s) {
-      pre[s] = run;
-      run += dense ? p.dense_len : (int64_t)p.seg_len[s] + p.n_tail;
-    }
-    if (s_hi == nseg && s_lo <= nseg) pre[nseg] = run;
-    if (nseg == 0 && tid == 0) pre[0] = 0;
-  }
-  __syncthreads();
-  const int64_t total = pre[nseg];
+  build_row_prefix(p, pre, red);
+  const int64_t total = uniform64(pre[nseg]);
 
   // ---- segments with no rows at all produce zeros ----------------------
   for (int s = w; s < nseg; s += p.P) {
@@ -151,22 +317,23 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
     s = a;
   }
 
-  const char* kbytes = reinterpret_cast<const char*>(p.k);
-  const char* vbytes = reinterpret_cast<const char*>(p.v);
   const char* qbytes = reinterpret_cast<const char*>(p.q);
   const int j16 = lane & 15;   // key (QK) / head row (A operand) within a 16-group
   const int kg = lane >> 4;    // 16-byte chunk group (QK)
   const int cc = lane % C::kLPR;
   const int rp = lane / C::kLPR;
 
+  s = __builtin_amdgcn_readfirstlane(s);
   for (; s < nseg && pre[s] < hi; ++s) {
-    const int64_t seg_lo = pre[s], seg_hi = pre[s + 1];
+    const int64_t seg_lo = uniform64(pre[s]), seg_hi = uniform64(pre[s + 1]);
     const int64_t a = (lo > seg_lo ? lo : seg_lo) - seg_lo;
     const int64_t bnd = (hi < seg_hi ? hi : seg_hi) - seg_lo;
     if (a >= bnd) continue;
     const int bseq = s / p.Hkv;
     const int g = s - bseq * p.Hkv;
-    const int64_t row0 = dense ? (int64_t)s * p.dense_stride : p.seg_off[s];
+    const int64_t row0 = uniform64(dense ? (int64_t)s * p.dense_stride : p.seg_off[s]);
+    const char* kbase = reinterpret_cast<const char*>(p.k) + row0 * C::kRowBytes;
+    const char* vbase = reinterpret_cast<const char*>(p.v) + row0 * C::kRowBytes;
 
     // A operand: query head j16 of the group (zero beyond G), chunks kg + 4u.
     u32x4 qa[C::kChunks];
@@ -180,131 +347,65 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
       }
     }
 
-    float m_run[4], l_part[4];
+    WaveState<BF16, D, GP> st;
 #pragma unroll
-    for (int v = 0; v < 4; ++v) { m_run[v] = -INFINITY; l_part[v] = 0.f; }
-    float acc[GP][C::kCPL];
+    for (int v = 0; v < 4; ++v) { st.m[v] = -INFINITY; st.l[v] = 0.f; }
 #pragma unroll
     for (int h = 0; h < GP; ++h)
 #pragma unroll
-      for (int c = 0; c < C::kCPL; ++c) acc[h][c] = 0.f;
+      for (int c = 0; c < C::kCPL; ++c) st.acc[h][c] = 0.f;
 
-    const int64_t ntile = (bnd - a + kTK - 1) / kTK;
-    const int64_t last = bnd - 1;
-    const bool head_lanes = 4 * kg < GP;
-
-    for (int64_t t = wave; t < ntile; t += kWaves) {
-      const int64_t rbase = a + t * kTK;
-      u32x4 kf[C::kKG][C::kChunks];
-      u32x4 vf[C::kRPT];
-#pragma unroll
-      for (int kk = 0; kk < C::kKG; ++kk) {
-        int64_t key = rbase + 16 * kk + j16;
-        key = key < last ? key : last;
-        const char* src = kbytes + (row0 + key) * C::kRowBytes + 16 * kg;
-#pragma unroll
-        for (int u = 0; u < C::kChunks; ++u) kf[kk][u] = *reinterpret_cast<const u32x4*>(src + 64 * u);
+    // Rows are addressed through buffer descriptors over at most kSubRows
+    // rows at a time (32-bit offsets); the ragged end of each range reads
+    // zeros and is masked out of the softmax.
+    const uint32_t k_lane = (uint32_t)(j16 * C::kRowBytes + 16 * kg);
+    const uint32_t v_lane = (uint32_t)(rp * C::kRowBytes + 16 * cc);
+    Tile<BF16, D, GP> ta, tb;
+    for (int64_t a2 = a; a2 < bnd; a2 += C::kSubRows) {
+      const uint32_t nrows = (uint32_t)((bnd - a2) < C::kSubRows ? (bnd - a2) : C::kSubRows);
+      const __amdgpu_buffer_rsrc_t kr = make_rsrc(kbase + a2 * C::kRowBytes, nrows * C::kRowBytes);
+      const __amdgpu_buffer_rsrc_t vr = make_rsrc(vbase + a2 * C::kRowBytes, nrows * C::kRowBytes);
+      const uint32_t ntile = (nrows + kTK - 1) / kTK;
+      // Two register tiles: the next tile of this wave is loading while the
+      // current one is computed.
+      uint32_t t = wave;
+      if (t < ntile) load_tile(ta, kr, vr, t * kTK, k_lane, v_lane);
+      while (t < ntile) {
+        const uint32_t t1 = t + kWaves;
+        if (t1 < ntile) load_tile(tb, kr, vr, t1 * kTK, k_lane, v_lane);
+        compute_tile(st, ta, qa, t * kTK, nrows, p.scale_log2, pbuf[wave], abuf[wave], j16, kg, rp);
+        t = t1;
+        if (t >= ntile) break;
+        const uint32_t t2 = t + kWaves;
+        if (t2 < ntile) load_tile(ta, kr, vr, t2 * kTK, k_lane, v_lane);
+        compute_tile(st, tb, qa, t * kTK, nrows, p.scale_log2, pbuf[wave], abuf[wave], j16, kg, rp);
+        t = t2;
       }
-#pragma unroll
-      for (int i = 0; i < C::kRPT; ++i) {
-        int64_t key = rbase + C::kRP * i + rp;
-        key = key < last ? key : last;
-        vf[i] = *reinterpret_cast<const u32x4*>(vbytes + (row0 + key) * C::kRowBytes + 16 * cc);
-      }
-
-      // scores: lane j16 + 16*kg holds key 16*kk + j16, heads 4*kg + v
-      float sc[C::kKG][4];
-#pragma unroll
-      for (int kk = 0; kk < C::kKG; ++kk) {
-        f32x4 c = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int u = 0; u < C::kChunks; ++u) c = qk_mfma(qa[u], kf[kk][u], c, BF16);
-        const bool valid = rbase + 16 * kk + j16 <= last;
-#pragma unroll
-        for (int v = 0; v < 4; ++v) sc[kk][v] = valid ? c[v] * p.scale_log2 : -INFINITY;
-      }
-
-      float alpha[4];
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        float mt = sc[0][v];
-#pragma unroll
-        for (int kk = 1; kk < C::kKG; ++kk) mt = fmaxf(mt, sc[kk][v]);
-        mt = row16_max(mt);
-        const float m_new = fmaxf(m_run[v], mt);
-        const float m_use = m_new == -INFINITY ? 0.f : m_new;
-        alpha[v] = fast_exp2(m_run[v] - m_use);
-        float psum = 0.f;
-#pragma unroll
-        for (int kk = 0; kk < C::kKG; ++kk) {
-          sc[kk][v] = fast_exp2(sc[kk][v] - m_use);
-          psum += sc[kk][v];
-        }
-        l_part[v] = l_part[v] * alpha[v] + psum;
-        m_run[v] = m_new;
-      }
-
-      if (head_lanes) {
-#pragma unroll
-        for (int kk = 0; kk < C::kKG; ++kk) {
-          f32x4 pv = {sc[kk][0], sc[kk][1], sc[kk][2], sc[kk][3]};
-          *reinterpret_cast<f32x4*>(&pbuf[wave][16 * kk + j16][4 * kg]) = pv;
-        }
-        if (j16 == 0) {
-          f32x4 av = {alpha[0], alpha[1], alpha[2], alpha[3]};
-          *reinterpret_cast<f32x4*>(&abuf[wave][4 * kg]) = av;
-        }
-      }
-      wave_lds_fence();
-
-#pragma unroll
-      for (int h4 = 0; h4 < GP / 4; ++h4) {
-        const f32x4 al = *reinterpret_cast<const f32x4*>(&abuf[wave][4 * h4]);
-#pragma unroll
-        for (int v = 0; v < 4; ++v)
-#pragma unroll
-          for (int c = 0; c < C::kCPL; ++c) acc[4 * h4 + v][c] *= al[v];
-      }
-#pragma unroll
-      for (int i = 0; i < C::kRPT; ++i) {
-        float vv[C::kCPL];
-        widen16<BF16>(vf[i], vv);
-        const int r = C::kRP * i + rp;
-#pragma unroll
-        for (int h4 = 0; h4 < GP / 4; ++h4) {
-          const f32x4 pr = *reinterpret_cast<const f32x4*>(&pbuf[wave][r][4 * h4]);
-#pragma unroll
-          for (int v = 0; v < 4; ++v)
-#pragma unroll
-            for (int c = 0; c < C::kCPL; ++c) acc[4 * h4 + v][c] = fmaf(pr[v], vv[c], acc[4 * h4 + v][c]);
-        }
-      }
-      wave_lds_fence();
     }
 
     // ---- wave state -> LDS ---------------------------------------------
 #pragma unroll
-    for (int v = 0; v < 4; ++v) l_part[v] = row16_sum(l_part[v]);
+    for (int v = 0; v < 4; ++v) st.l[v] = row16_sum(st.l[v]);
 #pragma unroll
     for (int h = 0; h < GP; ++h)
 #pragma unroll
       for (int c = 0; c < C::kCPL; ++c) {
-        float x = acc[h][c];
+        float x = st.acc[h][c];
 #pragma unroll
         for (int o = C::kLPR; o < kWave; o <<= 1) x += __shfl_xor(x, o, kWave);
-        acc[h][c] = x;
+        st.acc[h][c] = x;
       }
     if (rp == 0) {
 #pragma unroll
       for (int h = 0; h < GP; ++h)
 #pragma unroll
-        for (int c = 0; c < C::kCPL; ++c) wacc[wave][h][cc * C::kCPL + c] = acc[h][c];
+        for (int c = 0; c < C::kCPL; ++c) wacc[wave][h][cc * C::kCPL + c] = st.acc[h][c];
     }
-    if (j16 == 0 && head_lanes) {
+    if (j16 == 0 && 4 * kg < GP) {
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        wm[wave][4 * kg + v] = m_run[v];
-        wl[wave][4 * kg + v] = l_part[v];
+        wm[wave][4 * kg + v] = st.m[v];
+        wl[wave][4 * kg + v] = st.l[v];
       }
     }
     __syncthreads();
@@ -338,49 +439,131 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
         }
       }
     }
-    if (!single) {
-      __threadfence();
-      __syncthreads();
-      if (tid == 0) {
-        const int prev = atomicAdd(p.counters + s, 1);
-        last_flag = prev == (int)(w_last - w_first);
-      }
-      __syncthreads();
-      if (last_flag) {
-        __threadfence();
-        const float* first = p.partials + (w_first + s) * C::kRec;
-        const int npieces = (int)(w_last - w_first + 1);
-        for (int idx = tid; idx < p.G * D; idx += kThreads) {
-          const int h = idx / D, c = idx - (idx / D) * D;
-          float M = -INFINITY;
-          for (int k = 0; k < npieces; ++k) M = fmaxf(M, first[(int64_t)k * C::kRec + h]);
-          const float Mu = M == -INFINITY ? 0.f : M;
-          float L = 0.f, A = 0.f;
-          for (int k = 0; k < npieces; ++k) {
-            const float* r = first + (int64_t)k * C::kRec;
-            const float f = fast_exp2(r[h] - Mu);
-            L += f * r[GP + h];
-            A += f * r[2 * GP + h * D + c];
-          }
-          outp[idx] = L > 0.f ? A / L : 0.f;
-        }
-        if (tid == 0) p.counters[s] = 0;
-      }
-    }
-    __syncthreads();
+    __syncthreads();  // LDS is reused by the next piece
   }
 }
 
-template <bool BF16, int D>
-hipError_t launch_d(const DecodeParams& p, int GP, hipStream_t stream) {
+// Block-wide max / sum of one float per thread (every thread gets the result).
+__device__ __forceinline__ float block_max(float x, float* tmp) {
+  x = group_max<kWave>(x);
+  if ((threadIdx.x & (kWave - 1)) == 0) tmp[threadIdx.x / kWave] = x;
+  __syncthreads();
+  float r = tmp[0];
+#pragma unroll
+  for (int q = 1; q < kWaves; ++q) r = fmaxf(r, tmp[q]);
+  __syncthreads();
+  return r;
+}
+
+__device__ __forceinline__ float block_sum(float x, float* tmp) {
+  x = group_sum<kWave>(x);
+  if ((threadIdx.x & (kWave - 1)) == 0) tmp[threadIdx.x / kWave] = x;
+  __syncthreads();
+  float r = tmp[0];
+#pragma unroll
+  for (int q = 1; q < kWaves; ++q) r += tmp[q];
+  __syncthreads();
+  return r;
+}
+
+// Combine kernel: one workgroup per (segment, query head).  It rebuilds the
+// attention kernel's flat row prefix and split, finds the pieces of its
+// segment and merges their records in slot order:
+//   M = max_k m_k,  w_k = 2^(m_k - M),  out = sum_k w_k acc_k / sum_k w_k l_k.
+// Segments with no rows or a single piece were finished by the attention
+// kernel.  The kernel boundary makes the records visible, so neither kernel
+// needs device-scope fences or counters.
+template <int D, int GP>
+__global__ __launch_bounds__(kThreads) void decode_merge_kernel(DecodeParams p) {
+  constexpr int kRec = GP * (D + 2);
+  constexpr int kQuads = D / 4;              // float4 column groups per head row
+  constexpr int kPhases = kThreads / kQuads; // pieces handled side by side
+  extern __shared__ __align__(16) int64_t pre[];
+  __shared__ float fw[kDecodeMaxWG];
+  __shared__ __align__(16) float xb[kThreads * 4];
+  __shared__ int64_t red[kWaves + 1];
+  __shared__ float tmp[kWaves];
+
+  build_row_prefix(p, pre, red);
+  const int64_t total = pre[p.nseg];
+  const int s = blockIdx.x / p.G;
+  const int h = blockIdx.x - s * p.G;
+  const int64_t seg_lo = pre[s], seg_hi = pre[s + 1];
+  if (seg_hi == seg_lo) return;
+  const int64_t P = total < p.P ? total : p.P;
+  const int64_t w_first = owner_of(seg_lo, total, P);
+  const int n = (int)(owner_of(seg_hi - 1, total, P) - w_first + 1);
+  if (n == 1) return;
+  const float* first = p.partials + (w_first + s) * kRec;
+  const int tid = threadIdx.x;
+
+  float mx = -INFINITY;
+  for (int k = tid; k < n; k += kThreads) mx = fmaxf(mx, first[(int64_t)k * kRec + h]);
+  mx = block_max(mx, tmp);
+  const float Mu = mx == -INFINITY ? 0.f : mx;
+  float ls = 0.f;
+  for (int k = tid; k < n; k += kThreads) {
+    const float* r = first + (int64_t)k * kRec;
+    const float f = fast_exp2(r[h] - Mu);
+    fw[k] = f;
+    ls += f * r[GP + h];
+  }
+  const float L = block_sum(ls, tmp);  // its barriers also publish fw
+
+  const int cq = tid % kQuads, ph = tid / kQuads;
+  const float* base = first + 2 * GP + h * D + 4 * cq;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
+  for (int k = ph; k < n; k += kPhases) acc += fw[k] * *reinterpret_cast<const f32x4*>(base + (int64_t)k * kRec);
+  *reinterpret_cast<f32x4*>(&xb[4 * tid]) = acc;
+  __syncthreads();
+  if (tid < kQuads) {
+    f32x4 sum = acc;
+    for (int q = 1; q < kPhases; ++q) sum += *reinterpret_cast<const f32x4*>(&xb[4 * (tid + q * kQuads)]);
+    const int bseq = s / p.Hkv, g = s - bseq * p.Hkv;
+    float* o = p.out + ((int64_t)bseq * p.Hq + (int64_t)g * p.G + h) * D + 4 * cq;
+    *reinterpret_cast<f32x4*>(o) = sum * (L > 0.f ? 1.f / L : 0.f);
+  }
+}
+
+// Split count: about one 128-row slice per workgroup, capped at the number of
+// workgroups the device holds at once (so every slice starts immediately and
+// all finish together) and at the workspace bound.
+template <typename K>
+int32_t split_count(K kernel, size_t lds, int64_t rows_hint) {
+  int dev = 0, cus = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+    cus = 256;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, lds) != hipSuccess || per_cu <= 0)
+    per_cu = 1;
+  int64_t cap = (int64_t)cus * per_cu;
+  if (cap > kDecodeMaxWG) cap = kDecodeMaxWG;
+  if (rows_hint <= 0) return (int32_t)cap;
+  int64_t P = (rows_hint + 127) / 128;
+  return (int32_t)(P < 1 ? 1 : (P > cap ? cap : P));
+}
+
+template <bool BF16, int D, int GP>
+hipError_t launch_g(DecodeParams p, int64_t rows_hint, hipStream_t stream) {
   const size_t lds = ((size_t)p.nseg + 1) * sizeof(int64_t);
+  p.P = split_count(decode_kernel<BF16, D, GP>, lds, rows_hint);
+  hipLaunchKernelGGL((decode_kernel<BF16, D, GP>), dim3(p.P), dim3(kThreads), lds, stream, p);
+  // Segments split over several workgroups are finished by the combine
+  // kernel; when the call has a single split there is nothing to combine.
+  if (p.P > 1)
+    hipLaunchKernelGGL((decode_merge_kernel<D, GP>), dim3(p.nseg * p.G), dim3(kThreads), lds, stream, p);
+  return hipGetLastError();
+}
+
+template <bool BF16, int D>
+hipError_t launch_d(const DecodeParams& p, int GP, int64_t rows_hint, hipStream_t stream) {
   switch (GP) {
-    case 4: hipLaunchKernelGGL((decode_kernel<BF16, D, 4>), dim3(p.P), dim3(kThreads), lds, stream, p); break;
-    case 8: hipLaunchKernelGGL((decode_kernel<BF16, D, 8>), dim3(p.P), dim3(kThreads), lds, stream, p); break;
-    case 16: hipLaunchKernelGGL((decode_kernel<BF16, D, 16>), dim3(p.P), dim3(kThreads), lds, stream, p); break;
+    case 4: return launch_g<BF16, D, 4>(p, rows_hint, stream);
+    case 8: return launch_g<BF16, D, 8>(p, rows_hint, stream);
+    case 16: return launch_g<BF16, D, 16>(p, rows_hint, stream);
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 
 }  // namespace
@@ -392,14 +575,15 @@ size_t decode_partials_bytes(int nseg, int G, int head_dim) {
   return ((size_t)kDecodeMaxWG + nseg) * rec;
 }
 
-hipError_t launch_decode(const DecodeParams& p, dkv_dtype dtype, int head_dim, hipStream_t stream) {
+hipError_t launch_decode(const DecodeParams& p, dkv_dtype dtype, int head_dim, int64_t rows_hint,
+                         hipStream_t stream) {
   const int GP = decode_group_pad(p.G);
   if (dtype == DKV_BF16) {
-    if (head_dim == 128) return launch_d<true, 128>(p, GP, stream);
-    if (head_dim == 64) return launch_d<true, 64>(p, GP, stream);
+    if (head_dim == 128) return launch_d<true, 128>(p, GP, rows_hint, stream);
+    if (head_dim == 64) return launch_d<true, 64>(p, GP, rows_hint, stream);
   } else {
-    if (head_dim == 128) return launch_d<false, 128>(p, GP, stream);
-    if (head_dim == 64) return launch_d<false, 64>(p, GP, stream);
+    if (head_dim == 128) return launch_d<false, 128>(p, GP, rows_hint, stream);
+    if (head_dim == 64) return launch_d<false, 64>(p, GP, rows_hint, stream);
   }
   return hipErrorInvalidValue;
 }

@@ -14,8 +14,6 @@
 
 namespace {
 
-constexpr size_t kDecodeCounterBytes = (size_t)DKV_MAX_SEGMENTS * 4;
-
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 bool head_dim_ok(int32_t d) { return d == 64 || d == 128; }
@@ -43,26 +41,6 @@ int32_t uniform_width(const int32_t* e, int32_t D) {
   for (int32_t k = 0; k <= D; ++k)
     if ((int64_t)e[k] != (int64_t)W * k) return 0;
   return W;
-}
-
-int device_cu_count() {
-  int dev = 0, cus = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return 256;
-  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
-    return 256;
-  return cus;
-}
-
-// Split count: about one 128-row slice per workgroup, at most two
-// workgroups per compute unit (the kernel's occupancy) and the workspace cap.
-int32_t decode_split(int64_t rows_hint) {
-  int64_t cap = 2LL * device_cu_count();
-  if (cap > dkv::kDecodeMaxWG) cap = dkv::kDecodeMaxWG;
-  if (rows_hint <= 0) return (int32_t)cap;
-  int64_t P = (rows_hint + 127) / 128;
-  if (P < 1) P = 1;
-  if (P > cap) P = cap;
-  return (int32_t)P;
 }
 
 dkv_status check_decode_common(int dtype, int32_t batch, int32_t hq, int32_t hkv, int32_t d,
@@ -224,9 +202,7 @@ size_t dkv_decode_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t nu
       (int64_t)batch * num_kv_heads > DKV_MAX_SEGMENTS)
     return 0;
   const int nseg = batch * num_kv_heads;
-  // Counters sit in a fixed region sized for the largest call, so a workspace
-  // can be shared by calls of different shapes without clearing it again.
-  return kDecodeCounterBytes + dkv::decode_partials_bytes(nseg, num_q_heads / num_kv_heads, head_dim);
+  return dkv::decode_partials_bytes(nseg, num_q_heads / num_kv_heads, head_dim);
 }
 
 dkv_status dkv_decode_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
@@ -253,10 +229,8 @@ dkv_status dkv_decode_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_heads, 
   p.G = num_q_heads / num_kv_heads;
   p.scale_log2 = sm_scale * 1.4426950408889634f;
   p.out = out;
-  p.counters = static_cast<int32_t*>(workspace);
-  p.partials = reinterpret_cast<float*>(static_cast<char*>(workspace) + kDecodeCounterBytes);
-  p.P = decode_split(rows_hint);
-  return hip_status(dkv::launch_decode(p, dtype, head_dim, (hipStream_t)stream));
+  p.partials = static_cast<float*>(workspace);
+  return hip_status(dkv::launch_decode(p, dtype, head_dim, rows_hint, (hipStream_t)stream));
 }
 
 dkv_status dkv_dense_decode_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
@@ -280,10 +254,8 @@ dkv_status dkv_dense_decode_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_h
   p.G = num_q_heads / num_kv_heads;
   p.scale_log2 = sm_scale * 1.4426950408889634f;
   p.out = out;
-  p.counters = static_cast<int32_t*>(workspace);
-  p.partials = reinterpret_cast<float*>(static_cast<char*>(workspace) + kDecodeCounterBytes);
-  p.P = decode_split((int64_t)p.nseg * n_valid);
-  return hip_status(dkv::launch_decode(p, dtype, head_dim, (hipStream_t)stream));
+  p.partials = static_cast<float*>(workspace);
+  return hip_status(dkv::launch_decode(p, dtype, head_dim, (int64_t)p.nseg * n_valid, (hipStream_t)stream));
 }
 
 }  // extern "C"

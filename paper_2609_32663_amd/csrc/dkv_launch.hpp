@@ -69,12 +69,13 @@ struct DecodeParams {
   int32_t nseg, Hkv, Hq, G;
   float scale_log2;        // sm_scale * log2(e)
   float* out;              // [B][Hq][d] fp32
-  int32_t* counters;       // [DKV_MAX_SEGMENTS], zero between calls
   float* partials;         // [(P + nseg)][GP][d + 2]
-  int32_t P;               // workgroups launched
+  int32_t P;               // workgroups launched (set by launch_decode)
 };
 int decode_group_pad(int G);
 size_t decode_partials_bytes(int nseg, int G, int head_dim);  // partial records only
-hipError_t launch_decode(const DecodeParams& p, dkv_dtype dtype, int head_dim, hipStream_t stream);
+// rows_hint: expected total rows of the call (0 = unknown); sizes the split.
+hipError_t launch_decode(const DecodeParams& p, dkv_dtype dtype, int head_dim, int64_t rows_hint,
+                         hipStream_t stream);
 
 }  // namespace dkv

@@ -321,6 +321,18 @@ def test_decode_many_pieces_and_determinism(d, rows_hint):
         assert torch.equal(out, out2)  # fixed merge order: bitwise reproducible
 
 
+def test_decode_workspace_needs_no_clearing(d):
+    rng = np.random.default_rng(322)
+    got, want, args = _decode_case(d, rng, 2, 4, 4, 6000, 128, torch.bfloat16, 0.35, 1)
+    q, k_c, v_c, seg_off, seg_len, out, dws, scale = args
+    dws.copy_(torch.from_numpy(rng.integers(0, 256, dws.numel(), dtype=np.uint8)).to(DEV))
+    out2 = torch.empty_like(out)
+    d.dkv_decode_attn(q, k_c, v_c, seg_off, seg_len, 1, scale, out2, dws, 4)
+    torch.cuda.synchronize()
+    assert torch.equal(out, out2)
+    assert row_rel_err(got, want) <= ATTN_TOL
+
+
 def test_decode_large_logits_are_stable(d):
     rng = np.random.default_rng(321)
     got, want, _ = _decode_case(d, rng, 1, 2, 4, 5000, 128, torch.bfloat16, 0.5, 1, sm_scale=8.0)
