@@ -185,38 +185,35 @@ def main():
     ws_bytes = dws.numel()
     layer_rows = [int(lens[layer * B:(layer + 1) * B].sum()) for layer in range(L)]
 
-    def append_args(layer, n_tail, dense):
-        so, sl = (dseg_off, dseg_len) if dense else (seg_off, seg_len)
-        kc, vc = (kd, vd) if dense else (k_c, v_c)
+    def packed_args(layer, n_tail, sh):
+        """dkv_append_decode_attn: append this step's token at n_tail, attend."""
+        off = layer * nseg_layer
         kn, vn = new_kv[layer]
-        off = layer * nseg_layer
-        return (d.DKV_BF16, nseg_layer, dim, P(kn.data_ptr()), P(vn.data_ptr()), 1, n_tail, cap,
-                P(kc.data_ptr()), P(vc.data_ptr()), P(so.data_ptr() + 8 * off),
-                P(sl.data_ptr() + 4 * off), P(sh))
-
-    def decode_args(layer, n_tail):
-        off = layer * nseg_layer
-        return (d.DKV_BF16, B, Hq, Hkv, dim, P(q_layers[layer].data_ptr()), P(k_c.data_ptr()),
-                P(v_c.data_ptr()), P(seg_off.data_ptr() + 8 * off), P(seg_len.data_ptr() + 4 * off),
-                n_tail, w.sm_scale, layer_rows[layer] + nseg_layer * n_tail, P(out.data_ptr()),
-                P(dws.data_ptr()), ws_bytes, P(sh))
-
-    def dense_args(layer, n_valid):
-        kl = kd[layer * B:(layer + 1) * B]
-        vl = vd[layer * B:(layer + 1) * B]
-        return (d.DKV_BF16, B, Hq, Hkv, dim, P(q_layers[layer].data_ptr()), P(kl.data_ptr()),
-                P(vl.data_ptr()), t_cap, n_valid, w.sm_scale, P(out.data_ptr()), P(dws.data_ptr()),
+        return (d.DKV_BF16, B, Hq, Hkv, dim, P(q_layers[layer].data_ptr()), P(kn.data_ptr()),
+                P(vn.data_ptr()), 1, n_tail, cap, P(k_c.data_ptr()), P(v_c.data_ptr()),
+                P(seg_off.data_ptr() + 8 * off), P(seg_len.data_ptr() + 4 * off), w.sm_scale,
+                layer_rows[layer] + nseg_layer * (n_tail + 1), P(out.data_ptr()), P(dws.data_ptr()),
                 ws_bytes, P(sh))
 
-    def step_args(step, dense):
+    def dense_args(layer, n_valid, sh):
+        """dkv_dense_append_decode_attn: write the token at row n_valid, attend."""
+        kl = kd[layer * B:(layer + 1) * B]
+        vl = vd[layer * B:(layer + 1) * B]
+        kn, vn = new_kv[layer]
+        return (d.DKV_BF16, B, Hq, Hkv, dim, P(q_layers[layer].data_ptr()), P(kn.data_ptr()),
+                P(vn.data_ptr()), 1, P(kl.data_ptr()), P(vl.data_ptr()), t_cap, n_valid, w.sm_scale,
+                P(out.data_ptr()), P(dws.data_ptr()), ws_bytes, P(sh))
+
+    def step_args(step, dense, sh):
+        """One decode step: per layer, one call that appends the step's token
+        and attends over the cache."""
         slot = step % cap
         acts = []
         for layer in range(L):
-            acts.append((lib.dkv_append, append_args(layer, slot, dense)))
             if dense:
-                acts.append((lib.dkv_dense_decode_attn, dense_args(layer, T + slot + 1)))
+                acts.append((lib.dkv_dense_append_decode_attn, dense_args(layer, T + slot, sh)))
             else:
-                acts.append((lib.dkv_decode_attn, decode_args(layer, slot + 1)))
+                acts.append((lib.dkv_append_decode_attn, packed_args(layer, slot, sh)))
         return acts
 
     def run(acts):
@@ -230,44 +227,76 @@ def main():
         rows_step = (N * Hkv * (T + n_tail)) if dense else (retained + N * Hkv * n_tail)
         return rows_step * dim * elem * 2 + L * B * Hq * dim * (elem + 4) + L * nseg_layer * 12
 
+    cap_stream = torch.cuda.Stream()
+
     def timed(dense, steps, warmup):
-        plans = [step_args(s, dense) for s in range(warmup + steps)]
+        """Step time as HIP-graph replays (one graph per step: each keeps its
+        own append slot), plus the same steps launched eagerly."""
+        run(step_args(0, dense, sh))  # warm: first launches load code objects
+        torch.cuda.synchronize()
+        graphs = []
+        for s in range(warmup + steps):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=cap_stream):
+                run(step_args(s, dense, cap_stream.cuda_stream))
+            graphs.append(g)
+        for s in range(warmup):
+            graphs[s].replay()
+        torch.cuda.synchronize()
+        a, b = ev(), ev()
+        a.record(stream)
+        for s in range(warmup, warmup + steps):
+            graphs[s].replay()
+        b.record(stream)
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b) / steps
+        plans = [step_args(s, dense, sh) for s in range(warmup + steps)]
         for s in range(warmup):
             run(plans[s])
         torch.cuda.synchronize()
-        a, b = ev(), ev()
         a.record(stream)
         for s in range(warmup, warmup + steps):
             run(plans[s])
         b.record(stream)
         torch.cuda.synchronize()
-        ms = a.elapsed_time(b) / steps
+        eager_ms = a.elapsed_time(b) / steps
         nbytes = sum(decode_bytes(s, dense) for s in range(warmup, warmup + steps)) / steps
-        return ms, nbytes
+        return ms, eager_ms, nbytes
+
+    def sleep_cycles_for(ms_target):
+        n = 1 << 22
+        a, b = ev(), ev()
+        a.record(stream)
+        torch.cuda._sleep(n)
+        b.record(stream)
+        torch.cuda.synchronize()
+        return int(n * ms_target / max(a.elapsed_time(b), 1e-3))
 
     def per_launch(dense, steps=2):
-        """Average duration of the attention kernel alone, events around each launch."""
-        plans = [step_args(s, dense) for s in range(steps)]
+        """Average duration of one attention call (split kernel + combine
+        kernel), HIP events around each call on the launch stream.  A spin
+        kernel holds the stream while the host enqueues, so the intervals
+        contain GPU work only."""
+        plans = [step_args(s, dense, sh) for s in range(steps)]
         pairs = []
+        torch.cuda._sleep(spin)
         for plan in plans:
-            for i, (fn, a) in enumerate(plan):
-                if i % 2 == 1:
-                    e_a, e_b = ev(), ev()
-                    e_a.record(stream)
-                    fn(*a)
-                    e_b.record(stream)
-                    pairs.append((e_a, e_b, a))
-                else:
-                    fn(*a)
+            for fn, a in plan:
+                e_a, e_b = ev(), ev()
+                e_a.record(stream)
+                fn(*a)
+                e_b.record(stream)
+                pairs.append((e_a, e_b))
         torch.cuda.synchronize()
-        durs = [x.elapsed_time(y) for x, y, _ in pairs]
+        durs = [x.elapsed_time(y) for x, y in pairs]
         return sum(durs) / len(durs)
 
+    spin = sleep_cycles_for(30.0)
     log("timing packed decode")
-    ms, nbytes = timed(False, args.steps, args.warmup)
+    ms, eager_ms, nbytes = timed(False, args.steps, args.warmup)
     launch_ms = per_launch(False)
     log("timing dense decode")
-    dms, dbytes = timed(True, args.steps, args.warmup)
+    dms, deager_ms, dbytes = timed(True, args.steps, args.warmup)
     dlaunch_ms = per_launch(True)
 
     if args.copy_probe:
@@ -294,6 +323,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
+        "eager_ms_per_step": round(eager_ms, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -302,15 +332,19 @@ def main():
         "config": {"workload": WORKLOAD, "layers": L, "batch": B, "q_heads": Hq, "kv_heads": Hkv,
                    "head_dim": dim, "context_len": T, "sink": w.sink, "recent": w.recent,
                    "bins": w.num_bins, "retained_fraction": round(phys_frac, 4),
-                   "step": "per layer: dkv_append of 1 token + dkv_decode_attn"},
+                   "step": "per layer: dkv_append_decode_attn (append 1 token, attend); timed as HIP-graph "
+                           "replays, one graph per step"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
                      "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
-                     "traffic": traffic, "kernel": "decode_kernel<bf16,128,4>",
+                     "traffic": traffic,
+                     "kernel": "dkv_append_decode_attn call: decode_kernel<bf16,128,4> + "
+                               "decode_merge_kernel",
                      "avg_launch_us": round(launch_ms * 1e3, 2),
                      "bytes_per_launch": int(per_launch_bytes)},
         "cpu_baseline": cpu,
         "us_per_step": round(ms * 1e3, 1),
-        "dense": {"ms_per_step": round(dms, 4), "gb_per_s": round(dbytes / (dms * 1e-3) / 1e9, 2),
+        "dense": {"ms_per_step": round(dms, 4), "eager_ms_per_step": round(deager_ms, 4),
+                  "gb_per_s": round(dbytes / (dms * 1e-3) / 1e9, 2),
                   "avg_launch_us": round(dlaunch_ms * 1e3, 2),
                   "launch_frac_of_peak": round(dbytes / L / (dlaunch_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)},
         "speedup_vs_dense": round(dms / ms, 3),

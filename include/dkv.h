@@ -195,6 +195,27 @@ dkv_status dkv_decode_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_heads,
                            size_t workspace_bytes, void *stream);
 
 /*
+ * dkv_append_decode_attn -- dkv_append followed by dkv_decode_attn, in one
+ * launch: the decode step of a serving loop (Sec. 3.4: a new token's K/V is
+ * appended and retained, then the step attends to the packed context plus
+ * every appended token).
+ *
+ * k_new, v_new  [B * Hkv][n_new][d], written to packed rows
+ *               seg_off[s] + seg_len[s] + n_tail + t exactly as dkv_append
+ *               does; then every segment attends rows
+ *               [seg_off[s], seg_off[s] + seg_len[s] + n_tail + n_new).
+ * n_tail + n_new must not exceed append_cap (DKV_ERR_CAPACITY).  The result
+ * equals the two separate calls with the same rows_hint, bit for bit.
+ */
+dkv_status dkv_append_decode_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_heads,
+                                  int32_t num_kv_heads, int32_t head_dim, const void *q,
+                                  const void *k_new, const void *v_new, int32_t n_new,
+                                  int32_t n_tail, int32_t append_cap, void *k_c, void *v_c,
+                                  const int64_t *seg_off, const int32_t *seg_len, float sm_scale,
+                                  int64_t rows_hint, float *out, void *workspace,
+                                  size_t workspace_bytes, void *stream);
+
+/*
  * dkv_dense_decode_attn -- the same attention over an uncompressed cache
  * k, v [B][Hkv][t_cap][d]; every segment attends rows [0, n_valid),
  * n_valid <= t_cap.  Same workspace rules as dkv_decode_attn.
@@ -204,6 +225,19 @@ dkv_status dkv_dense_decode_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_h
                                  const void *k, const void *v, int64_t t_cap,
                                  int32_t n_valid, float sm_scale, float *out,
                                  void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * dkv_dense_append_decode_attn -- dense comparator of dkv_append_decode_attn:
+ * writes k_new, v_new ([B * Hkv][n_new][d]) to rows n_valid .. n_valid+n_new-1
+ * of every dense segment, then attends rows [0, n_valid + n_new).
+ * n_valid + n_new must not exceed t_cap (DKV_ERR_CAPACITY).
+ */
+dkv_status dkv_dense_append_decode_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_heads,
+                                        int32_t num_kv_heads, int32_t head_dim, const void *q,
+                                        const void *k_new, const void *v_new, int32_t n_new,
+                                        void *k, void *v, int64_t t_cap, int32_t n_valid,
+                                        float sm_scale, float *out, void *workspace,
+                                        size_t workspace_bytes, void *stream);
 
 /* Static description of a status code. */
 const char *dkv_status_string(dkv_status status);

@@ -18,6 +18,7 @@ __all__ = [
     "DkvError", "Layout", "make_layout", "library", "library_path", "dtype_code",
     "dkv_map_pattern", "dkv_compact_workspace_bytes", "dkv_compact", "dkv_append",
     "dkv_decode_workspace_bytes", "dkv_decode_attn", "dkv_dense_decode_attn",
+    "dkv_append_decode_attn", "dkv_dense_append_decode_attn",
     "dkv_status_string",
 ]
 
@@ -86,6 +87,10 @@ def library():
                                   VP, SZ, VP]),
         "dkv_dense_decode_attn": (I32, [I32, I32, I32, I32, I32, VP, VP, VP, I64, I32, F32, VP, VP,
                                         SZ, VP]),
+        "dkv_append_decode_attn": (I32, [I32, I32, I32, I32, I32, VP, VP, VP, I32, I32, I32, VP, VP,
+                                         VP, VP, F32, I64, VP, VP, SZ, VP]),
+        "dkv_dense_append_decode_attn": (I32, [I32, I32, I32, I32, I32, VP, VP, VP, I32, VP, VP, I64,
+                                               I32, F32, VP, VP, SZ, VP]),
         "dkv_status_string": (ctypes.c_char_p, [I32]),
     }
     for name, (res, args) in sigs.items():
@@ -181,6 +186,31 @@ def dkv_decode_attn(q, k_c, v_c, seg_off, seg_len, n_tail, sm_scale, out, worksp
         dtype_code(q.dtype), B, Hq, int(num_kv_heads), d, _dev(q, "q"), _dev(k_c, "k_c"),
         _dev(v_c, "v_c"), _dev(seg_off, "seg_off"), _dev(seg_len, "seg_len"), int(n_tail),
         float(sm_scale), int(rows_hint), _dev(out, "out"), _dev(workspace, "workspace"),
+        workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def dkv_append_decode_attn(q, k_new, v_new, n_tail, append_cap, k_c, v_c, seg_off, seg_len,
+                           sm_scale, out, workspace, num_kv_heads, rows_hint=0, stream=None):
+    """q: [B][Hq][d]; k_new, v_new: [B*Hkv][n_new][d]."""
+    B, Hq, d = q.shape
+    n_new = k_new.shape[1]
+    _check("dkv_append_decode_attn", library().dkv_append_decode_attn(
+        dtype_code(q.dtype), B, Hq, int(num_kv_heads), d, _dev(q, "q"), _dev(k_new, "k_new"),
+        _dev(v_new, "v_new"), n_new, int(n_tail), int(append_cap), _dev(k_c, "k_c"),
+        _dev(v_c, "v_c"), _dev(seg_off, "seg_off"), _dev(seg_len, "seg_len"), float(sm_scale),
+        int(rows_hint), _dev(out, "out"), _dev(workspace, "workspace"),
+        workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def dkv_dense_append_decode_attn(q, k_new, v_new, k, v, n_valid, sm_scale, out, workspace,
+                                 stream=None):
+    """q: [B][Hq][d]; k_new, v_new: [B*Hkv][n_new][d]; k, v: [B][Hkv][t_cap][d]."""
+    B, Hq, d = q.shape
+    _, Hkv, t_cap, _ = k.shape
+    _check("dkv_dense_append_decode_attn", library().dkv_dense_append_decode_attn(
+        dtype_code(q.dtype), B, Hq, Hkv, d, _dev(q, "q"), _dev(k_new, "k_new"), _dev(v_new, "v_new"),
+        k_new.shape[1], _dev(k, "k"), _dev(v, "v"), t_cap, int(n_valid), float(sm_scale),
+        _dev(out, "out"), _dev(workspace, "workspace"),
         workspace.numel() * workspace.element_size(), _stream(stream)))
 
 

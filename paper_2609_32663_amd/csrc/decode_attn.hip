@@ -36,6 +36,8 @@
 // The decode step is a GEMV per KV row (about G flop per byte), far below the
 // MFMA ridge, so the kernel is built to keep HBM busy rather than the ALUs.
 
+#include <atomic>
+
 #include "dkv_device.hpp"
 #include "dkv_launch.hpp"
 
@@ -136,10 +138,15 @@ __device__ __forceinline__ int64_t uniform64(int64_t x) {
   return (int64_t)(((uint64_t)hi << 32) | lo);
 }
 
+// Cache policy of the K/V loads: non-temporal.  Every K/V byte is read once
+// per step, so keeping it out of the caches' normal replacement is worth
+// about 10-15% of streaming bandwidth on this part.
+constexpr int kStreamLoad = 2;
+
 // Loads the K and V rows [row, row + kTK) of a piece.  k_lane / v_lane are
 // the lane-constant byte offsets (key j16 chunk kg, and row phase rp column
-// chunk cc).  The whole offset stays in the vector offset, which is what the
-// descriptor's range check covers.
+// chunk cc).  The whole offset stays in the vector offset; loads past the
+// descriptor's range return zeros.
 template <bool BF16, int D, int GP>
 __device__ __forceinline__ void load_tile(Tile<BF16, D, GP>& t, __amdgpu_buffer_rsrc_t kr, __amdgpu_buffer_rsrc_t vr,
                                           uint32_t row, uint32_t k_lane, uint32_t v_lane) {
@@ -149,12 +156,13 @@ __device__ __forceinline__ void load_tile(Tile<BF16, D, GP>& t, __amdgpu_buffer_
     const uint32_t vo = k_lane + (row + 16 * kk) * C::kRowBytes;
 #pragma unroll
     for (int u = 0; u < C::kChunks; ++u)
-      t.k[kk][u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(kr, vo + 64 * u, 0, 0));
+      t.k[kk][u] = __builtin_bit_cast(
+          u32x4, __builtin_amdgcn_raw_buffer_load_b128(kr, vo + 64 * u, 0, kStreamLoad));
   }
 #pragma unroll
   for (int i = 0; i < C::kRPT; ++i) {
     const uint32_t vo = v_lane + (row + C::kRP * i) * C::kRowBytes;
-    t.v[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(vr, vo, 0, 0));
+    t.v[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(vr, vo, 0, kStreamLoad));
   }
 }
 
@@ -252,12 +260,12 @@ __device__ __forceinline__ void build_row_prefix(const DecodeParams& p, int64_t*
   const int s_lo = tid * per;
   const int s_hi = min(nseg, s_lo + per);
   int64_t sum = 0;
-  for (int s = s_lo; s < s_hi; ++s) sum += dense ? p.dense_len : (int64_t)p.seg_len[s] + p.n_tail;
+  for (int s = s_lo; s < s_hi; ++s) sum += (dense ? p.dense_len : (int64_t)p.seg_len[s] + p.n_tail) + p.n_new;
   int64_t total_unused;
   int64_t run = block_exclusive_scan<kThreads>(sum, red, &total_unused);
   for (int s = s_lo; s < s_hi; ++s) {
     pre[s] = run;
-    run += dense ? p.dense_len : (int64_t)p.seg_len[s] + p.n_tail;
+    run += (dense ? p.dense_len : (int64_t)p.seg_len[s] + p.n_tail) + p.n_new;
   }
   if (s_hi == nseg && s_lo <= nseg) pre[nseg] = run;
   if (nseg == 0 && tid == 0) pre[0] = 0;
@@ -299,6 +307,10 @@ void decode_kernel(DecodeParams p) {
       const int b = s / p.Hkv, g = s - (s / p.Hkv) * p.Hkv;
       float* o = p.out + ((int64_t)b * p.Hq + (int64_t)g * p.G) * D;
       for (int i = tid; i < p.G * D; i += kThreads) o[i] = 0.f;
+      if (tid == 0) {
+        p.seg_meta[2 * s] = 0;
+        p.seg_meta[2 * s + 1] = 0;  // nothing to combine
+      }
     }
   }
   const int64_t P = total < p.P ? total : p.P;
@@ -334,6 +346,29 @@ void decode_kernel(DecodeParams p) {
     const int64_t row0 = uniform64(dense ? (int64_t)s * p.dense_stride : p.seg_off[s]);
     const char* kbase = reinterpret_cast<const char*>(p.k) + row0 * C::kRowBytes;
     const char* vbase = reinterpret_cast<const char*>(p.v) + row0 * C::kRowBytes;
+
+    // Tokens appended by this call are the segment's last n_new rows.  The
+    // workgroup whose slice holds them writes them into the cache (they stay
+    // for later steps) and is also the only one that reads them, so a
+    // workgroup-scope fence and barrier order the writes before its loads.
+    if (p.n_new > 0) {
+      const int64_t base_len = seg_hi - seg_lo - p.n_new;
+      const int64_t t_lo = (a > base_len ? a : base_len) - base_len;
+      const int64_t t_hi = (bnd < base_len + p.n_new ? bnd : base_len + p.n_new) - base_len;
+      if (t_lo < t_hi) {
+        const u32x4* ks = reinterpret_cast<const u32x4*>(p.k_new) + ((int64_t)s * p.n_new) * C::kLPR;
+        const u32x4* vs = reinterpret_cast<const u32x4*>(p.v_new) + ((int64_t)s * p.n_new) * C::kLPR;
+        u32x4* kd = reinterpret_cast<u32x4*>(const_cast<char*>(kbase) + base_len * C::kRowBytes);
+        u32x4* vd = reinterpret_cast<u32x4*>(const_cast<char*>(vbase) + base_len * C::kRowBytes);
+        for (int64_t i = t_lo * C::kLPR + tid; i < t_hi * C::kLPR; i += kThreads) {
+          kd[i] = ks[i];
+          vd[i] = vs[i];
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+        __syncthreads();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+      }
+    }
 
     // A operand: query head j16 of the group (zero beyond G), chunks kg + 4u.
     u32x4 qa[C::kChunks];
@@ -414,6 +449,12 @@ void decode_kernel(DecodeParams p) {
     const int64_t w_first = owner_of(seg_lo, total, P);
     const int64_t w_last = owner_of(seg_hi - 1, total, P);
     const bool single = w_first == w_last;
+    if (w == w_first && tid == 0) {
+      // the combine kernel reads where the segment's records start and how
+      // many there are (1: finished here, nothing to combine)
+      p.seg_meta[2 * s] = (int32_t)(w_first + s);
+      p.seg_meta[2 * s + 1] = (int32_t)(w_last - w_first + 1);
+    }
     float* rec = p.partials + (int64_t)(w + s) * C::kRec;
     float* outp = p.out + ((int64_t)bseq * p.Hq + (int64_t)g * p.G) * D;
     for (int idx = tid; idx < p.G * D; idx += kThreads) {
@@ -443,100 +484,124 @@ void decode_kernel(DecodeParams p) {
   }
 }
 
-// Block-wide max / sum of one float per thread (every thread gets the result).
-__device__ __forceinline__ float block_max(float x, float* tmp) {
-  x = group_max<kWave>(x);
-  if ((threadIdx.x & (kWave - 1)) == 0) tmp[threadIdx.x / kWave] = x;
-  __syncthreads();
-  float r = tmp[0];
-#pragma unroll
-  for (int q = 1; q < kWaves; ++q) r = fmaxf(r, tmp[q]);
-  __syncthreads();
-  return r;
-}
-
-__device__ __forceinline__ float block_sum(float x, float* tmp) {
-  x = group_sum<kWave>(x);
-  if ((threadIdx.x & (kWave - 1)) == 0) tmp[threadIdx.x / kWave] = x;
-  __syncthreads();
-  float r = tmp[0];
-#pragma unroll
-  for (int q = 1; q < kWaves; ++q) r += tmp[q];
-  __syncthreads();
-  return r;
-}
-
-// Combine kernel: one workgroup per (segment, query head).  It rebuilds the
-// attention kernel's flat row prefix and split, finds the pieces of its
-// segment and merges their records in slot order:
-//   M = max_k m_k,  w_k = 2^(m_k - M),  out = sum_k w_k acc_k / sum_k w_k l_k.
-// Segments with no rows or a single piece were finished by the attention
-// kernel.  The kernel boundary makes the records visible, so neither kernel
-// needs device-scope fences or counters.
+// Combine kernel: one workgroup per (segment, query head).  The attention
+// kernel left, per segment, the first record slot and the number of pieces
+// (n <= 1: nothing to combine).  Thread (ph, cq) folds pieces
+// k = ph, ph + kPhases, ... of columns 4cq..4cq+3 into its own running
+// (max, sum, accumulator), loading kBatch pieces' records at once so that the
+// merge costs one memory round trip per batch; the kPhases partial states are
+// then folded through LDS in phase order:
+//   M = max_k m_k,  out = sum_k 2^(m_k - M) acc_k / sum_k 2^(m_k - M) l_k.
+// The order of combination is fixed, so the result does not depend on timing.
+// The kernel boundary makes the records visible: neither kernel needs
+// device-scope fences or counters.
 template <int D, int GP>
 __global__ __launch_bounds__(kThreads) void decode_merge_kernel(DecodeParams p) {
   constexpr int kRec = GP * (D + 2);
-  constexpr int kQuads = D / 4;              // float4 column groups per head row
-  constexpr int kPhases = kThreads / kQuads; // pieces handled side by side
-  extern __shared__ __align__(16) int64_t pre[];
-  __shared__ float fw[kDecodeMaxWG];
-  __shared__ __align__(16) float xb[kThreads * 4];
-  __shared__ int64_t red[kWaves + 1];
-  __shared__ float tmp[kWaves];
+  constexpr int kQuads = D / 4;               // float4 column groups per head row
+  constexpr int kPhases = kThreads / kQuads;  // pieces folded side by side
+  constexpr int kBatch = 8;                   // pieces per thread per round trip
+  __shared__ __align__(16) float xa[kThreads * 4];
+  __shared__ float xm[kThreads], xl[kThreads];
 
-  build_row_prefix(p, pre, red);
-  const int64_t total = pre[p.nseg];
   const int s = blockIdx.x / p.G;
   const int h = blockIdx.x - s * p.G;
-  const int64_t seg_lo = pre[s], seg_hi = pre[s + 1];
-  if (seg_hi == seg_lo) return;
-  const int64_t P = total < p.P ? total : p.P;
-  const int64_t w_first = owner_of(seg_lo, total, P);
-  const int n = (int)(owner_of(seg_hi - 1, total, P) - w_first + 1);
-  if (n == 1) return;
-  const float* first = p.partials + (w_first + s) * kRec;
+  const int n = p.seg_meta[2 * s + 1];
+  if (n <= 1) return;
+  const float* first = p.partials + (int64_t)p.seg_meta[2 * s] * kRec;
   const int tid = threadIdx.x;
-
-  float mx = -INFINITY;
-  for (int k = tid; k < n; k += kThreads) mx = fmaxf(mx, first[(int64_t)k * kRec + h]);
-  mx = block_max(mx, tmp);
-  const float Mu = mx == -INFINITY ? 0.f : mx;
-  float ls = 0.f;
-  for (int k = tid; k < n; k += kThreads) {
-    const float* r = first + (int64_t)k * kRec;
-    const float f = fast_exp2(r[h] - Mu);
-    fw[k] = f;
-    ls += f * r[GP + h];
-  }
-  const float L = block_sum(ls, tmp);  // its barriers also publish fw
-
   const int cq = tid % kQuads, ph = tid / kQuads;
-  const float* base = first + 2 * GP + h * D + 4 * cq;
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 8
-  for (int k = ph; k < n; k += kPhases) acc += fw[k] * *reinterpret_cast<const f32x4*>(base + (int64_t)k * kRec);
-  *reinterpret_cast<f32x4*>(&xb[4 * tid]) = acc;
+
+  float M = -INFINITY, L = 0.f;
+  f32x4 A = {0.f, 0.f, 0.f, 0.f};
+  for (int k0 = ph; k0 < n; k0 += kPhases * kBatch) {
+    float m[kBatch], l[kBatch];
+    f32x4 a[kBatch];
+#pragma unroll
+    for (int i = 0; i < kBatch; ++i) {
+      const int k = k0 + i * kPhases;
+      if (k < n) {
+        const float* r = first + (int64_t)k * kRec;
+        m[i] = r[h];
+        l[i] = r[GP + h];
+        a[i] = *reinterpret_cast<const f32x4*>(r + 2 * GP + h * D + 4 * cq);
+      } else {
+        m[i] = -INFINITY;
+        l[i] = 0.f;
+        a[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+    float mb = M;
+#pragma unroll
+    for (int i = 0; i < kBatch; ++i) mb = fmaxf(mb, m[i]);
+    const float mu = mb == -INFINITY ? 0.f : mb;
+    const float rs = fast_exp2(M - mu);
+    L *= rs;
+    A *= rs;
+#pragma unroll
+    for (int i = 0; i < kBatch; ++i) {
+      const float f = fast_exp2(m[i] - mu);
+      L += f * l[i];
+      A += f * a[i];
+    }
+    M = mb;
+  }
+  xm[tid] = M;
+  xl[tid] = L;
+  *reinterpret_cast<f32x4*>(&xa[4 * tid]) = A;
   __syncthreads();
   if (tid < kQuads) {
-    f32x4 sum = acc;
-    for (int q = 1; q < kPhases; ++q) sum += *reinterpret_cast<const f32x4*>(&xb[4 * (tid + q * kQuads)]);
+    float Mx = -INFINITY;
+    for (int q = 0; q < kPhases; ++q) Mx = fmaxf(Mx, xm[tid + q * kQuads]);
+    const float mu = Mx == -INFINITY ? 0.f : Mx;
+    float Lt = 0.f;
+    f32x4 At = {0.f, 0.f, 0.f, 0.f};
+    for (int q = 0; q < kPhases; ++q) {
+      const int t = tid + q * kQuads;
+      const float f = fast_exp2(xm[t] - mu);
+      Lt += f * xl[t];
+      At += f * *reinterpret_cast<const f32x4*>(&xa[4 * t]);
+    }
     const int bseq = s / p.Hkv, g = s - bseq * p.Hkv;
     float* o = p.out + ((int64_t)bseq * p.Hq + (int64_t)g * p.G + h) * D + 4 * cq;
-    *reinterpret_cast<f32x4*>(o) = sum * (L > 0.f ? 1.f / L : 0.f);
+    *reinterpret_cast<f32x4*>(o) = At * (Lt > 0.f ? 1.f / Lt : 0.f);
   }
 }
 
 // Split count: about one 128-row slice per workgroup, capped at the number of
 // workgroups the device holds at once (so every slice starts immediately and
 // all finish together) and at the workspace bound.
+// The device's compute-unit count and the kernel's resident workgroups per
+// CU are looked up once per (device, kernel) and cached: the queries cost
+// more host time than a launch.  The occupancy is taken with the largest
+// dynamic LDS a call may request, so the cache holds for every call.
+constexpr int kMaxDevices = 64;
+
+inline int device_cus(int dev) {
+  static std::atomic<int> cache[kMaxDevices];
+  if (dev < 0 || dev >= kMaxDevices) dev = 0;
+  int c = cache[dev].load(std::memory_order_relaxed);
+  if (c <= 0) {
+    if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || c <= 0) c = 256;
+    cache[dev].store(c, std::memory_order_relaxed);
+  }
+  return c;
+}
+
 template <typename K>
-int32_t split_count(K kernel, size_t lds, int64_t rows_hint) {
-  int dev = 0, cus = 0, per_cu = 0;
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
-    cus = 256;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, lds) != hipSuccess || per_cu <= 0)
-    per_cu = 1;
+int32_t split_count(K kernel, int64_t rows_hint) {
+  static std::atomic<int> occ_cache[kMaxDevices];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) dev = 0;
+  const int cus = device_cus(dev);
+  int per_cu = occ_cache[dev].load(std::memory_order_relaxed);
+  if (per_cu <= 0) {
+    const size_t lds_max = ((size_t)DKV_MAX_SEGMENTS + 1) * sizeof(int64_t);
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, lds_max) != hipSuccess ||
+        per_cu <= 0)
+      per_cu = 1;
+    occ_cache[dev].store(per_cu, std::memory_order_relaxed);
+  }
   int64_t cap = (int64_t)cus * per_cu;
   if (cap > kDecodeMaxWG) cap = kDecodeMaxWG;
   if (rows_hint <= 0) return (int32_t)cap;
@@ -547,12 +612,12 @@ int32_t split_count(K kernel, size_t lds, int64_t rows_hint) {
 template <bool BF16, int D, int GP>
 hipError_t launch_g(DecodeParams p, int64_t rows_hint, hipStream_t stream) {
   const size_t lds = ((size_t)p.nseg + 1) * sizeof(int64_t);
-  p.P = split_count(decode_kernel<BF16, D, GP>, lds, rows_hint);
+  p.P = split_count(decode_kernel<BF16, D, GP>, rows_hint);
   hipLaunchKernelGGL((decode_kernel<BF16, D, GP>), dim3(p.P), dim3(kThreads), lds, stream, p);
   // Segments split over several workgroups are finished by the combine
   // kernel; when the call has a single split there is nothing to combine.
   if (p.P > 1)
-    hipLaunchKernelGGL((decode_merge_kernel<D, GP>), dim3(p.nseg * p.G), dim3(kThreads), lds, stream, p);
+    hipLaunchKernelGGL((decode_merge_kernel<D, GP>), dim3(p.nseg * p.G), dim3(kThreads), 0, stream, p);
   return hipGetLastError();
 }
 
@@ -573,6 +638,10 @@ int decode_group_pad(int G) { return G <= 4 ? 4 : (G <= 8 ? 8 : 16); }
 size_t decode_partials_bytes(int nseg, int G, int head_dim) {
   const size_t rec = (size_t)decode_group_pad(G) * (head_dim + 2) * 4;
   return ((size_t)kDecodeMaxWG + nseg) * rec;
+}
+
+size_t decode_workspace_bytes(int nseg, int G, int head_dim) {
+  return decode_partials_bytes(nseg, G, head_dim) + (size_t)nseg * 2 * sizeof(int32_t);
 }
 
 hipError_t launch_decode(const DecodeParams& p, dkv_dtype dtype, int head_dim, int64_t rows_hint,

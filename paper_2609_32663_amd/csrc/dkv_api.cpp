@@ -202,19 +202,27 @@ size_t dkv_decode_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t nu
       (int64_t)batch * num_kv_heads > DKV_MAX_SEGMENTS)
     return 0;
   const int nseg = batch * num_kv_heads;
-  return dkv::decode_partials_bytes(nseg, num_q_heads / num_kv_heads, head_dim);
+  return dkv::decode_workspace_bytes(nseg, num_q_heads / num_kv_heads, head_dim);
 }
 
-dkv_status dkv_decode_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
-                           int32_t head_dim, const void* q, const void* k_c, const void* v_c,
-                           const int64_t* seg_off, const int32_t* seg_len, int32_t n_tail, float sm_scale,
-                           int64_t rows_hint, float* out, void* workspace, size_t workspace_bytes,
-                           void* stream) {
-  dkv_status st = check_decode_common(dtype, batch, num_q_heads, num_kv_heads, head_dim, q, k_c, v_c, out,
-                                      workspace, workspace_bytes, sm_scale);
-  if (st != DKV_OK || batch == 0) return st;
-  if (n_tail < 0) return DKV_ERR_INVALID_ARG;
+}  // extern "C"
+
+namespace {
+
+// Packed-cache attention, optionally appending n_new tokens first.
+dkv_status decode_packed(dkv_dtype dtype, int32_t batch, int32_t hq, int32_t hkv, int32_t d, const void* q,
+                         const void* k_new, const void* v_new, int32_t n_new, int32_t n_tail,
+                         int32_t append_cap, const void* k_c, const void* v_c, const int64_t* seg_off,
+                         const int32_t* seg_len, float sm_scale, int64_t rows_hint, float* out, void* ws,
+                         size_t ws_bytes, void* stream) {
+  dkv_status st = check_decode_common(dtype, batch, hq, hkv, d, q, k_c, v_c, out, ws, ws_bytes, sm_scale);
+  if (st != DKV_OK) return st;
+  if (n_tail < 0 || n_new < 0) return DKV_ERR_INVALID_ARG;
+  if (n_new > 0 && (int64_t)n_tail + n_new > append_cap) return DKV_ERR_CAPACITY;
+  if (batch == 0) return DKV_OK;
   if (seg_off == nullptr || seg_len == nullptr) return DKV_ERR_INVALID_ARG;
+  if (n_new > 0 && (k_new == nullptr || v_new == nullptr)) return DKV_ERR_INVALID_ARG;
+  if (n_new > 0 && (!aligned16(k_new) || !aligned16(v_new))) return DKV_ERR_MISALIGNED;
   dkv::DecodeParams p;
   std::memset(&p, 0, sizeof(p));
   p.q = q;
@@ -223,24 +231,33 @@ dkv_status dkv_decode_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_heads, 
   p.seg_off = seg_off;
   p.seg_len = seg_len;
   p.n_tail = n_tail;
-  p.nseg = batch * num_kv_heads;
-  p.Hkv = num_kv_heads;
-  p.Hq = num_q_heads;
-  p.G = num_q_heads / num_kv_heads;
+  p.k_new = k_new;
+  p.v_new = v_new;
+  p.n_new = n_new;
+  p.nseg = batch * hkv;
+  p.Hkv = hkv;
+  p.Hq = hq;
+  p.G = hq / hkv;
   p.scale_log2 = sm_scale * 1.4426950408889634f;
   p.out = out;
-  p.partials = static_cast<float*>(workspace);
-  return hip_status(dkv::launch_decode(p, dtype, head_dim, rows_hint, (hipStream_t)stream));
+  p.partials = static_cast<float*>(ws);
+  p.seg_meta = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + dkv::decode_partials_bytes(p.nseg, p.G, d));
+  return hip_status(dkv::launch_decode(p, dtype, d, rows_hint, (hipStream_t)stream));
 }
 
-dkv_status dkv_dense_decode_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
-                                 int32_t head_dim, const void* q, const void* k, const void* v, int64_t t_cap,
-                                 int32_t n_valid, float sm_scale, float* out, void* workspace,
-                                 size_t workspace_bytes, void* stream) {
-  dkv_status st = check_decode_common(dtype, batch, num_q_heads, num_kv_heads, head_dim, q, k, v, out,
-                                      workspace, workspace_bytes, sm_scale);
-  if (st != DKV_OK || batch == 0) return st;
-  if (n_valid < 0 || t_cap < n_valid) return DKV_ERR_INVALID_ARG;
+// Dense-cache attention over rows [0, n_valid + n_new), optionally writing
+// the n_new tokens at rows n_valid.. first.
+dkv_status decode_dense(dkv_dtype dtype, int32_t batch, int32_t hq, int32_t hkv, int32_t d, const void* q,
+                        const void* k_new, const void* v_new, int32_t n_new, const void* k, const void* v,
+                        int64_t t_cap, int32_t n_valid, float sm_scale, float* out, void* ws, size_t ws_bytes,
+                        void* stream) {
+  dkv_status st = check_decode_common(dtype, batch, hq, hkv, d, q, k, v, out, ws, ws_bytes, sm_scale);
+  if (st != DKV_OK) return st;
+  if (n_valid < 0 || n_new < 0 || t_cap < 0) return DKV_ERR_INVALID_ARG;
+  if ((int64_t)n_valid + n_new > t_cap) return n_new > 0 ? DKV_ERR_CAPACITY : DKV_ERR_INVALID_ARG;
+  if (batch == 0) return DKV_OK;
+  if (n_new > 0 && (k_new == nullptr || v_new == nullptr)) return DKV_ERR_INVALID_ARG;
+  if (n_new > 0 && (!aligned16(k_new) || !aligned16(v_new))) return DKV_ERR_MISALIGNED;
   dkv::DecodeParams p;
   std::memset(&p, 0, sizeof(p));
   p.q = q;
@@ -248,14 +265,60 @@ dkv_status dkv_dense_decode_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_h
   p.v = v;
   p.dense_stride = t_cap;
   p.dense_len = n_valid;
-  p.nseg = batch * num_kv_heads;
-  p.Hkv = num_kv_heads;
-  p.Hq = num_q_heads;
-  p.G = num_q_heads / num_kv_heads;
+  p.k_new = k_new;
+  p.v_new = v_new;
+  p.n_new = n_new;
+  p.nseg = batch * hkv;
+  p.Hkv = hkv;
+  p.Hq = hq;
+  p.G = hq / hkv;
   p.scale_log2 = sm_scale * 1.4426950408889634f;
   p.out = out;
-  p.partials = static_cast<float*>(workspace);
-  return hip_status(dkv::launch_decode(p, dtype, head_dim, (int64_t)p.nseg * n_valid, (hipStream_t)stream));
+  p.partials = static_cast<float*>(ws);
+  p.seg_meta = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + dkv::decode_partials_bytes(p.nseg, p.G, d));
+  return hip_status(dkv::launch_decode(p, dtype, d, (int64_t)p.nseg * ((int64_t)n_valid + n_new),
+                                       (hipStream_t)stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+dkv_status dkv_decode_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                           int32_t head_dim, const void* q, const void* k_c, const void* v_c,
+                           const int64_t* seg_off, const int32_t* seg_len, int32_t n_tail, float sm_scale,
+                           int64_t rows_hint, float* out, void* workspace, size_t workspace_bytes,
+                           void* stream) {
+  return decode_packed(dtype, batch, num_q_heads, num_kv_heads, head_dim, q, nullptr, nullptr, 0, n_tail, 0,
+                       k_c, v_c, seg_off, seg_len, sm_scale, rows_hint, out, workspace, workspace_bytes, stream);
+}
+
+dkv_status dkv_append_decode_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                  int32_t head_dim, const void* q, const void* k_new, const void* v_new,
+                                  int32_t n_new, int32_t n_tail, int32_t append_cap, void* k_c, void* v_c,
+                                  const int64_t* seg_off, const int32_t* seg_len, float sm_scale,
+                                  int64_t rows_hint, float* out, void* workspace, size_t workspace_bytes,
+                                  void* stream) {
+  return decode_packed(dtype, batch, num_q_heads, num_kv_heads, head_dim, q, k_new, v_new, n_new, n_tail,
+                       append_cap, k_c, v_c, seg_off, seg_len, sm_scale, rows_hint, out, workspace,
+                       workspace_bytes, stream);
+}
+
+dkv_status dkv_dense_decode_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                 int32_t head_dim, const void* q, const void* k, const void* v, int64_t t_cap,
+                                 int32_t n_valid, float sm_scale, float* out, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+  return decode_dense(dtype, batch, num_q_heads, num_kv_heads, head_dim, q, nullptr, nullptr, 0, k, v, t_cap,
+                      n_valid, sm_scale, out, workspace, workspace_bytes, stream);
+}
+
+dkv_status dkv_dense_append_decode_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_heads,
+                                        int32_t num_kv_heads, int32_t head_dim, const void* q,
+                                        const void* k_new, const void* v_new, int32_t n_new, void* k, void* v,
+                                        int64_t t_cap, int32_t n_valid, float sm_scale, float* out,
+                                        void* workspace, size_t workspace_bytes, void* stream) {
+  return decode_dense(dtype, batch, num_q_heads, num_kv_heads, head_dim, q, k_new, v_new, n_new, k, v, t_cap,
+                      n_valid, sm_scale, out, workspace, workspace_bytes, stream);
 }
 
 }  // extern "C"

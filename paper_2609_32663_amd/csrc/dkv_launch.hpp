@@ -66,14 +66,19 @@ struct DecodeParams {
   int64_t dense_stride;    // rows between dense segments (t_cap)
   int32_t dense_len;       // rows attended per dense segment (n_valid)
   int32_t n_tail;
+  const void* k_new;       // [nseg][n_new][d] tokens appended by this call (or null)
+  const void* v_new;
+  int32_t n_new;           // 0: attend only
   int32_t nseg, Hkv, Hq, G;
   float scale_log2;        // sm_scale * log2(e)
   float* out;              // [B][Hq][d] fp32
   float* partials;         // [(P + nseg)][GP][d + 2]
+  int32_t* seg_meta;       // [nseg][2]: first record slot, piece count
   int32_t P;               // workgroups launched (set by launch_decode)
 };
 int decode_group_pad(int G);
-size_t decode_partials_bytes(int nseg, int G, int head_dim);  // partial records only
+size_t decode_partials_bytes(int nseg, int G, int head_dim);   // partial records
+size_t decode_workspace_bytes(int nseg, int G, int head_dim);  // records + segment metadata
 // rows_hint: expected total rows of the call (0 = unknown); sizes the split.
 hipError_t launch_decode(const DecodeParams& p, dkv_dtype dtype, int head_dim, int64_t rows_hint,
                          hipStream_t stream);

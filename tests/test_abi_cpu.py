@@ -147,6 +147,25 @@ def test_decode_validation():
     assert _decode(B=0, q=NUL, out=NUL) == d.DKV_OK
 
 
+def test_fused_append_decode_validation():
+    lib = d.library()
+    ws = d.dkv_decode_workspace_bytes(1, 32, 8, 128)
+
+    def call(n_new=1, n_tail=0, cap=4, kn=A, vn=A):
+        return lib.dkv_append_decode_attn(d.DKV_BF16, 1, 32, 8, 128, A, kn, vn, n_new, n_tail, cap, A, A,
+                                          A, A, 1.0, 0, A, A, ws, NUL)
+
+    assert call(n_new=2, n_tail=3, cap=4) == d.DKV_ERR_CAPACITY
+    assert call(n_new=-1) == d.DKV_ERR_INVALID_ARG
+    assert call(kn=NUL) == d.DKV_ERR_INVALID_ARG
+    assert call(vn=MIS) == d.DKV_ERR_MISALIGNED
+    dws = d.dkv_decode_workspace_bytes(1, 8, 2, 64)
+    assert lib.dkv_dense_append_decode_attn(d.DKV_F32, 1, 8, 2, 64, A, A, A, 2, A, A, 100, 99, 1.0, A, A,
+                                            dws, NUL) == d.DKV_ERR_CAPACITY
+    assert lib.dkv_dense_append_decode_attn(d.DKV_F32, 1, 8, 2, 64, A, NUL, A, 1, A, A, 100, 50, 1.0, A,
+                                            A, dws, NUL) == d.DKV_ERR_INVALID_ARG
+
+
 def test_dense_decode_validation():
     lib = d.library()
     ws = d.dkv_decode_workspace_bytes(1, 8, 2, 64)

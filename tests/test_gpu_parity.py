@@ -333,6 +333,89 @@ def test_decode_workspace_needs_no_clearing(d):
     assert row_rel_err(got, want) <= ATTN_TOL
 
 
+@pytest.mark.parametrize("dtype,dim,G", [(torch.bfloat16, 128, 4), (torch.float32, 64, 2),
+                                         (torch.bfloat16, 128, 8), (torch.bfloat16, 64, 7)])
+def test_fused_append_decode_equals_separate_calls(d, dtype, dim, G):
+    rng = np.random.default_rng(330 + dim + G)
+    B, Hkv, T, cap = 2, 3, 7000, 8
+    for rows_hint in (0, 64):
+        got, want, args = _decode_case(d, rng, B, Hkv, G, T, dim, dtype, 0.3, 2, cap=cap,
+                                       rows_hint=rows_hint)
+        q, k_c, v_c, seg_off, seg_len, out, dws, scale = args
+        # rows 0..1 of the tail are filled; append 3 more at n_tail = 2 both ways
+        kn = _rand_kv(rng, (B * Hkv, 3, dim), dtype)
+        vn = _rand_kv(rng, (B * Hkv, 3, dim), dtype)
+        k2, v2 = k_c.clone(), v_c.clone()
+        sep = torch.empty_like(out)
+        d.dkv_append(kn, vn, 2, cap, k_c, v_c, seg_off, seg_len)
+        d.dkv_decode_attn(q, k_c, v_c, seg_off, seg_len, 5, scale, sep, dws, Hkv, rows_hint=rows_hint)
+        fused = torch.empty_like(out)
+        d.dkv_append_decode_attn(q, kn, vn, 2, cap, k2, v2, seg_off, seg_len, scale, fused, dws, Hkv,
+                                 rows_hint=rows_hint)
+        torch.cuda.synchronize()
+        assert torch.equal(sep, fused)
+        # the appended rows landed where dkv_append puts them
+        for s in range(B * Hkv):
+            lo = int(seg_off[s]) + int(seg_len[s])
+            assert torch.equal(k2[lo + 2:lo + 5], kn[s]) and torch.equal(v2[lo + 2:lo + 5], vn[s])
+        with pytest.raises(d.DkvError) as e:
+            d.dkv_append_decode_attn(q, kn, vn, 6, cap, k2, v2, seg_off, seg_len, scale, fused, dws, Hkv)
+        assert e.value.status == d.DKV_ERR_CAPACITY
+
+
+def test_dense_fused_append_decode_matches_oracle(d):
+    rng = np.random.default_rng(331)
+    B, Hkv, G, t_cap, n_valid, dim = 2, 4, 4, 3000, 2990, 128
+    k = _rand_kv(rng, (B, Hkv, t_cap, dim), torch.bfloat16)
+    v = _rand_kv(rng, (B, Hkv, t_cap, dim), torch.bfloat16)
+    q = _rand_kv(rng, (B, Hkv * G, dim), torch.bfloat16)
+    kn = _rand_kv(rng, (B * Hkv, 2, dim), torch.bfloat16)
+    vn = _rand_kv(rng, (B * Hkv, 2, dim), torch.bfloat16)
+    out = torch.empty((B, Hkv * G, dim), dtype=torch.float32, device=DEV)
+    ws = torch.empty(d.dkv_decode_workspace_bytes(B, Hkv * G, Hkv, dim), dtype=torch.uint8, device=DEV)
+    d.dkv_dense_append_decode_attn(q, kn, vn, k, v, n_valid, 0.09, out, ws)
+    torch.cuda.synchronize()
+    kb, vb = bits(k), bits(v)
+    kb[:, :, n_valid:n_valid + 2] = bits(kn).reshape(B, Hkv, 2, dim)
+    vb[:, :, n_valid:n_valid + 2] = bits(vn).reshape(B, Hkv, 2, dim)
+    np.testing.assert_array_equal(bits(k), kb)
+    want = o.dense_decode_attn(bits(q), kb, vb, n_valid + 2, 0.09, o.BF16)
+    assert row_rel_err(out.cpu().numpy(), want) <= ATTN_TOL
+    with pytest.raises(d.DkvError) as e:
+        d.dkv_dense_append_decode_attn(q, kn, vn, k, v, t_cap - 1, 0.09, out, ws)
+    assert e.value.status == d.DKV_ERR_CAPACITY
+
+
+def test_append_decode_graph_replays_match_eager(d):
+    """append + decode captured in a HIP graph: every replay (with eager work
+    and synchronisation in between) equals the eager result bit for bit."""
+    rng = np.random.default_rng(323)
+    B, Hkv, G, T, dim, cap = 1, 8, 4, 9000, 128, 4
+    got, want, args = _decode_case(d, rng, B, Hkv, G, T, dim, torch.bfloat16, 0.35, 0, cap=cap)
+    q, k_c, v_c, seg_off, seg_len, out, dws, scale = args
+    kn = _rand_kv(rng, (B * Hkv, 1, dim), torch.bfloat16)
+    vn = _rand_kv(rng, (B * Hkv, 1, dim), torch.bfloat16)
+    d.dkv_append(kn, vn, 0, cap, k_c, v_c, seg_off, seg_len)
+    eager = torch.empty_like(out)
+    d.dkv_decode_attn(q, k_c, v_c, seg_off, seg_len, 1, scale, eager, dws, Hkv, rows_hint=20000)
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    gout = torch.zeros_like(out)
+    with torch.cuda.graph(g, stream=s):
+        d.dkv_append(kn, vn, 0, cap, k_c, v_c, seg_off, seg_len, stream=s)
+        d.dkv_decode_attn(q, k_c, v_c, seg_off, seg_len, 1, scale, gout, dws, Hkv, rows_hint=20000,
+                          stream=s)
+    for _ in range(3):
+        gout.zero_()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(gout, eager)
+        scratch = torch.empty_like(out)  # eager work between replays
+        d.dkv_decode_attn(q, k_c, v_c, seg_off, seg_len, 0, scale, scratch, dws, Hkv)
+        torch.cuda.synchronize()
+
+
 def test_decode_large_logits_are_stable(d):
     rng = np.random.default_rng(321)
     got, want, _ = _decode_case(d, rng, 1, 2, 4, 5000, 128, torch.bfloat16, 0.5, 1, sm_scale=8.0)
