@@ -224,13 +224,17 @@ __device__ __forceinline__ void compute_tile(WaveState<BF16, D, GP>& st, const T
   }
   wave_lds_fence();
 
+  // Once the running maxima settle they rarely move, and then every factor
+  // is exactly 1: the whole wave skips the rescale.
+  if (__builtin_amdgcn_ballot_w64(alpha[0] != 1.f || alpha[1] != 1.f || alpha[2] != 1.f || alpha[3] != 1.f)) {
 #pragma unroll
-  for (int h4 = 0; h4 < GP / 4; ++h4) {
-    const f32x4 al = *reinterpret_cast<const f32x4*>(&ab[4 * h4]);
+    for (int h4 = 0; h4 < GP / 4; ++h4) {
+      const f32x4 al = *reinterpret_cast<const f32x4*>(&ab[4 * h4]);
 #pragma unroll
-    for (int v = 0; v < 4; ++v)
+      for (int v = 0; v < 4; ++v)
 #pragma unroll
-      for (int c = 0; c < C::kCPL; ++c) st.acc[4 * h4 + v][c] *= al[v];
+        for (int c = 0; c < C::kCPL; ++c) st.acc[4 * h4 + v][c] *= al[v];
+    }
   }
 #pragma unroll
   for (int i = 0; i < C::kRPT; ++i) {
@@ -249,41 +253,70 @@ __device__ __forceinline__ void compute_tile(WaveState<BF16, D, GP>& st, const T
   wave_lds_fence();
 }
 
-// Flat row prefix over the call's segments: pre[s] = rows of segments < s,
-// pre[nseg] = total.  Called by every thread of a workgroup; `red` holds
-// kWaves + 1 int64 of LDS.
-__device__ __forceinline__ void build_row_prefix(const DecodeParams& p, int64_t* pre, int64_t* red) {
+// Work units of segment s in the flat split: its rows plus, when it has any,
+// `seg_cost` units that stand for the fixed cost of a piece (loading the
+// query, the cross-wave fold and the record).  A workgroup whose slice
+// crosses a segment boundary pays that cost twice, so charging it here gives
+// such a workgroup fewer rows and keeps the slowest workgroup close to the
+// median.
+__device__ __forceinline__ int64_t segment_units(const DecodeParams& p, int s, int64_t seg_cost) {
+  const int64_t rows = (p.seg_len == nullptr ? p.dense_len : (int64_t)p.seg_len[s] + p.n_tail) + p.n_new;
+  return rows > 0 ? rows + seg_cost : 0;
+}
+
+// Flat prefix of work units over the call's segments: pre[s] = units of
+// segments < s, pre[nseg] = total.  A non-empty segment s covers
+// [pre[s], pre[s + 1]); its first seg_cost units are the fixed cost and its
+// rows are the units after them.  The packed cache's segment offsets are
+// copied to offs[] in the same pass, so the workgroup learns where its rows
+// are after a single round trip to memory.  Called by every thread of a
+// workgroup; `red` holds kWaves + 1 int64 of LDS.
+__device__ __forceinline__ void build_row_prefix(const DecodeParams& p, int64_t seg_cost, int64_t* pre,
+                                                 int64_t* offs, int64_t* red) {
   const int tid = threadIdx.x;
   const int nseg = p.nseg;
-  const bool dense = p.seg_len == nullptr;
   const int per = (nseg + kThreads - 1) / kThreads;
   const int s_lo = tid * per;
   const int s_hi = min(nseg, s_lo + per);
   int64_t sum = 0;
-  for (int s = s_lo; s < s_hi; ++s) sum += (dense ? p.dense_len : (int64_t)p.seg_len[s] + p.n_tail) + p.n_new;
+  for (int s = s_lo; s < s_hi; ++s) {
+    if (p.seg_len != nullptr) offs[s] = p.seg_off[s];
+    const int64_t u = segment_units(p, s, seg_cost);
+    pre[s] = u;  // this thread's own slots: units now, prefix after the scan
+    sum += u;
+  }
   int64_t total_unused;
   int64_t run = block_exclusive_scan<kThreads>(sum, red, &total_unused);
   for (int s = s_lo; s < s_hi; ++s) {
+    const int64_t u = pre[s];
     pre[s] = run;
-    run += (dense ? p.dense_len : (int64_t)p.seg_len[s] + p.n_tail) + p.n_new;
+    run += u;
   }
   if (s_hi == nseg && s_lo <= nseg) pre[nseg] = run;
   if (nseg == 0 && tid == 0) pre[0] = 0;
   __syncthreads();
 }
 
-// Two waves per SIMD where the double-buffered tiles and the accumulators fit
-// in 256 VGPRs without spilling; one otherwise.
+// Register tiles in flight per wave (pipeline depth of the K/V stream).
+template <bool BF16, int D, int GP>
+constexpr int decode_stages() {
+  return (!BF16 && D == 128) ? 2 : 3;  // fp32 d128 tiles are twice as large
+}
+
+// Waves per SIMD the register budget is sized for: two only for a two-stage
+// ring small enough to fit 256 VGPRs; otherwise one wave per SIMD with up to
+// 512 registers, relying on the ring's depth for bytes in flight.
 template <bool BF16, int D, int GP>
 constexpr int decode_waves_per_eu() {
-  return (GP == 4 && (BF16 || D == 64)) ? 2 : 1;
+  return (decode_stages<BF16, D, GP>() == 2 && GP == 4 && (BF16 || D == 64)) ? 2 : 1;
 }
 
 template <bool BF16, int D, int GP>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(decode_waves_per_eu<BF16, D, GP>())))
 void decode_kernel(DecodeParams p) {
   using C = DecodeCfg<BF16, D, GP>;
-  extern __shared__ __align__(16) int64_t pre[];          // [nseg + 1] row prefix
+  extern __shared__ __align__(16) int64_t pre[];          // [nseg + 1] unit prefix, then [nseg] offsets
+  int64_t* offs = pre + p.nseg + 1;
   __shared__ __align__(16) float pbuf[kWaves][kTK][GP];   // probabilities per wave tile
   __shared__ __align__(16) float abuf[kWaves][GP];        // rescale factors per wave
   __shared__ __align__(16) float wacc[kWaves][GP][D];     // per-wave accumulators
@@ -298,7 +331,11 @@ void decode_kernel(DecodeParams p) {
   const int nseg = p.nseg;
   const bool dense = p.seg_len == nullptr;
 
-  build_row_prefix(p, pre, red);
+  // fixed cost of a piece, in rows: about as long as streaming 128 KiB of K
+  // and V (measured: a second piece adds about 6 us to a workgroup that
+  // streams about 43 bf16 d128 rows per us)
+  constexpr int64_t kSegCost = 131072 / (2 * C::kRowBytes);
+  build_row_prefix(p, kSegCost, pre, offs, red);
   const int64_t total = uniform64(pre[nseg]);
 
   // ---- segments with no rows at all produce zeros ----------------------
@@ -337,13 +374,15 @@ void decode_kernel(DecodeParams p) {
 
   s = __builtin_amdgcn_readfirstlane(s);
   for (; s < nseg && pre[s] < hi; ++s) {
-    const int64_t seg_lo = uniform64(pre[s]), seg_hi = uniform64(pre[s + 1]);
+    // rows of segment s are the units [seg_lo, seg_hi); a workgroup whose
+    // slice holds only the segment's fixed-cost units has no piece of it
+    const int64_t seg_lo = uniform64(pre[s]) + kSegCost, seg_hi = uniform64(pre[s + 1]);
     const int64_t a = (lo > seg_lo ? lo : seg_lo) - seg_lo;
     const int64_t bnd = (hi < seg_hi ? hi : seg_hi) - seg_lo;
     if (a >= bnd) continue;
     const int bseq = s / p.Hkv;
     const int g = s - bseq * p.Hkv;
-    const int64_t row0 = uniform64(dense ? (int64_t)s * p.dense_stride : p.seg_off[s]);
+    const int64_t row0 = uniform64(dense ? (int64_t)s * p.dense_stride : offs[s]);
     const char* kbase = reinterpret_cast<const char*>(p.k) + row0 * C::kRowBytes;
     const char* vbase = reinterpret_cast<const char*>(p.v) + row0 * C::kRowBytes;
 
@@ -395,26 +434,43 @@ void decode_kernel(DecodeParams p) {
     // zeros and is masked out of the softmax.
     const uint32_t k_lane = (uint32_t)(j16 * C::kRowBytes + 16 * kg);
     const uint32_t v_lane = (uint32_t)(rp * C::kRowBytes + 16 * cc);
-    Tile<BF16, D, GP> ta, tb;
+    constexpr int S = decode_stages<BF16, D, GP>();
+    Tile<BF16, D, GP> tl[S];
     for (int64_t a2 = a; a2 < bnd; a2 += C::kSubRows) {
       const uint32_t nrows = (uint32_t)((bnd - a2) < C::kSubRows ? (bnd - a2) : C::kSubRows);
       const __amdgpu_buffer_rsrc_t kr = make_rsrc(kbase + a2 * C::kRowBytes, nrows * C::kRowBytes);
       const __amdgpu_buffer_rsrc_t vr = make_rsrc(vbase + a2 * C::kRowBytes, nrows * C::kRowBytes);
       const uint32_t ntile = (nrows + kTK - 1) / kTK;
-      // Two register tiles: the next tile of this wave is loading while the
-      // current one is computed.
+      // A ring of S register tiles per wave: S - 1 later tiles are loading
+      // while one is computed.  The ring is unrolled so each stage keeps its
+      // own registers (reusing the registers of a tile still in flight makes
+      // the compiler wait for it).  Prefetches are unconditional: past the
+      // last tile their offsets fall outside the descriptor and read zeros
+      // without touching memory, whereas a load under a branch makes the
+      // compiler wait for every outstanding load.
+      // Scheduling barriers keep every stage's loads ahead of its compute
+      // and the prologue's tiles in ring order, so each compute waits only
+      // for its own tile.
       uint32_t t = wave;
-      if (t < ntile) load_tile(ta, kr, vr, t * kTK, k_lane, v_lane);
-      while (t < ntile) {
-        const uint32_t t1 = t + kWaves;
-        if (t1 < ntile) load_tile(tb, kr, vr, t1 * kTK, k_lane, v_lane);
-        compute_tile(st, ta, qa, t * kTK, nrows, p.scale_log2, pbuf[wave], abuf[wave], j16, kg, rp);
-        t = t1;
-        if (t >= ntile) break;
-        const uint32_t t2 = t + kWaves;
-        if (t2 < ntile) load_tile(ta, kr, vr, t2 * kTK, k_lane, v_lane);
-        compute_tile(st, tb, qa, t * kTK, nrows, p.scale_log2, pbuf[wave], abuf[wave], j16, kg, rp);
-        t = t2;
+#pragma unroll
+      for (int i = 0; i < S - 1; ++i) {
+        load_tile(tl[i], kr, vr, (t + i * kWaves) * kTK, k_lane, v_lane);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      // The loop runs whole rounds of S stages and has a single exit: an
+      // exit after any stage makes the register allocator copy in-flight
+      // tiles at the loop head, which waits for every outstanding load.
+      // Stages past the last tile only issue (zero-returning) loads.
+      const uint32_t n_round = t < ntile ? (ntile - t + S * kWaves - 1) / (S * kWaves) : 0;
+      for (uint32_t r = 0; r < n_round; ++r) {
+#pragma unroll
+        for (int i = 0; i < S; ++i) {
+          load_tile(tl[(i + S - 1) % S], kr, vr, (t + (S - 1) * kWaves) * kTK, k_lane, v_lane);
+          __builtin_amdgcn_sched_barrier(0);
+          if (t < ntile)
+            compute_tile(st, tl[i], qa, t * kTK, nrows, p.scale_log2, pbuf[wave], abuf[wave], j16, kg, rp);
+          t += kWaves;
+        }
       }
     }
 
@@ -425,10 +481,7 @@ void decode_kernel(DecodeParams p) {
     for (int h = 0; h < GP; ++h)
 #pragma unroll
       for (int c = 0; c < C::kCPL; ++c) {
-        float x = st.acc[h][c];
-#pragma unroll
-        for (int o = C::kLPR; o < kWave; o <<= 1) x += __shfl_xor(x, o, kWave);
-        st.acc[h][c] = x;
+        st.acc[h][c] = lane_xor_sum<C::kLPR>(st.acc[h][c]);
       }
     if (rp == 0) {
 #pragma unroll
@@ -596,7 +649,7 @@ int32_t split_count(K kernel, int64_t rows_hint) {
   const int cus = device_cus(dev);
   int per_cu = occ_cache[dev].load(std::memory_order_relaxed);
   if (per_cu <= 0) {
-    const size_t lds_max = ((size_t)DKV_MAX_SEGMENTS + 1) * sizeof(int64_t);
+    const size_t lds_max = (2 * (size_t)DKV_MAX_SEGMENTS + 1) * sizeof(int64_t);
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, lds_max) != hipSuccess ||
         per_cu <= 0)
       per_cu = 1;
@@ -611,7 +664,7 @@ int32_t split_count(K kernel, int64_t rows_hint) {
 
 template <bool BF16, int D, int GP>
 hipError_t launch_g(DecodeParams p, int64_t rows_hint, hipStream_t stream) {
-  const size_t lds = ((size_t)p.nseg + 1) * sizeof(int64_t);
+  const size_t lds = (2 * (size_t)p.nseg + 1) * sizeof(int64_t);
   p.P = split_count(decode_kernel<BF16, D, GP>, rows_hint);
   hipLaunchKernelGGL((decode_kernel<BF16, D, GP>), dim3(p.P), dim3(kThreads), lds, stream, p);
   // Segments split over several workgroups are finished by the combine

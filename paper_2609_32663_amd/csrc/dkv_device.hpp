@@ -45,6 +45,23 @@ __device__ __forceinline__ float row16_sum(float x) {
   return x;
 }
 
+// Sum over the lanes of a wave that share (lane % FROM), FROM in {8, 16, 32}:
+// lanes i and i ^ 8 meet through a rotation by 8 inside each 16-lane row,
+// i ^ 16 and i ^ 32 through the permlane swaps (each swap exchanges half of
+// one copy with the other half of a second copy, so adding the two copies
+// gives every lane its partner's value).  Every lane ends with the sum.
+template <int FROM>
+__device__ __forceinline__ float lane_xor_sum(float x) {
+  static_assert(FROM == 8 || FROM == 16 || FROM == 32, "unsupported stride");
+  if constexpr (FROM <= 8) x += dpp_mov<0x128>(x);  // row_ror:8
+  if constexpr (FROM <= 16) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    x = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  }
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // Keeps the compiler from moving LDS accesses of one wave across this point.
 // LDS instructions of a single wave execute in issue order, so no wait is
 // needed between a lane's write and another lane's later read.
