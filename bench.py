@@ -32,7 +32,8 @@ METRIC = "compacted-KV decode attn: HBM GB/s + µs/step vs dense decode, 8B-shap
 WORKLOAD = "llama8b_stack_128k"
 PEAK_HBM_GBPS = 8000.0
 PMC_FILE = os.path.join(ROOT, "profiles", "decode_attn_llama8b_stack_128k_pmc.json")
-KERNEL_SRC = os.path.join(ROOT, "paper_2609_32663_amd", "csrc", "decode_attn.hip")
+KERNEL_SRCS = [os.path.join(ROOT, "paper_2609_32663_amd", "csrc", f)
+               for f in ("decode_attn.hip", "dkv_device.hpp", "dkv_launch.hpp")]
 
 
 def parse():
@@ -44,20 +45,134 @@ def parse():
                     help="skip the oracle timing (for profiler runs)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 1 GiB device copy (HBM-counter calibration)")
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="summarise two rocprofv3 --pmc runs of this script (FETCH_SIZE, then "
+                         "WRITE_SIZE, each with --copy-probe --no-cpu-baseline) into the traffic file")
+    ap.add_argument("--trace-summary", nargs=2, metavar=("TRACE_DIR", "BENCH_LOG"),
+                    help="summarise a rocprofv3 --kernel-trace --stats run of this script (csv output "
+                         "named run_*) and its JSON line into the kernel-trace profile")
+    ap.add_argument("--pmc-command", default="",
+                    help="command line recorded by --pmc-summary / --trace-summary")
     return ap.parse_args()
 
 
 def kernel_hash():
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of the decode kernels' sources (the kernel file and the headers it
+    includes): stored counter results apply only to the code they measured."""
+    h = hashlib.sha256()
+    for path in KERNEL_SRCS:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+def pmc_per_dispatch(path, counter):
+    """{dispatch id: (kernel name, counter value)} from a rocprofv3 counter CSV."""
+    import csv
+    out = {}
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            if r["Counter_Name"] != counter:
+                continue
+            i = int(r["Dispatch_Id"])
+            name, val = out.get(i, (r["Kernel_Name"], 0.0))
+            out[i] = (name, val + float(r["Counter_Value"]))
+    return [out[i] for i in sorted(out)]
+
+
+TRACE_FILE = os.path.join(ROOT, "profiles", "decode_attn_llama8b_stack_128k.txt")
+
+
+def trace_summary(trace_dir, bench_log, command):
+    """Per-kernel durations of a kernel-trace run of this script, next to the
+    JSON line that run printed.  After the parity calls (one per layer, when
+    the oracle baseline runs) the packed calls come first in the trace and
+    the dense comparator's calls follow, equally many."""
+    import csv
+    import statistics as st
+    stats = list(csv.DictReader(open(os.path.join(trace_dir, "run_kernel_stats.csv"))))
+    rows = sorted(csv.DictReader(open(os.path.join(trace_dir, "run_kernel_trace.csv"))),
+                  key=lambda r: int(r["Start_Timestamp"]))
+    b = None
+    for line in open(bench_log):
+        if line.startswith("{"):
+            b = json.loads(line)
+    pairs = []
+    for i in range(len(rows) - 1):
+        a, m = rows[i], rows[i + 1]
+        if "decode_kernel" in a["Kernel_Name"] and "decode_merge_kernel" in m["Kernel_Name"]:
+            s0, e0 = int(a["Start_Timestamp"]), int(a["End_Timestamp"])
+            s1, e1 = int(m["Start_Timestamp"]), int(m["End_Timestamp"])
+            pairs.append(((e0 - s0) / 1e3, (e1 - s1) / 1e3, (e1 - s0) / 1e3))
+    # with the oracle baseline, one parity call per layer precedes the timing
+    front = b["config"]["layers"] if b.get("parity_layer0") else 0
+    timed_pairs = pairs[front:]
+    packed, dense = timed_pairs[: len(timed_pairs) // 2], timed_pairs[len(timed_pairs) // 2:]
+    lines = [f"# rocprofv3 kernel trace of bench.py ({WORKLOAD}: 32 layers x 32q/8kv x d128, "
+             f"T=131072, {b['config']['retained_fraction'] * 100:.1f}% retained)",
+             f"# command: {command}",
+             "# per-kernel statistics (rocprofv3 --stats, dkv kernels only; us):",
+             f"{'kernel':58s} {'calls':>6s} {'avg':>9s} {'min':>9s} {'max':>9s}"]
+    for r in stats:
+        if "dkv" in r["Name"]:
+            nm = r["Name"].replace("(anonymous namespace)::", "").replace("dkv::", "")
+            lines.append(f"{nm[:58]:58s} {r['Calls']:>6s} {float(r['AverageNs']) / 1e3:9.2f} "
+                         f"{float(r['MinNs']) / 1e3:9.2f} {float(r['MaxNs']) / 1e3:9.2f}")
+    for name, ps in (("packed", packed), ("dense", dense)):
+        lines.append(f"{name:6s} calls {len(ps):4d}: decode_kernel mean {st.mean(p[0] for p in ps):7.2f}  "
+                     f"decode_merge_kernel mean {st.mean(p[1] for p in ps):6.2f}  "
+                     f"call (split start to combine end) mean {st.mean(p[2] for p in ps):7.2f} us")
+    lines += ["",
+              "# JSON line of the same run (timed region = HIP-graph replays; the profiler adds overhead):",
+              f"ms_per_step {b['ms_per_step']}  value {b['value']} GB/s  roofline.avg_launch_us "
+              f"{b['roofline']['avg_launch_us']}  frac {b['roofline']['frac']}",
+              f"dense ms_per_step {b['dense']['ms_per_step']}  speedup_vs_dense {b['speedup_vs_dense']}",
+              f"cpu_baseline {json.dumps(b['cpu_baseline'])}",
+              f"parity_layer0 {json.dumps(b['parity_layer0'])}"]
+    with open(TRACE_FILE, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def pmc_summary(fetch_csv, write_csv, command):
+    """HBM traffic of one packed attention call from FETCH_SIZE / WRITE_SIZE
+    (KiB per dispatch).  Each counter is scaled by what it reads for the
+    1 GiB device copy run at the end (which reads and writes exactly 1 GiB),
+    and the packed calls are the first half of the decode/combine dispatch
+    pairs (the script times the packed path before the dense one)."""
+    import statistics
+    res = {"kernel_sha256_16": kernel_hash(), "command": command, "unit": "bytes per call"}
+    per_call = {}
+    for key, path, counter in (("fetch", fetch_csv, "FETCH_SIZE"), ("write", write_csv, "WRITE_SIZE")):
+        rows = pmc_per_dispatch(path, counter)
+        copies = [v for n, v in rows if "copy" in n.lower() or "elementwise" in n.lower()]
+        calib = (1 << 30) / (copies[-1] * 1024.0)
+        calls = [rows[i][1] + rows[i + 1][1] for i in range(len(rows) - 1)
+                 if "decode_kernel" in rows[i][0] and "decode_merge_kernel" in rows[i + 1][0]]
+        packed = calls[: len(calls) // 2]
+        per_call[key] = statistics.mean(packed) * 1024.0 * calib
+        res[f"{key}_calibration"] = round(calib, 4)
+        res[f"{key}_bytes_per_call"] = int(per_call[key])
+        res[f"{key}_calls_counted"] = len(packed)
+    res["traffic_bytes_per_launch"] = int(per_call["fetch"] + per_call["write"])
+    with open(PMC_FILE, "w") as f:
+        json.dump(res, f, indent=1)
+        f.write("\n")
+    print(json.dumps(res))
+
+
 def main():
     args = parse()
+    if args.pmc_summary:
+        pmc_summary(*args.pmc_summary, args.pmc_command)
+        return
+    if args.trace_summary:
+        trace_summary(*args.trace_summary, args.pmc_command)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py runs on one GPU only: the Distance-KV path here is a single-GPU "
@@ -274,10 +389,11 @@ def main():
     dlaunch_ms = dms / L
 
     if args.copy_probe:
-        src = torch.empty(1 << 29, dtype=torch.int16, device=dev)  # 1 GiB
+        # an elementwise kernel (not a DMA/blit copy) that reads and writes 1 GiB
+        src = torch.ones(1 << 29, dtype=torch.int16, device=dev)
         dst = torch.empty_like(src)
         for _ in range(3):
-            dst.copy_(src)
+            torch.mul(src, 1, out=dst)
         torch.cuda.synchronize()
 
     per_launch_bytes = nbytes / L
