@@ -388,6 +388,42 @@ def main():
     launch_ms = ms / L
     dlaunch_ms = dms / L
 
+    # ---------------- achievable read bandwidth at this launch size -------
+    # The streaming-read probe (same 16-byte non-temporal buffer loads as the
+    # decode kernel's K/V stream) over L slices of one decode launch's size,
+    # one launch per slice, captured and replayed like a decode step.
+    per = (int(nbytes / L) + 15) // 16 * 16
+    pbuf = torch.ones(L * per // 2, dtype=torch.int16, device=dev)
+    psink = torch.zeros(4, dtype=torch.int32, device=dev)
+    probe_gbps = {}
+    for wg in (256, 512, 1024, 2048):
+        def probe_step(shp, wg=wg):
+            for layer in range(L):
+                st_ = lib.dkv_probe_stream_read(P(pbuf.data_ptr() + layer * per), per,
+                                                P(psink.data_ptr()), wg, P(shp))
+                if st_ != 0:
+                    raise d.DkvError("dkv_probe_stream_read", st_)
+        probe_step(sh)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=cap_stream):
+            probe_step(cap_stream.cuda_stream)
+        for _ in range(args.warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        a, b = ev(), ev()
+        a.record(stream)
+        for _ in range(args.steps):
+            g.replay()
+        b.record(stream)
+        torch.cuda.synchronize()
+        probe_gbps[wg] = round(L * per / (a.elapsed_time(b) / args.steps * 1e-3) / 1e9, 1)
+    del pbuf
+    achievable = {"kind": "dkv_probe_stream_read: streaming read, one launch per layer-sized slice, "
+                          "HIP-graph replays", "bytes_per_launch": per,
+                  "gb_per_s_by_workgroups": probe_gbps, "best_gb_per_s": max(probe_gbps.values())}
+    log(f"probe {probe_gbps}")
+
     if args.copy_probe:
         # an elementwise kernel (not a DMA/blit copy) that reads and writes 1 GiB
         src = torch.ones(1 << 29, dtype=torch.int16, device=dev)
@@ -432,6 +468,7 @@ def main():
                      "avg_launch_us": round(launch_ms * 1e3, 2),
                      "bytes_per_launch": int(per_launch_bytes)},
         "cpu_baseline": cpu,
+        "achievable_read": achievable,
         "us_per_step": round(ms * 1e3, 1),
         "dense": {"ms_per_step": round(dms, 4), "eager_ms_per_step": round(deager_ms, 4),
                   "gb_per_s": round(dbytes / (dms * 1e-3) / 1e9, 2),

@@ -19,7 +19,7 @@ __all__ = [
     "dkv_map_pattern", "dkv_compact_workspace_bytes", "dkv_compact", "dkv_append",
     "dkv_decode_workspace_bytes", "dkv_decode_attn", "dkv_dense_decode_attn",
     "dkv_append_decode_attn", "dkv_dense_append_decode_attn",
-    "dkv_status_string",
+    "dkv_status_string", "dkv_probe_stream_read",
 ]
 
 (DKV_OK, DKV_ERR_INVALID_ARG, DKV_ERR_UNSUPPORTED, DKV_ERR_MISALIGNED, DKV_ERR_CAPACITY,
@@ -92,6 +92,7 @@ def library():
         "dkv_dense_append_decode_attn": (I32, [I32, I32, I32, I32, I32, VP, VP, VP, I32, VP, VP, I64,
                                                I32, F32, VP, VP, SZ, VP]),
         "dkv_status_string": (ctypes.c_char_p, [I32]),
+        "dkv_probe_stream_read": (I32, [VP, I64, VP, I32, VP]),
     }
     for name, (res, args) in sigs.items():
         f = getattr(lib, name)
@@ -222,3 +223,11 @@ def dkv_dense_decode_attn(q, k, v, n_valid, sm_scale, out, workspace, stream=Non
         dtype_code(q.dtype), B, Hq, Hkv, d, _dev(q, "q"), _dev(k, "k"), _dev(v, "v"), t_cap,
         int(n_valid), float(sm_scale), _dev(out, "out"), _dev(workspace, "workspace"),
         workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def dkv_probe_stream_read(src, sink, workgroups, nbytes=None, stream=None):
+    """Streaming-read probe (measurement aid): reads `nbytes` (default: all)
+    bytes of the device tensor `src`; `sink` is a device tensor of >= 16 bytes."""
+    n = src.numel() * src.element_size() if nbytes is None else int(nbytes)
+    _check("dkv_probe_stream_read", library().dkv_probe_stream_read(
+        _dev(src, "src"), n, _dev(sink, "sink"), int(workgroups), _stream(stream)))

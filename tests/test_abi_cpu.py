@@ -15,7 +15,8 @@ import pytest
 import paper_2609_32663_amd as d
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "dkv.h")
+HEADERS = [os.path.join(ROOT, "include", f) for f in sorted(os.listdir(os.path.join(ROOT, "include")))
+           if f.endswith(".h")]
 
 A = ctypes.c_void_p(0x10000)      # fake 16-byte-aligned device address
 MIS = ctypes.c_void_p(0x10008)    # fake misaligned address
@@ -23,7 +24,7 @@ NUL = None
 
 
 def declared_functions():
-    text = open(HEADER).read()
+    text = "".join(open(h).read() for h in HEADERS)
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(dkv_[a-z_]+)\s*\(", text)))
 
@@ -177,6 +178,20 @@ def test_dense_decode_validation():
                                      NUL) == d.DKV_ERR_MISALIGNED
     assert lib.dkv_dense_decode_attn(d.DKV_F32, 1, 8, 2, 64, A, A, A, 100, 10, 1.0, A, A, ws - 4,
                                      NUL) == d.DKV_ERR_WORKSPACE
+
+
+def test_probe_validation():
+    lib = d.library()
+    assert lib.dkv_probe_stream_read(A, 0, NUL, 1, NUL) == d.DKV_OK  # nothing to read
+    assert lib.dkv_probe_stream_read(A, -16, A, 1, NUL) == d.DKV_ERR_INVALID_ARG
+    assert lib.dkv_probe_stream_read(A, 24, A, 1, NUL) == d.DKV_ERR_INVALID_ARG
+    assert lib.dkv_probe_stream_read(A, 4096, A, 0, NUL) == d.DKV_ERR_INVALID_ARG
+    assert lib.dkv_probe_stream_read(A, 4096, A, 65536, NUL) == d.DKV_ERR_INVALID_ARG
+    assert lib.dkv_probe_stream_read(NUL, 4096, A, 1, NUL) == d.DKV_ERR_INVALID_ARG
+    assert lib.dkv_probe_stream_read(A, 4096, NUL, 1, NUL) == d.DKV_ERR_INVALID_ARG
+    assert lib.dkv_probe_stream_read(MIS, 4096, A, 1, NUL) == d.DKV_ERR_MISALIGNED
+    assert lib.dkv_probe_stream_read(A, 4096, MIS, 1, NUL) == d.DKV_ERR_MISALIGNED
+    assert lib.dkv_probe_stream_read(A, (1 << 32) + 16, A, 1, NUL) == d.DKV_ERR_UNSUPPORTED
 
 
 def test_binding_rejects_host_tensors():

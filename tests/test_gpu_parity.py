@@ -539,3 +539,13 @@ def test_path_llama70b_batched_budgets(d, budget):
     want = o.decode_attn(bits(q), ref["k_c"], ref["v_c"], ref["seg_off"], ref["seg_len"], 0,
                          w.sm_scale, w.num_kv_heads, o.BF16)
     assert row_rel_err(out.cpu().numpy(), want) <= ATTN_TOL
+
+
+def test_probe_stream_read_runs(d):
+    """The bandwidth probe reads a ragged buffer with several grid shapes
+    (no result to compare: it only must not fail)."""
+    src = torch.ones((1 << 20) + 48, dtype=torch.uint8, device=DEV)
+    sink = torch.zeros(4, dtype=torch.int32, device=DEV)
+    for wg in (1, 3, 256, 2048):
+        d.dkv_probe_stream_read(src, sink, wg)
+    torch.cuda.synchronize()
