@@ -15,6 +15,10 @@ What it computes (Distance-KV, Sec. 3.4 "Static-Pattern Inference"):
 * the one-time prune-and-pack of the KV cache, which keeps retained rows in
   their original token order (Sec. 3.4, Fig. 2(b));
 * the append of new tokens, which are always retained (Sec. 3.4);
+* attention of the query block (the tokens after the context, Sec. 3.4):
+  each query token attends to the packed context, the tokens appended before
+  the block, and causally to the block's own tokens, which are appended like
+  any new token;
 * decode attention over the packed cache.  Attention restricted to a fixed
   retained set is exactly dense attention with every other position masked to
   -inf, so the oracle writes out that plain definition twice, once over the
@@ -60,6 +64,7 @@ __all__ = [
     "append",
     "decode_attn",
     "dense_decode_attn",
+    "query_attn",
     "masked_dense_attn",
 ]
 
@@ -312,6 +317,37 @@ def dense_decode_attn(q, k, v, n_valid, sm_scale, dtype):
             vr = widen(v[b, g, :n_valid], dtype)
             for h in range(g * G, (g + 1) * G):
                 out[b, h] = _softmax_attend(qf[b, h], kr, vr, sm_scale)
+    return out
+
+
+def query_attn(q, k_c, v_c, seg_off, seg_len, n_tail, sm_scale, num_kv_heads, dtype):
+    """Attention of a query block over the packed cache (Sec. 3.4).
+
+    After the one-time compaction the query tokens attend to the compressed
+    context; their own K/V are appended like every new token and kept.
+    q: [B][n_q][Hq][d], token-major; the block's K/V must already sit in the
+    segment's rows [seg_len + n_tail, seg_len + n_tail + n_q) (after the
+    packed context and the n_tail tokens appended before the block).  Query
+    token i attends to rows [seg_off, seg_off + seg_len + n_tail + i + 1): the
+    context, the earlier appended tokens, and the block causally up to
+    itself.  Every query head of group g attends to segment b * Hkv + g.
+    Returns float64 [B][n_q][Hq][d].
+    """
+    qf = widen(q, dtype)
+    B, n_q, Hq, d = qf.shape
+    G = Hq // num_kv_heads
+    out = np.zeros((B, n_q, Hq, d), dtype=np.float64)
+    for b in range(B):
+        for g in range(num_kv_heads):
+            s = b * num_kv_heads + g
+            lo = int(seg_off[s])
+            base = int(seg_len[s]) + int(n_tail)
+            kr = widen(k_c[lo:lo + base + n_q], dtype)
+            vr = widen(v_c[lo:lo + base + n_q], dtype)
+            for i in range(n_q):
+                for h in range(g * G, (g + 1) * G):
+                    out[b, i, h] = _softmax_attend(qf[b, i, h], kr[:base + i + 1], vr[:base + i + 1],
+                                                   sm_scale)
     return out
 
 

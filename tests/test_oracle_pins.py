@@ -415,3 +415,76 @@ def test_decode_bf16_matches_sdpa_on_widened_values():
     out = o.decode_attn(qb, r["k_c"], r["v_c"], r["seg_off"], r["seg_len"], 0, 0.5, 2, o.BF16)
     ref = sdpa(o.widen(qb, o.BF16), o.widen(kb, o.BF16), o.widen(vb, o.BF16), 0.5)
     np.testing.assert_allclose(out, ref, rtol=1e-12, atol=1e-13)
+
+
+# ---------------------------------------------------------------------------
+# query-block attention
+# ---------------------------------------------------------------------------
+
+def _query_case(rng, B, n_kv, G, T, d, n_tail, n_q, keep):
+    """Dense context with a keep mask, n_tail appended tokens, then a block of
+    n_q query tokens whose K/V are appended after them."""
+    k = rng.standard_normal((B, n_kv, T, d)).astype(np.float32)
+    v = rng.standard_normal((B, n_kv, T, d)).astype(np.float32)
+    m = (rng.uniform(size=(B, n_kv, T)) < keep).astype(np.uint8)
+    kt = rng.standard_normal((B, n_kv, n_tail + n_q, d)).astype(np.float32)
+    vt = rng.standard_normal((B, n_kv, n_tail + n_q, d)).astype(np.float32)
+    q = rng.standard_normal((B, n_q, n_kv * G, d)).astype(np.float32)
+    return q, k, v, m, kt, vt
+
+
+def test_query_attn_matches_sdpa_with_causal_block_mask():
+    """Against torch SDPA over the dense cache: pruned context positions
+    masked out, earlier appended tokens visible, the block causal."""
+    rng = np.random.default_rng(40)
+    for trial in range(6):
+        B, n_kv, G, T, d = 2, 2, int(rng.integers(1, 4)), 37, 8
+        n_tail, n_q = int(rng.integers(0, 3)), int(rng.integers(1, 6))
+        q, k, v, m, kt, vt = _query_case(rng, B, n_kv, G, T, d, n_tail, n_q, 0.4)
+        r = o.compact(k, v, m, n_tail + n_q)
+        kc, vc = o.append(r["k_c"], r["v_c"], r["seg_off"], r["seg_len"], kt, vt, 0)
+        out = o.query_attn(q, kc, vc, r["seg_off"], r["seg_len"], n_tail, 0.45, n_kv, o.F32)
+        kd = np.concatenate([k, kt], axis=2).astype(np.float64)
+        vd = np.concatenate([v, vt], axis=2).astype(np.float64)
+        allow = np.zeros((B, n_kv * G, n_q, T + n_tail + n_q), bool)
+        for b in range(B):
+            for h in range(n_kv * G):
+                for i in range(n_q):
+                    allow[b, h, i, :T] = m[b, h // G] == 1
+                    allow[b, h, i, T:T + n_tail + i + 1] = True
+        qt = torch.from_numpy(q.astype(np.float64)).transpose(1, 2)  # [B][Hq][n_q][d]
+        ref = torch.nn.functional.scaled_dot_product_attention(
+            qt, torch.from_numpy(kd), torch.from_numpy(vd), attn_mask=torch.from_numpy(allow),
+            scale=0.45, enable_gqa=True).transpose(1, 2).numpy()
+        np.testing.assert_allclose(out, ref, rtol=1e-12, atol=1e-13)
+
+
+def test_query_attn_zero_query_is_causal_running_mean():
+    """q = 0: every visible row has the same weight, so token i's output is
+    the mean of the first seg_len + n_tail + i + 1 rows of its segment."""
+    rng = np.random.default_rng(41)
+    B, n_kv, G, T, d, n_tail, n_q = 1, 2, 2, 20, 4, 2, 4
+    _, k, v, m, kt, vt = _query_case(rng, B, n_kv, G, T, d, n_tail, n_q, 0.5)
+    q = np.zeros((B, n_q, n_kv * G, d), np.float32)
+    r = o.compact(k, v, m, n_tail + n_q)
+    kc, vc = o.append(r["k_c"], r["v_c"], r["seg_off"], r["seg_len"], kt, vt, 0)
+    out = o.query_attn(q, kc, vc, r["seg_off"], r["seg_len"], n_tail, 1.0, n_kv, o.F32)
+    for g in range(n_kv):
+        rows = np.concatenate([v[0, g][m[0, g] == 1], vt[0, g]]).astype(np.float64)
+        base = int(m[0, g].sum()) + n_tail
+        for i in range(n_q):
+            for h in range(g * G, g * G + G):
+                np.testing.assert_allclose(out[0, i, h], rows[:base + i + 1].mean(0), rtol=1e-13,
+                                           atol=1e-14)
+
+
+def test_query_attn_single_token_is_decode_step():
+    """A one-token block is one decode step with the token appended."""
+    rng = np.random.default_rng(42)
+    B, n_kv, G, T, d, n_tail = 2, 3, 2, 30, 8, 1
+    q, k, v, m, kt, vt = _query_case(rng, B, n_kv, G, T, d, n_tail, 1, 0.3)
+    r = o.compact(k, v, m, n_tail + 1)
+    kc, vc = o.append(r["k_c"], r["v_c"], r["seg_off"], r["seg_len"], kt, vt, 0)
+    out = o.query_attn(q, kc, vc, r["seg_off"], r["seg_len"], n_tail, 0.7, n_kv, o.F32)
+    dec = o.decode_attn(q[:, 0], kc, vc, r["seg_off"], r["seg_len"], n_tail + 1, 0.7, n_kv, o.F32)
+    np.testing.assert_allclose(out[:, 0], dec, rtol=1e-13, atol=1e-14)
