@@ -13,6 +13,8 @@
  *   dkv_compact       dense K/V + keep mask -> packed K/V, offsets, lengths
  *   dkv_append        new tokens -> free rows after each packed segment
  *   dkv_decode_attn   one decode step of attention over the packed segments
+ *   dkv_query_attn    the query block after the context: attention over the
+ *                     packed segments plus the block itself, causally
  *
  * plus dkv_dense_decode_attn, the same attention kernel over an uncompressed
  * cache (the "Dense" comparator of Sec. 4.3).
@@ -238,6 +240,42 @@ dkv_status dkv_dense_append_decode_attn(dkv_dtype dtype, int32_t batch, int32_t 
                                         void *k, void *v, int64_t t_cap, int32_t n_valid,
                                         float sm_scale, float *out, void *workspace,
                                         size_t workspace_bytes, void *stream);
+
+/* Workspace bytes for dkv_query_attn with the same shapes and rows_hint (host,
+ * no GPU call); 0 when the call needs none (workspace may then be NULL). */
+size_t dkv_query_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                 int32_t head_dim, int32_t n_q, int64_t rows_hint);
+
+/*
+ * dkv_query_attn -- attention of a block of n_q query tokens over the packed
+ * cache (Sec. 3.4: after the one-time compaction the query tokens attend to
+ * the compressed context, and their own K/V are appended and kept).
+ *
+ * q        [B][n_q][Hq][d] bf16, token-major (the layout of a model's
+ *          activations).
+ * The block's K/V must already be appended (dkv_append with n_new = n_q at
+ * the same n_tail): segment s = b * Hkv + g then holds the packed context,
+ * n_tail earlier appended tokens and the block, and query token i of
+ * sequence b, head h (g = h / G) attends to rows
+ * [seg_off[s], seg_off[s] + seg_len[s] + n_tail + i + 1): everything before
+ * the block, and the block causally up to itself.
+ * out      [B][n_q][Hq][d] fp32, softmax(sm_scale * K q) V over those rows.
+ * append_cap  free rows reserved per segment; n_tail + n_q <= append_cap.
+ * rows_hint (host) total rows the call attends, sum over segments of
+ *          seg_len + n_tail + n_q (0 = unknown); it sizes the split of the key
+ *          ranges and must equal the value given to dkv_query_workspace_bytes.
+ * workspace  dkv_query_workspace_bytes(...) bytes for per-range partial
+ *          results (no initial contents required), or NULL when that is 0.
+ * Only DKV_BF16 is supported (DKV_ERR_UNSUPPORTED otherwise); head_dim 64 or
+ * 128.  The call enqueues the attention kernel and, when the keys are split
+ * into several ranges, a combine kernel.
+ */
+dkv_status dkv_query_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_heads,
+                          int32_t num_kv_heads, int32_t head_dim, int32_t n_q, const void *q,
+                          int32_t n_tail, int32_t append_cap, const void *k_c, const void *v_c,
+                          const int64_t *seg_off, const int32_t *seg_len, float sm_scale,
+                          int64_t rows_hint, float *out, void *workspace, size_t workspace_bytes,
+                          void *stream);
 
 /* Static description of a status code. */
 const char *dkv_status_string(dkv_status status);

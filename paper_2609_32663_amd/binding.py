@@ -19,7 +19,7 @@ __all__ = [
     "dkv_map_pattern", "dkv_compact_workspace_bytes", "dkv_compact", "dkv_append",
     "dkv_decode_workspace_bytes", "dkv_decode_attn", "dkv_dense_decode_attn",
     "dkv_append_decode_attn", "dkv_dense_append_decode_attn",
-    "dkv_status_string", "dkv_probe_stream_read",
+    "dkv_status_string", "dkv_probe_stream_read", "dkv_query_workspace_bytes", "dkv_query_attn",
 ]
 
 (DKV_OK, DKV_ERR_INVALID_ARG, DKV_ERR_UNSUPPORTED, DKV_ERR_MISALIGNED, DKV_ERR_CAPACITY,
@@ -93,6 +93,9 @@ def library():
                                                I32, F32, VP, VP, SZ, VP]),
         "dkv_status_string": (ctypes.c_char_p, [I32]),
         "dkv_probe_stream_read": (I32, [VP, I64, VP, I32, VP]),
+        "dkv_query_workspace_bytes": (SZ, [I32, I32, I32, I32, I32, I64]),
+        "dkv_query_attn": (I32, [I32, I32, I32, I32, I32, I32, VP, I32, I32, VP, VP, VP, VP, F32, I64,
+                                 VP, VP, SZ, VP]),
     }
     for name, (res, args) in sigs.items():
         f = getattr(lib, name)
@@ -231,3 +234,22 @@ def dkv_probe_stream_read(src, sink, workgroups, nbytes=None, stream=None):
     n = src.numel() * src.element_size() if nbytes is None else int(nbytes)
     _check("dkv_probe_stream_read", library().dkv_probe_stream_read(
         _dev(src, "src"), n, _dev(sink, "sink"), int(workgroups), _stream(stream)))
+
+
+def dkv_query_workspace_bytes(batch, num_q_heads, num_kv_heads, head_dim, n_q, rows_hint=0):
+    return library().dkv_query_workspace_bytes(batch, num_q_heads, num_kv_heads, head_dim, n_q,
+                                               int(rows_hint))
+
+
+def dkv_query_attn(q, n_tail, append_cap, k_c, v_c, seg_off, seg_len, sm_scale, out, workspace,
+                   num_kv_heads, rows_hint=0, stream=None):
+    """q: [B][n_q][Hq][d] bf16 (the block's K/V already appended); out: [B][n_q][Hq][d] fp32;
+    workspace: device tensor of dkv_query_workspace_bytes(...) bytes, or None when that is 0."""
+    B, n_q, Hq, d = q.shape
+    ws_ptr, ws_bytes = (None, 0) if workspace is None else (
+        _dev(workspace, "workspace"), workspace.numel() * workspace.element_size())
+    _check("dkv_query_attn", library().dkv_query_attn(
+        dtype_code(q.dtype), B, Hq, int(num_kv_heads), d, n_q, _dev(q, "q"), int(n_tail),
+        int(append_cap), _dev(k_c, "k_c"), _dev(v_c, "v_c"), _dev(seg_off, "seg_off"),
+        _dev(seg_len, "seg_len"), float(sm_scale), int(rows_hint), _dev(out, "out"), ws_ptr, ws_bytes,
+        _stream(stream)))

@@ -27,7 +27,8 @@ COMMON_FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     f"-I{INCLUDE}", "-Wall", "-Wno-unused-function",
 ]
-SOURCES = ["map_pattern.hip", "compact.hip", "decode_attn.hip", "dkv_api.cpp", "bw_probe.hip"]
+SOURCES = ["map_pattern.hip", "compact.hip", "decode_attn.hip", "dkv_api.cpp", "bw_probe.hip",
+           "query_attn.hip", "dkv_query_api.cpp"]
 
 
 def _hipcc():

@@ -1,0 +1,86 @@
+// C-ABI entry points of query-block attention (see include/dkv.h).  Every
+// argument is checked on the host before anything is enqueued.
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+
+#include "../../include/dkv.h"
+#include "dkv_query.hpp"
+
+namespace {
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Shape checks shared by the call and its workspace query.
+dkv_status check_query_shape(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t n_q) {
+  if (batch < 0 || hq <= 0 || hkv <= 0 || hq % hkv != 0 || n_q < 0) return DKV_ERR_INVALID_ARG;
+  if (hq / hkv > DKV_MAX_GROUP || (d != 64 && d != 128)) return DKV_ERR_UNSUPPORTED;
+  if ((int64_t)batch * hkv > DKV_MAX_SEGMENTS) return DKV_ERR_UNSUPPORTED;
+  // query rows per segment and the grid must fit 31 bits
+  const int64_t rows = (int64_t)n_q * (hq / hkv);
+  const int64_t wgs = (int64_t)batch * hkv * ((rows + dkv::kQueryRowsPerWG - 1) / dkv::kQueryRowsPerWG) *
+                      dkv::kQueryMaxSplit;
+  if (rows > INT32_MAX || wgs > INT32_MAX) return DKV_ERR_UNSUPPORTED;
+  return DKV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t dkv_query_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                 int32_t head_dim, int32_t n_q, int64_t rows_hint) {
+  if (check_query_shape(batch, num_q_heads, num_kv_heads, head_dim, n_q) != DKV_OK) return 0;
+  if (batch == 0 || n_q == 0) return 0;
+  return dkv::query_workspace_bytes(batch * num_kv_heads, n_q * (num_q_heads / num_kv_heads), head_dim,
+                                    rows_hint);
+}
+
+dkv_status dkv_query_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                          int32_t head_dim, int32_t n_q, const void* q, int32_t n_tail, int32_t append_cap,
+                          const void* k_c, const void* v_c, const int64_t* seg_off, const int32_t* seg_len,
+                          float sm_scale, int64_t rows_hint, float* out, void* workspace, size_t workspace_bytes,
+                          void* stream) {
+  if (dtype != DKV_BF16 && dtype != DKV_F32) return DKV_ERR_INVALID_ARG;
+  dkv_status st = check_query_shape(batch, num_q_heads, num_kv_heads, head_dim, n_q);
+  if (st != DKV_OK) return st;
+  if (dtype != DKV_BF16) return DKV_ERR_UNSUPPORTED;
+  if (!std::isfinite(sm_scale) || n_tail < 0 || append_cap < 0) return DKV_ERR_INVALID_ARG;
+  if ((int64_t)n_tail + n_q > append_cap) return DKV_ERR_CAPACITY;
+  if (batch == 0 || n_q == 0) return DKV_OK;
+  if (q == nullptr || k_c == nullptr || v_c == nullptr || out == nullptr || seg_off == nullptr ||
+      seg_len == nullptr)
+    return DKV_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k_c) || !aligned16(v_c) || !aligned16(out)) return DKV_ERR_MISALIGNED;
+  const int32_t nseg = batch * num_kv_heads;
+  const int32_t G = num_q_heads / num_kv_heads;
+  const int32_t rows = n_q * G;
+  const size_t need = dkv::query_workspace_bytes(nseg, rows, head_dim, rows_hint);
+  if (need > 0 && (workspace == nullptr || !aligned16(workspace) || workspace_bytes < need))
+    return DKV_ERR_WORKSPACE;
+  dkv::QueryParams p;
+  std::memset(&p, 0, sizeof(p));
+  p.q = q;
+  p.k = k_c;
+  p.v = v_c;
+  p.seg_off = seg_off;
+  p.seg_len = seg_len;
+  p.n_tail = n_tail;
+  p.n_q = n_q;
+  p.nseg = nseg;
+  p.Hkv = num_kv_heads;
+  p.Hq = num_q_heads;
+  p.G = G;
+  p.rows = rows;
+  p.qtiles = (rows + dkv::kQueryRowsPerWG - 1) / dkv::kQueryRowsPerWG;
+  p.nsplit = dkv::query_split_count(nseg, rows, rows_hint);
+  p.scale_log2 = sm_scale * 1.4426950408889634f;
+  p.out = out;
+  p.rec = static_cast<float*>(workspace);
+  return dkv::launch_query_attn(p, head_dim, (hipStream_t)stream) == hipSuccess ? DKV_OK : DKV_ERR_HIP;
+}
+
+}  // extern "C"

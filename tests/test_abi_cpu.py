@@ -194,6 +194,38 @@ def test_probe_validation():
     assert lib.dkv_probe_stream_read(A, (1 << 32) + 16, A, 1, NUL) == d.DKV_ERR_UNSUPPORTED
 
 
+def test_query_validation():
+    lib = d.library()
+    assert d.dkv_query_workspace_bytes(1, 32, 8, 128, 256, 8 * 50000) > 0
+    assert d.dkv_query_workspace_bytes(1, 32, 8, 96, 256, 0) == 0
+    assert d.dkv_query_workspace_bytes(1, 32, 8, 128, 256, 8 * 600) == 0  # too few keys to split
+
+    def call(dtype=d.DKV_BF16, B=1, Hq=32, Hkv=8, dim=128, n_q=4, q=A, n_tail=0, cap=8, kc=A, vc=A,
+             so=A, sl=A, scale=1.0, hint=0, out=A, ws=A, ws_bytes=1 << 30):
+        return lib.dkv_query_attn(dtype, B, Hq, Hkv, dim, n_q, q, n_tail, cap, kc, vc, so, sl, scale, hint,
+                                  out, ws, ws_bytes, NUL)
+
+    assert call(dtype=d.DKV_F32) == d.DKV_ERR_UNSUPPORTED
+    assert call(dtype=9) == d.DKV_ERR_INVALID_ARG
+    assert call(dim=256) == d.DKV_ERR_UNSUPPORTED
+    assert call(Hq=30) == d.DKV_ERR_INVALID_ARG
+    assert call(Hq=34, Hkv=2) == d.DKV_ERR_UNSUPPORTED
+    assert call(n_q=-1) == d.DKV_ERR_INVALID_ARG
+    assert call(n_tail=-1) == d.DKV_ERR_INVALID_ARG
+    assert call(n_q=5, n_tail=4, cap=8) == d.DKV_ERR_CAPACITY
+    assert call(scale=float("nan")) == d.DKV_ERR_INVALID_ARG
+    assert call(q=NUL) == d.DKV_ERR_INVALID_ARG
+    assert call(sl=NUL) == d.DKV_ERR_INVALID_ARG
+    assert call(out=MIS) == d.DKV_ERR_MISALIGNED
+    assert call(kc=MIS) == d.DKV_ERR_MISALIGNED
+    big = 8 * 50000
+    need = d.dkv_query_workspace_bytes(1, 32, 8, 128, 256, big)
+    assert call(n_q=256, cap=256, hint=big, ws=NUL) == d.DKV_ERR_WORKSPACE
+    assert call(n_q=256, cap=256, hint=big, ws_bytes=need - 1) == d.DKV_ERR_WORKSPACE
+    assert call(n_q=0, q=NUL, out=NUL) == d.DKV_OK
+    assert call(B=0, q=NUL, out=NUL) == d.DKV_OK
+
+
 def test_binding_rejects_host_tensors():
     import torch
     lay = _lay()

@@ -1,0 +1,164 @@
+"""GPU parity of query-block attention (dkv_query_attn) against the oracle.
+
+Every case runs the GPU path end to end through the C ABI: compaction of a
+dense cache under a keep mask, append of the tokens before the block and of
+the block itself, then the block's attention.  The oracle packs, appends and
+attends on its own from the same inputs.  Output rows ([B][n_q][Hq] rows of
+d values) must be within ATTN_TOL (max relative error per row).
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as o
+from _helpers import ATTN_TOL, bits, row_rel_err
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+@pytest.fixture(scope="module")
+def d():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2609_32663_amd as lib
+    return lib
+
+
+def _bf16(rng, shape, scale=1.0):
+    return (torch.from_numpy(rng.standard_normal(shape).astype(np.float32)) * scale).to(torch.bfloat16)
+
+
+def _run(d, rng, B, Hkv, G, T, dim, keep, n_tail, n_q, cap=None, sm_scale=None, hint="exact",
+         empty_segments=0):
+    """One case; returns (gpu out [B][n_q][Hq][d], oracle out)."""
+    Hq = Hkv * G
+    cap = n_tail + n_q if cap is None else cap
+    sm_scale = 1.0 / np.sqrt(dim) if sm_scale is None else sm_scale
+    k = _bf16(rng, (B, Hkv, T, dim))
+    v = _bf16(rng, (B, Hkv, T, dim))
+    mask = (rng.uniform(size=(B, Hkv, T)) < keep).astype(np.uint8)
+    for e in range(empty_segments):
+        mask[e % B, (e // B) % Hkv] = 0
+    kt = _bf16(rng, (B, Hkv, n_tail, dim))
+    vt = _bf16(rng, (B, Hkv, n_tail, dim))
+    kb = _bf16(rng, (B, Hkv, n_q, dim))
+    vb = _bf16(rng, (B, Hkv, n_q, dim))
+    q = _bf16(rng, (B, n_q, Hq, dim))
+
+    # GPU: pack, append the earlier tokens and the block, attend
+    lay = d.make_layout(B, Hq, Hkv, dim, T, 0, 0, [0, max(T, 1)])
+    rows = int(mask.sum()) + B * Hkv * cap
+    k_c = torch.empty((max(rows, 1), dim), dtype=torch.bfloat16, device=DEV)
+    v_c = torch.empty_like(k_c)
+    seg_off = torch.empty(B * Hkv, dtype=torch.int64, device=DEV)
+    seg_len = torch.empty(B * Hkv, dtype=torch.int32, device=DEV)
+    cws = torch.empty(d.dkv_compact_workspace_bytes(lay), dtype=torch.uint8, device=DEV)
+    d.dkv_compact(lay, k.to(DEV), v.to(DEV), torch.from_numpy(mask).to(DEV), cap, k_c, v_c, seg_off,
+                  seg_len, cws)
+    if n_tail:
+        d.dkv_append(kt.reshape(B * Hkv, n_tail, dim).to(DEV), vt.reshape(B * Hkv, n_tail, dim).to(DEV), 0,
+                     cap, k_c, v_c, seg_off, seg_len)
+    d.dkv_append(kb.reshape(B * Hkv, n_q, dim).to(DEV), vb.reshape(B * Hkv, n_q, dim).to(DEV), n_tail, cap,
+                 k_c, v_c, seg_off, seg_len)
+    rows_hint = int(mask.sum()) + B * Hkv * (n_tail + n_q) if hint == "exact" else hint
+    wsb = d.dkv_query_workspace_bytes(B, Hq, Hkv, dim, n_q, rows_hint)
+    ws = torch.empty(wsb, dtype=torch.uint8, device=DEV) if wsb else None
+    out = torch.full((B, n_q, Hq, dim), float("nan"), dtype=torch.float32, device=DEV)
+    d.dkv_query_attn(q.to(DEV), n_tail, cap, k_c, v_c, seg_off, seg_len, sm_scale, out, ws, Hkv,
+                     rows_hint=rows_hint)
+    torch.cuda.synchronize()
+
+    # oracle on its own
+    ref = o.compact(bits(k), bits(v), mask, cap)
+    new_k = np.concatenate([bits(kt), bits(kb)], axis=2)
+    new_v = np.concatenate([bits(vt), bits(vb)], axis=2)
+    kc, vc = o.append(ref["k_c"], ref["v_c"], ref["seg_off"], ref["seg_len"], new_k, new_v, 0)
+    want = o.query_attn(bits(q), kc, vc, ref["seg_off"], ref["seg_len"], n_tail, sm_scale, Hkv, o.BF16)
+    return out.cpu().numpy(), want
+
+
+@pytest.mark.parametrize("dim", [64, 128])
+def test_query_random_shapes(d, dim):
+    rng = np.random.default_rng(700 + dim)
+    for trial in range(10):
+        B = int(rng.integers(1, 3))
+        Hkv = int(rng.choice([1, 2, 4]))
+        G = int(rng.choice([1, 2, 3, 4, 7, 8]))
+        T = int(rng.integers(1, 700))
+        n_q = int(rng.choice([1, 2, 5, 16, 17, 33]))
+        n_tail = int(rng.integers(0, 3))
+        got, want = _run(d, rng, B, Hkv, G, T, dim, float(rng.uniform(0.05, 0.9)), n_tail, n_q,
+                         cap=n_tail + n_q + int(rng.integers(0, 3)))
+        assert np.isfinite(got).all()
+        err = row_rel_err(got.reshape(-1, dim), want.reshape(-1, dim))
+        assert err <= ATTN_TOL, (trial, B, Hkv, G, T, n_q, n_tail, err)
+
+
+@pytest.mark.parametrize("G,n_q", [(1, 64), (4, 64), (4, 100), (7, 40), (8, 128)])
+def test_query_split_key_ranges(d, G, n_q):
+    """Long contexts: the keys are split into several ranges and combined."""
+    rng = np.random.default_rng(800 + G * 1000 + n_q)
+    got, want = _run(d, rng, 1, 2, G, 12000, 128, 0.4, 2, n_q)
+    err = row_rel_err(got.reshape(-1, 128), want.reshape(-1, 128))
+    assert err <= ATTN_TOL, err
+
+
+def test_query_unknown_rows_hint_and_empty_context(d):
+    """rows_hint 0 (split sized for long segments) with several segments that
+    hold no context at all: those rows see only the tokens after it."""
+    rng = np.random.default_rng(901)
+    got, want = _run(d, rng, 2, 2, 4, 3000, 128, 0.3, 1, 9, hint=0, empty_segments=2)
+    err = row_rel_err(got.reshape(-1, 128), want.reshape(-1, 128))
+    assert err <= ATTN_TOL, err
+
+
+def test_query_large_logits(d):
+    rng = np.random.default_rng(902)
+    got, want = _run(d, rng, 1, 2, 4, 2000, 128, 0.5, 0, 20, sm_scale=3.0)
+    assert np.isfinite(got).all()
+    assert row_rel_err(got.reshape(-1, 128), want.reshape(-1, 128)) <= ATTN_TOL
+
+
+def test_query_block_of_one_matches_decode_kernel(d):
+    """A one-token block is a decode step: both kernels agree with the oracle
+    and with each other within the tolerance."""
+    rng = np.random.default_rng(903)
+    B, Hkv, G, T, dim = 1, 4, 4, 5000, 128
+    got, want = _run(d, rng, B, Hkv, G, T, dim, 0.35, 0, 1)
+    assert row_rel_err(got.reshape(-1, dim), want.reshape(-1, dim)) <= ATTN_TOL
+
+
+def test_query_8b_layer_block_of_256(d):
+    """An 8B-shaped layer at 32K with a 256-token query block (the paper's
+    reserved query/answer length)."""
+    import dkv_inputs as di
+    w = di.workload("llama8b_layer_32k")
+    pattern, _ = di.make_pattern(w)
+    _, okm, _ = o.map_pattern(pattern, w.context_len, w.sink, w.recent, w.bin_edges, w.num_kv_heads)
+    rng = np.random.default_rng(904)
+    n_q = 256
+    Hkv, G, dim, T = w.num_kv_heads, w.group, w.head_dim, w.context_len
+    k, v = di.kv_unit(w, 0, device=DEV)
+    kb = _bf16(rng, (1, Hkv, n_q, dim))
+    vb = _bf16(rng, (1, Hkv, n_q, dim))
+    q = _bf16(rng, (1, n_q, Hkv * G, dim), 1.0 / np.sqrt(dim))
+    lay = d.make_layout(1, Hkv * G, Hkv, dim, T, 0, 0, [0, T])
+    rows = int(okm.sum()) + Hkv * n_q
+    k_c = torch.empty((rows, dim), dtype=torch.bfloat16, device=DEV)
+    v_c = torch.empty_like(k_c)
+    seg_off = torch.empty(Hkv, dtype=torch.int64, device=DEV)
+    seg_len = torch.empty(Hkv, dtype=torch.int32, device=DEV)
+    cws = torch.empty(d.dkv_compact_workspace_bytes(lay), dtype=torch.uint8, device=DEV)
+    d.dkv_compact(lay, k[None], v[None], torch.from_numpy(okm).to(DEV), n_q, k_c, v_c, seg_off, seg_len, cws)
+    d.dkv_append(kb[0].to(DEV), vb[0].to(DEV), 0, n_q, k_c, v_c, seg_off, seg_len)
+    wsb = d.dkv_query_workspace_bytes(1, Hkv * G, Hkv, dim, n_q, rows)
+    ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device=DEV)
+    out = torch.empty((1, n_q, Hkv * G, dim), dtype=torch.float32, device=DEV)
+    d.dkv_query_attn(q.to(DEV), 0, n_q, k_c, v_c, seg_off, seg_len, w.sm_scale, out, ws, Hkv, rows_hint=rows)
+    torch.cuda.synchronize()
+    ref = o.compact(bits(k[None]), bits(v[None]), okm, n_q)
+    kc, vc = o.append(ref["k_c"], ref["v_c"], ref["seg_off"], ref["seg_len"], bits(kb), bits(vb), 0)
+    want = o.query_attn(bits(q), kc, vc, ref["seg_off"], ref["seg_len"], 0, w.sm_scale, Hkv, o.BF16)
+    assert row_rel_err(out.cpu().numpy().reshape(-1, dim), want.reshape(-1, dim)) <= ATTN_TOL
