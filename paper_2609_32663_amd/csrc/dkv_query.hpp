@@ -8,7 +8,7 @@
 
 namespace dkv {
 
-constexpr int kQueryRowsPerWG = 64;   // query rows (tokens x heads of a group) per workgroup
+constexpr int kQueryRowsPerWG = 128;  // query rows (tokens x heads of a group) per workgroup
 constexpr int kQueryMaxSplit = 16;    // upper bound on key ranges per query tile
 
 struct QueryParams {

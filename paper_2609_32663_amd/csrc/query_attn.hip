@@ -6,7 +6,7 @@
 // R = n_q * G query rows; row r is token r / G of query head g * G + r % G
 // and sees the segment's first seg_len + n_tail + r / G + 1 rows (the packed
 // context, the tokens appended before the block, and the block causally up
-// to its own token).  A workgroup takes 64 query rows (16 per wave) of one
+// to its own token).  A workgroup takes 128 query rows (8 waves of 16) of one
 // segment and one of `nsplit` equal key ranges.  With one range it writes the
 // output; with several, each range writes (max, sum, unnormalised output)
 // per row and a combine kernel folds the ranges in order.
@@ -20,12 +20,15 @@
 //   * Online softmax per query row: max over the lane's 16 scores, then over
 //     the row's 4 lanes (permlane swaps); probabilities stay fp32 until the
 //     product.
-//   * O += P V with v_mfma_f32_16x16x16_bf16: the probabilities are the A
-//     operand exactly as the scores sit in the lanes, split into a bf16 high
-//     part and a bf16 remainder (two products, ~16 significant bits kept);
-//     the B operand (4 keys of one V column per lane) is gathered from
-//     row-major LDS with 16-bit reads, free of bank conflicts with a row
-//     stride of d + 4 elements.
+//   * O += P V with v_mfma_f32_16x16x32_bf16 per 32 keys: the probabilities
+//     are the A operand as the scores sit in the lanes (lane (query n, kg)
+//     holds keys 4kg..4kg+3 of two 16-key blocks: its eight K slots), split
+//     into a bf16 high part and a bf16 remainder (two products, ~16
+//     significant bits kept).  The B operand needs, per lane, the same eight
+//     keys of one V column; two ds_read_b64_tr_b16 transpose reads fetch them
+//     from the row-major V tile in LDS (within each 16-lane group, lanes
+//     4r..4r+3 address row r of a 4 x 16 block and lane i receives its column
+//     i).
 // Attention here is a dense contraction (G * n_q query rows against every
 // key), so it is MFMA work, unlike the one-query decode step.
 
@@ -38,17 +41,21 @@ namespace dkv {
 
 namespace {
 
-constexpr int kQThreads = 256;
+constexpr int kQThreads = 512;
 constexpr int kQRows = kQueryRowsPerWG;  // 16 query rows per wave
+constexpr int kQDepth = 2;               // register stages: key tiles whose global loads are in flight
 constexpr int kQKeys = 64;               // keys per tile
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 template <int D>
 struct QCfg {
   static constexpr int kRowBytes = D * 2;
   static constexpr int kKStride = D + 8;   // bf16 per K row in LDS (rows 16-byte aligned)
-  static constexpr int kVStride = D + 4;   // bf16 per V row in LDS (conflict-free column gathers)
+  static constexpr int kVStride = D + 16;  // bf16 per V row in LDS (16-byte rows, stride = 32 B mod 128)
   static constexpr int kChunks = D / 32;   // 16-byte chunks of a row per lane (QK)
   static constexpr int kBlocks = D / 16;   // 16-column output blocks per lane
   static constexpr int kRowChunks = D / 8; // 16-byte chunks per row
@@ -70,10 +77,14 @@ __device__ __forceinline__ int64_t q_uniform64(int64_t x) {
   return (int64_t)(((uint64_t)hi << 32) | lo);
 }
 
-// bf16 of x, rounded to nearest even (x finite).
-__device__ __forceinline__ uint32_t bf16_rne(float x) {
-  const uint32_t u = __float_as_uint(x);
-  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+// Two probabilities as a bf16 pair (round to nearest even) and the bf16 pair
+// of what that rounding left out: a + b carries ~16 significant bits.
+__device__ __forceinline__ void bf16_split(float x0, float x1, uint32_t& a, uint32_t& b) {
+  const f32x2 x = {x0, x1};
+  const bf16x2 h = __builtin_convertvector(x, bf16x2);
+  const bf16x2 l = __builtin_convertvector(x - __builtin_convertvector(h, f32x2), bf16x2);
+  a = __builtin_bit_cast(uint32_t, h);
+  b = __builtin_bit_cast(uint32_t, l);
 }
 
 // Maximum over the lanes that share (lane % 16).
@@ -87,19 +98,18 @@ __device__ __forceinline__ float row4_max(float x) {
 template <int D>
 __global__ __launch_bounds__(kQThreads) void query_attn_kernel(QueryParams p) {
   using C = QCfg<D>;
-  __shared__ __align__(16) uint16_t ks_lds[kQKeys * C::kKStride];
-  __shared__ __align__(16) uint16_t vs_lds[kQKeys * C::kVStride];
+  __shared__ __align__(16) uint16_t ks_lds[2][kQKeys * C::kKStride];
+  __shared__ __align__(16) uint16_t vs_lds[2][kQKeys * C::kVStride];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int n16 = lane & 15;
   const int kg = lane >> 4;
-  int x = blockIdx.x;
-  const int ks = x % p.nsplit;
-  x /= p.nsplit;
-  const int qt = x % p.qtiles;
-  const int s = x / p.qtiles;
+  const int slot = blockIdx.x;  // (segment, query tile, key range), range fastest
+  const int ks = slot % p.nsplit;
+  const int qt = (slot / p.nsplit) % p.qtiles;
+  const int s = slot / p.nsplit / p.qtiles;
   const int bseq = s / p.Hkv;
   const int g = s - bseq * p.Hkv;
   const int64_t base_len = q_uniform64((int64_t)p.seg_len[s] + p.n_tail);  // rows every query row sees
@@ -113,10 +123,13 @@ __global__ __launch_bounds__(kQThreads) void query_attn_kernel(QueryParams p) {
   // this workgroup's key range
   const int r_last = min(p.rows - 1, qt * kQRows + kQRows - 1);
   const int64_t lim_max = base_len + r_last / p.G + 1;
+  // (all workgroup-uniform; readfirstlane keeps them in scalar registers)
   const int64_t chunk = ((lim_max + p.nsplit - 1) / p.nsplit + kQKeys - 1) / kQKeys * kQKeys;
-  const int64_t k_lo = (int64_t)ks * chunk;
-  const int64_t k_hi = k_lo + chunk < lim_max ? k_lo + chunk : lim_max;
+  const int64_t k_lo = q_uniform64((int64_t)ks * chunk);
+  const int64_t k_hi = q_uniform64(k_lo + chunk < lim_max ? k_lo + chunk : lim_max);
   const int64_t cut = limit < k_hi ? limit : k_hi;  // keys [k_lo, cut) count for this row
+  // every row of the workgroup sees all keys below this one
+  const int64_t all_see = q_uniform64(base_len + 1 < k_hi ? base_len + 1 : k_hi);
 
   // B operand of QK: query row r, dims 32u + 8kg .. +7
   u32x4 qb[C::kChunks];
@@ -139,11 +152,16 @@ __global__ __launch_bounds__(kQThreads) void query_attn_kernel(QueryParams p) {
 
   const char* kbase = reinterpret_cast<const char*>(p.k) + row0 * C::kRowBytes;
   const char* vbase = reinterpret_cast<const char*>(p.v) + row0 * C::kRowBytes;
-  u32x4 kreg[C::kStage], vreg[C::kStage];
+  // A ring of kQDepth register stages: while one tile is computed, the
+  // global loads of the next kQDepth tiles are in flight.
+  u32x4 kreg[kQDepth][C::kStage], vreg[kQDepth][C::kStage];
   // Global -> registers for the tile at key kt: chunk c of the tile is key
-  // c / kRowChunks, bytes 16 * (c % kRowChunks); keys past k_hi read zeros.
-  auto load_stage = [&](int64_t kt) {
-    const uint32_t nk = (uint32_t)(k_hi - kt < kQKeys ? k_hi - kt : kQKeys);
+  // c / kRowChunks, bytes 16 * (c % kRowChunks).  Keys past k_hi (a whole
+  // tile past it included) read zeros without touching memory, so the loads
+  // can be issued unconditionally.
+  auto load_stage = [&](u32x4 (&kreg)[C::kStage], u32x4 (&vreg)[C::kStage], int64_t kt) {
+    const int64_t left = k_hi - kt;
+    const uint32_t nk = (uint32_t)(left <= 0 ? 0 : (left < kQKeys ? left : kQKeys));
     const __amdgpu_buffer_rsrc_t kr = q_rsrc(kbase + kt * C::kRowBytes, nk * C::kRowBytes);
     const __amdgpu_buffer_rsrc_t vr = q_rsrc(vbase + kt * C::kRowBytes, nk * C::kRowBytes);
 #pragma unroll
@@ -155,41 +173,40 @@ __global__ __launch_bounds__(kQThreads) void query_attn_kernel(QueryParams p) {
     }
   };
 
-  if (k_lo < k_hi) load_stage(k_lo);
-  for (int64_t kt = k_lo; kt < k_hi; kt += kQKeys) {
-    __syncthreads();  // every wave is done with the previous tile
-#pragma unroll
-    for (int i = 0; i < C::kStage; ++i) {
-      const int c = i * kQThreads + tid;
-      const int key = c / C::kRowChunks;
-      const int part = c % C::kRowChunks;
-      *reinterpret_cast<u32x4*>(&ks_lds[key * C::kKStride + part * 8]) = kreg[i];
-      uint2* vd = reinterpret_cast<uint2*>(&vs_lds[key * C::kVStride + part * 8]);
-      vd[0] = uint2{vreg[i][0], vreg[i][1]};
-      vd[1] = uint2{vreg[i][2], vreg[i][3]};
-    }
-    __syncthreads();
-    if (kt + kQKeys < k_hi) load_stage(kt + kQKeys);
-
-    // ---- scores S^T[key][query] of the 4 blocks of 16 keys ----------------
-    float sc[4][4];
+  // ---- scores S^T[key][query] of the tile at key kt (K in LDS at kb) --------
+  auto qk = [&](const uint16_t* kb, int64_t kt, float (&sc)[4][4]) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int u = 0; u < C::kChunks; ++u) {
-        const u32x4 a = *reinterpret_cast<const u32x4*>(&ks_lds[(16 * j + n16) * C::kKStride + 32 * u + 8 * kg]);
+        const u32x4 a = *reinterpret_cast<const u32x4*>(&kb[(16 * j + n16) * C::kKStride + 32 * u + 8 * kg]);
         acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, qb[u]),
                                                       acc, 0, 0, 0);
       }
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int64_t key = kt + 16 * j + 4 * kg + v;
-        sc[j][v] = key < cut ? acc[v] * p.scale_log2 : -INFINITY;
-      }
+      for (int v = 0; v < 4; ++v) sc[j][v] = acc[v];
+    }
+  };
+
+  // ---- softmax of the tile's scores and O += P V (V in LDS at vb) ---------
+  auto softmax_pv = [&](float (&sc)[4][4], const uint16_t* vb, int64_t kt) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) sc[j][v] *= p.scale_log2;
+    // keys past a row's causal limit or past the range: only in the tiles
+    // that reach min over rows of that limit
+    if (kt + kQKeys > all_see) {
+      const int64_t lim = cut - kt;  // keys [0, lim) of this tile count for the row
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          if (16 * j + 4 * kg + v >= lim) sc[j][v] = -INFINITY;
     }
 
-    // ---- online softmax of row n16 -----------------------------------------
+    // online softmax of row n16
     float mx = sc[0][0];
 #pragma unroll
     for (int j = 0; j < 4; ++j)
@@ -210,39 +227,95 @@ __global__ __launch_bounds__(kQThreads) void query_attn_kernel(QueryParams p) {
     l = l * alpha + ps;
     m = m_new;
     // output rows of this lane are queries 4kg + v: their factors live in
-    // the lanes of those rows
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const float av = __shfl(alpha, 4 * kg + v, 64);
-#pragma unroll
-      for (int b = 0; b < C::kBlocks; ++b) o[b][v] *= av;
-    }
-
-    // ---- O += P V ------------------------------------------------------------
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      uint32_t hi[4], lo[4];
+    // the lanes of those rows.  Once the maxima settle every factor is 1 and
+    // the wave skips the rescale.
+    if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        hi[v] = bf16_rne(sc[j][v]);
-        lo[v] = bf16_rne(sc[j][v] - __uint_as_float(hi[v] << 16));
+        const float av = __shfl(alpha, 4 * kg + v, 64);
+#pragma unroll
+        for (int b = 0; b < C::kBlocks; ++b) o[b][v] *= av;
       }
-      const s16x4 ph = {(short)hi[0], (short)hi[1], (short)hi[2], (short)hi[3]};
-      const s16x4 pl = {(short)lo[0], (short)lo[1], (short)lo[2], (short)lo[3]};
-      const uint16_t* vrow = &vs_lds[(16 * j + 4 * kg) * C::kVStride + n16];
+    }
+
+    // O += P V, 32 keys per product.  K slot e of lane group kg is key
+    // 32h + 4kg + e (e < 4) or 32h + 16 + 4kg + (e - 4): the lane's scores of
+    // blocks 2h and 2h + 1.
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      u32x4 ph, pl;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        uint32_t a, b;
+        bf16_split(sc[2 * h + (e >> 1)][2 * (e & 1)], sc[2 * h + (e >> 1)][2 * (e & 1) + 1], a, b);
+        ph[e] = a;
+        pl[e] = b;
+      }
+      // transpose-read addresses: lane 4r + q of group kg reads row
+      // 32h + 4kg + r (and the row 16 below), columns 16b + 4q .. +3
+      const uint16_t* v0 = &vb[(32 * h + 4 * kg + (n16 >> 2)) * C::kVStride + 4 * (n16 & 3)];
 #pragma unroll
       for (int b = 0; b < C::kBlocks; ++b) {
-        const s16x4 vb = {(short)vrow[16 * b], (short)vrow[C::kVStride + 16 * b],
-                          (short)vrow[2 * C::kVStride + 16 * b], (short)vrow[3 * C::kVStride + 16 * b]};
-        o[b] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ph, vb, o[b], 0, 0, 0);
-        o[b] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pl, vb, o[b], 0, 0, 0);
+        const s16x4 t0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(v0 + 16 * b));
+        const s16x4 t1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(v0 + 16 * C::kVStride + 16 * b));
+        const uint2 w0 = __builtin_bit_cast(uint2, t0);
+        const uint2 w1 = __builtin_bit_cast(uint2, t1);
+        const u32x4 vbo = {w0.x, w0.y, w1.x, w1.y};
+        o[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ph), __builtin_bit_cast(bf16x8, vbo),
+                                                       o[b], 0, 0, 0);
+        o[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, pl), __builtin_bit_cast(bf16x8, vbo),
+                                                       o[b], 0, 0, 0);
       }
+    }
+  };
+
+  auto store_tile = [&](const u32x4 (&kr)[C::kStage], const u32x4 (&vr)[C::kStage], uint16_t* kb, uint16_t* vb) {
+#pragma unroll
+    for (int c0 = 0; c0 < C::kStage; ++c0) {
+      const int c = c0 * kQThreads + tid;
+      const int key = c / C::kRowChunks;
+      const int part = c % C::kRowChunks;
+      *reinterpret_cast<u32x4*>(&kb[key * C::kKStride + part * 8]) = kr[c0];
+      *reinterpret_cast<u32x4*>(&vb[key * C::kVStride + part * 8]) = vr[c0];
+    }
+  };
+
+  // Software pipeline over key tiles.  Tile t sits in LDS buffer t % 2; the
+  // global loads of tiles t + 1 and t + 2 are in flight in the two register
+  // stages.  Iteration t stores tile t + 1 into the other buffer, issues the
+  // score products of tile t + 1 and then does the softmax and P V of tile t,
+  // so the matrix unit works on tile t + 1 while the vector unit works on
+  // tile t.  Loads are issued in ring order (scheduling barriers keep them
+  // there), so every store waits only for its own stage.  Tiles past k_hi
+  // hold zeros and all their keys are masked, so they change nothing.
+  load_stage(kreg[0], vreg[0], k_lo);
+  __builtin_amdgcn_sched_barrier(0);
+  load_stage(kreg[1], vreg[1], k_lo + kQKeys);
+  __builtin_amdgcn_sched_barrier(0);
+  store_tile(kreg[0], vreg[0], ks_lds[0], vs_lds[0]);
+  __syncthreads();
+  load_stage(kreg[0], vreg[0], k_lo + 2 * kQKeys);
+  float sc[2][4][4];
+  qk(ks_lds[0], k_lo, sc[0]);
+  const int64_t ntile = k_hi > k_lo ? (k_hi - k_lo + kQKeys - 1) / kQKeys : 0;
+  const int64_t nround = q_uniform64((ntile + 1) / 2);
+  int64_t kt = k_lo;
+  for (int64_t rd = 0; rd < nround; ++rd) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      __syncthreads();  // every wave is done with tile t - 1 (buffer 1 - i)
+      store_tile(kreg[1 - i], vreg[1 - i], ks_lds[1 - i], vs_lds[1 - i]);
+      __syncthreads();
+      load_stage(kreg[1 - i], vreg[1 - i], kt + 3 * kQKeys);
+      qk(ks_lds[1 - i], kt + kQKeys, sc[1 - i]);
+      softmax_pv(sc[i], vs_lds[i], kt);
+      kt += kQKeys;
     }
   }
 
   // ---- row totals; write the output or this range's record ------------------
   l = lane_xor_sum<16>(l);
-  float* rec = p.rec + (int64_t)blockIdx.x * kQRows * C::kRec;
+  float* rec = p.rec + (int64_t)slot * kQRows * C::kRec;
 #pragma unroll
   for (int v = 0; v < 4; ++v) {
     const int rr = wave * 16 + 4 * kg + v;  // row within the tile
