@@ -31,6 +31,8 @@ if ROOT not in sys.path:
 METRIC = "compacted-KV decode attn: HBM GB/s + µs/step vs dense decode, 8B-shape @128K"
 WORKLOAD = "llama8b_stack_128k"
 PEAK_HBM_GBPS = 8000.0
+PEAK_BF16_TFLOPS = 2500.0  # dense bf16 matrix peak
+QUERY_TOKENS = 256
 PMC_FILE = os.path.join(ROOT, "profiles", "decode_attn_llama8b_stack_128k_pmc.json")
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2609_32663_amd", "csrc", f)
                for f in ("decode_attn.hip", "dkv_device.hpp", "dkv_launch.hpp")]
@@ -244,6 +246,26 @@ def main():
     phys_frac = retained / float(N * Hkv * T)
     log(f"map {map_us:.0f} us, compact {compact_us:.0f} us, retained {phys_frac:.4f}")
 
+    # ---------------- query block: a second pack with room for it ----------
+    # The tokens after the context (the paper reserves 256 for query and
+    # answer) are appended to every segment and attend to the packed context
+    # and causally to themselves.
+    NQ = QUERY_TOKENS
+    rows_q = int((lens + NQ).sum())
+    k_q = torch.empty((rows_q, dim), dtype=torch.bfloat16, device=dev)
+    v_q = torch.empty_like(k_q)
+    seg_off_q = torch.empty(N * Hkv, dtype=torch.int64, device=dev)
+    seg_len_q = torch.empty(N * Hkv, dtype=torch.int32, device=dev)
+    d.dkv_compact(lay, k, v, kv_mask, NQ, k_q, v_q, seg_off_q, seg_len_q, cws)
+    q_blocks = []
+    for layer in range(L):
+        qb, kb, vb = di.query_block(w, layer, NQ, device=dev)
+        segs = slice(layer * nseg_layer, (layer + 1) * nseg_layer)
+        d.dkv_append(kb.reshape(nseg_layer, NQ, dim).contiguous(), vb.reshape(nseg_layer, NQ, dim).contiguous(),
+                     0, NQ, k_q, v_q, seg_off_q[segs], seg_len_q[segs])
+        q_blocks.append(qb.contiguous())
+    torch.cuda.synchronize()
+
     # ---------------- CPU oracle baseline + parity sample (layer 0) --------
     cpu = None
     parity = None
@@ -268,6 +290,8 @@ def main():
             vb = v[units].cpu().view(torch.int16).numpy().view(np.uint16)
             qb = q_layers[layer].cpu().view(torch.int16).numpy().view(np.uint16)
             _, okm, _ = o.map_pattern(pattern[units], T, w.sink, w.recent, w.bin_edges, Hkv)
+            if layer == 0:  # kept for the query-block oracle sample
+                k0_bits, v0_bits, okm0 = kb, vb, okm
             ref = o.compact(kb, vb, okm, cap)
             with threadpool_limits(1):
                 t0 = time.perf_counter()
@@ -400,6 +424,80 @@ def main():
     launch_ms = ms / L
     dlaunch_ms = dms / L
 
+    # ---------------- query-block attention, all layers ------------------
+    log("timing query-block attention")
+    q_hints = [layer_rows[layer] + nseg_layer * NQ for layer in range(L)]
+    q_wsb = max(d.dkv_query_workspace_bytes(B, Hq, Hkv, dim, NQ, h) for h in q_hints)
+    q_ws = torch.empty(max(q_wsb, 16), dtype=torch.uint8, device=dev)
+    q_out = torch.empty((B, NQ, Hq, dim), dtype=torch.float32, device=dev)
+
+    def query_call(layer, shp):
+        off = layer * nseg_layer
+        st_ = lib.dkv_query_attn(d.DKV_BF16, B, Hq, Hkv, dim, NQ, P(q_blocks[layer].data_ptr()), 0, NQ,
+                                 P(k_q.data_ptr()), P(v_q.data_ptr()), P(seg_off_q.data_ptr() + 8 * off),
+                                 P(seg_len_q.data_ptr() + 4 * off), w.sm_scale, q_hints[layer],
+                                 P(q_out.data_ptr()), P(q_ws.data_ptr()), q_ws.numel(), P(shp))
+        if st_ != 0:
+            raise d.DkvError("dkv_query_attn", st_)
+
+    for layer in range(L):
+        query_call(layer, sh)
+    torch.cuda.synchronize()
+    gq = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(gq, stream=cap_stream):
+        for layer in range(L):
+            query_call(layer, cap_stream.cuda_stream)
+    for _ in range(args.warmup):
+        gq.replay()
+    torch.cuda.synchronize()
+    a, b = ev(), ev()
+    a.record(stream)
+    for _ in range(args.steps):
+        gq.replay()
+    b.record(stream)
+    torch.cuda.synchronize()
+    q_ms = a.elapsed_time(b) / args.steps
+    # algorithmic flops: 4 d per visible (query row, key) pair; query token i
+    # of a segment with n retained rows sees n + i + 1 keys, for G heads
+    lens_np = lens.numpy().reshape(L, nseg_layer)
+    q_flops = float(sum(4.0 * dim * w.group * (NQ * lens_np[layer].sum() + nseg_layer * NQ * (NQ + 1) / 2)
+                        for layer in range(L)))
+    q_tflops = q_flops / (q_ms * 1e-3) / 1e12
+    query_res = {"n_q": NQ, "ms_per_step": round(q_ms, 4), "us_per_layer": round(q_ms * 1e3 / L, 1),
+                 "tflop_per_step": round(q_flops / 1e12, 3),
+                 "roofline": {"bound": "mfma", "achieved": round(q_tflops, 1), "peak": PEAK_BF16_TFLOPS,
+                              "unit": "TFLOP/s", "frac": round(q_tflops / PEAK_BF16_TFLOPS, 4),
+                              "traffic": None,
+                              "kernel": "dkv_query_attn call: query_attn_kernel<128> + query_merge_kernel"},
+                 "cpu_baseline": None, "parity_layer0": None}
+    if not args.no_cpu_baseline:
+        import oracle as o
+        from threadpoolctl import threadpool_limits
+        nqs = 32  # oracle sample: the block's first 32 tokens of layer 0
+        qb0, kb0, vb0 = di.query_block(w, 0, NQ, device=dev)
+        query_call(0, sh)
+        torch.cuda.synchronize()
+        got = q_out[:, :nqs].cpu().numpy()
+        ref = o.compact(k0_bits, v0_bits, okm0, NQ)
+        kc, vc = o.append(ref["k_c"], ref["v_c"], ref["seg_off"], ref["seg_len"],
+                          kb0.cpu().view(torch.int16).numpy().view(np.uint16),
+                          vb0.cpu().view(torch.int16).numpy().view(np.uint16), 0)
+        qs = qb0[:, :nqs].contiguous().cpu().view(torch.int16).numpy().view(np.uint16)
+        with threadpool_limits(1):
+            t0 = time.perf_counter()
+            want = o.query_attn(qs, kc, vc, ref["seg_off"], ref["seg_len"], 0, w.sm_scale, Hkv, o.BF16)
+            cpu_q = time.perf_counter() - t0
+        flops_s = 4.0 * dim * w.group * (nqs * lens_np[0].sum() + nseg_layer * nqs * (nqs + 1) / 2)
+        err = float((np.abs(got - want).max(-1) / np.maximum(np.abs(want).max(-1), 1e-30)).max())
+        query_res["cpu_baseline"] = {"value": round(flops_s / cpu_q / 1e9, 3), "unit": "GFLOP/s", "cores": 1,
+                                     "kind": "oracle",
+                                     "sample": f"the first {nqs} of the {NQ} block tokens of layer 0 by the fp64 "
+                                               f"NumPy oracle with 1 BLAS thread: {cpu_q:.2f} s for "
+                                               f"{flops_s / 1e9:.1f} GFLOP"}
+        query_res["parity_layer0"] = {"tokens": nqs, "max_rel_err": err}
+        log(f"query oracle {cpu_q:.2f} s, parity err {err:.2e}")
+    log(f"query block {q_ms * 1e3 / L:.1f} us/layer, {q_tflops:.1f} TFLOP/s")
+
     # ---------------- achievable read bandwidth at this launch size -------
     # The streaming-read probe (same 16-byte non-temporal buffer loads as the
     # decode kernel's K/V stream) over L slices of one decode launch's size,
@@ -481,6 +579,7 @@ def main():
                      "bytes_per_launch": int(per_launch_bytes)},
         "cpu_baseline": cpu,
         "achievable_read": achievable,
+        "query_block": query_res,
         "us_per_step": round(ms * 1e3, 1),
         "dense": {"ms_per_step": round(dms, 4), "eager_ms_per_step": round(deager_ms, 4),
                   "gb_per_s": round(dbytes / (dms * 1e-3) / 1e9, 2),

@@ -43,10 +43,12 @@ __all__ = [
     "kv_unit",
     "q_step",
     "kv_new_step",
+    "query_block",
 ]
 
 # stream ids of the seed derivation
 STREAM_PATTERN, STREAM_K, STREAM_V, STREAM_Q, STREAM_NEW_K, STREAM_NEW_V = range(6)
+STREAM_BLOCK_Q, STREAM_BLOCK_K, STREAM_BLOCK_V = 6, 7, 8
 
 
 def seed_of(*parts):
@@ -340,3 +342,16 @@ def kv_new_step(w, layer, step, n_new=1, device="cpu"):
     k = _randn(shape, seed_of(w.cfg_id, layer, STREAM_NEW_K, step), device, 1.0, dt)
     v = _randn(shape, seed_of(w.cfg_id, layer, STREAM_NEW_V, step), device, 1.0, dt)
     return k, v
+
+
+def query_block(w, layer, n_q, device="cpu"):
+    """The n_q query tokens after the context (the question), one layer:
+    q [B][n_q][Hq][d] ~ N(0, q_std^2), token-major, and the block's own
+    K, V [B][Hkv][n_q][d] ~ N(0, 1), which are appended to the cache."""
+    dt = _torch_dtype(w)
+    q = _randn((w.batch, n_q, w.num_q_heads, w.head_dim), seed_of(w.cfg_id, layer, STREAM_BLOCK_Q, n_q),
+               device, w.q_std, dt)
+    shape = (w.batch, w.num_kv_heads, n_q, w.head_dim)
+    k = _randn(shape, seed_of(w.cfg_id, layer, STREAM_BLOCK_K, n_q), device, 1.0, dt)
+    v = _randn(shape, seed_of(w.cfg_id, layer, STREAM_BLOCK_V, n_q), device, 1.0, dt)
+    return q, k, v
