@@ -162,3 +162,57 @@ def test_query_8b_layer_block_of_256(d):
     kc, vc = o.append(ref["k_c"], ref["v_c"], ref["seg_off"], ref["seg_len"], bits(kb), bits(vb), 0)
     want = o.query_attn(bits(q), kc, vc, ref["seg_off"], ref["seg_len"], 0, w.sm_scale, Hkv, o.BF16)
     assert row_rel_err(out.cpu().numpy().reshape(-1, dim), want.reshape(-1, dim)) <= ATTN_TOL
+
+
+def test_multi_turn_reuse_of_one_pack(d):
+    """Several query rounds over one compacted cache (the shared-context
+    multi-turn setting of Sec. 4.2: one fixed pattern and one compression
+    serve successive queries).  Each turn appends its query block
+    from n_tail = 0, overwriting the previous turn's tokens, attends with the
+    block, then decodes a few tokens appended after the block; every call is
+    checked against the oracle, which repeats the same bookkeeping."""
+    rng = np.random.default_rng(905)
+    B, Hkv, G, T, dim = 2, 2, 4, 3000, 128
+    Hq = Hkv * G
+    turns = [(12, 3), (5, 2), (20, 4)]  # (block tokens, decode steps) per turn
+    cap = max(n_q + steps for n_q, steps in turns)
+    k = _bf16(rng, (B, Hkv, T, dim))
+    v = _bf16(rng, (B, Hkv, T, dim))
+    mask = (rng.uniform(size=(B, Hkv, T)) < 0.3).astype(np.uint8)
+    lay = d.make_layout(B, Hq, Hkv, dim, T, 0, 0, [0, T])
+    rows = int(mask.sum()) + B * Hkv * cap
+    k_c = torch.empty((rows, dim), dtype=torch.bfloat16, device=DEV)
+    v_c = torch.empty_like(k_c)
+    seg_off = torch.empty(B * Hkv, dtype=torch.int64, device=DEV)
+    seg_len = torch.empty(B * Hkv, dtype=torch.int32, device=DEV)
+    cws = torch.empty(d.dkv_compact_workspace_bytes(lay), dtype=torch.uint8, device=DEV)
+    d.dkv_compact(lay, k.to(DEV), v.to(DEV), torch.from_numpy(mask).to(DEV), cap, k_c, v_c, seg_off, seg_len, cws)
+    ref = o.compact(bits(k), bits(v), mask, cap)
+    dws = torch.zeros(d.dkv_decode_workspace_bytes(B, Hq, Hkv, dim), dtype=torch.uint8, device=DEV)
+    for turn, (n_q, steps) in enumerate(turns):
+        kb = _bf16(rng, (B, Hkv, n_q, dim))
+        vb = _bf16(rng, (B, Hkv, n_q, dim))
+        q = _bf16(rng, (B, n_q, Hq, dim), 1.0 / np.sqrt(dim))
+        d.dkv_append(kb.reshape(B * Hkv, n_q, dim).to(DEV), vb.reshape(B * Hkv, n_q, dim).to(DEV), 0, cap, k_c,
+                     v_c, seg_off, seg_len)
+        kc_t, vc_t = o.append(ref["k_c"], ref["v_c"], ref["seg_off"], ref["seg_len"], bits(kb), bits(vb), 0)
+        wsb = d.dkv_query_workspace_bytes(B, Hq, Hkv, dim, n_q, 0)
+        ws = torch.empty(wsb, dtype=torch.uint8, device=DEV) if wsb else None
+        out = torch.empty((B, n_q, Hq, dim), dtype=torch.float32, device=DEV)
+        d.dkv_query_attn(q.to(DEV), 0, cap, k_c, v_c, seg_off, seg_len, 1.0, out, ws, Hkv)
+        torch.cuda.synchronize()
+        want = o.query_attn(bits(q), kc_t, vc_t, ref["seg_off"], ref["seg_len"], 0, 1.0, Hkv, o.BF16)
+        assert row_rel_err(out.cpu().numpy().reshape(-1, dim), want.reshape(-1, dim)) <= ATTN_TOL, (turn, "query")
+        for step in range(steps):
+            kn = _bf16(rng, (B * Hkv, 1, dim))
+            vn = _bf16(rng, (B * Hkv, 1, dim))
+            qd = _bf16(rng, (B, Hq, dim), 1.0 / np.sqrt(dim))
+            od = torch.empty((B, Hq, dim), dtype=torch.float32, device=DEV)
+            d.dkv_append_decode_attn(qd.to(DEV), kn.to(DEV), vn.to(DEV), n_q + step, cap, k_c, v_c, seg_off,
+                                     seg_len, 1.0, od, dws, Hkv)
+            torch.cuda.synchronize()
+            kc_t, vc_t = o.append(kc_t, vc_t, ref["seg_off"], ref["seg_len"], bits(kn).reshape(B, Hkv, 1, dim),
+                                  bits(vn).reshape(B, Hkv, 1, dim), n_q + step)
+            want = o.decode_attn(bits(qd), kc_t, vc_t, ref["seg_off"], ref["seg_len"], n_q + step + 1, 1.0, Hkv,
+                                 o.BF16)
+            assert row_rel_err(od.cpu().numpy(), want) <= ATTN_TOL, (turn, step)
