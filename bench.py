@@ -87,6 +87,7 @@ def pmc_per_dispatch(path, counter):
 
 
 TRACE_FILE = os.path.join(ROOT, "profiles", "decode_attn_llama8b_stack_128k.txt")
+QUERY_TRACE_FILE = os.path.join(ROOT, "profiles", "query_attn_llama8b_stack_128k.txt")
 
 
 def trace_summary(trace_dir, bench_log, command):
@@ -138,6 +139,39 @@ def trace_summary(trace_dir, bench_log, command):
     with open(TRACE_FILE, "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
+
+    # query-block attention: attention kernel (+ combine) per layer call
+    qpairs = []
+    for i, r in enumerate(rows):
+        if "query_attn_kernel" in r["Kernel_Name"]:
+            s0, e0 = int(r["Start_Timestamp"]), int(r["End_Timestamp"])
+            e1 = e0
+            if i + 1 < len(rows) and "query_merge_kernel" in rows[i + 1]["Kernel_Name"]:
+                e1 = int(rows[i + 1]["End_Timestamp"])
+            qpairs.append(((e0 - s0) / 1e3, (e1 - e0) / 1e3, (e1 - s0) / 1e3))
+    if qpairs and b.get("query_block"):
+        qb = b["query_block"]
+        ql = [f"# rocprofv3 kernel trace of bench.py, query-block attention ({WORKLOAD}: {qb['n_q']} tokens after "
+              f"the context, every layer)",
+              f"# command: {command}",
+              "# per-kernel statistics (rocprofv3 --stats; us):",
+              f"{'kernel':58s} {'calls':>6s} {'avg':>9s} {'min':>9s} {'max':>9s}"]
+        for r in stats:
+            if "query" in r["Name"]:
+                nm = r["Name"].replace("(anonymous namespace)::", "").replace("dkv::", "")
+                ql.append(f"{nm[:58]:58s} {r['Calls']:>6s} {float(r['AverageNs']) / 1e3:9.2f} "
+                          f"{float(r['MinNs']) / 1e3:9.2f} {float(r['MaxNs']) / 1e3:9.2f}")
+        ql += [f"calls {len(qpairs)}: query_attn_kernel mean {st.mean(x[0] for x in qpairs):8.2f}  "
+               f"combine (end to end) mean {st.mean(x[1] for x in qpairs):6.2f}  call mean "
+               f"{st.mean(x[2] for x in qpairs):8.2f} us",
+               "",
+               "# JSON line of the same run (timed region = HIP-graph replays; the profiler adds overhead):",
+               f"query_block us_per_layer {qb['us_per_layer']}  roofline {json.dumps(qb['roofline'])}",
+               f"cpu_baseline {json.dumps(qb['cpu_baseline'])}",
+               f"parity_layer0 {json.dumps(qb['parity_layer0'])}"]
+        with open(QUERY_TRACE_FILE, "w") as f:
+            f.write("\n".join(ql) + "\n")
+        print("\n".join(ql))
 
 
 def pmc_summary(fetch_csv, write_csv, command):

@@ -342,50 +342,71 @@ __global__ __launch_bounds__(kQThreads) void query_attn_kernel(QueryParams p) {
   }
 }
 
-// Combine kernel: one workgroup per (segment, query tile); thread items are
-// (row, 4 columns); the nsplit records of a row are folded in range order:
+// Combine kernel: thread item (row, 4 columns) of one (segment, query tile);
+// kMergeThreads items per workgroup.  A thread loads the row's max and sum
+// and its 4 columns from every key range at once (one memory round trip),
+// then folds the ranges in order:
 //   M = max_k m_k,  out = sum_k 2^(m_k - M) o_k / sum_k 2^(m_k - M) l_k.
+constexpr int kMergeThreads = 256;
+
 template <int D>
-__global__ __launch_bounds__(kQThreads) void query_merge_kernel(QueryParams p) {
+__global__ __launch_bounds__(kMergeThreads) void query_merge_kernel(QueryParams p) {
   using C = QCfg<D>;
-  const int s = blockIdx.x / p.qtiles;
-  const int qt = blockIdx.x - s * p.qtiles;
+  constexpr int kItems = kQRows * (D / 4);                 // items per query tile
+  constexpr int kParts = kItems / kMergeThreads;           // workgroups per query tile
+  const int tile = blockIdx.x / kParts;                    // s * qtiles + qt
+  const int item = (blockIdx.x - tile * kParts) * kMergeThreads + threadIdx.x;
+  const int s = tile / p.qtiles;
+  const int qt = tile - s * p.qtiles;
+  const int rr = item / (D / 4);
+  const int c4 = item - rr * (D / 4);
+  const int rq = qt * kQRows + rr;
+  if (rq >= p.rows) return;
   const int bseq = s / p.Hkv;
   const int g = s - bseq * p.Hkv;
-  const float* recs = p.rec + (int64_t)blockIdx.x * p.nsplit * kQRows * C::kRec;
-  for (int idx = threadIdx.x; idx < kQRows * (D / 4); idx += kQThreads) {
-    const int rr = idx / (D / 4);
-    const int c4 = idx - rr * (D / 4);
-    const int rq = qt * kQRows + rr;
-    if (rq >= p.rows) continue;
-    float M = -INFINITY;
-    for (int k = 0; k < p.nsplit; ++k) M = fmaxf(M, recs[((int64_t)k * kQRows + rr) * C::kRec]);
-    const float Mu = M == -INFINITY ? 0.f : M;
-    float L = 0.f;
-    f32x4 A = {0.f, 0.f, 0.f, 0.f};
-    for (int k = 0; k < p.nsplit; ++k) {
-      const float* rrow = recs + ((int64_t)k * kQRows + rr) * C::kRec;
-      const float f = fast_exp2(rrow[0] - Mu);
-      L += f * rrow[1];
-      const float* a = rrow + 2 + 4 * c4;
-      A[0] += f * a[0];
-      A[1] += f * a[1];
-      A[2] += f * a[2];
-      A[3] += f * a[3];
+  const float* recs = p.rec + (int64_t)tile * p.nsplit * kQRows * C::kRec + (int64_t)rr * C::kRec;
+  float mk[kQueryMaxSplit], lk[kQueryMaxSplit];
+  f32x4 ak[kQueryMaxSplit];
+#pragma unroll
+  for (int k = 0; k < kQueryMaxSplit; ++k) {
+    if (k < p.nsplit) {
+      const float* r = recs + (int64_t)k * kQRows * C::kRec;
+      mk[k] = r[0];
+      lk[k] = r[1];
+      ak[k] = *reinterpret_cast<const f32x4*>(r + 2 + 4 * c4);
+    } else {
+      mk[k] = -INFINITY;
+      lk[k] = 0.f;
+      ak[k] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-    const float inv = L > 0.f ? 1.f / L : 0.f;
-    const int tq = rq / p.G;
-    float* orow = p.out + (((int64_t)bseq * p.n_q + tq) * p.Hq + (int64_t)g * p.G + (rq - tq * p.G)) * D;
-    *reinterpret_cast<f32x4*>(orow + 4 * c4) = A * inv;
   }
+  float M = -INFINITY;
+#pragma unroll
+  for (int k = 0; k < kQueryMaxSplit; ++k) M = fmaxf(M, mk[k]);
+  const float Mu = M == -INFINITY ? 0.f : M;
+  float L = 0.f;
+  f32x4 A = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int k = 0; k < kQueryMaxSplit; ++k) {
+    const float f = fast_exp2(mk[k] - Mu);
+    L += f * lk[k];
+    A += f * ak[k];
+  }
+  const float inv = L > 0.f ? 1.f / L : 0.f;
+  const int tq = rq / p.G;
+  float* orow = p.out + (((int64_t)bseq * p.n_q + tq) * p.Hq + (int64_t)g * p.G + (rq - tq * p.G)) * D;
+  *reinterpret_cast<f32x4*>(orow + 4 * c4) = A * inv;
 }
 
 template <int D>
 hipError_t launch_d(const QueryParams& p, hipStream_t stream) {
   const int64_t wgs = (int64_t)p.nseg * p.qtiles * p.nsplit;
   hipLaunchKernelGGL((query_attn_kernel<D>), dim3((unsigned)wgs), dim3(kQThreads), 0, stream, p);
-  if (p.nsplit > 1)
-    hipLaunchKernelGGL((query_merge_kernel<D>), dim3((unsigned)(p.nseg * p.qtiles)), dim3(kQThreads), 0, stream, p);
+  if (p.nsplit > 1) {
+    const int64_t parts = (int64_t)kQRows * (D / 4) / kMergeThreads;
+    hipLaunchKernelGGL((query_merge_kernel<D>), dim3((unsigned)(p.nseg * p.qtiles * parts)), dim3(kMergeThreads), 0,
+                       stream, p);
+  }
   return hipGetLastError();
 }
 
