@@ -44,11 +44,14 @@ __all__ = [
     "q_step",
     "kv_new_step",
     "query_block",
+    "page_table",
+    "fill_pages",
 ]
 
 # stream ids of the seed derivation
 STREAM_PATTERN, STREAM_K, STREAM_V, STREAM_Q, STREAM_NEW_K, STREAM_NEW_V = range(6)
 STREAM_BLOCK_Q, STREAM_BLOCK_K, STREAM_BLOCK_V = 6, 7, 8
+STREAM_PAGES = 9
 
 
 def seed_of(*parts):
@@ -355,3 +358,43 @@ def query_block(w, layer, n_q, device="cpu"):
     k = _randn(shape, seed_of(w.cfg_id, layer, STREAM_BLOCK_K, n_q), device, 1.0, dt)
     v = _randn(shape, seed_of(w.cfg_id, layer, STREAM_BLOCK_V, n_q), device, 1.0, dt)
     return q, k, v
+
+
+# ---------------------------------------------------------------------------
+# paged caches (the layout a page allocator leaves behind after prefill)
+# ---------------------------------------------------------------------------
+
+def page_table(num_segments, pages_per_segment, seed, spare=0):
+    """Physical page of every (segment, logical page): the first
+    num_segments * pages_per_segment values of a seeded permutation of
+    range(num_pages), num_pages = that product + spare, as an allocator that
+    hands out pages in no particular order would leave them.
+    Returns (int32 [num_segments][pages_per_segment], num_pages)."""
+    n = num_segments * pages_per_segment
+    num_pages = n + int(spare)
+    perm = np.random.default_rng(seed_of(STREAM_PAGES, seed)).permutation(num_pages)[:n]
+    return perm.reshape(num_segments, pages_per_segment).astype(np.int32), num_pages
+
+
+def fill_pages(pool, x, table, page_rows):
+    """Store dense per-segment rows in their pages: page table[s][p] of `pool`
+    ([num_pages][page_rows][...], numpy or torch) receives rows
+    [p * page_rows, (p + 1) * page_rows) of x[s] (x: [n][rows][...], n =
+    len(table)); slots past the end of x's rows are left as they are."""
+    table = np.asarray(table)
+    n, rows = x.shape[0], x.shape[1]
+    full = min(rows // page_rows, table.shape[1])
+    rest = tuple(x.shape[2:])
+    is_torch = not isinstance(pool, np.ndarray)
+    if full > 0:
+        idx = table[:, :full].reshape(-1)
+        src = x[:, :full * page_rows].reshape((n * full, page_rows) + rest)
+        if is_torch:
+            import torch
+            pool[torch.as_tensor(idx, dtype=torch.long, device=pool.device)] = src
+        else:
+            pool[idx] = src
+    r0 = full * page_rows
+    if r0 < rows and full < table.shape[1]:
+        for s in range(n):
+            pool[int(table[s, full]), :rows - r0] = x[s, r0:rows]

@@ -22,7 +22,13 @@ What it computes (Distance-KV, Sec. 3.4 "Static-Pattern Inference"):
 * decode attention over the packed cache.  Attention restricted to a fixed
   retained set is exactly dense attention with every other position masked to
   -inf, so the oracle writes out that plain definition twice, once over the
-  packed rows and once over the dense cache with a mask.
+  packed rows and once over the dense cache with a mask;
+* the zero-copy alternative to the pack: the retained set of a segment is a
+  union of contiguous distance bins plus the sink and the recent window
+  (Eq. (4), Eq. (5), union of Sec. 3.4), so in a cache kept in fixed pages of
+  consecutive positions it can be listed in place as runs within pages, and
+  decode can read those rows where they are.  The oracle lists the runs from
+  their definition and attends to exactly the rows they name.
 
 Everything is plain NumPy in float64; bf16 inputs are carried as their uint16
 bit patterns and widened exactly.  Loops are over segments and heads only, so
@@ -66,6 +72,10 @@ __all__ = [
     "dense_decode_attn",
     "query_attn",
     "masked_dense_attn",
+    "PAGE_ENTRY_FIELDS",
+    "page_select",
+    "paged_append",
+    "paged_decode_attn",
 ]
 
 BF16 = "bf16"
@@ -380,4 +390,118 @@ def masked_dense_attn(q, k, v, kv_mask, k_tail, v_tail, sm_scale, dtype):
                 continue
             p = np.exp(s - s.max())
             out[b, h] = (p @ vals) / p.sum()
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Zero-copy paged variant
+# ---------------------------------------------------------------------------
+#
+# A paged cache keeps the rows of segment s in pages of `page_rows`
+# consecutive positions: logical page p (positions [p * page_rows,
+# (p + 1) * page_rows)) lives in physical page page_table[s][p] of a pool
+# [num_pages][page_rows][d].  Nothing about this layout comes from the paper;
+# it is the paged-cache idea the paper cites as prior art, used to keep the
+# retained rows in place instead of packing them.
+
+PAGE_ENTRY_FIELDS = ("page", "logical_page", "lo", "hi")
+
+
+def page_select(kv_mask, page_table, page_rows, append_cap):
+    """Runs of retained positions of every segment, referenced in place.
+
+    kv_mask uint8 [nseg][T] (nonzero = retained), page_table int32
+    [nseg][pages_per_seg].  For each segment, in position order: every
+    maximal run of retained context positions that stays within one logical
+    page, as the entry (physical page, logical page, lo, hi) covering slots
+    [lo, hi) of that page; then the append region [T, T + append_cap), one
+    entry per logical page it touches (appended tokens are always retained,
+    Sec. 3.4).  A page is used when some entry names it.
+
+    Returns dict(entries = list per segment of int32 [n][4] arrays,
+    n_entries int32 [nseg], seg_len int32 [nseg] (retained context
+    positions), page_used uint8 [nseg][pages_per_seg]).
+    """
+    kv_mask = np.asarray(kv_mask)
+    table = np.asarray(page_table)
+    nseg, T = kv_mask.shape
+    pr = int(page_rows)
+    n_pages = table.shape[1]
+    ctx_pages = -(-T // pr)
+    entries = []
+    n_entries = np.zeros(nseg, dtype=np.int32)
+    seg_len = np.zeros(nseg, dtype=np.int32)
+    page_used = np.zeros((nseg, n_pages), dtype=np.uint8)
+    for s in range(nseg):
+        kept = np.zeros(ctx_pages * pr, dtype=np.int8)
+        kept[:T] = kv_mask[s] != 0
+        seg_len[s] = int(kept.sum())
+        # one row per logical page, a zero on either side: a run can then
+        # neither start before a page nor end after it
+        framed = np.zeros((ctx_pages, pr + 2), dtype=np.int8)
+        framed[:, 1:-1] = kept.reshape(ctx_pages, pr)
+        step = np.diff(framed, axis=1)
+        starts = np.argwhere(step == 1)   # (logical page, first slot), row-major = position order
+        ends = np.argwhere(step == -1)    # (logical page, end slot)
+        rows = [(int(table[s, lp]), int(lp), int(lo), int(hi))
+                for (lp, lo), (_, hi) in zip(starts, ends)]
+        if append_cap > 0:
+            for lp in range(T // pr, (T + append_cap - 1) // pr + 1):
+                lo = max(T, lp * pr) - lp * pr
+                hi = min(T + append_cap, (lp + 1) * pr) - lp * pr
+                rows.append((int(table[s, lp]), lp, lo, hi))
+        e = np.array(rows, dtype=np.int32).reshape(-1, 4)
+        entries.append(e)
+        n_entries[s] = len(e)
+        page_used[s, e[:, 1]] = 1
+    return dict(entries=entries, n_entries=n_entries, seg_len=seg_len, page_used=page_used)
+
+
+def paged_append(k_pages, v_pages, page_table, page_rows, context_len, k_new, v_new, n_tail):
+    """Write new tokens into their pages (Sec. 3.4: appended and retained).
+
+    k_new, v_new [nseg][n_new][d]; token t of segment s is position
+    P = context_len + n_tail + t, stored at slot P % page_rows of page
+    page_table[s][P // page_rows].  Returns updated copies of the pools.
+    """
+    k_pages = np.array(k_pages, copy=True)
+    v_pages = np.array(v_pages, copy=True)
+    nseg, n_new = np.asarray(k_new).shape[:2]
+    for s in range(nseg):
+        for t in range(n_new):
+            pos = int(context_len) + int(n_tail) + t
+            page = int(page_table[s][pos // page_rows])
+            k_pages[page, pos % page_rows] = k_new[s][t]
+            v_pages[page, pos % page_rows] = v_new[s][t]
+    return k_pages, v_pages
+
+
+def paged_decode_attn(q, k_pages, v_pages, entries, page_rows, context_len, n_tail, sm_scale,
+                      num_kv_heads, dtype):
+    """One decode step over a paged cache, through page_select's entries.
+
+    Segment s = b * Hkv + g attends to every slot [lo, hi) of every entry
+    whose position (logical page * page_rows + slot) is below
+    context_len + n_tail: the retained context and the tokens appended so
+    far.  Every query head of group g attends to all of them (union of
+    Sec. 3.4).  Returns float64 [B][Hq][d].
+    """
+    qf = widen(q, dtype)
+    B, Hq, d = qf.shape
+    G = Hq // num_kv_heads
+    limit = int(context_len) + int(n_tail)
+    out = np.zeros((B, Hq, d), dtype=np.float64)
+    for b in range(B):
+        for g in range(num_kv_heads):
+            s = b * num_kv_heads + g
+            pages, slots = [], []
+            for page, lp, lo, hi in np.asarray(entries[s]).reshape(-1, 4):
+                for slot in range(int(lo), int(hi)):
+                    if int(lp) * page_rows + slot < limit:
+                        pages.append(int(page))
+                        slots.append(slot)
+            kr = widen(np.asarray(k_pages)[pages, slots].reshape(len(pages), d), dtype)
+            vr = widen(np.asarray(v_pages)[pages, slots].reshape(len(pages), d), dtype)
+            for h in range(g * G, (g + 1) * G):
+                out[b, h] = _softmax_attend(qf[b, h], kr, vr, sm_scale)
     return out

@@ -488,3 +488,131 @@ def test_query_attn_single_token_is_decode_step():
     out = o.query_attn(q, kc, vc, r["seg_off"], r["seg_len"], n_tail, 0.7, n_kv, o.F32)
     dec = o.decode_attn(q[:, 0], kc, vc, r["seg_off"], r["seg_len"], n_tail + 1, 0.7, n_kv, o.F32)
     np.testing.assert_allclose(out[:, 0], dec, rtol=1e-13, atol=1e-14)
+
+
+# ---------------------------------------------------------------------------
+# zero-copy paged variant
+# ---------------------------------------------------------------------------
+
+def test_page_select_hand_example():
+    g = _golden("page_select_small.json")
+    r = o.page_select(np.array([g["kv_mask"]], np.uint8), np.array([g["page_table"]], np.int32),
+                      g["page_rows"], g["append_cap"])
+    np.testing.assert_array_equal(r["entries"][0], np.array(g["entries"], np.int32))
+    assert r["n_entries"][0] == len(g["entries"])
+    assert r["seg_len"][0] == g["seg_len"]
+    np.testing.assert_array_equal(r["page_used"][0], g["page_used"])
+
+
+def _walk_positions(mask_row, table_row, pr, T, cap):
+    """Brute force, position by position: (page, slot) of every retained
+    context position, then of every append position, in position order."""
+    out = []
+    for pos in range(T + cap):
+        if pos >= T or mask_row[pos]:
+            out.append((int(table_row[pos // pr]), pos % pr))
+    return out
+
+
+def test_page_select_covers_exactly_the_retained_positions():
+    rng = np.random.default_rng(50)
+    for trial in range(40):
+        nseg = int(rng.integers(1, 4))
+        T = int(rng.integers(0, 60))
+        pr = int(rng.choice([1, 2, 3, 4, 8]))
+        cap = int(rng.integers(0, 10))
+        pages = -(-(T + cap) // pr) + int(rng.integers(0, 3))
+        m = (rng.uniform(size=(nseg, T)) < rng.uniform()).astype(np.uint8) * rng.integers(1, 255, (nseg, T),
+                                                                                              dtype=np.uint8)
+        table, _ = di.page_table(nseg, pages, seed=trial, spare=3)
+        r = o.page_select(m, table, pr, cap)
+        for s in range(nseg):
+            e = r["entries"][s]
+            want = _walk_positions(m[s], table[s], pr, T, cap)
+            got = [(int(p), slot) for p, lp, lo, hi in e for slot in range(lo, hi)]
+            assert got == want, (trial, s)
+            assert r["seg_len"][s] == int((m[s] != 0).sum())
+            assert r["n_entries"][s] == len(e)
+            for p, lp, lo, hi in e:
+                assert 0 <= lo < hi <= pr and table[s, lp] == p
+            # maximal: two entries of one logical page never touch
+            for a, b in zip(e[:-1], e[1:]):
+                assert a[1] < b[1] or a[3] < b[2] or (a[1] * pr + a[3] == T)
+            used = np.zeros(pages, np.uint8)
+            for p, slot in want:
+                used[list(table[s]).index(p)] = 1
+            np.testing.assert_array_equal(r["page_used"][s], used)
+
+
+def test_page_select_paper_layout_is_whole_pages():
+    """The paper's layout (Appendix A: 128 sink, 1,024 recent, 128-token
+    bins) at T = 130,816 with 128-row pages: every bin, the sink and the
+    recent window are whole pages, so every context entry is a full page and
+    the entries hold exactly the retained positions."""
+    g = _golden("paper_layout.json")
+    T = g["layouts"][0]["context_len"]
+    D = g["layouts"][0]["num_bins"]
+    S, R, W = g["sink"], g["recent"], g["bin_width"]
+    rng = np.random.default_rng(51)
+    pattern = (rng.uniform(size=(1, 2, D)) < 0.3).astype(np.uint8)
+    _, km = paint_masks(pattern, T, S, R, [W * k for k in range(D + 1)], 1)
+    table, _ = di.page_table(1, T // W + 1, seed=1)
+    r = o.page_select(km[0], table, W, 64)
+    e = r["entries"][0]
+    ctx = e[e[:, 1] * W < T]
+    assert (ctx[:, 2] == 0).all() and (ctx[:, 3] == W).all()
+    assert len(ctx) * W == int(km.sum())
+
+
+def test_paged_decode_equals_masked_sdpa():
+    """Attention through the entries of a shuffled page pool equals torch
+    SDPA over the dense cache with pruned positions masked out and the
+    appended tokens visible."""
+    rng = np.random.default_rng(52)
+    for trial in range(8):
+        B, n_kv, G, d = 2, 2, int(rng.integers(1, 4)), 8
+        T = int(rng.integers(1, 50))
+        pr = int(rng.choice([2, 4, 8]))
+        cap = int(rng.integers(1, 6))
+        n_tail = int(rng.integers(0, cap + 1))
+        nseg = B * n_kv
+        q = rng.standard_normal((B, n_kv * G, d)).astype(np.float32)
+        k = rng.standard_normal((B, n_kv, T + cap, d)).astype(np.float32)
+        v = rng.standard_normal((B, n_kv, T + cap, d)).astype(np.float32)
+        m = (rng.uniform(size=(B, n_kv, T)) < 0.5).astype(np.uint8)
+        table, n_pages = di.page_table(nseg, -(-(T + cap) // pr), seed=100 + trial, spare=2)
+        kp = np.zeros((n_pages, pr, d), np.float32)
+        vp = np.zeros((n_pages, pr, d), np.float32)
+        di.fill_pages(kp, k.reshape(nseg, T + cap, d), table, pr)
+        di.fill_pages(vp, v.reshape(nseg, T + cap, d), table, pr)
+        sel = o.page_select(m.reshape(nseg, T), table, pr, cap)
+        out = o.paged_decode_attn(q, kp, vp, sel["entries"], pr, T, n_tail, 0.6, n_kv, o.F32)
+        allow = np.zeros((B, n_kv * G, 1, T + cap), bool)
+        for b in range(B):
+            for h in range(n_kv * G):
+                allow[b, h, 0, :T] = m[b, h // G] == 1
+                allow[b, h, 0, T:T + n_tail] = True
+        ref = sdpa(q.astype(np.float64), k.astype(np.float64), v.astype(np.float64), 0.6,
+                   torch.from_numpy(allow))
+        # SDPA yields NaN for a row with nothing visible; the oracle's rule is zeros
+        ref = np.nan_to_num(ref, nan=0.0)
+        np.testing.assert_allclose(out, ref, rtol=1e-12, atol=1e-13)
+
+
+def test_paged_append_writes_each_token_at_its_position():
+    rng = np.random.default_rng(53)
+    nseg, T, pr, cap, d, n_tail, n_new = 3, 13, 4, 7, 2, 2, 3
+    table, n_pages = di.page_table(nseg, -(-(T + cap) // pr), seed=7)
+    kp = rng.standard_normal((n_pages, pr, d)).astype(np.float32)
+    vp = rng.standard_normal((n_pages, pr, d)).astype(np.float32)
+    kn = rng.standard_normal((nseg, n_new, d)).astype(np.float32)
+    vn = rng.standard_normal((nseg, n_new, d)).astype(np.float32)
+    k2, v2 = o.paged_append(kp, vp, table, pr, T, kn, vn, n_tail)
+    touched = np.zeros((n_pages, pr), bool)
+    for s in range(nseg):
+        for t in range(n_new):
+            pos = T + n_tail + t          # 15, 16, 17: pages 3 and 4 of the segment
+            page, slot = table[s, pos // pr], pos % pr
+            assert np.array_equal(k2[page, slot], kn[s, t]) and np.array_equal(v2[page, slot], vn[s, t])
+            touched[page, slot] = True
+    assert np.array_equal(k2[~touched], kp[~touched]) and np.array_equal(v2[~touched], vp[~touched])
