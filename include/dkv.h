@@ -15,6 +15,9 @@
  *   dkv_decode_attn   one decode step of attention over the packed segments
  *   dkv_query_attn    the query block after the context: attention over the
  *                     packed segments plus the block itself, causally
+ *   dkv_page_select   zero-copy alternative to the pack: the retained runs
+ *                     of a paged cache, listed in place
+ *   dkv_paged_decode_attn  decode over a paged cache through those entries
  *
  * plus dkv_dense_decode_attn, the same attention kernel over an uncompressed
  * cache (the "Dense" comparator of Sec. 4.3).
@@ -276,6 +279,120 @@ dkv_status dkv_query_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_heads,
                           const int64_t *seg_off, const int32_t *seg_len, float sm_scale,
                           int64_t rows_hint, float *out, void *workspace, size_t workspace_bytes,
                           void *stream);
+
+/*
+ * Zero-copy paged variant
+ * -----------------------
+ * The retained set of a segment is its sink, its recent window and a union
+ * of whole distance bins (Eq. (4), Eq. (5) and the union of Sec. 3.4), i.e. a
+ * few long runs of consecutive positions.  When the cache is kept in pages of
+ * page_rows consecutive positions, those runs can be referenced where they
+ * are instead of being packed (dkv_compact): with the paper's 128-token bins
+ * (Appendix A) and 128-row pages every retained bin is a whole page.
+ *
+ * Paged cache: K and V pools [num_pages][page_rows][d]; page_table
+ * [nseg][pages_per_seg] (int32) gives the physical page that holds positions
+ * [p * page_rows, (p + 1) * page_rows) of segment s (logical page p).
+ * page_rows is 32, 64, 128, 256, 512 or 1024.
+ *
+ * Entry: four int32 (physical page, logical page, lo, hi) naming slots
+ * [lo, hi) of one page.  A segment's entries are listed in position order:
+ * every maximal run of retained context positions within one page, then
+ * the append region [T, T + append_cap) page by page.  Decode attends to the
+ * slots of the entries whose positions are below T + (tokens appended).
+ */
+#define DKV_PAGE_ENTRY_INTS 4
+
+/* Workspace bytes of dkv_page_select (host, no GPU call). */
+size_t dkv_page_select_workspace_bytes(int32_t num_segments, int32_t context_len);
+
+/*
+ * Upper bound on the entries of one segment for keep masks made by
+ * dkv_map_pattern with this layout (host): pages of the context, plus one
+ * per bin, the sink and the recent window, plus the append region's pages.
+ * Returns -1 for invalid arguments.
+ */
+int64_t dkv_page_entries_bound(const dkv_layout *layout, int32_t append_cap, int32_t page_rows);
+
+/*
+ * dkv_page_select -- the zero-copy alternative to dkv_compact: list the
+ * retained rows of every segment in place (Sec. 3.4 keeps retained rows in
+ * original order; here they keep their original pages too).
+ *
+ * kv_mask     uint8 [nseg][T], nonzero = retained (e.g. dkv_map_pattern's
+ *             kv_mask with nseg = N * Hkv); 16-byte aligned.
+ * page_table  int32 [nseg][pages_per_seg]; pages_per_seg * page_rows must be
+ *             >= T + append_cap (DKV_ERR_INVALID_ARG otherwise).
+ * entries     out, int32 [nseg][max_entries][4], 16-byte aligned.  Entries
+ *             at index >= max_entries are not written.
+ * n_entries   out, int32 [nseg]: the segment's entry count, even when it is
+ *             larger than max_entries (the caller must then enlarge the
+ *             array: decode reads at most max_entries entries and cannot
+ *             append to a segment whose append entries are missing).
+ * seg_len     out, int32 [nseg]: retained context positions (as kv_len).
+ * page_used   out, optional uint8 [nseg][pages_per_seg]: 1 for every page an
+ *             entry names; pages marked 0 hold no retained row and no append
+ *             slot and may be returned to the pool -- that is where the
+ *             memory reduction comes from.
+ * workspace   dkv_page_select_workspace_bytes(nseg, T) bytes, no initial
+ *             contents required.
+ * Nothing is copied: the pools are neither read nor written.
+ */
+dkv_status dkv_page_select(int32_t num_segments, int32_t context_len, int32_t append_cap,
+                           int32_t page_rows, const uint8_t *kv_mask, const int32_t *page_table,
+                           int32_t pages_per_seg, int32_t max_entries, int32_t *entries,
+                           int32_t *n_entries, int32_t *seg_len, uint8_t *page_used,
+                           void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * dkv_paged_decode_attn -- one decode step over a paged cache (Sec. 3.4),
+ * reading the retained rows in place through dkv_page_select's entries.
+ *
+ * q           [B][Hq][d]; segment s = b * Hkv + g.
+ * k_pages, v_pages  the pools, num_pages pages of page_rows rows of d
+ *             elements of `dtype`.
+ * entries, n_entries, max_entries  as written by dkv_page_select for these
+ *             segments (for a subset of a larger selection, offset entries
+ *             by first * max_entries * 4 and n_entries by first).
+ * context_len T of the selection; n_tail (host) tokens appended so far,
+ *             at positions [T, T + n_tail).
+ * Every query head of group g attends to the slots of segment (b, g)'s
+ * entries whose positions lie below T + n_tail: the retained context and the
+ * appended tokens (the union of Sec. 3.4).  An entry that names a page
+ * outside [0, num_pages) or slots outside [0, page_rows) attends nothing.
+ * The result is that of dkv_decode_attn over a packed cache of the same rows.
+ * rows_hint (host) expected sum over segments of entries * page_rows (0 =
+ * unknown); it only sizes the split.  out, workspace: as dkv_decode_attn,
+ * with the same workspace size (dkv_decode_workspace_bytes).
+ */
+dkv_status dkv_paged_decode_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_heads,
+                                 int32_t num_kv_heads, int32_t head_dim, const void *q,
+                                 const void *k_pages, const void *v_pages, int64_t num_pages,
+                                 int32_t page_rows, const int32_t *entries,
+                                 const int32_t *n_entries, int32_t max_entries,
+                                 int32_t context_len, int32_t n_tail, float sm_scale,
+                                 int64_t rows_hint, float *out, void *workspace,
+                                 size_t workspace_bytes, void *stream);
+
+/*
+ * dkv_paged_append_decode_attn -- the decode step of a serving loop over a
+ * paged cache: token t of k_new, v_new ([B * Hkv][n_new][d]) is position
+ * T + n_tail + t and is written to its slot of the page its append-region
+ * entry names (Sec. 3.4: appended and retained), then the step attends as
+ * dkv_paged_decode_attn with n_tail + n_new tokens appended, in one launch.
+ * append_cap must be the value given to dkv_page_select, and n_tail + n_new
+ * must not exceed it (DKV_ERR_CAPACITY).  A segment whose entry count
+ * exceeded max_entries is not appended to.
+ */
+dkv_status dkv_paged_append_decode_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_heads,
+                                        int32_t num_kv_heads, int32_t head_dim, const void *q,
+                                        const void *k_new, const void *v_new, int32_t n_new,
+                                        int32_t n_tail, int32_t append_cap, void *k_pages,
+                                        void *v_pages, int64_t num_pages, int32_t page_rows,
+                                        const int32_t *entries, const int32_t *n_entries,
+                                        int32_t max_entries, int32_t context_len,
+                                        float sm_scale, int64_t rows_hint, float *out,
+                                        void *workspace, size_t workspace_bytes, void *stream);
 
 /* Static description of a status code. */
 const char *dkv_status_string(dkv_status status);

@@ -20,6 +20,8 @@ __all__ = [
     "dkv_decode_workspace_bytes", "dkv_decode_attn", "dkv_dense_decode_attn",
     "dkv_append_decode_attn", "dkv_dense_append_decode_attn",
     "dkv_status_string", "dkv_probe_stream_read", "dkv_query_workspace_bytes", "dkv_query_attn",
+    "dkv_page_select_workspace_bytes", "dkv_page_entries_bound", "dkv_page_select",
+    "dkv_paged_decode_attn", "dkv_paged_append_decode_attn",
 ]
 
 (DKV_OK, DKV_ERR_INVALID_ARG, DKV_ERR_UNSUPPORTED, DKV_ERR_MISALIGNED, DKV_ERR_CAPACITY,
@@ -96,6 +98,13 @@ def library():
         "dkv_query_workspace_bytes": (SZ, [I32, I32, I32, I32, I32, I64]),
         "dkv_query_attn": (I32, [I32, I32, I32, I32, I32, I32, VP, I32, I32, VP, VP, VP, VP, F32, I64,
                                  VP, VP, SZ, VP]),
+        "dkv_page_select_workspace_bytes": (SZ, [I32, I32]),
+        "dkv_page_entries_bound": (I64, [P, I32, I32]),
+        "dkv_page_select": (I32, [I32, I32, I32, I32, VP, VP, I32, I32, VP, VP, VP, VP, VP, SZ, VP]),
+        "dkv_paged_decode_attn": (I32, [I32, I32, I32, I32, I32, VP, VP, VP, I64, I32, VP, VP, I32, I32,
+                                        I32, F32, I64, VP, VP, SZ, VP]),
+        "dkv_paged_append_decode_attn": (I32, [I32, I32, I32, I32, I32, VP, VP, VP, I32, I32, I32, VP, VP,
+                                               I64, I32, VP, VP, I32, I32, F32, I64, VP, VP, SZ, VP]),
     }
     for name, (res, args) in sigs.items():
         f = getattr(lib, name)
@@ -253,3 +262,53 @@ def dkv_query_attn(q, n_tail, append_cap, k_c, v_c, seg_off, seg_len, sm_scale, 
         int(append_cap), _dev(k_c, "k_c"), _dev(v_c, "v_c"), _dev(seg_off, "seg_off"),
         _dev(seg_len, "seg_len"), float(sm_scale), int(rows_hint), _dev(out, "out"), ws_ptr, ws_bytes,
         _stream(stream)))
+
+
+def dkv_page_select_workspace_bytes(num_segments, context_len):
+    return library().dkv_page_select_workspace_bytes(int(num_segments), int(context_len))
+
+
+def dkv_page_entries_bound(layout, append_cap, page_rows):
+    return library().dkv_page_entries_bound(ctypes.byref(layout), int(append_cap), int(page_rows))
+
+
+def dkv_page_select(kv_mask, page_table, page_rows, append_cap, entries, n_entries, seg_len, workspace,
+                    page_used=None, stream=None):
+    """kv_mask: uint8, nseg rows of T positions ([nseg][T] or [N][Hkv][T]);
+    page_table: int32 [nseg][pages_per_seg]; entries: int32 [nseg][max_entries][4];
+    n_entries, seg_len: int32 [nseg]; page_used: optional uint8 [nseg][pages_per_seg]."""
+    nseg, pps = page_table.shape
+    T = kv_mask.shape[-1]
+    _check("dkv_page_select", library().dkv_page_select(
+        nseg, T, int(append_cap), int(page_rows), _dev(kv_mask, "kv_mask"), _dev(page_table, "page_table"),
+        pps, entries.shape[1], _dev(entries, "entries"), _dev(n_entries, "n_entries"),
+        _dev(seg_len, "seg_len"), _dev(page_used, "page_used", optional=True), _dev(workspace, "workspace"),
+        workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def dkv_paged_decode_attn(q, k_pages, v_pages, entries, n_entries, context_len, n_tail, sm_scale, out,
+                          workspace, num_kv_heads, rows_hint=0, stream=None):
+    """q: [B][Hq][d]; k_pages, v_pages: [num_pages][page_rows][d];
+    entries: int32 [B*Hkv][max_entries][4]; n_entries: int32 [B*Hkv]."""
+    B, Hq, d = q.shape
+    num_pages, page_rows = k_pages.shape[0], k_pages.shape[1]
+    _check("dkv_paged_decode_attn", library().dkv_paged_decode_attn(
+        dtype_code(q.dtype), B, Hq, int(num_kv_heads), d, _dev(q, "q"), _dev(k_pages, "k_pages"),
+        _dev(v_pages, "v_pages"), num_pages, page_rows, _dev(entries, "entries"), _dev(n_entries, "n_entries"),
+        entries.shape[1], int(context_len), int(n_tail), float(sm_scale), int(rows_hint), _dev(out, "out"),
+        _dev(workspace, "workspace"), workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def dkv_paged_append_decode_attn(q, k_new, v_new, n_tail, append_cap, k_pages, v_pages, entries, n_entries,
+                                 context_len, sm_scale, out, workspace, num_kv_heads, rows_hint=0,
+                                 stream=None):
+    """q: [B][Hq][d]; k_new, v_new: [B*Hkv][n_new][d]; pools and entries as
+    dkv_paged_decode_attn."""
+    B, Hq, d = q.shape
+    num_pages, page_rows = k_pages.shape[0], k_pages.shape[1]
+    _check("dkv_paged_append_decode_attn", library().dkv_paged_append_decode_attn(
+        dtype_code(q.dtype), B, Hq, int(num_kv_heads), d, _dev(q, "q"), _dev(k_new, "k_new"),
+        _dev(v_new, "v_new"), k_new.shape[1], int(n_tail), int(append_cap), _dev(k_pages, "k_pages"),
+        _dev(v_pages, "v_pages"), num_pages, page_rows, _dev(entries, "entries"), _dev(n_entries, "n_entries"),
+        entries.shape[1], int(context_len), float(sm_scale), int(rows_hint), _dev(out, "out"),
+        _dev(workspace, "workspace"), workspace.numel() * workspace.element_size(), _stream(stream)))

@@ -28,7 +28,7 @@ COMMON_FLAGS = [
     f"-I{INCLUDE}", "-Wall", "-Wno-unused-function",
 ]
 SOURCES = ["map_pattern.hip", "compact.hip", "decode_attn.hip", "dkv_api.cpp", "bw_probe.hip",
-           "query_attn.hip", "dkv_query_api.cpp"]
+           "query_attn.hip", "dkv_query_api.cpp", "page_select.hip", "dkv_paged_api.cpp"]
 
 
 def _hipcc():

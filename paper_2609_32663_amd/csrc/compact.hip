@@ -25,22 +25,6 @@ constexpr int kThreads = 256;
 constexpr int kPerThread = 16;
 static_assert(kThreads * kPerThread == kCompactTile, "tile = threads x 16 positions");
 
-// The 16 mask bytes of positions [j0, j0+16) of one row, zero beyond T.
-__device__ __forceinline__ u32x4 load_mask16(const uint8_t* row, int64_t j0, int32_t T) {
-  u32x4 w = {0u, 0u, 0u, 0u};
-  if ((T & 15) == 0) {
-    if (j0 < T) w = *reinterpret_cast<const u32x4*>(row + j0);
-  } else {
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int64_t j = j0 + e;
-      const uint32_t b = (j < T && row[j] != 0) ? 1u : 0u;
-      w[e >> 2] |= b << (8 * (e & 3));
-    }
-  }
-  return w;
-}
-
 __global__ __launch_bounds__(kThreads) void compact_count_kernel(CompactParams p) {
   __shared__ int64_t red[kThreads / kWave + 1];
   const int tile = blockIdx.x;

@@ -35,6 +35,16 @@
 //     16 bytes of columns of rows rp, rp + RP, ... for every head.
 // The decode step is a GEMV per KV row (about G flop per byte), far below the
 // MFMA ridge, so the kernel is built to keep HBM busy rather than the ALUs.
+//
+// Paged addressing (the zero-copy variant): K and V stay in a page pool and a
+// segment's rows are the page_rows slots of each of its entries (page, logical
+// page, lo, hi), so the split, the ring and the combine are the same.  Tiles
+// are aligned to the 32-row grid of that row space and never straddle a page;
+// each tile gets its own buffer descriptor over the page rows from the tile's
+// start to the end of the attended slots, so slots past an entry's end (and
+// past the tokens appended so far) read zeros without touching memory, and the
+// softmax masks every slot outside [lo, hi).  Entries are staged through LDS
+// in chunks.
 
 #include <atomic>
 
@@ -111,12 +121,14 @@ __device__ __forceinline__ float group_sum(float x) {
   return x;
 }
 
-// K and V registers of one wave tile.
+// K and V registers of one wave tile.  Paged tiles also carry the range
+// [lo, hi) of their 32 rows that is attended.
 template <bool BF16, int D, int GP>
 struct Tile {
   using C = DecodeCfg<BF16, D, GP>;
   u32x4 k[C::kKG][C::kChunks];
   u32x4 v[C::kRPT];
+  int32_t lo, hi;
 };
 
 // Buffer descriptor over `bytes` bytes at `base` (raw buffer, stride 0).  A
@@ -175,7 +187,9 @@ struct WaveState {
   float acc[GP][C::kCPL];     // unnormalised output, columns cc*CPL.., rows of phase rp
 };
 
-template <bool BF16, int D, int GP>
+// Packed tiles attend rows row + r < nrows of their range; paged tiles the
+// rows r in [t.lo, t.hi) (row and nrows unused).
+template <bool BF16, int D, int GP, bool PAGED>
 __device__ __forceinline__ void compute_tile(WaveState<BF16, D, GP>& st, const Tile<BF16, D, GP>& t,
                                              const u32x4* qa, uint32_t row, uint32_t nrows, float scale_log2,
                                              float (*pb)[GP], float* ab, int j16, int kg, int rp) {
@@ -186,7 +200,8 @@ __device__ __forceinline__ void compute_tile(WaveState<BF16, D, GP>& st, const T
     f32x4 c = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int u = 0; u < C::kChunks; ++u) c = qk_mfma(qa[u], t.k[kk][u], c, BF16);
-    const bool valid = row + 16 * kk + j16 < nrows;
+    const int r = 16 * kk + j16;
+    const bool valid = PAGED ? (r >= t.lo && r < t.hi) : row + r < nrows;
 #pragma unroll
     for (int v = 0; v < 4; ++v) sc[kk][v] = valid ? c[v] * scale_log2 : -INFINITY;
   }
@@ -259,18 +274,25 @@ __device__ __forceinline__ void compute_tile(WaveState<BF16, D, GP>& st, const T
 // crosses a segment boundary pays that cost twice, so charging it here gives
 // such a workgroup fewer rows and keeps the slowest workgroup close to the
 // median.
-__device__ __forceinline__ int64_t segment_units(const DecodeParams& p, int s, int64_t seg_cost) {
-  const int64_t rows = (p.seg_len == nullptr ? p.dense_len : (int64_t)p.seg_len[s] + p.n_tail) + p.n_new;
-  return rows > 0 ? rows + seg_cost : 0;
+// Paged segments have page_rows units per entry (the slots outside an
+// entry's range are masked, not removed).
+template <bool PAGED>
+__device__ __forceinline__ int64_t segment_rows(const DecodeParams& p, int s) {
+  if (PAGED) {
+    const int32_t n = p.n_entries[s];
+    return (int64_t)(n < 0 ? 0 : (n > p.max_entries ? p.max_entries : n)) * p.page_rows;
+  }
+  return (p.seg_len == nullptr ? p.dense_len : (int64_t)p.seg_len[s] + p.n_tail) + p.n_new;
 }
 
 // Flat prefix of work units over the call's segments: pre[s] = units of
 // segments < s, pre[nseg] = total.  A non-empty segment s covers
 // [pre[s], pre[s + 1]); its first seg_cost units are the fixed cost and its
-// rows are the units after them.  The packed cache's segment offsets are
-// copied to offs[] in the same pass, so the workgroup learns where its rows
-// are after a single round trip to memory.  Called by every thread of a
-// workgroup; `red` holds kWaves + 1 int64 of LDS.
+// rows are the units after them.  The packed cache's segment offsets (the
+// paged cache's row counts) are copied to offs[] in the same pass, so the
+// workgroup learns where its rows are after a single round trip to memory.
+// Called by every thread of a workgroup; `red` holds kWaves + 1 int64 of LDS.
+template <bool PAGED>
 __device__ __forceinline__ void build_row_prefix(const DecodeParams& p, int64_t seg_cost, int64_t* pre,
                                                  int64_t* offs, int64_t* red) {
   const int tid = threadIdx.x;
@@ -280,8 +302,10 @@ __device__ __forceinline__ void build_row_prefix(const DecodeParams& p, int64_t 
   const int s_hi = min(nseg, s_lo + per);
   int64_t sum = 0;
   for (int s = s_lo; s < s_hi; ++s) {
-    if (p.seg_len != nullptr) offs[s] = p.seg_off[s];
-    const int64_t u = segment_units(p, s, seg_cost);
+    if (!PAGED && p.seg_len != nullptr) offs[s] = p.seg_off[s];
+    const int64_t rows = segment_rows<PAGED>(p, s);
+    if (PAGED) offs[s] = rows;
+    const int64_t u = rows > 0 ? rows + seg_cost : 0;
     pre[s] = u;  // this thread's own slots: units now, prefix after the scan
     sum += u;
   }
@@ -311,12 +335,56 @@ constexpr int decode_waves_per_eu() {
   return (decode_stages<BF16, D, GP>() == 2 && GP == 4 && (BF16 || D == 64)) ? 2 : 1;
 }
 
+constexpr int kEntryChunk = 64;  // paged entries staged in LDS at a time
+
+// Descriptors of paged tile `t` of the current entry chunk: the tile's rows
+// [row0, row0 + 32) lie in one page; the attended ones are [lo, hi) of the
+// tile, clipped to the piece [a, bnd), the entry's slots and the positions
+// below `limit`.  The descriptors start at row lo, so rows before it get a
+// wrapped (huge) offset and rows from hi on lie past the range: both read
+// zeros without touching memory.  `row` is what load_tile adds to a row
+// index to get the row's offset in the descriptor.  Tiles past the chunk
+// read nothing.
 template <bool BF16, int D, int GP>
+__device__ __forceinline__ void paged_tile(const DecodeParams& p, const int32_t (*ent)[4], int64_t c0, int64_t c1,
+                                           int64_t k0, uint32_t ntile, uint32_t t, int64_t a, int64_t bnd,
+                                           int64_t limit, __amdgpu_buffer_rsrc_t& kr, __amdgpu_buffer_rsrc_t& vr,
+                                           uint32_t& row, int32_t& lo, int32_t& hi) {
+  using C = DecodeCfg<BF16, D, GP>;
+  const int64_t pr = p.page_rows;
+  const int64_t row0 = (k0 + t) * kTK;
+  const int64_t e = row0 / pr;
+  const int64_t li = e - c0 < c1 - c0 - 1 ? e - c0 : c1 - c0 - 1;
+  const int32_t page = __builtin_amdgcn_readfirstlane(ent[li][0]);
+  const int32_t lpage = __builtin_amdgcn_readfirstlane(ent[li][1]);
+  const int32_t e_lo = __builtin_amdgcn_readfirstlane(ent[li][2]);
+  const int32_t e_hi = __builtin_amdgcn_readfirstlane(ent[li][3]);
+  const int64_t slot0 = row0 - e * pr;
+  int64_t l = a - row0;
+  if (e_lo - slot0 > l) l = e_lo - slot0;
+  if (l < 0) l = 0;
+  if (l > kTK) l = kTK;
+  int64_t h = bnd - row0;
+  if (e_hi - slot0 < h) h = e_hi - slot0;
+  if (limit - ((int64_t)lpage * pr + slot0) < h) h = limit - ((int64_t)lpage * pr + slot0);
+  if (h > kTK) h = kTK;
+  if (t >= ntile || h < l) h = l;
+  lo = (int32_t)l;
+  hi = (int32_t)h;
+  row = (uint32_t)(-(int32_t)l);
+  const int64_t off = ((int64_t)page * pr + slot0 + l) * C::kRowBytes;
+  const uint32_t bytes = (uint32_t)(h - l) * C::kRowBytes;
+  kr = make_rsrc(reinterpret_cast<const char*>(p.k) + off, bytes);
+  vr = make_rsrc(reinterpret_cast<const char*>(p.v) + off, bytes);
+}
+
+template <bool BF16, int D, int GP, bool PAGED>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(decode_waves_per_eu<BF16, D, GP>())))
 void decode_kernel(DecodeParams p) {
   using C = DecodeCfg<BF16, D, GP>;
-  extern __shared__ __align__(16) int64_t pre[];          // [nseg + 1] unit prefix, then [nseg] offsets
+  extern __shared__ __align__(16) int64_t pre[];          // [nseg + 1] unit prefix, then [nseg] offsets / rows
   int64_t* offs = pre + p.nseg + 1;
+  __shared__ __align__(16) int32_t ent[PAGED ? kEntryChunk : 1][4];  // staged paged entries
   __shared__ __align__(16) float pbuf[kWaves][kTK][GP];   // probabilities per wave tile
   __shared__ __align__(16) float abuf[kWaves][GP];        // rescale factors per wave
   __shared__ __align__(16) float wacc[kWaves][GP][D];     // per-wave accumulators
@@ -329,13 +397,13 @@ void decode_kernel(DecodeParams p) {
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int w = blockIdx.x;
   const int nseg = p.nseg;
-  const bool dense = p.seg_len == nullptr;
+  const bool dense = !PAGED && p.seg_len == nullptr;
 
   // fixed cost of a piece, in rows: about as long as streaming 128 KiB of K
   // and V (measured: a second piece adds about 6 us to a workgroup that
   // streams about 43 bf16 d128 rows per us)
   constexpr int64_t kSegCost = 131072 / (2 * C::kRowBytes);
-  build_row_prefix(p, kSegCost, pre, offs, red);
+  build_row_prefix<PAGED>(p, kSegCost, pre, offs, red);
   const int64_t total = uniform64(pre[nseg]);
 
   // ---- segments with no rows at all produce zeros ----------------------
@@ -382,7 +450,7 @@ void decode_kernel(DecodeParams p) {
     if (a >= bnd) continue;
     const int bseq = s / p.Hkv;
     const int g = s - bseq * p.Hkv;
-    const int64_t row0 = uniform64(dense ? (int64_t)s * p.dense_stride : offs[s]);
+    const int64_t row0 = PAGED ? 0 : uniform64(dense ? (int64_t)s * p.dense_stride : offs[s]);
     const char* kbase = reinterpret_cast<const char*>(p.k) + row0 * C::kRowBytes;
     const char* vbase = reinterpret_cast<const char*>(p.v) + row0 * C::kRowBytes;
 
@@ -390,7 +458,42 @@ void decode_kernel(DecodeParams p) {
     // workgroup whose slice holds them writes them into the cache (they stay
     // for later steps) and is also the only one that reads them, so a
     // workgroup-scope fence and barrier order the writes before its loads.
-    if (p.n_new > 0) {
+    if (PAGED && p.n_new > 0) {
+      // Paged: token k goes to position ctx_len + n_tail + k, a slot of one
+      // of the segment's last tail_entries entries (the append region).  It
+      // is written only when that entry is present and names the position.
+      const int64_t pr = p.page_rows;
+      const int64_t n_e = uniform64(offs[s]) / pr;
+      const int32_t* ents = p.entries + (int64_t)s * p.max_entries * 4;
+      bool wrote = false;
+      if (p.n_entries[s] <= p.max_entries && n_e >= p.tail_entries) {
+        const int64_t first = n_e - p.tail_entries;
+        for (int k = 0; k < p.n_new; ++k) {
+          const int64_t pos = (int64_t)p.ctx_len + p.n_tail + k;
+          const int64_t e = first + (pos / pr - p.ctx_len / pr);
+          const int64_t slot = pos - (pos / pr) * pr;
+          const int64_t row = e * pr + slot;
+          if (row < a || row >= bnd) continue;
+          const int32_t page = ents[e * 4], lpage = ents[e * 4 + 1];
+          if (page < 0 || page >= p.num_pages || lpage != pos / pr || slot < ents[e * 4 + 2] ||
+              slot >= ents[e * 4 + 3])
+            continue;
+          const int64_t dst = ((int64_t)page * pr + slot) * C::kLPR;
+          const int64_t src = ((int64_t)s * p.n_new + k) * C::kLPR;
+          for (int i = tid; i < C::kLPR; i += kThreads) {
+            reinterpret_cast<u32x4*>(const_cast<void*>(p.k))[dst + i] = reinterpret_cast<const u32x4*>(p.k_new)[src + i];
+            reinterpret_cast<u32x4*>(const_cast<void*>(p.v))[dst + i] = reinterpret_cast<const u32x4*>(p.v_new)[src + i];
+          }
+          wrote = true;
+        }
+      }
+      if (wrote) {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+        __syncthreads();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+      }
+    }
+    if (!PAGED && p.n_new > 0) {
       const int64_t base_len = seg_hi - seg_lo - p.n_new;
       const int64_t t_lo = (a > base_len ? a : base_len) - base_len;
       const int64_t t_hi = (bnd < base_len + p.n_new ? bnd : base_len + p.n_new) - base_len;
@@ -436,7 +539,61 @@ void decode_kernel(DecodeParams p) {
     const uint32_t v_lane = (uint32_t)(rp * C::kRowBytes + 16 * cc);
     constexpr int S = decode_stages<BF16, D, GP>();
     Tile<BF16, D, GP> tl[S];
-    for (int64_t a2 = a; a2 < bnd; a2 += C::kSubRows) {
+    if constexpr (PAGED) {
+      // Entries are staged kEntryChunk at a time; within a chunk the ring is
+      // the packed one, with descriptors built per tile.
+      const int64_t pr = p.page_rows;
+      const int64_t limit = (int64_t)p.ctx_len + p.n_tail + p.n_new;
+      const int32_t* ents = p.entries + (int64_t)s * p.max_entries * 4;
+      const int64_t e_end = (bnd + pr - 1) / pr;
+      for (int64_t c0 = a / pr; c0 < e_end; c0 += kEntryChunk) {
+        const int64_t c1 = c0 + kEntryChunk < e_end ? c0 + kEntryChunk : e_end;
+        __syncthreads();  // the previous chunk's entries are no longer read
+        if (tid < c1 - c0) {
+          const int4 e = *reinterpret_cast<const int4*>(ents + (c0 + tid) * 4);
+          // an entry naming a page outside the pool or slots outside a page
+          // attends nothing
+          const bool ok = e.x >= 0 && e.x < p.num_pages && e.y >= 0 && e.z >= 0 && e.z < e.w && e.w <= pr;
+          ent[tid][0] = ok ? e.x : 0;
+          ent[tid][1] = ok ? e.y : 0;
+          ent[tid][2] = ok ? e.z : 0;
+          ent[tid][3] = ok ? e.w : 0;
+        }
+        __syncthreads();
+        const int64_t r_lo = a > c0 * pr ? a : c0 * pr;
+        const int64_t r_hi = bnd < c1 * pr ? bnd : c1 * pr;
+        const int64_t k0 = r_lo / kTK;
+        const uint32_t ntile = (uint32_t)((r_hi + kTK - 1) / kTK - k0);
+        uint32_t t = wave;
+#pragma unroll
+        for (int i = 0; i < S - 1; ++i) {
+          __amdgpu_buffer_rsrc_t kr, vr;
+          uint32_t rr;
+          paged_tile<BF16, D, GP>(p, ent, c0, c1, k0, ntile, t + i * kWaves, a, bnd, limit, kr, vr, rr, tl[i].lo,
+                                  tl[i].hi);
+          load_tile(tl[i], kr, vr, rr, k_lane, v_lane);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        const uint32_t n_round = t < ntile ? (ntile - t + S * kWaves - 1) / (S * kWaves) : 0;
+        for (uint32_t r = 0; r < n_round; ++r) {
+#pragma unroll
+          for (int i = 0; i < S; ++i) {
+            Tile<BF16, D, GP>& nx = tl[(i + S - 1) % S];
+            __amdgpu_buffer_rsrc_t kr, vr;
+            uint32_t rr;
+            paged_tile<BF16, D, GP>(p, ent, c0, c1, k0, ntile, t + (S - 1) * kWaves, a, bnd, limit, kr, vr, rr,
+                                    nx.lo, nx.hi);
+            load_tile(nx, kr, vr, rr, k_lane, v_lane);
+            __builtin_amdgcn_sched_barrier(0);
+            if (t < ntile)
+              compute_tile<BF16, D, GP, true>(st, tl[i], qa, 0, 0, p.scale_log2, pbuf[wave], abuf[wave], j16, kg,
+                                              rp);
+            t += kWaves;
+          }
+        }
+      }
+    }
+    for (int64_t a2 = a; !PAGED && a2 < bnd; a2 += C::kSubRows) {
       const uint32_t nrows = (uint32_t)((bnd - a2) < C::kSubRows ? (bnd - a2) : C::kSubRows);
       const __amdgpu_buffer_rsrc_t kr = make_rsrc(kbase + a2 * C::kRowBytes, nrows * C::kRowBytes);
       const __amdgpu_buffer_rsrc_t vr = make_rsrc(vbase + a2 * C::kRowBytes, nrows * C::kRowBytes);
@@ -468,7 +625,8 @@ void decode_kernel(DecodeParams p) {
           load_tile(tl[(i + S - 1) % S], kr, vr, (t + (S - 1) * kWaves) * kTK, k_lane, v_lane);
           __builtin_amdgcn_sched_barrier(0);
           if (t < ntile)
-            compute_tile(st, tl[i], qa, t * kTK, nrows, p.scale_log2, pbuf[wave], abuf[wave], j16, kg, rp);
+            compute_tile<BF16, D, GP, false>(st, tl[i], qa, t * kTK, nrows, p.scale_log2, pbuf[wave], abuf[wave],
+                                             j16, kg, rp);
           t += kWaves;
         }
       }
@@ -641,9 +799,11 @@ inline int device_cus(int dev) {
   return c;
 }
 
-template <typename K>
-int32_t split_count(K kernel, int64_t rows_hint) {
+// One occupancy cache per kernel instantiation.
+template <bool BF16, int D, int GP, bool PAGED>
+int32_t split_count(int64_t rows_hint) {
   static std::atomic<int> occ_cache[kMaxDevices];
+  const auto kernel = decode_kernel<BF16, D, GP, PAGED>;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) dev = 0;
   const int cus = device_cus(dev);
@@ -665,8 +825,13 @@ int32_t split_count(K kernel, int64_t rows_hint) {
 template <bool BF16, int D, int GP>
 hipError_t launch_g(DecodeParams p, int64_t rows_hint, hipStream_t stream) {
   const size_t lds = (2 * (size_t)p.nseg + 1) * sizeof(int64_t);
-  p.P = split_count(decode_kernel<BF16, D, GP>, rows_hint);
-  hipLaunchKernelGGL((decode_kernel<BF16, D, GP>), dim3(p.P), dim3(kThreads), lds, stream, p);
+  if (p.entries != nullptr) {
+    p.P = split_count<BF16, D, GP, true>(rows_hint);
+    hipLaunchKernelGGL((decode_kernel<BF16, D, GP, true>), dim3(p.P), dim3(kThreads), lds, stream, p);
+  } else {
+    p.P = split_count<BF16, D, GP, false>(rows_hint);
+    hipLaunchKernelGGL((decode_kernel<BF16, D, GP, false>), dim3(p.P), dim3(kThreads), lds, stream, p);
+  }
   // Segments split over several workgroups are finished by the combine
   // kernel; when the call has a single split there is nothing to combine.
   if (p.P > 1)

@@ -122,4 +122,21 @@ __device__ __forceinline__ uint32_t nonzero_byte_bits(u32x4 w) {
   return bits;
 }
 
+// The 16 mask bytes of positions [j0, j0+16) of one mask row, zero beyond T
+// (16-byte loads when every row starts 16-byte aligned, bytes otherwise).
+__device__ __forceinline__ u32x4 load_mask16(const uint8_t* row, int64_t j0, int32_t T) {
+  u32x4 w = {0u, 0u, 0u, 0u};
+  if ((T & 15) == 0) {
+    if (j0 < T) w = *reinterpret_cast<const u32x4*>(row + j0);
+  } else {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int64_t j = j0 + e;
+      const uint32_t b = (j < T && row[j] != 0) ? 1u : 0u;
+      w[e >> 2] |= b << (8 * (e & 3));
+    }
+  }
+  return w;
+}
+
 }  // namespace dkv

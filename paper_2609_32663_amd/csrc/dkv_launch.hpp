@@ -54,6 +54,22 @@ struct AppendParams {
 };
 hipError_t launch_append(const AppendParams& p, hipStream_t stream);
 
+// ------------------------------------------------------ zero-copy page select
+struct PageSelectParams {
+  const uint8_t* mask;     // [nseg][T]
+  const int32_t* table;    // [nseg][pages_per_seg]
+  int32_t* entries;        // [nseg][max_entries][4]: page, logical page, lo, hi
+  int32_t* n_entries;      // [nseg]
+  int32_t* seg_len;        // [nseg]
+  uint8_t* page_used;      // [nseg][pages_per_seg] or null
+  int32_t* tile_cnt;       // [nseg][ntiles] runs starting in each tile (workspace)
+  int32_t* tile_kept;      // [nseg][ntiles] retained positions per tile (workspace)
+  int32_t* tile_base;      // [nseg][ntiles] first entry of each tile (workspace)
+  int32_t T, nseg, ntiles, page_rows, pages_per_seg, max_entries, cap;
+};
+size_t page_select_workspace_bytes(int64_t nseg, int64_t T);
+hipError_t launch_page_select(const PageSelectParams& p, hipStream_t stream);
+
 // ------------------------------------------------------------ decode attention
 constexpr int kDecodeMaxWG = 1024;  // upper bound on the split count
 
@@ -75,6 +91,16 @@ struct DecodeParams {
   float* partials;         // [(P + nseg)][GP][d + 2]
   int32_t* seg_meta;       // [nseg][2]: first record slot, piece count
   int32_t P;               // workgroups launched (set by launch_decode)
+  // Paged addressing (entries != null): k and v are page pools
+  // [num_pages][page_rows][d]; the rows of segment s are the page_rows slots
+  // of each of its entries, in entry order, and a slot is attended when it
+  // lies in the entry's [lo, hi) and its position (logical page * page_rows
+  // + slot) is below ctx_len + n_tail + n_new.
+  const int32_t* entries;    // [nseg][max_entries][4]: page, logical page, lo, hi
+  const int32_t* n_entries;  // [nseg]
+  int64_t num_pages;
+  int32_t max_entries, page_rows, ctx_len;
+  int32_t tail_entries;      // entries of the append region (the last ones of a segment)
 };
 int decode_group_pad(int G);
 size_t decode_partials_bytes(int nseg, int G, int head_dim);   // partial records

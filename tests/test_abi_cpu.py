@@ -226,6 +226,78 @@ def test_query_validation():
     assert call(B=0, q=NUL, out=NUL) == d.DKV_OK
 
 
+def test_page_select_validation():
+    lib = d.library()
+    assert d.dkv_page_select_workspace_bytes(256, 131072) == 3 * 4 * 256 * 32
+    assert d.dkv_page_select_workspace_bytes(-1, 10) == 0
+    lay = _lay(T=131072, S=128, R=1024, edges=tuple(128 * k for k in range(1016)))
+    # 1024 context pages + 1015 bins + sink + recent, and one page of the append region
+    assert d.dkv_page_entries_bound(lay, 64, 128) == 1024 + 1017 + 1
+    assert d.dkv_page_entries_bound(lay, 0, 128) == 1024 + 1017
+    assert d.dkv_page_entries_bound(lay, 64, 100) == -1
+
+    def call(nseg=4, T=1000, cap=24, pr=128, mask=A, table=A, pps=8, max_e=40, ent=A, ne=A, sl=A,
+             used=NUL, ws=A, ws_bytes=1 << 20):
+        return lib.dkv_page_select(nseg, T, cap, pr, mask, table, pps, max_e, ent, ne, sl, used, ws, ws_bytes,
+                                   NUL)
+
+    assert call(pr=48) == d.DKV_ERR_UNSUPPORTED
+    assert call(pr=16) == d.DKV_ERR_UNSUPPORTED
+    assert call(nseg=70000) == d.DKV_ERR_UNSUPPORTED
+    assert call(pps=7) == d.DKV_ERR_INVALID_ARG        # 7 * 128 < 1000 + 24
+    assert call(T=-1) == d.DKV_ERR_INVALID_ARG
+    assert call(cap=-1) == d.DKV_ERR_INVALID_ARG
+    assert call(max_e=-1) == d.DKV_ERR_INVALID_ARG
+    assert call(mask=NUL) == d.DKV_ERR_INVALID_ARG
+    assert call(table=NUL) == d.DKV_ERR_INVALID_ARG
+    assert call(ent=NUL) == d.DKV_ERR_INVALID_ARG
+    assert call(ne=NUL) == d.DKV_ERR_INVALID_ARG
+    assert call(sl=NUL) == d.DKV_ERR_INVALID_ARG
+    assert call(mask=MIS) == d.DKV_ERR_MISALIGNED
+    assert call(ent=MIS) == d.DKV_ERR_MISALIGNED
+    assert call(ws=NUL) == d.DKV_ERR_WORKSPACE
+    assert call(ws_bytes=3 * 4 * 4 - 1) == d.DKV_ERR_WORKSPACE
+    assert call(nseg=0, mask=NUL, table=NUL, ent=NUL, ne=NUL, sl=NUL, ws=NUL) == d.DKV_OK
+
+
+def test_paged_decode_validation():
+    lib = d.library()
+    ws = d.dkv_decode_workspace_bytes(1, 32, 8, 128)
+
+    def call(dtype=d.DKV_BF16, B=1, Hq=32, Hkv=8, dim=128, q=A, kn=NUL, vn=NUL, n_new=0, n_tail=0, cap=0,
+             kp=A, vp=A, n_pages=100, pr=128, ent=A, ne=A, max_e=10, T=1000, scale=1.0, out=A, w=A,
+             w_bytes=ws):
+        if n_new == 0 and kn == NUL:
+            return lib.dkv_paged_decode_attn(dtype, B, Hq, Hkv, dim, q, kp, vp, n_pages, pr, ent, ne, max_e, T,
+                                             n_tail, scale, 0, out, w, w_bytes, NUL)
+        return lib.dkv_paged_append_decode_attn(dtype, B, Hq, Hkv, dim, q, kn, vn, n_new, n_tail, cap, kp, vp,
+                                                n_pages, pr, ent, ne, max_e, T, scale, 0, out, w, w_bytes, NUL)
+
+    assert call(dtype=9) == d.DKV_ERR_INVALID_ARG
+    assert call(dim=96) == d.DKV_ERR_UNSUPPORTED
+    assert call(Hq=34, Hkv=2) == d.DKV_ERR_UNSUPPORTED
+    assert call(B=300) == d.DKV_ERR_UNSUPPORTED
+    assert call(pr=100) == d.DKV_ERR_UNSUPPORTED
+    assert call(n_tail=-1) == d.DKV_ERR_INVALID_ARG
+    assert call(T=-1) == d.DKV_ERR_INVALID_ARG
+    assert call(max_e=-1) == d.DKV_ERR_INVALID_ARG
+    assert call(n_pages=-1) == d.DKV_ERR_INVALID_ARG
+    assert call(scale=float("inf")) == d.DKV_ERR_INVALID_ARG
+    assert call(q=NUL) == d.DKV_ERR_INVALID_ARG
+    assert call(kp=NUL) == d.DKV_ERR_INVALID_ARG
+    assert call(ne=NUL) == d.DKV_ERR_INVALID_ARG
+    assert call(ent=NUL) == d.DKV_ERR_INVALID_ARG
+    assert call(out=MIS) == d.DKV_ERR_MISALIGNED
+    assert call(vp=MIS) == d.DKV_ERR_MISALIGNED
+    assert call(ent=MIS) == d.DKV_ERR_MISALIGNED
+    assert call(w=NUL) == d.DKV_ERR_WORKSPACE
+    assert call(w_bytes=ws - 1) == d.DKV_ERR_WORKSPACE
+    assert call(kn=A, vn=A, n_new=1, n_tail=8, cap=8) == d.DKV_ERR_CAPACITY
+    assert call(kn=NUL, vn=A, n_new=1, cap=8) == d.DKV_ERR_INVALID_ARG
+    assert call(kn=MIS, vn=A, n_new=1, cap=8) == d.DKV_ERR_MISALIGNED
+    assert call(B=0, q=NUL, out=NUL, kp=NUL, vp=NUL) == d.DKV_OK
+
+
 def test_binding_rejects_host_tensors():
     import torch
     lay = _lay()
