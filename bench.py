@@ -9,8 +9,11 @@ synthetic tensors generated on the GPU.
 One step is one decode step of the whole stack: for each layer, append the new
 token's K/V (dkv_append) and attend over the packed cache (dkv_decode_attn).
 The one-time pattern mapping and compaction, and the same step over the dense
-cache (dkv_dense_decode_attn), are timed in the same run.  Every number comes
-from HIP events on the stream the kernels run on.
+cache (dkv_dense_decode_attn), are timed in the same run, and so are the
+zero-copy paged variant (the stack in 128-row pages, the retained runs listed
+in place by dkv_page_select, one dkv_paged_append_decode_attn per layer) and
+the query block after the context.  Every number comes from HIP events on the
+stream the kernels run on.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W]
 
@@ -33,6 +36,7 @@ WORKLOAD = "llama8b_stack_128k"
 PEAK_HBM_GBPS = 8000.0
 PEAK_BF16_TFLOPS = 2500.0  # dense bf16 matrix peak
 QUERY_TOKENS = 256
+PAGE_ROWS = 128  # rows per page of the zero-copy paged variant
 PMC_FILE = os.path.join(ROOT, "profiles", "decode_attn_llama8b_stack_128k_pmc.json")
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2609_32663_amd", "csrc", f)
                for f in ("decode_attn.hip", "dkv_device.hpp", "dkv_launch.hpp")]
@@ -66,6 +70,14 @@ def kernel_hash():
         with open(path, "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
+
+
+def is_paged_kernel(name):
+    """Whether a decode_kernel instantiation is the paged one (its last
+    template argument)."""
+    import re
+    m = re.search(r"decode_kernel<([^>]*)>", name)
+    return bool(m) and m.group(1).replace(" ", "").split(",")[-1] == "true"
 
 
 def log(msg):
@@ -104,13 +116,14 @@ def trace_summary(trace_dir, bench_log, command):
     for line in open(bench_log):
         if line.startswith("{"):
             b = json.loads(line)
-    pairs = []
+    pairs, paged = [], []
     for i in range(len(rows) - 1):
         a, m = rows[i], rows[i + 1]
         if "decode_kernel" in a["Kernel_Name"] and "decode_merge_kernel" in m["Kernel_Name"]:
             s0, e0 = int(a["Start_Timestamp"]), int(a["End_Timestamp"])
             s1, e1 = int(m["Start_Timestamp"]), int(m["End_Timestamp"])
-            pairs.append(((e0 - s0) / 1e3, (e1 - s1) / 1e3, (e1 - s0) / 1e3))
+            (paged if is_paged_kernel(a["Kernel_Name"]) else pairs).append(
+                ((e0 - s0) / 1e3, (e1 - s1) / 1e3, (e1 - s0) / 1e3))
     # with the oracle baseline, one parity call per layer precedes the timing
     front = b["config"]["layers"] if b.get("parity_layer0") else 0
     timed_pairs = pairs[front:]
@@ -125,7 +138,8 @@ def trace_summary(trace_dir, bench_log, command):
             nm = r["Name"].replace("(anonymous namespace)::", "").replace("dkv::", "")
             lines.append(f"{nm[:58]:58s} {r['Calls']:>6s} {float(r['AverageNs']) / 1e3:9.2f} "
                          f"{float(r['MinNs']) / 1e3:9.2f} {float(r['MaxNs']) / 1e3:9.2f}")
-    for name, ps in (("packed", packed), ("dense", dense)):
+    groups = [("packed", packed), ("dense", dense)] + ([("paged", paged)] if paged else [])
+    for name, ps in groups:
         lines.append(f"{name:6s} calls {len(ps):4d}: decode_kernel mean {st.mean(p[0] for p in ps):7.2f}  "
                      f"decode_merge_kernel mean {st.mean(p[1] for p in ps):6.2f}  "
                      f"call (split start to combine end) mean {st.mean(p[2] for p in ps):7.2f} us")
@@ -134,6 +148,8 @@ def trace_summary(trace_dir, bench_log, command):
               f"ms_per_step {b['ms_per_step']}  value {b['value']} GB/s  roofline.avg_launch_us "
               f"{b['roofline']['avg_launch_us']}  frac {b['roofline']['frac']}",
               f"dense ms_per_step {b['dense']['ms_per_step']}  speedup_vs_dense {b['speedup_vs_dense']}",
+              *([f"paged ms_per_step {b['paged']['ms_per_step']}  avg_launch_us {b['paged']['avg_launch_us']}  "
+                 f"select_us {b['paged']['select_us']}"] if b.get("paged") else []),
               f"cpu_baseline {json.dumps(b['cpu_baseline'])}",
               f"parity_layer0 {json.dumps(b['parity_layer0'])}"]
     with open(TRACE_FILE, "w") as f:
@@ -188,7 +204,8 @@ def pmc_summary(fetch_csv, write_csv, command):
         copies = [v for n, v in rows if "copy" in n.lower() or "elementwise" in n.lower()]
         calib = (1 << 30) / (copies[-1] * 1024.0)
         calls = [rows[i][1] + rows[i + 1][1] for i in range(len(rows) - 1)
-                 if "decode_kernel" in rows[i][0] and "decode_merge_kernel" in rows[i + 1][0]]
+                 if "decode_kernel" in rows[i][0] and "decode_merge_kernel" in rows[i + 1][0]
+                 and not is_paged_kernel(rows[i][0])]
         packed = calls[: len(calls) // 2]
         per_call[key] = statistics.mean(packed) * 1024.0 * calib
         res[f"{key}_calibration"] = round(calib, 4)
@@ -389,14 +406,16 @@ def main():
                 P(vn.data_ptr()), 1, P(kl.data_ptr()), P(vl.data_ptr()), t_cap, n_valid, w.sm_scale,
                 P(out.data_ptr()), P(dws.data_ptr()), ws_bytes, P(sh))
 
-    def step_args(step, dense, sh):
+    def step_args(step, mode, sh):
         """One decode step: per layer, one call that appends the step's token
         and attends over the cache."""
         slot = step % cap
         acts = []
         for layer in range(L):
-            if dense:
+            if mode == "dense":
                 acts.append((lib.dkv_dense_append_decode_attn, dense_args(layer, T + slot, sh)))
+            elif mode == "paged":
+                acts.append((lib.dkv_paged_append_decode_attn, paged_args(layer, slot, sh)))
             else:
                 acts.append((lib.dkv_append_decode_attn, packed_args(layer, slot, sh)))
         return acts
@@ -407,23 +426,23 @@ def main():
             if st != 0:
                 raise d.DkvError(fn.__name__, st)
 
-    def decode_bytes(step, dense):
+    def decode_bytes(step, mode):
         n_tail = step % cap + 1
-        rows_step = (N * Hkv * (T + n_tail)) if dense else (retained + N * Hkv * n_tail)
+        rows_step = (N * Hkv * (T + n_tail)) if mode == "dense" else (retained + N * Hkv * n_tail)
         return rows_step * dim * elem * 2 + L * B * Hq * dim * (elem + 4) + L * nseg_layer * 12
 
     cap_stream = torch.cuda.Stream()
 
-    def timed(dense, steps, warmup):
+    def timed(mode, steps, warmup):
         """Step time as HIP-graph replays (one graph per step: each keeps its
         own append slot), plus the same steps launched eagerly."""
-        run(step_args(0, dense, sh))  # warm: first launches load code objects
+        run(step_args(0, mode, sh))  # warm: first launches load code objects
         torch.cuda.synchronize()
         graphs = []
         for s in range(warmup + steps):
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g, stream=cap_stream):
-                run(step_args(s, dense, cap_stream.cuda_stream))
+                run(step_args(s, mode, cap_stream.cuda_stream))
             graphs.append(g)
         for s in range(warmup):
             graphs[s].replay()
@@ -435,7 +454,7 @@ def main():
         b.record(stream)
         torch.cuda.synchronize()
         ms = a.elapsed_time(b) / steps
-        plans = [step_args(s, dense, sh) for s in range(warmup + steps)]
+        plans = [step_args(s, mode, sh) for s in range(warmup + steps)]
         for s in range(warmup):
             run(plans[s])
         torch.cuda.synchronize()
@@ -445,18 +464,121 @@ def main():
         b.record(stream)
         torch.cuda.synchronize()
         eager_ms = a.elapsed_time(b) / steps
-        nbytes = sum(decode_bytes(s, dense) for s in range(warmup, warmup + steps)) / steps
+        nbytes = sum(decode_bytes(s, mode) for s in range(warmup, warmup + steps)) / steps
         return ms, eager_ms, nbytes
 
+    paged_state = {}
+
+    def paged_args(layer, n_tail, sh):
+        """dkv_paged_append_decode_attn: write the token at position T + n_tail
+        of its page, attend through the layer's entries."""
+        ps = paged_state
+        off = layer * nseg_layer
+        kn, vn = new_kv[layer]
+        return (d.DKV_BF16, B, Hq, Hkv, dim, P(q_layers[layer].data_ptr()), P(kn.data_ptr()),
+                P(vn.data_ptr()), 1, n_tail, cap, P(ps["k_pool"].data_ptr()), P(ps["v_pool"].data_ptr()),
+                ps["n_pages"], PAGE_ROWS, P(ps["entries"].data_ptr() + off * ps["max_e"] * 16),
+                P(ps["n_ent"].data_ptr() + 4 * off), ps["max_e"], T, w.sm_scale, ps["rows"][layer],
+                P(out.data_ptr()), P(dws.data_ptr()), ws_bytes, P(sh))
+
     log("timing packed decode")
-    ms, eager_ms, nbytes = timed(False, args.steps, args.warmup)
+    ms, eager_ms, nbytes = timed("packed", args.steps, args.warmup)
     log("timing dense decode")
-    dms, deager_ms, dbytes = timed(True, args.steps, args.warmup)
+    dms, deager_ms, dbytes = timed("dense", args.steps, args.warmup)
     # A step is exactly one attention call per layer on one stream, so the
     # average duration of a call (split + combine kernel, with the gaps
     # between them) is the timed region's event interval over L calls.
     launch_ms = ms / L
     dlaunch_ms = dms / L
+
+    # ---------------- zero-copy paged variant -----------------------------
+    # The stack kept in 128-row pages of one pool (context plus append region
+    # per segment; each layer's pages shuffled within the layer's range, as an
+    # allocator would leave them).  dkv_page_select lists every segment's
+    # retained runs in place -- no K/V byte moves -- and a step runs one
+    # dkv_paged_append_decode_attn per layer.
+    log("paged variant: pools, selection")
+    PR = PAGE_ROWS
+    pps = -(-t_cap // PR)
+    n_pages = N * Hkv * pps
+    tables = []
+    for layer in range(L):
+        t_l, _ = di.page_table(nseg_layer, pps, seed=layer)
+        tables.append(t_l + layer * nseg_layer * pps)
+    k_pool = torch.empty((n_pages, PR, dim), dtype=torch.bfloat16, device=dev)
+    v_pool = torch.empty_like(k_pool)
+    for layer in range(L):
+        u = slice(layer * B, (layer + 1) * B)
+        di.fill_pages(k_pool, kd[u].reshape(nseg_layer, t_cap, dim), tables[layer], PR)
+        di.fill_pages(v_pool, vd[u].reshape(nseg_layer, t_cap, dim), tables[layer], PR)
+    del kd, vd  # the dense comparator is done
+    torch.cuda.empty_cache()
+    table_d = torch.from_numpy(np.concatenate(tables)).to(dev)
+    max_e = int(d.dkv_page_entries_bound(lay, cap, PR))
+    entries = torch.empty((N * Hkv, max_e, 4), dtype=torch.int32, device=dev)
+    n_ent = torch.empty(N * Hkv, dtype=torch.int32, device=dev)
+    p_len = torch.empty(N * Hkv, dtype=torch.int32, device=dev)
+    used = torch.empty((N * Hkv, pps), dtype=torch.uint8, device=dev)
+    sws = torch.empty(d.dkv_page_select_workspace_bytes(N * Hkv, T), dtype=torch.uint8, device=dev)
+    kvm = kv_mask.view(N * Hkv, T)
+    d.dkv_page_select(kvm, table_d, PR, cap, entries, n_ent, p_len, sws, page_used=used)
+    torch.cuda.synchronize()
+    a, b = ev(), ev()
+    a.record(stream)
+    for _ in range(5):
+        d.dkv_page_select(kvm, table_d, PR, cap, entries, n_ent, p_len, sws, page_used=used)
+    b.record(stream)
+    torch.cuda.synchronize()
+    select_us = a.elapsed_time(b) * 1e3 / 5
+    n_ent_h = n_ent.cpu().to(torch.int64)
+    assert int(n_ent_h.max()) <= max_e and torch.equal(p_len.cpu(), kv_len.cpu().view(-1))
+    paged_state.update(k_pool=k_pool, v_pool=v_pool, n_pages=n_pages, entries=entries, n_ent=n_ent,
+                       max_e=max_e,
+                       rows=[int(n_ent_h[layer * nseg_layer:(layer + 1) * nseg_layer].sum()) * PR
+                             for layer in range(L)])
+    pages_used = int(used.to(torch.int64).sum())
+    page_bytes = PR * dim * elem * 2
+    paged_parity = None
+    if not args.no_cpu_baseline:
+        # layer 0, one step: the token appended at position T, then attention
+        st_ = lib.dkv_paged_append_decode_attn(*paged_args(0, 0, sh))
+        if st_ != 0:
+            raise d.DkvError("dkv_paged_append_decode_attn", st_)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy()
+        n0 = nseg_layer * pps  # layer 0 owns pages [0, n0)
+        kp0 = k_pool[:n0].cpu().view(torch.int16).numpy().view(np.uint16)
+        vp0 = v_pool[:n0].cpu().view(torch.int16).numpy().view(np.uint16)
+        sel0 = o.page_select(okm0.reshape(nseg_layer, T), tables[0], PR, cap)
+        ent0 = entries[:nseg_layer].cpu().numpy()
+        same = all(np.array_equal(ent0[s_, :sel0["n_entries"][s_]], sel0["entries"][s_])
+                   for s_ in range(nseg_layer))
+        same &= bool(np.array_equal(n_ent[:nseg_layer].cpu().numpy(), sel0["n_entries"]))
+        qb0 = q_layers[0].cpu().view(torch.int16).numpy().view(np.uint16)
+        want = o.paged_decode_attn(qb0, kp0, vp0, sel0["entries"], PR, T, 1, w.sm_scale, Hkv, o.BF16)
+        err = float((np.abs(got - want).max(-1) / np.maximum(np.abs(want).max(-1), 1e-30)).max())
+        paged_parity = {"layers": 1, "max_rel_err": err, "entries_equal": bool(same)}
+        del kp0, vp0
+        log(f"paged parity layer 0: err {err:.2e}, entries equal {same}")
+    log("timing paged decode")
+    pms, peager_ms, pbytes = timed("paged", args.steps, args.warmup)
+    paged_res = {
+        "page_rows": PR, "ms_per_step": round(pms, 4), "eager_ms_per_step": round(peager_ms, 4),
+        "us_per_layer": round(pms * 1e3 / L, 2), "avg_launch_us": round(pms * 1e3 / L, 2),
+        "gb_per_s": round(pbytes / (pms * 1e-3) / 1e9, 2),
+        "launch_frac_of_peak": round(pbytes / L / (pms / L * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+        "vs_packed": round(ms / pms, 3), "speedup_vs_dense": round(dms / pms, 3),
+        "select_us": round(select_us, 1), "compact_us": round(compact_us, 1),
+        "entries_per_segment": {"mean": round(float(n_ent_h.float().mean()), 1), "max": int(n_ent_h.max()),
+                                "bound": max_e},
+        "slots_per_retained_row": round(float(n_ent_h.sum()) * PR / retained, 4),
+        "kv_cache_gib": {"pool": round(n_pages * page_bytes / 2 ** 30, 3),
+                         "pages_used": round(pages_used * page_bytes / 2 ** 30, 3)},
+        "kernel": "dkv_paged_append_decode_attn call: decode_kernel<bf16,128,4,paged> + decode_merge_kernel",
+        "parity_layer0": paged_parity,
+    }
+    log(f"paged: {pms:.3f} ms/step ({pms * 1e3 / L:.1f} us/layer), select {select_us:.0f} us, "
+        f"pages used {paged_res['kv_cache_gib']['pages_used']} GiB")
 
     # ---------------- query-block attention, all layers ------------------
     log("timing query-block attention")
@@ -620,6 +742,7 @@ def main():
                   "avg_launch_us": round(dlaunch_ms * 1e3, 2),
                   "launch_frac_of_peak": round(dbytes / L / (dlaunch_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)},
         "speedup_vs_dense": round(dms / ms, 3),
+        "paged": paged_res,
         "one_time": {"map_us": round(map_us, 1), "compact_us": round(compact_us, 1),
                      "compact_gb_per_s": round(compact_bytes / (compact_us * 1e-6) / 1e9, 1)},
         "kv_cache_gib": {"dense": round(N * Hkv * T * dim * elem * 2 / 2 ** 30, 3),

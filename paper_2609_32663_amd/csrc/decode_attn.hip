@@ -43,8 +43,8 @@
 // each tile gets its own buffer descriptor over the page rows from the tile's
 // start to the end of the attended slots, so slots past an entry's end (and
 // past the tokens appended so far) read zeros without touching memory, and the
-// softmax masks every slot outside [lo, hi).  Entries are staged through LDS
-// in chunks.
+// softmax masks every slot outside [lo, hi).  Each wave holds a chunk of 64
+// entries in registers, one per lane, and reads a tile's entry with readlane.
 
 #include <atomic>
 
@@ -275,7 +275,7 @@ __device__ __forceinline__ void compute_tile(WaveState<BF16, D, GP>& st, const T
 // such a workgroup fewer rows and keeps the slowest workgroup close to the
 // median.
 // Paged segments have page_rows units per entry (the slots outside an
-// entry's range are masked, not removed).
+// entry's range are masked, not removed).  Row counts are multiples of 32.
 template <bool PAGED>
 __device__ __forceinline__ int64_t segment_rows(const DecodeParams& p, int s) {
   if (PAGED) {
@@ -289,7 +289,7 @@ __device__ __forceinline__ int64_t segment_rows(const DecodeParams& p, int s) {
 // segments < s, pre[nseg] = total.  A non-empty segment s covers
 // [pre[s], pre[s + 1]); its first seg_cost units are the fixed cost and its
 // rows are the units after them.  The packed cache's segment offsets (the
-// paged cache's row counts) are copied to offs[] in the same pass, so the
+// paged cache's row counts and flags) are copied to offs[] in the same pass, so the
 // workgroup learns where its rows are after a single round trip to memory.
 // Called by every thread of a workgroup; `red` holds kWaves + 1 int64 of LDS.
 template <bool PAGED>
@@ -304,7 +304,9 @@ __device__ __forceinline__ void build_row_prefix(const DecodeParams& p, int64_t 
   for (int s = s_lo; s < s_hi; ++s) {
     if (!PAGED && p.seg_len != nullptr) offs[s] = p.seg_off[s];
     const int64_t rows = segment_rows<PAGED>(p, s);
-    if (PAGED) offs[s] = rows;
+    // paged: the row count, with bit 0 set when the segment's entry list was
+    // cut at max_entries (its append-region entries may then be missing)
+    if (PAGED) offs[s] = rows | (p.n_entries[s] > p.max_entries ? 1 : 0);
     const int64_t u = rows > 0 ? rows + seg_cost : 0;
     pre[s] = u;  // this thread's own slots: units now, prefix after the scan
     sum += u;
@@ -335,44 +337,58 @@ constexpr int decode_waves_per_eu() {
   return (decode_stages<BF16, D, GP>() == 2 && GP == 4 && (BF16 || D == 64)) ? 2 : 1;
 }
 
-constexpr int kEntryChunk = 64;  // paged entries staged in LDS at a time
+constexpr int kEntryChunk = kWave;  // paged entries held per wave (one per lane)
 
-// Descriptors of paged tile `t` of the current entry chunk: the tile's rows
-// [row0, row0 + 32) lie in one page; the attended ones are [lo, hi) of the
-// tile, clipped to the piece [a, bnd), the entry's slots and the positions
-// below `limit`.  The descriptors start at row lo, so rows before it get a
-// wrapped (huge) offset and rows from hi on lie past the range: both read
-// zeros without touching memory.  `row` is what load_tile adds to a row
-// index to get the row's offset in the descriptor.  Tiles past the chunk
-// read nothing.
+// An entry as validated when a wave loads it: one naming a page outside the
+// pool or slots outside a page becomes empty.
+struct PagedEntry {
+  int32_t page, lpage, lo, hi;
+};
+
+// Chunk-relative bounds of a paged piece, all in rows of the segment's row
+// space counted from the chunk's first entry (they fit 32 bits: a chunk
+// holds at most kEntryChunk pages).
+struct PagedChunk {
+  int32_t r_base;  // first tile's row
+  int32_t a, b;    // the piece [a, b), clamped to [-1, INT32_MAX]
+  int32_t n;       // entries in the chunk
+  uint32_t ntile;  // tiles of the piece in the chunk
+};
+
+// Descriptors of paged tile `t` of the current chunk: the tile's rows
+// [r0, r0 + 32) lie in one page; the attended ones are [lo, hi) of the tile,
+// clipped to the piece, the entry's slots and the positions below `limit`.
+// The descriptors start at row lo, so rows before it get a wrapped (huge)
+// offset and rows from hi on lie past the range: both read zeros without
+// touching memory.  `row` is what load_tile adds to a row index to get the
+// row's offset in the descriptor.  Tiles past the chunk read nothing.
 template <bool BF16, int D, int GP>
-__device__ __forceinline__ void paged_tile(const DecodeParams& p, const int32_t (*ent)[4], int64_t c0, int64_t c1,
-                                           int64_t k0, uint32_t ntile, uint32_t t, int64_t a, int64_t bnd,
-                                           int64_t limit, __amdgpu_buffer_rsrc_t& kr, __amdgpu_buffer_rsrc_t& vr,
-                                           uint32_t& row, int32_t& lo, int32_t& hi) {
+__device__ __forceinline__ void paged_tile(const DecodeParams& p, const PagedEntry& ent, const PagedChunk& ck,
+                                           uint32_t t, int32_t limit, __amdgpu_buffer_rsrc_t& kr,
+                                           __amdgpu_buffer_rsrc_t& vr, uint32_t& row, int32_t& lo, int32_t& hi) {
   using C = DecodeCfg<BF16, D, GP>;
-  const int64_t pr = p.page_rows;
-  const int64_t row0 = (k0 + t) * kTK;
-  const int64_t e = row0 / pr;
-  const int64_t li = e - c0 < c1 - c0 - 1 ? e - c0 : c1 - c0 - 1;
-  const int32_t page = __builtin_amdgcn_readfirstlane(ent[li][0]);
-  const int32_t lpage = __builtin_amdgcn_readfirstlane(ent[li][1]);
-  const int32_t e_lo = __builtin_amdgcn_readfirstlane(ent[li][2]);
-  const int32_t e_hi = __builtin_amdgcn_readfirstlane(ent[li][3]);
-  const int64_t slot0 = row0 - e * pr;
-  int64_t l = a - row0;
+  const int sh = p.page_shift;  // page sizes are powers of two
+  const int32_t r0 = ck.r_base + (int32_t)t * kTK;
+  const int32_t e = r0 >> sh;
+  const int li = e < ck.n - 1 ? e : ck.n - 1;
+  const int32_t page = __builtin_amdgcn_readlane(ent.page, li);
+  const int32_t lpage = __builtin_amdgcn_readlane(ent.lpage, li);
+  const int32_t e_lo = __builtin_amdgcn_readlane(ent.lo, li);
+  const int32_t e_hi = __builtin_amdgcn_readlane(ent.hi, li);
+  const int32_t slot0 = r0 & ((1 << sh) - 1);
+  int32_t l = ck.a - r0;
   if (e_lo - slot0 > l) l = e_lo - slot0;
   if (l < 0) l = 0;
   if (l > kTK) l = kTK;
-  int64_t h = bnd - row0;
+  int32_t h = ck.b - r0;
   if (e_hi - slot0 < h) h = e_hi - slot0;
-  if (limit - ((int64_t)lpage * pr + slot0) < h) h = limit - ((int64_t)lpage * pr + slot0);
+  if (limit - (lpage << sh) - slot0 < h) h = limit - (lpage << sh) - slot0;
   if (h > kTK) h = kTK;
-  if (t >= ntile || h < l) h = l;
-  lo = (int32_t)l;
-  hi = (int32_t)h;
-  row = (uint32_t)(-(int32_t)l);
-  const int64_t off = ((int64_t)page * pr + slot0 + l) * C::kRowBytes;
+  if (t >= ck.ntile || h < l) h = l;
+  lo = l;
+  hi = h;
+  row = (uint32_t)(-l);
+  const int64_t off = (((int64_t)page << sh) + slot0 + l) * C::kRowBytes;
   const uint32_t bytes = (uint32_t)(h - l) * C::kRowBytes;
   kr = make_rsrc(reinterpret_cast<const char*>(p.k) + off, bytes);
   vr = make_rsrc(reinterpret_cast<const char*>(p.v) + off, bytes);
@@ -384,7 +400,6 @@ void decode_kernel(DecodeParams p) {
   using C = DecodeCfg<BF16, D, GP>;
   extern __shared__ __align__(16) int64_t pre[];          // [nseg + 1] unit prefix, then [nseg] offsets / rows
   int64_t* offs = pre + p.nseg + 1;
-  __shared__ __align__(16) int32_t ent[PAGED ? kEntryChunk : 1][4];  // staged paged entries
   __shared__ __align__(16) float pbuf[kWaves][kTK][GP];   // probabilities per wave tile
   __shared__ __align__(16) float abuf[kWaves][GP];        // rescale factors per wave
   __shared__ __align__(16) float wacc[kWaves][GP][D];     // per-wave accumulators
@@ -458,41 +473,7 @@ void decode_kernel(DecodeParams p) {
     // workgroup whose slice holds them writes them into the cache (they stay
     // for later steps) and is also the only one that reads them, so a
     // workgroup-scope fence and barrier order the writes before its loads.
-    if (PAGED && p.n_new > 0) {
-      // Paged: token k goes to position ctx_len + n_tail + k, a slot of one
-      // of the segment's last tail_entries entries (the append region).  It
-      // is written only when that entry is present and names the position.
-      const int64_t pr = p.page_rows;
-      const int64_t n_e = uniform64(offs[s]) / pr;
-      const int32_t* ents = p.entries + (int64_t)s * p.max_entries * 4;
-      bool wrote = false;
-      if (p.n_entries[s] <= p.max_entries && n_e >= p.tail_entries) {
-        const int64_t first = n_e - p.tail_entries;
-        for (int k = 0; k < p.n_new; ++k) {
-          const int64_t pos = (int64_t)p.ctx_len + p.n_tail + k;
-          const int64_t e = first + (pos / pr - p.ctx_len / pr);
-          const int64_t slot = pos - (pos / pr) * pr;
-          const int64_t row = e * pr + slot;
-          if (row < a || row >= bnd) continue;
-          const int32_t page = ents[e * 4], lpage = ents[e * 4 + 1];
-          if (page < 0 || page >= p.num_pages || lpage != pos / pr || slot < ents[e * 4 + 2] ||
-              slot >= ents[e * 4 + 3])
-            continue;
-          const int64_t dst = ((int64_t)page * pr + slot) * C::kLPR;
-          const int64_t src = ((int64_t)s * p.n_new + k) * C::kLPR;
-          for (int i = tid; i < C::kLPR; i += kThreads) {
-            reinterpret_cast<u32x4*>(const_cast<void*>(p.k))[dst + i] = reinterpret_cast<const u32x4*>(p.k_new)[src + i];
-            reinterpret_cast<u32x4*>(const_cast<void*>(p.v))[dst + i] = reinterpret_cast<const u32x4*>(p.v_new)[src + i];
-          }
-          wrote = true;
-        }
-      }
-      if (wrote) {
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-        __syncthreads();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-      }
-    }
+    // (Paged segments append inside the entry loop below.)
     if (!PAGED && p.n_new > 0) {
       const int64_t base_len = seg_hi - seg_lo - p.n_new;
       const int64_t t_lo = (a > base_len ? a : base_len) - base_len;
@@ -540,37 +521,76 @@ void decode_kernel(DecodeParams p) {
     constexpr int S = decode_stages<BF16, D, GP>();
     Tile<BF16, D, GP> tl[S];
     if constexpr (PAGED) {
-      // Entries are staged kEntryChunk at a time; within a chunk the ring is
-      // the packed one, with descriptors built per tile.
+      // Each wave loads the piece's entries kEntryChunk at a time, one per
+      // lane; within a chunk the ring is the packed one, with descriptors
+      // built per tile.
       const int64_t pr = p.page_rows;
-      const int64_t limit = (int64_t)p.ctx_len + p.n_tail + p.n_new;
+      const int sh = p.page_shift;
+      const int32_t limit = p.ctx_len + p.n_tail + p.n_new;  // checked to fit 31 bits
       const int32_t* ents = p.entries + (int64_t)s * p.max_entries * 4;
-      const int64_t e_end = (bnd + pr - 1) / pr;
-      for (int64_t c0 = a / pr; c0 < e_end; c0 += kEntryChunk) {
+      const int64_t e_end = (bnd + pr - 1) >> sh;
+      const int64_t enc = uniform64(offs[s]);
+      // the append region is the last tail_entries entries, unless the list
+      // was cut short
+      const int64_t tail0 = (enc & 1) ? -1 : (enc >> sh) - p.tail_entries;
+      for (int64_t c0 = a >> sh; c0 < e_end; c0 += kEntryChunk) {
         const int64_t c1 = c0 + kEntryChunk < e_end ? c0 + kEntryChunk : e_end;
-        __syncthreads();  // the previous chunk's entries are no longer read
-        if (tid < c1 - c0) {
-          const int4 e = *reinterpret_cast<const int4*>(ents + (c0 + tid) * 4);
-          // an entry naming a page outside the pool or slots outside a page
-          // attends nothing
-          const bool ok = e.x >= 0 && e.x < p.num_pages && e.y >= 0 && e.z >= 0 && e.z < e.w && e.w <= pr;
-          ent[tid][0] = ok ? e.x : 0;
-          ent[tid][1] = ok ? e.y : 0;
-          ent[tid][2] = ok ? e.z : 0;
-          ent[tid][3] = ok ? e.w : 0;
+        PagedEntry ent = {0, 0, 0, 0};
+        if (lane < c1 - c0) {
+          const int4 e = *reinterpret_cast<const int4*>(ents + (c0 + lane) * 4);
+          // positions (logical page << shift) + slot must fit 31 bits
+          const bool ok = e.x >= 0 && e.x < p.num_pages && e.y >= 0 && e.y <= (INT32_MAX >> sh) && e.z >= 0 &&
+                          e.z < e.w && e.w <= pr;
+          if (ok) ent = PagedEntry{e.x, e.y, e.z, e.w};
         }
-        __syncthreads();
-        const int64_t r_lo = a > c0 * pr ? a : c0 * pr;
-        const int64_t r_hi = bnd < c1 * pr ? bnd : c1 * pr;
+        // Appended token k is position ctx_len + n_tail + k, a slot of one of
+        // the append-region entries; the workgroup whose piece holds that
+        // slot's row writes it, from the staged entry, before loading it.
+        if (p.n_new > 0 && tail0 >= 0) {
+          bool wrote = false;
+          for (int k = 0; k < p.n_new; ++k) {
+            const int64_t pos = (int64_t)p.ctx_len + p.n_tail + k;
+            const int64_t e = tail0 + ((pos >> sh) - ((int64_t)p.ctx_len >> sh));
+            const int64_t slot = pos & (pr - 1);
+            const int64_t row = (e << sh) + slot;
+            if (row < a || row >= bnd || e < c0 || e >= c1) continue;
+            const int li = (int)(e - c0);
+            if (__builtin_amdgcn_readlane(ent.lpage, li) != (pos >> sh) || slot < __builtin_amdgcn_readlane(ent.lo, li) ||
+                slot >= __builtin_amdgcn_readlane(ent.hi, li))
+              continue;
+            const int64_t dst = (((int64_t)__builtin_amdgcn_readlane(ent.page, li) << sh) + slot) * C::kLPR;
+            const int64_t src = ((int64_t)s * p.n_new + k) * C::kLPR;
+            for (int i = tid; i < C::kLPR; i += kThreads) {
+              reinterpret_cast<u32x4*>(const_cast<void*>(p.k))[dst + i] =
+                  reinterpret_cast<const u32x4*>(p.k_new)[src + i];
+              reinterpret_cast<u32x4*>(const_cast<void*>(p.v))[dst + i] =
+                  reinterpret_cast<const u32x4*>(p.v_new)[src + i];
+            }
+            wrote = true;
+          }
+          if (wrote) {
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+            __syncthreads();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+          }
+        }
+        const int64_t cb = c0 << sh;
+        const int64_t r_lo = a > cb ? a : cb;
+        const int64_t r_hi = bnd < (c1 << sh) ? bnd : (c1 << sh);
         const int64_t k0 = r_lo / kTK;
-        const uint32_t ntile = (uint32_t)((r_hi + kTK - 1) / kTK - k0);
+        PagedChunk ck;
+        ck.r_base = (int32_t)(k0 * kTK - cb);
+        ck.a = (int32_t)(a - cb < -1 ? -1 : a - cb);
+        ck.b = (int32_t)(bnd - cb > INT32_MAX ? INT32_MAX : bnd - cb);
+        ck.n = (int32_t)(c1 - c0);
+        ck.ntile = (uint32_t)((r_hi + kTK - 1) / kTK - k0);
+        const uint32_t ntile = ck.ntile;
         uint32_t t = wave;
 #pragma unroll
         for (int i = 0; i < S - 1; ++i) {
           __amdgpu_buffer_rsrc_t kr, vr;
           uint32_t rr;
-          paged_tile<BF16, D, GP>(p, ent, c0, c1, k0, ntile, t + i * kWaves, a, bnd, limit, kr, vr, rr, tl[i].lo,
-                                  tl[i].hi);
+          paged_tile<BF16, D, GP>(p, ent, ck, t + i * kWaves, limit, kr, vr, rr, tl[i].lo, tl[i].hi);
           load_tile(tl[i], kr, vr, rr, k_lane, v_lane);
           __builtin_amdgcn_sched_barrier(0);
         }
@@ -581,8 +601,7 @@ void decode_kernel(DecodeParams p) {
             Tile<BF16, D, GP>& nx = tl[(i + S - 1) % S];
             __amdgpu_buffer_rsrc_t kr, vr;
             uint32_t rr;
-            paged_tile<BF16, D, GP>(p, ent, c0, c1, k0, ntile, t + (S - 1) * kWaves, a, bnd, limit, kr, vr, rr,
-                                    nx.lo, nx.hi);
+            paged_tile<BF16, D, GP>(p, ent, ck, t + (S - 1) * kWaves, limit, kr, vr, rr, nx.lo, nx.hi);
             load_tile(nx, kr, vr, rr, k_lane, v_lane);
             __builtin_amdgcn_sched_barrier(0);
             if (t < ntile)

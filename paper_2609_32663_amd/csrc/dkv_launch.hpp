@@ -99,7 +99,7 @@ struct DecodeParams {
   const int32_t* entries;    // [nseg][max_entries][4]: page, logical page, lo, hi
   const int32_t* n_entries;  // [nseg]
   int64_t num_pages;
-  int32_t max_entries, page_rows, ctx_len;
+  int32_t max_entries, page_rows, page_shift, ctx_len;  // page_rows = 1 << page_shift
   int32_t tail_entries;      // entries of the append region (the last ones of a segment)
 };
 int decode_group_pad(int G);

@@ -75,6 +75,7 @@ dkv_status paged_decode(dkv_dtype dtype, int32_t batch, int32_t hq, int32_t hkv,
   p.num_pages = num_pages;
   p.max_entries = max_entries;
   p.page_rows = page_rows;
+  p.page_shift = __builtin_ctz((unsigned)page_rows);
   p.ctx_len = context_len;
   p.tail_entries = n_new > 0 ? tail_entry_count(context_len, append_cap, page_rows) : 0;
   // the kernel tells paged from packed addressing by a non-null entry
