@@ -194,24 +194,32 @@ def pmc_summary(fetch_csv, write_csv, command):
     """HBM traffic of one packed attention call from FETCH_SIZE / WRITE_SIZE
     (KiB per dispatch).  Each counter is scaled by what it reads for the
     1 GiB device copy run at the end (which reads and writes exactly 1 GiB),
-    and the packed calls are the first half of the decode/combine dispatch
-    pairs (the script times the packed path before the dense one)."""
+    and the packed calls are the first half of the non-paged decode/combine
+    dispatch pairs (the script times the packed path before the dense one);
+    the paged calls, told apart by the kernel's template flag, are averaged
+    on their own."""
     import statistics
     res = {"kernel_sha256_16": kernel_hash(), "command": command, "unit": "bytes per call"}
-    per_call = {}
+    per_call, per_paged = {}, {}
     for key, path, counter in (("fetch", fetch_csv, "FETCH_SIZE"), ("write", write_csv, "WRITE_SIZE")):
         rows = pmc_per_dispatch(path, counter)
         copies = [v for n, v in rows if "copy" in n.lower() or "elementwise" in n.lower()]
         calib = (1 << 30) / (copies[-1] * 1024.0)
-        calls = [rows[i][1] + rows[i + 1][1] for i in range(len(rows) - 1)
-                 if "decode_kernel" in rows[i][0] and "decode_merge_kernel" in rows[i + 1][0]
-                 and not is_paged_kernel(rows[i][0])]
+        pairs = [(is_paged_kernel(rows[i][0]), rows[i][1] + rows[i + 1][1]) for i in range(len(rows) - 1)
+                 if "decode_kernel" in rows[i][0] and "decode_merge_kernel" in rows[i + 1][0]]
+        calls = [v for pg, v in pairs if not pg]
         packed = calls[: len(calls) // 2]
+        paged = [v for pg, v in pairs if pg]
         per_call[key] = statistics.mean(packed) * 1024.0 * calib
         res[f"{key}_calibration"] = round(calib, 4)
         res[f"{key}_bytes_per_call"] = int(per_call[key])
         res[f"{key}_calls_counted"] = len(packed)
+        if paged:
+            per_paged[key] = statistics.mean(paged) * 1024.0 * calib
+            res[f"paged_{key}_bytes_per_call"] = int(per_paged[key])
     res["traffic_bytes_per_launch"] = int(per_call["fetch"] + per_call["write"])
+    if len(per_paged) == 2:
+        res["paged_traffic_bytes_per_launch"] = int(per_paged["fetch"] + per_paged["write"])
     with open(PMC_FILE, "w") as f:
         json.dump(res, f, indent=1)
         f.write("\n")
@@ -575,6 +583,7 @@ def main():
         "kv_cache_gib": {"pool": round(n_pages * page_bytes / 2 ** 30, 3),
                          "pages_used": round(pages_used * page_bytes / 2 ** 30, 3)},
         "kernel": "dkv_paged_append_decode_attn call: decode_kernel<bf16,128,4,paged> + decode_merge_kernel",
+        "bytes_per_launch": int(pbytes / L), "traffic": None,
         "parity_layer0": paged_parity,
     }
     log(f"paged: {pms:.3f} ms/step ({pms * 1e3 / L:.1f} us/layer), select {select_us:.0f} us, "
@@ -706,6 +715,7 @@ def main():
             pmc = json.load(f)
         if pmc.get("kernel_sha256_16") == kernel_hash():
             traffic = pmc.get("traffic_bytes_per_launch")
+            paged_res["traffic"] = pmc.get("paged_traffic_bytes_per_launch")
 
     res = {
         "metric": METRIC,
