@@ -46,12 +46,16 @@ __all__ = [
     "query_block",
     "page_table",
     "fill_pages",
+    "retention_probs",
+    "PATTERN_FAMILIES",
+    "pattern_family",
 ]
 
 # stream ids of the seed derivation
 STREAM_PATTERN, STREAM_K, STREAM_V, STREAM_Q, STREAM_NEW_K, STREAM_NEW_V = range(6)
 STREAM_BLOCK_Q, STREAM_BLOCK_K, STREAM_BLOCK_V = 6, 7, 8
 STREAM_PAGES = 9
+STREAM_PROBS, STREAM_FAMILY = 10, 11
 
 
 def seed_of(*parts):
@@ -122,12 +126,13 @@ class Workload:
     q_std: float
     budget: float = None          # physical retained fraction; None: Bernoulli rate
     keep_prob: float = None       # plain Bernoulli(p) per (q head, bin) when budget is None
-    family: str = "bernoulli"     # "bernoulli" or "mixture"
+    family: str = "bernoulli"     # "bernoulli", "mixture" or "topk" (exact-budget export)
     always_keep_bins: tuple = ()  # bins kept by every query head
     recent_only_frac: float = 0.0  # fraction of groups that keep only always_keep_bins
     decode_steps: int = 1
     append_cap: int = 16
     budgets: tuple = field(default=())  # extra budgets measured on the same shape
+    rho: float = None             # logical retention ratio of a "topk" workload
 
     @property
     def num_units(self):
@@ -175,6 +180,11 @@ WORKLOADS = {
         bin_edges=log_bin_edges(32768, 24), dtype="bf16", sm_scale=1.0,
         q_std=1.0 / math.sqrt(128), budget=0.20, always_keep_bins=(0,),
         recent_only_frac=0.2, decode_steps=16, append_cap=16, budgets=(0.10, 0.20, 0.50)),
+    "llama8b_stack_128k_paper_bins": Workload(
+        name="llama8b_stack_128k_paper_bins", cfg_id=6, num_layers=32, batch=1, num_q_heads=32,
+        num_kv_heads=8, head_dim=128, context_len=131072, sink=128, recent=1024,
+        bin_edges=uniform_bin_edges(128, (131072 - 128 - 1024) // 128), dtype="bf16", sm_scale=1.0,
+        q_std=1.0 / math.sqrt(128), family="topk", rho=0.2, decode_steps=64, append_cap=64),
     "qwen7b_stack_bs4_128k": Workload(
         name="qwen7b_stack_bs4_128k", cfg_id=5, num_layers=28, batch=4, num_q_heads=28,
         num_kv_heads=4, head_dim=128, context_len=131072, sink=128, recent=1024,
@@ -239,6 +249,9 @@ def make_pattern(w, budget=None, all_keep=False):
     G = w.group
     if all_keep:
         return np.ones((N, Hq, D), dtype=np.uint8), {"target": 1.0}
+    if w.family == "topk":
+        raise ValueError(f"{w.name}: the pattern is the exact-budget export of retention_probs "
+                         "(dkv_topk_pattern, or the oracle's topk_mask), not an input recipe")
 
     def rng_of_unit(n, sub=0):
         return np.random.default_rng(seed_of(w.cfg_id, n, STREAM_PATTERN, sub))
@@ -398,3 +411,100 @@ def fill_pages(pool, x, table, page_rows):
     if r0 < rows and full < table.shape[1]:
         for s in range(n):
             pool[int(table[s, full]), :rows - r0] = x[s, r0:rows]
+
+
+# ---------------------------------------------------------------------------
+# retention probabilities and the ablation pattern families
+# ---------------------------------------------------------------------------
+
+def retention_probs(num_layers, num_q_heads, num_kv_heads, num_bins, seed, group_weight=1.5):
+    """Stand-in for learned gate probabilities p[layer][query head][bin] in
+    [0.001, 0.999] (the clip range of the paper's gates), float32.
+
+    Each (layer, KV group) draws a distance profile -- near-favouring,
+    far-favouring or bimodal, with random strength -- shared by its query
+    heads with weight `group_weight`; each query head adds its own noise, so
+    heads of a group agree more than independent heads would (the union then
+    keeps fewer positions).  Probabilities are quantised to steps of 1/1024,
+    so exact ties occur.
+    """
+    rng = np.random.default_rng(seed_of(STREAM_PROBS, seed))
+    L, H, Hkv, D = int(num_layers), int(num_q_heads), int(num_kv_heads), int(num_bins)
+    G = H // Hkv
+    x = np.arange(D, dtype=np.float64) / max(D - 1, 1)
+    prof = np.empty((L, Hkv, D))
+    for layer in range(L):
+        for g in range(Hkv):
+            kind = rng.integers(3)
+            a = rng.uniform(2.0, 8.0)
+            if kind == 0:
+                prof[layer, g] = -a * x
+            elif kind == 1:
+                prof[layer, g] = -a * (1.0 - x)
+            else:
+                prof[layer, g] = -a * np.minimum(x, 1.0 - x) * 2.0
+            prof[layer, g] += rng.normal(0.0, 0.5, size=D)
+    logits = group_weight * np.repeat(prof, G, axis=1) + rng.normal(0.0, 1.0, size=(L, H, D))
+    p = 1.0 / (1.0 + np.exp(-logits))
+    p = np.clip(np.round(p * 1024.0) / 1024.0, 0.001, 0.999)
+    return p.astype(np.float32)
+
+
+PATTERN_FAMILIES = ("head_only", "distance_only", "distance_shuffled", "fully_shuffled")
+
+
+def pattern_family(base, kind, num_kv_heads, seed):
+    """Structural variants of a pattern [N][Hq][D], built to keep its physical
+    cost (the number of (unit, KV group, bin) cells some query head of the
+    group keeps) when bins have equal widths -- the controls of the paper's
+    ablation (Sec. 4.4; Appendix, task-level ablation):
+
+    head_only          each query head keeps all of its bins or none: the
+                       groups with the most kept cells keep every bin, with
+                       the heads that kept anything (n_keep = round(cells/D));
+    distance_only      one bin set per unit shared by all query heads: the
+                       round(cells_n / Hkv) bins the most groups keep (ties to
+                       the lower bin);
+    distance_shuffled  one random bin permutation per (unit, group), applied
+                       to all its heads: per-head counts and the group's cell
+                       count are kept, the distances are not;
+    fully_shuffled     the (unit, group, bin) cells, each the G-bit vector of
+                       the group's heads, are permuted over all units, groups
+                       and bins, and each vector's bits among its heads:
+                       logical entries and kept cells are kept, nothing else.
+    """
+    base = np.asarray(base, dtype=np.uint8) != 0
+    N, H, D = base.shape
+    Hkv = int(num_kv_heads)
+    G = H // Hkv
+    rng = np.random.default_rng(seed_of(STREAM_FAMILY, PATTERN_FAMILIES.index(kind), seed))
+    cells = base.reshape(N, Hkv, G, D)            # [unit][group][head in group][bin]
+    kept = cells.any(axis=2)                      # [unit][group][bin]
+    out = np.zeros((N, Hkv, G, D), dtype=bool)
+    if kind == "head_only":
+        n_keep = int(round(kept.sum() / float(D)))
+        score = kept.sum(axis=2).reshape(-1)      # cells per (unit, group)
+        order = np.lexsort((np.arange(score.size), -score))[:n_keep]
+        heads = cells.any(axis=3).reshape(N * Hkv, G)
+        flat = out.reshape(N * Hkv, G, D)
+        for c in order:
+            who = heads[c] if heads[c].any() else np.eye(G, dtype=bool)[0]
+            flat[c, who, :] = True
+    elif kind == "distance_only":
+        for n in range(N):
+            c = int(round(kept[n].sum() / float(Hkv)))
+            votes = kept[n].sum(axis=0)           # groups keeping each bin
+            bins = np.lexsort((np.arange(D), -votes))[:c]
+            out[n, :, :, bins] = True
+    elif kind == "distance_shuffled":
+        for n in range(N):
+            for g in range(Hkv):
+                out[n, g] = cells[n, g][:, rng.permutation(D)]
+    elif kind == "fully_shuffled":
+        vec = cells.transpose(0, 1, 3, 2).reshape(-1, G)   # one G-bit vector per cell
+        vec = vec[rng.permutation(vec.shape[0])]
+        vec = np.array([v[rng.permutation(G)] for v in vec])
+        out = vec.reshape(N, Hkv, D, G).transpose(0, 1, 3, 2)
+    else:
+        raise ValueError(f"unknown pattern family {kind!r}")
+    return np.ascontiguousarray(out.reshape(N, H, D)).astype(np.uint8)

@@ -18,6 +18,8 @@
  *   dkv_page_select   zero-copy alternative to the pack: the retained runs
  *                     of a paged cache, listed in place
  *   dkv_paged_decode_attn  decode over a paged cache through those entries
+ *   dkv_topk_pattern  the exact-budget export of a pattern from retention
+ *                     probabilities (K_rho largest entries)
  *
  * plus dkv_dense_decode_attn, the same attention kernel over an uncompressed
  * cache (the "Dense" comparator of Sec. 4.3).
@@ -279,6 +281,42 @@ dkv_status dkv_query_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_heads,
                           const int64_t *seg_off, const int32_t *seg_len, float sm_scale,
                           int64_t rows_hint, float *out, void *workspace, size_t workspace_bytes,
                           void *stream);
+
+/*
+ * Exact-budget pattern export (Sec. 3.3, Eq. (topk-pattern); Appendix A,
+ * exact-budget refinement).  The learned pattern keeps the K_rho entries of
+ * the L x H x D tensor of retention probabilities with the largest
+ * probability, K_rho = round(rho L H D) for a logical retention ratio rho.
+ */
+
+/* K_rho = round(rho * L * H * D), halves rounded up (the paper leaves them
+ * open), computed in double (host).  Returns -1 unless 0 <= rho <= 1 and the
+ * sizes are non-negative. */
+int64_t dkv_budget_entries(double rho, int32_t num_layers, int32_t num_q_heads, int32_t num_bins);
+
+/* Workspace bytes of dkv_topk_pattern (host, no GPU call); 0 for an empty or
+ * too large tensor. */
+size_t dkv_topk_workspace_bytes(int32_t num_layers, int32_t num_q_heads, int32_t num_bins);
+
+/*
+ * dkv_topk_pattern -- TopKMask(P, k): pattern[l][h][d] = 1 for the k largest
+ * probs[l][h][d] over the whole tensor, 0 elsewhere.
+ *
+ * probs    float32 [L][Hq][D], 16-byte aligned (any values; NaN ranks below
+ *          every number, -0 equals +0).
+ * k        0 <= k <= L * Hq * D (DKV_ERR_INVALID_ARG otherwise), e.g.
+ *          dkv_budget_entries(rho, L, Hq, D).
+ * pattern  out, uint8 [L][Hq][D], 4-byte aligned, with exactly k ones: the
+ *          pattern argument of dkv_map_pattern (one unit per layer).
+ * workspace  dkv_topk_workspace_bytes(...) bytes, 4-byte aligned, no initial
+ *          contents required (DKV_ERR_WORKSPACE otherwise).
+ * Ties at the k-th value go to the lowest flat (layer, head, bin) indices, so
+ * the result is unique and deterministic.  L * Hq * D < 2^31.  A radix
+ * select of eleven small launches; nothing is read back to the host.
+ */
+dkv_status dkv_topk_pattern(int32_t num_layers, int32_t num_q_heads, int32_t num_bins,
+                            const float *probs, int64_t k, uint8_t *pattern, void *workspace,
+                            size_t workspace_bytes, void *stream);
 
 /*
  * Zero-copy paged variant

@@ -23,6 +23,11 @@ What it computes (Distance-KV, Sec. 3.4 "Static-Pattern Inference"):
   retained set is exactly dense attention with every other position masked to
   -inf, so the oracle writes out that plain definition twice, once over the
   packed rows and once over the dense cache with a mask;
+* the exact-budget export of a pattern from retention probabilities (Sec. 3.3,
+  Eq. (topk-pattern) and Appendix A's exact-budget refinement): K = round(rho L H D)
+  entries, the K largest probabilities, kept; and the logical (pattern entries)
+  against physical (retained positions after the union) retention report of
+  Sec. 3.4 and the experimental setup;
 * the zero-copy alternative to the pack: the retained set of a segment is a
   union of contiguous distance bins plus the sink and the recent window
   (Eq. (4), Eq. (5), union of Sec. 3.4), so in a cache kept in fixed pages of
@@ -55,6 +60,8 @@ design notes):
 * an empty segment (no rows at all) produces a zero output.
 """
 
+import math
+
 import numpy as np
 
 __all__ = [
@@ -72,6 +79,9 @@ __all__ = [
     "dense_decode_attn",
     "query_attn",
     "masked_dense_attn",
+    "budget_entries",
+    "topk_mask",
+    "retention_report",
     "PAGE_ENTRY_FIELDS",
     "page_select",
     "paged_append",
@@ -391,6 +401,54 @@ def masked_dense_attn(q, k, v, kv_mask, k_tail, v_tail, sm_scale, dtype):
             p = np.exp(s - s.max())
             out[b, h] = (p @ vals) / p.sum()
     return out
+
+
+# ---------------------------------------------------------------------------
+# Exact-budget pattern export (Sec. 3.3; Appendix A, exact-budget refinement)
+# ---------------------------------------------------------------------------
+
+def budget_entries(rho, num_layers, num_q_heads, num_bins):
+    """K_rho = round(rho * L * H * D), the number of active pattern entries at
+    logical retention ratio rho.  The paper does not say how halves round;
+    they round up here (floor(x + 0.5) of the float64 product)."""
+    return int(math.floor(float(rho) * int(num_layers) * int(num_q_heads) * int(num_bins) + 0.5))
+
+
+def topk_mask(probs, k):
+    """TopKMask(P, K): the k largest entries of P set to one, all others zero,
+    globally over every (layer, query head, bin) entry.  Ties (equal
+    probabilities, +0 and -0 alike) go to the lower flat index in row-major
+    (layer, head, bin) order; NaN ranks below every number.  Returns uint8 of
+    P's shape."""
+    p = np.asarray(probs, dtype=np.float64)
+    flat = p.reshape(-1)
+    nan = np.isnan(flat)
+    value = np.where(nan, 0.0, flat)
+    # lexsort orders by the last key first: numbers before NaN, then larger
+    # probability first, then lower index
+    order = np.lexsort((np.arange(flat.size), -value, nan))
+    out = np.zeros(flat.size, dtype=np.uint8)
+    out[order[:int(k)]] = 1
+    return out.reshape(p.shape)
+
+
+def retention_report(pattern, context_len, sink, recent, bin_edges, num_kv_heads):
+    """Logical against physical retention (Sec. 3.4, last paragraph).
+
+    logical: fraction of pattern entries that are one, ||M||_0 / (N Hq D);
+    physical: fraction of cache positions a KV head keeps after the union,
+    sink and recent included, sum of retained lengths / (N Hkv T).
+    Returns dict(logical, physical, kept_entries, retained_positions).
+    """
+    pattern = np.asarray(pattern, dtype=np.uint8)
+    n_units, n_q, n_bins = pattern.shape
+    lengths = closed_form_lengths(pattern, context_len, sink, recent, bin_edges, num_kv_heads)
+    kept = int(np.count_nonzero(pattern))
+    positions = int(lengths.sum())
+    total = n_units * num_kv_heads * int(context_len)
+    return dict(logical=kept / float(pattern.size) if pattern.size else 0.0,
+                physical=positions / float(total) if total else 0.0,
+                kept_entries=kept, retained_positions=positions)
 
 
 # ---------------------------------------------------------------------------

@@ -21,7 +21,8 @@ __all__ = [
     "dkv_append_decode_attn", "dkv_dense_append_decode_attn",
     "dkv_status_string", "dkv_probe_stream_read", "dkv_query_workspace_bytes", "dkv_query_attn",
     "dkv_page_select_workspace_bytes", "dkv_page_entries_bound", "dkv_page_select",
-    "dkv_paged_decode_attn", "dkv_paged_append_decode_attn",
+    "dkv_paged_decode_attn", "dkv_paged_append_decode_attn", "dkv_budget_entries",
+    "dkv_topk_workspace_bytes", "dkv_topk_pattern",
 ]
 
 (DKV_OK, DKV_ERR_INVALID_ARG, DKV_ERR_UNSUPPORTED, DKV_ERR_MISALIGNED, DKV_ERR_CAPACITY,
@@ -74,7 +75,7 @@ def library():
         return _lib
     if not os.path.exists(library_path):
         raise ImportError(
-            f"{library_path} is missing: build it with `python -m paper_2609_32663_amd.build` "
+            f"{library_path} is missing: build it with `python paper_2609_32663_amd/build.py` "
             "(the Distance-KV path has no fallback)")
     lib = ctypes.CDLL(library_path)
     P, I32, I64, SZ, F32, VP = (ctypes.POINTER(Layout), ctypes.c_int32, ctypes.c_int64,
@@ -105,6 +106,9 @@ def library():
                                         I32, F32, I64, VP, VP, SZ, VP]),
         "dkv_paged_append_decode_attn": (I32, [I32, I32, I32, I32, I32, VP, VP, VP, I32, I32, I32, VP, VP,
                                                I64, I32, VP, VP, I32, I32, F32, I64, VP, VP, SZ, VP]),
+        "dkv_budget_entries": (I64, [ctypes.c_double, I32, I32, I32]),
+        "dkv_topk_workspace_bytes": (SZ, [I32, I32, I32]),
+        "dkv_topk_pattern": (I32, [I32, I32, I32, VP, I64, VP, VP, SZ, VP]),
     }
     for name, (res, args) in sigs.items():
         f = getattr(lib, name)
@@ -312,3 +316,22 @@ def dkv_paged_append_decode_attn(q, k_new, v_new, n_tail, append_cap, k_pages, v
         _dev(v_pages, "v_pages"), num_pages, page_rows, _dev(entries, "entries"), _dev(n_entries, "n_entries"),
         entries.shape[1], int(context_len), float(sm_scale), int(rows_hint), _dev(out, "out"),
         _dev(workspace, "workspace"), workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def dkv_budget_entries(rho, num_layers, num_q_heads, num_bins):
+    return library().dkv_budget_entries(float(rho), int(num_layers), int(num_q_heads), int(num_bins))
+
+
+def dkv_topk_workspace_bytes(num_layers, num_q_heads, num_bins):
+    return library().dkv_topk_workspace_bytes(int(num_layers), int(num_q_heads), int(num_bins))
+
+
+def dkv_topk_pattern(probs, k, pattern, workspace, stream=None):
+    """probs: float32 [L][Hq][D]; pattern: uint8 [L][Hq][D] (out); workspace:
+    device tensor of dkv_topk_workspace_bytes(L, Hq, D) bytes."""
+    L, H, D = probs.shape
+    if probs.dtype != torch.float32 or pattern.dtype != torch.uint8 or tuple(pattern.shape) != (L, H, D):
+        raise ValueError("probs must be float32 and pattern uint8 of the same [L][Hq][D] shape")
+    _check("dkv_topk_pattern", library().dkv_topk_pattern(
+        L, H, D, _dev(probs, "probs"), int(k), _dev(pattern, "pattern"), _dev(workspace, "workspace"),
+        workspace.numel() * workspace.element_size(), _stream(stream)))

@@ -1,6 +1,8 @@
 """Build libdkv.so (the C-ABI library) for gfx950 with hipcc, in-tree.
 
-    python -m paper_2609_32663_amd.build [--jobs N]
+    python paper_2609_32663_amd/build.py [--jobs N]
+
+(run as a script: importing the package loads the library, which this builds).
 
 Every kernel source is compiled for gfx950 only.  Packed-fp32 VALU
 instructions are disabled (`-target-feature -packed-fp32-ops`); hipcc's host
@@ -28,7 +30,8 @@ COMMON_FLAGS = [
     f"-I{INCLUDE}", "-Wall", "-Wno-unused-function",
 ]
 SOURCES = ["map_pattern.hip", "compact.hip", "decode_attn.hip", "dkv_api.cpp", "bw_probe.hip",
-           "query_attn.hip", "dkv_query_api.cpp", "page_select.hip", "dkv_paged_api.cpp"]
+           "query_attn.hip", "dkv_query_api.cpp", "page_select.hip", "dkv_paged_api.cpp",
+           "topk_pattern.hip", "dkv_pattern_api.cpp"]
 
 
 def _hipcc():

@@ -70,6 +70,18 @@ struct PageSelectParams {
 size_t page_select_workspace_bytes(int64_t nseg, int64_t T);
 hipError_t launch_page_select(const PageSelectParams& p, hipStream_t stream);
 
+// -------------------------------------------------------- exact-budget export
+struct TopkParams {
+  const float* probs;  // [n] retention probabilities
+  uint8_t* pattern;    // [n] out
+  uint32_t* state;     // workspace: prefix, count still to take, histogram, per-chunk tie counts
+  int64_t n;           // entries, < 2^31
+  int64_t k;           // 0 <= k <= n
+  int64_t chunk;       // entries per workgroup (set by the launcher)
+};
+size_t topk_workspace_bytes(int64_t n);
+hipError_t launch_topk_pattern(TopkParams p, hipStream_t stream);
+
 // ------------------------------------------------------------ decode attention
 constexpr int kDecodeMaxWG = 1024;  // upper bound on the split count
 

@@ -298,6 +298,47 @@ def test_paged_decode_validation():
     assert call(B=0, q=NUL, out=NUL, kp=NUL, vp=NUL) == d.DKV_OK
 
 
+def test_budget_and_topk_validation():
+    lib = d.library()
+    assert d.dkv_budget_entries(0.2, 32, 32, 1013) == 207462
+    assert d.dkv_budget_entries(0.5, 1, 1, 3) == 2
+    assert d.dkv_budget_entries(1.0, 2, 3, 4) == 24
+    assert d.dkv_budget_entries(-0.1, 1, 1, 1) == -1
+    assert d.dkv_budget_entries(1.1, 1, 1, 1) == -1
+    assert d.dkv_budget_entries(float("nan"), 1, 1, 1) == -1
+    assert d.dkv_budget_entries(0.2, -1, 1, 1) == -1
+    ws = d.dkv_topk_workspace_bytes(2, 3, 4)
+    assert ws > 0 and d.dkv_topk_workspace_bytes(0, 3, 4) == 0
+    assert d.dkv_topk_workspace_bytes(32, 32, 1015) >= d.dkv_topk_workspace_bytes(2, 3, 4)
+
+    def f(L=2, H=3, D=4, probs=A, k=5, pat=A, w=A, w_bytes=ws):
+        return lib.dkv_topk_pattern(L, H, D, probs, k, pat, w, w_bytes, NUL)
+
+    assert f(k=-1) == d.DKV_ERR_INVALID_ARG
+    assert f(k=25) == d.DKV_ERR_INVALID_ARG
+    assert f(probs=NUL) == d.DKV_ERR_INVALID_ARG
+    assert f(pat=NUL) == d.DKV_ERR_INVALID_ARG
+    assert f(probs=MIS) == d.DKV_ERR_MISALIGNED
+    assert f(pat=ctypes.c_void_p(0x10002)) == d.DKV_ERR_MISALIGNED
+    assert f(w=NUL) == d.DKV_ERR_WORKSPACE
+    assert f(w_bytes=ws - 1) == d.DKV_ERR_WORKSPACE
+    assert f(L=-2, k=0) == d.DKV_ERR_INVALID_ARG
+    assert f(L=2048, H=2048, D=1024) == d.DKV_ERR_UNSUPPORTED
+    assert f(L=0, k=0, probs=NUL, pat=NUL, w=NUL) == d.DKV_OK
+
+
+def test_build_script_loads_without_the_library():
+    """The build runs where no library exists yet: its script must load by
+    path without importing the package (which loads the library)."""
+    import subprocess
+    import sys
+    code = ("import importlib.util, sys; "
+            f"spec = importlib.util.spec_from_file_location('b', {os.path.join(ROOT, 'paper_2609_32663_amd', 'build.py')!r}); "
+            "m = importlib.util.module_from_spec(spec); spec.loader.exec_module(m); "
+            "assert callable(m.build); assert 'paper_2609_32663_amd' not in sys.modules")
+    subprocess.run([sys.executable, "-c", code], check=True, cwd=ROOT)
+
+
 def test_binding_rejects_host_tensors():
     import torch
     lay = _lay()

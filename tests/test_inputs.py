@@ -31,7 +31,7 @@ def test_seeds_are_distinct_and_stable():
     assert di.seed_of(3, 1, 2) == di.seed_of(3, 1, 2)
 
 
-@pytest.mark.parametrize("name", list(di.WORKLOADS))
+@pytest.mark.parametrize("name", [n for n, w in di.WORKLOADS.items() if w.family != "topk"])
 def test_pattern_budget_and_union_structure(name):
     w = di.WORKLOADS[name]
     for b in (w.budgets or (None,)):
@@ -74,3 +74,65 @@ def test_tensor_generators_shapes_and_seeding():
     assert q.shape == (1, 4, 64)
     kn, vn = di.kv_new_step(w, 0, 3, n_new=2)
     assert kn.shape == (1, 2, 2, 64)
+
+
+def test_topk_workload_pattern_is_not_an_input_recipe():
+    with pytest.raises(ValueError):
+        di.make_pattern(di.workload("llama8b_stack_128k_paper_bins"))
+
+
+def test_retention_probs_range_ties_and_seeding():
+    p = di.retention_probs(4, 8, 2, 50, seed=3)
+    assert p.dtype == np.float32 and p.shape == (4, 8, 50)
+    assert p.min() >= 0.001 and p.max() <= 0.999
+    assert len(np.unique(p)) < p.size // 2          # quantised: many exact ties
+    np.testing.assert_array_equal(p, di.retention_probs(4, 8, 2, 50, seed=3))
+    assert not np.array_equal(p, di.retention_probs(4, 8, 2, 50, seed=4))
+
+
+def test_paper_bins_workload_retention():
+    """The exact-budget export at rho = 0.2 over the stand-in probabilities
+    gives a physical retention near the paper's 34.6% at 128K."""
+    w = di.workload("llama8b_stack_128k_paper_bins")
+    assert w.num_bins == 1015 and w.bin_edges[1] == 128
+    p = di.retention_probs(w.num_layers, w.num_q_heads, w.num_kv_heads, w.num_bins, seed=w.cfg_id)
+    m = o.topk_mask(p, o.budget_entries(w.rho, w.num_layers, w.num_q_heads, w.num_bins))
+    rep = o.retention_report(m, w.context_len, w.sink, w.recent, w.bin_edges, w.num_kv_heads)
+    assert rep["logical"] == pytest.approx(0.2, abs=1e-6)
+    assert 0.30 < rep["physical"] < 0.40
+
+
+def _cells(pat, n_kv):
+    N, H, D = pat.shape
+    return (pat.reshape(N, n_kv, H // n_kv, D) != 0).any(axis=2)
+
+
+@pytest.mark.parametrize("kind", di.PATTERN_FAMILIES)
+def test_pattern_families_structure_and_cost(kind):
+    rng = np.random.default_rng(9)
+    N, H, n_kv, D = 3, 8, 2, 40
+    base = (rng.uniform(size=(N, H, D)) < 0.25).astype(np.uint8)
+    f = di.pattern_family(base, kind, n_kv, seed=1)
+    assert f.shape == base.shape and f.dtype == np.uint8 and set(np.unique(f)) <= {0, 1}
+    np.testing.assert_array_equal(f, di.pattern_family(base, kind, n_kv, seed=1))
+    cb, cf = _cells(base, n_kv), _cells(f, n_kv)
+    G = H // n_kv
+    if kind == "head_only":
+        assert all(f[n, h].all() or not f[n, h].any() for n in range(N) for h in range(H))
+        assert abs(int(cf.sum()) - int(cb.sum())) <= D // 2
+    elif kind == "distance_only":
+        assert all((f[n] == f[n, 0]).all() for n in range(N))
+        for n in range(N):
+            assert abs(int(cf[n].sum()) - int(cb[n].sum())) <= n_kv // 2 + n_kv
+    elif kind == "distance_shuffled":
+        np.testing.assert_array_equal(f.sum(axis=2), base.sum(axis=2))        # per-head counts
+        np.testing.assert_array_equal(cf.sum(axis=2), cb.sum(axis=2))        # per-group cells
+        # the same permutation for every head of a group
+        for n in range(N):
+            for g in range(n_kv):
+                hb = base[n, g * G:(g + 1) * G]
+                hf = f[n, g * G:(g + 1) * G]
+                assert sorted(map(tuple, hb.T.tolist())) == sorted(map(tuple, hf.T.tolist()))
+    else:
+        assert int(f.sum()) == int(base.sum()) and int(cf.sum()) == int(cb.sum())
+        assert not np.array_equal(f, base)

@@ -616,3 +616,72 @@ def test_paged_append_writes_each_token_at_its_position():
             assert np.array_equal(k2[page, slot], kn[s, t]) and np.array_equal(v2[page, slot], vn[s, t])
             touched[page, slot] = True
     assert np.array_equal(k2[~touched], kp[~touched]) and np.array_equal(v2[~touched], vp[~touched])
+
+
+# ---------------------------------------------------------------------------
+# exact-budget export and retention report
+# ---------------------------------------------------------------------------
+
+def test_budget_of_the_llama31_pattern():
+    g = _golden("exact_budget.json")
+    # L * H query heads in all; the budget depends only on their product
+    assert o.budget_entries(g["rho"], 1, g["query_heads"], g["num_bins"]) == g["k_rho"]
+    assert o.budget_entries(g["rho"], 32, 32, g["num_bins"]) == g["k_rho"]
+
+
+def test_budget_rounds_halves_up_and_hits_the_ends():
+    assert o.budget_entries(0.5, 1, 1, 3) == 2      # 1.5
+    assert o.budget_entries(0.5, 1, 1, 5) == 3      # 2.5
+    assert o.budget_entries(0.25, 1, 2, 5) == 3     # 2.5
+    assert o.budget_entries(0.0, 4, 4, 7) == 0
+    assert o.budget_entries(1.0, 4, 4, 7) == 112
+
+
+def _topk_brute(p, k):
+    """Sort the flat indices by (NaN last, larger first, lower index first)."""
+    flat = [float(x) for x in np.asarray(p, np.float64).reshape(-1)]
+    keyed = sorted(range(len(flat)), key=lambda i: (flat[i] != flat[i], -(flat[i] if flat[i] == flat[i] else 0.0), i))
+    out = [0] * len(flat)
+    for i in keyed[:k]:
+        out[i] = 1
+    return np.array(out, np.uint8).reshape(np.shape(p))
+
+
+def test_topk_mask_matches_a_brute_force_sort():
+    rng = np.random.default_rng(60)
+    for trial in range(60):
+        shape = tuple(int(x) for x in rng.integers(1, 6, size=3))
+        n = int(np.prod(shape))
+        # coarse values give many exact ties; some NaN, some signed zeros
+        p = (rng.integers(0, 5, size=shape) / 4.0).astype(np.float32)
+        if trial % 3 == 0:
+            p[rng.uniform(size=shape) < 0.2] = np.nan
+        if trial % 4 == 0:
+            p[rng.uniform(size=shape) < 0.3] = -0.0
+        k = int(rng.integers(0, n + 1))
+        got = o.topk_mask(p, k)
+        assert got.dtype == np.uint8 and got.shape == shape
+        assert int(got.sum()) == k
+        np.testing.assert_array_equal(got, _topk_brute(p, k))
+
+
+def test_topk_mask_special_cases():
+    p = np.full((2, 3, 4), 0.3, np.float32)
+    m = o.topk_mask(p, 5)                      # all tied: the first five flat entries
+    assert m.reshape(-1).tolist() == [1] * 5 + [0] * 19
+    assert o.topk_mask(p, 0).sum() == 0 and o.topk_mask(p, 24).sum() == 24
+    q = np.arange(24, dtype=np.float32).reshape(2, 3, 4)
+    assert o.topk_mask(q, 3).reshape(-1).tolist() == [0] * 21 + [1] * 3
+
+
+def test_retention_report_against_painted_masks():
+    rng = np.random.default_rng(61)
+    for _ in range(30):
+        T, S, R, edges, n_kv, pattern = random_layout(rng)
+        rep = o.retention_report(pattern, T, S, R, edges, n_kv)
+        _, km = paint_masks(pattern, T, S, R, edges, n_kv)
+        assert rep["kept_entries"] == int(pattern.sum())
+        assert rep["logical"] == pytest.approx(pattern.mean())
+        assert rep["retained_positions"] == int(km.sum())
+        if T:
+            assert rep["physical"] == pytest.approx(km.mean())
