@@ -379,6 +379,106 @@ def main():
         parity = {"layers": L, "max_rel_err": worst, "seg_len_equal": same_pack}
         log(f"oracle {cpu_s:.2f} s, worst parity err {worst:.2e}")
 
+    # ---------------- exact-budget export and the ablation families -------
+    # The paper's own bin layout (128-token bins: 1,015 at 131,072 tokens) on
+    # the same 8B-shaped stack and the same K/V: the pattern is the
+    # exact-budget export (K = round(0.2 L H D)) of stand-in retention
+    # probabilities, then each ablation family of it; every pattern is mapped,
+    # packed and decoded (32 layers, attend only) like the headline.
+    log("exact-budget export and pattern families")
+    wp = di.workload("llama8b_stack_128k_paper_bins")
+    Lp, Hp, Dp = wp.num_layers, wp.num_q_heads, wp.num_bins
+    probs = di.retention_probs(Lp, Hp, wp.num_kv_heads, Dp, seed=wp.cfg_id)
+    k_budget = d.dkv_budget_entries(wp.rho, Lp, Hp, Dp)
+    probs_d = torch.from_numpy(probs).to(dev)
+    pat_x = torch.empty((Lp, Hp, Dp), dtype=torch.uint8, device=dev)
+    tk_ws = torch.empty(d.dkv_topk_workspace_bytes(Lp, Hp, Dp), dtype=torch.uint8, device=dev)
+    d.dkv_topk_pattern(probs_d, k_budget, pat_x, tk_ws)
+    torch.cuda.synchronize()
+    a, b = ev(), ev()
+    a.record(stream)
+    for _ in range(20):
+        d.dkv_topk_pattern(probs_d, k_budget, pat_x, tk_ws)
+    b.record(stream)
+    torch.cuda.synchronize()
+    topk_us = a.elapsed_time(b) * 1e3 / 20
+    exported = pat_x.cpu().numpy()
+    n_entries = Lp * Hp * Dp
+    # bytes one export reads and writes: six passes over the probabilities
+    # (four digit rounds, tie count, write) and the pattern
+    topk_bytes = 6 * 4 * n_entries + n_entries
+    topk_res = {"entries": n_entries, "k": int(k_budget), "rho": wp.rho, "us": round(topk_us, 1),
+                "gb_per_s": round(topk_bytes / (topk_us * 1e-6) / 1e9, 1),
+                "launches": 11, "ones": int(exported.sum()), "cpu_baseline": None, "equal_to_oracle": None}
+    if not args.no_cpu_baseline:
+        t0 = time.perf_counter()
+        want_pat = o.topk_mask(probs, o.budget_entries(wp.rho, Lp, Hp, Dp))
+        topk_cpu = time.perf_counter() - t0
+        topk_res["equal_to_oracle"] = bool(np.array_equal(exported, want_pat))
+        topk_res["cpu_baseline"] = {"value": round(topk_cpu * 1e3, 2), "unit": "ms", "cores": 1, "kind": "oracle",
+                                    "sample": "the whole export (NumPy lexsort, one thread)"}
+    log(f"topk export {topk_us:.1f} us for {n_entries} entries")
+    lay_p = d.make_layout(N, Hq, Hkv, dim, T, wp.sink, wp.recent, list(wp.bin_edges))
+    fam_res = {}
+    fam_ws = torch.zeros(d.dkv_decode_workspace_bytes(B, Hq, Hkv, dim), dtype=torch.uint8, device=dev)
+    fam_out = torch.empty((B, Hq, dim), dtype=torch.float32, device=dev)
+    fam_stream = torch.cuda.Stream()
+    Pv = ctypes.c_void_p
+    for kind in ("exported",) + di.PATTERN_FAMILIES:
+        pat_f = exported if kind == "exported" else di.pattern_family(exported, kind, Hkv, seed=wp.cfg_id)
+        km_f = torch.empty((N, Hkv, T), dtype=torch.uint8, device=dev)
+        kl_f = torch.empty((N, Hkv), dtype=torch.int32, device=dev)
+        d.dkv_map_pattern(lay_p, torch.from_numpy(np.ascontiguousarray(pat_f)).to(dev), km_f, kl_f)
+        lens_f = kl_f.cpu().to(torch.int64)
+        rows_f = int(lens_f.sum())
+        kc_f = torch.empty((rows_f, dim), dtype=torch.bfloat16, device=dev)
+        vc_f = torch.empty_like(kc_f)
+        so_f = torch.empty(N * Hkv, dtype=torch.int64, device=dev)
+        sl_f = torch.empty(N * Hkv, dtype=torch.int32, device=dev)
+        cws_f = torch.empty(d.dkv_compact_workspace_bytes(lay_p), dtype=torch.uint8, device=dev)
+        d.dkv_compact(lay_p, k, v, km_f, 0, kc_f, vc_f, so_f, sl_f, cws_f)
+        del km_f
+        hints = [int(lens_f[layer * B:(layer + 1) * B].sum()) for layer in range(L)]
+
+        def fam_calls(shp):
+            for layer in range(L):
+                off = layer * nseg_layer
+                st_ = lib.dkv_decode_attn(d.DKV_BF16, B, Hq, Hkv, dim, Pv(q_layers[layer].data_ptr()),
+                                          Pv(kc_f.data_ptr()), Pv(vc_f.data_ptr()), Pv(so_f.data_ptr() + 8 * off),
+                                          Pv(sl_f.data_ptr() + 4 * off), 0, w.sm_scale, hints[layer],
+                                          Pv(fam_out.data_ptr()), Pv(fam_ws.data_ptr()), fam_ws.numel(), Pv(shp))
+                if st_ != 0:
+                    raise d.DkvError("dkv_decode_attn", st_)
+        fam_calls(sh)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=fam_stream):
+            fam_calls(fam_stream.cuda_stream)
+        for _ in range(args.warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        a.record(stream)
+        for _ in range(args.steps):
+            g.replay()
+        b.record(stream)
+        torch.cuda.synchronize()
+        f_ms = a.elapsed_time(b) / args.steps
+        f_bytes = rows_f * dim * elem * 2 + L * B * Hq * dim * (elem + 4) + L * nseg_layer * 12
+        per_head = lens_f.view(-1).to(torch.float64)
+        fam_res[kind] = {"logical": round(float(pat_f.mean()), 4),
+                         "physical": round(rows_f / float(N * Hkv * T), 4),
+                         "ms_per_step": round(f_ms, 4), "us_per_layer": round(f_ms * 1e3 / L, 2),
+                         "gb_per_s": round(f_bytes / (f_ms * 1e-3) / 1e9, 1),
+                         "segment_rows": {"min": int(per_head.min()), "max": int(per_head.max()),
+                                          "cv": round(float(per_head.std() / per_head.mean()), 3)},
+                         "lengths_equal_oracle": None}
+        if not args.no_cpu_baseline:
+            olen = o.closed_form_lengths(pat_f, T, wp.sink, wp.recent, wp.bin_edges, Hkv)
+            fam_res[kind]["lengths_equal_oracle"] = bool(np.array_equal(lens_f.numpy(), olen))
+        log(f"pattern {kind}: physical {fam_res[kind]['physical']}, {f_ms * 1e3 / L:.1f} us/layer")
+        del kc_f, vc_f, g
+        torch.cuda.empty_cache()
+
     # ---------------- dense comparator cache [L][B*Hkv][T+cap][d] ----------
     t_cap = T + cap
     kd = torch.zeros((N, Hkv, t_cap, dim), dtype=torch.bfloat16, device=dev)
@@ -753,6 +853,11 @@ def main():
                   "launch_frac_of_peak": round(dbytes / L / (dlaunch_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)},
         "speedup_vs_dense": round(dms / ms, 3),
         "paged": paged_res,
+        "topk_export": topk_res,
+        "pattern_families": {"workload": "llama8b_stack_128k_paper_bins: the same stack with 128-token bins "
+                                         "(1,015), pattern = exact-budget export at rho 0.2, then each family",
+                             "step": "per layer: dkv_decode_attn (attend only); HIP-graph replays",
+                             **fam_res},
         "one_time": {"map_us": round(map_us, 1), "compact_us": round(compact_us, 1),
                      "compact_gb_per_s": round(compact_bytes / (compact_us * 1e-6) / 1e9, 1)},
         "kv_cache_gib": {"dense": round(N * Hkv * T * dim * elem * 2 / 2 ** 30, 3),
