@@ -49,6 +49,7 @@ __all__ = [
     "retention_probs",
     "PATTERN_FAMILIES",
     "pattern_family",
+    "sequence_lengths",
 ]
 
 # stream ids of the seed derivation
@@ -56,6 +57,7 @@ STREAM_PATTERN, STREAM_K, STREAM_V, STREAM_Q, STREAM_NEW_K, STREAM_NEW_V = range
 STREAM_BLOCK_Q, STREAM_BLOCK_K, STREAM_BLOCK_V = 6, 7, 8
 STREAM_PAGES = 9
 STREAM_PROBS, STREAM_FAMILY = 10, 11
+STREAM_LENGTHS = 12
 
 
 def seed_of(*parts):
@@ -508,3 +510,15 @@ def pattern_family(base, kind, num_kv_heads, seed):
     else:
         raise ValueError(f"unknown pattern family {kind!r}")
     return np.ascontiguousarray(out.reshape(N, H, D)).astype(np.uint8)
+
+
+def sequence_lengths(w, seed=0, shortest=0.125):
+    """Context length of every unit for a ragged batch: sequence b draws T_b
+    uniformly from [shortest * T, T] (T = the workload's context length) and
+    every layer of that sequence shares it (units are layer-major), int32 [N].
+    The longest sequence is always T."""
+    rng = np.random.default_rng(seed_of(STREAM_LENGTHS, w.cfg_id, seed))
+    T = int(w.context_len)
+    per_seq = rng.integers(int(shortest * T), T + 1, size=w.batch)
+    per_seq[int(rng.integers(w.batch))] = T
+    return np.tile(per_seq, w.num_layers).astype(np.int32)

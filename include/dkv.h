@@ -10,6 +10,7 @@
  * This library runs those four steps on one GPU:
  *
  *   dkv_map_pattern   pattern -> per-KV-head keep masks and retained lengths
+ *                     (dkv_map_pattern_ragged: contexts of different lengths)
  *   dkv_compact       dense K/V + keep mask -> packed K/V, offsets, lengths
  *   dkv_append        new tokens -> free rows after each packed segment
  *   dkv_decode_attn   one decode step of attention over the packed segments
@@ -115,6 +116,25 @@ typedef struct dkv_layout {
 dkv_status dkv_map_pattern(const dkv_layout *layout, const uint8_t *pattern,
                            uint8_t *kv_mask, int32_t *kv_len, uint8_t *q_mask,
                            void *stream);
+
+/*
+ * dkv_map_pattern_ragged -- dkv_map_pattern for a batch of contexts of
+ * different lengths (e.g. sequences of a serving batch).
+ *
+ * unit_len  int32 [N] (device): unit n's context is the first unit_len[n]
+ *           positions of its mask row (values are clamped to
+ *           [0, context_len]).  Eq. (4) and Eq. (5) are applied with that
+ *           length: distances count from the end of the unit's own context,
+ *           so its sink, recent window and bins move with it, and positions
+ *           at or past unit_len[n] are not retained.
+ * layout->context_len is the row length of kv_mask, q_mask and the dense
+ * cache handed to dkv_compact (the longest context).  Everything else as
+ * dkv_map_pattern; packing, append and decode need no change, since they
+ * follow the masks and lengths.
+ */
+dkv_status dkv_map_pattern_ragged(const dkv_layout *layout, const int32_t *unit_len,
+                                  const uint8_t *pattern, uint8_t *kv_mask, int32_t *kv_len,
+                                  uint8_t *q_mask, void *stream);
 
 /* Workspace bytes dkv_compact needs for this layout (host, no GPU call). */
 size_t dkv_compact_workspace_bytes(const dkv_layout *layout);

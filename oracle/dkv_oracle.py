@@ -125,31 +125,39 @@ def bin_index(u, bin_edges):
 # Eq. (5): retention decision of each query head at each position
 # ---------------------------------------------------------------------------
 
-def q_keep_mask(pattern, context_len, sink, recent, bin_edges):
+def q_keep_mask(pattern, context_len, sink, recent, bin_edges, unit_len=None):
     """Logical keep mask m[n, h, j] (uint8), Eq. (5) of Sec. 3.4.
 
     pattern: uint8 [N][Hq][D], the binary Distance-KV pattern of Sec. 3.2.
     A position is kept if it is a sink position (j < S) or a recent position
     (delta < R); otherwise the pattern entry of its bin decides, and a
     position that no bin covers is dropped.
+
+    unit_len (optional, [N]): a batch of contexts of different lengths.
+    Unit n's context is its first unit_len[n] positions of the
+    context_len-long rows; distances are measured from the end of that
+    context, and the positions after it are not retained.
     """
     pattern = np.asarray(pattern, dtype=np.uint8)
     n_units, n_q, n_bins = pattern.shape
     assert len(bin_edges) == n_bins + 1
     T = int(context_len)
-    j = np.arange(T, dtype=np.int64)
-    delta = T - 1 - j
-    always = (j < sink) | (delta < recent)
-    u = delta - recent
-    k = bin_index(np.maximum(u, 0), bin_edges)
-    has_bin = (~always) & (k >= 0)
+    lens = [T] * n_units if unit_len is None else [int(x) for x in unit_len]
     out = np.zeros((n_units, n_q, T), dtype=np.uint8)
     for n in range(n_units):
+        Tn = lens[n]
+        assert 0 <= Tn <= T
+        j = np.arange(Tn, dtype=np.int64)
+        delta = Tn - 1 - j
+        always = (j < sink) | (delta < recent)
+        u = delta - recent
+        k = bin_index(np.maximum(u, 0), bin_edges)
+        has_bin = (~always) & (k >= 0)
         for h in range(n_q):
-            row = np.zeros(T, dtype=np.uint8)
+            row = np.zeros(Tn, dtype=np.uint8)
             row[always] = 1
             row[has_bin] = pattern[n, h, k[has_bin]]
-            out[n, h] = row
+            out[n, h, :Tn] = row
     return out
 
 
@@ -174,13 +182,14 @@ def kv_keep_mask(q_mask, num_kv_heads):
     return out
 
 
-def map_pattern(pattern, context_len, sink, recent, bin_edges, num_kv_heads):
+def map_pattern(pattern, context_len, sink, recent, bin_edges, num_kv_heads, unit_len=None):
     """Pattern -> (q_mask, kv_mask, kv_len): Eq. (5) then the GQA union.
 
     kv_len[n, g] is the number of retained positions of KV head g, the
-    physical per-head cache length after pruning.
+    physical per-head cache length after pruning.  unit_len: as in
+    q_keep_mask.
     """
-    qm = q_keep_mask(pattern, context_len, sink, recent, bin_edges)
+    qm = q_keep_mask(pattern, context_len, sink, recent, bin_edges, unit_len)
     km = kv_keep_mask(qm, num_kv_heads)
     kv_len = km.sum(axis=2, dtype=np.int64).astype(np.int32)
     return qm, km, kv_len

@@ -22,7 +22,7 @@ __all__ = [
     "dkv_status_string", "dkv_probe_stream_read", "dkv_query_workspace_bytes", "dkv_query_attn",
     "dkv_page_select_workspace_bytes", "dkv_page_entries_bound", "dkv_page_select",
     "dkv_paged_decode_attn", "dkv_paged_append_decode_attn", "dkv_budget_entries",
-    "dkv_topk_workspace_bytes", "dkv_topk_pattern",
+    "dkv_topk_workspace_bytes", "dkv_topk_pattern", "dkv_map_pattern_ragged",
 ]
 
 (DKV_OK, DKV_ERR_INVALID_ARG, DKV_ERR_UNSUPPORTED, DKV_ERR_MISALIGNED, DKV_ERR_CAPACITY,
@@ -108,6 +108,7 @@ def library():
                                                I64, I32, VP, VP, I32, I32, F32, I64, VP, VP, SZ, VP]),
         "dkv_budget_entries": (I64, [ctypes.c_double, I32, I32, I32]),
         "dkv_topk_workspace_bytes": (SZ, [I32, I32, I32]),
+        "dkv_map_pattern_ragged": (I32, [P, VP, VP, VP, VP, VP, VP]),
         "dkv_topk_pattern": (I32, [I32, I32, I32, VP, I64, VP, VP, SZ, VP]),
     }
     for name, (res, args) in sigs.items():
@@ -335,3 +336,10 @@ def dkv_topk_pattern(probs, k, pattern, workspace, stream=None):
     _check("dkv_topk_pattern", library().dkv_topk_pattern(
         L, H, D, _dev(probs, "probs"), int(k), _dev(pattern, "pattern"), _dev(workspace, "workspace"),
         workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def dkv_map_pattern_ragged(layout, unit_len, pattern, kv_mask, kv_len, q_mask=None, stream=None):
+    """unit_len: int32 [N] device tensor of per-unit context lengths."""
+    _check("dkv_map_pattern_ragged", library().dkv_map_pattern_ragged(
+        ctypes.byref(layout), _dev(unit_len, "unit_len"), _dev(pattern, "pattern"), _dev(kv_mask, "kv_mask"),
+        _dev(kv_len, "kv_len"), _dev(q_mask, "q_mask", optional=True), _stream(stream)))

@@ -76,8 +76,12 @@ const char* dkv_status_string(dkv_status status) {
   return "unknown status";
 }
 
-dkv_status dkv_map_pattern(const dkv_layout* layout, const uint8_t* pattern, uint8_t* kv_mask,
-                           int32_t* kv_len, uint8_t* q_mask, void* stream) {
+}  // extern "C"
+
+namespace {
+
+dkv_status map_pattern(const dkv_layout* layout, const int32_t* unit_len, const uint8_t* pattern,
+                       uint8_t* kv_mask, int32_t* kv_len, uint8_t* q_mask, void* stream) {
   dkv_status st = check_shape(layout);
   if (st != DKV_OK) return st;
   const dkv_layout& L = *layout;
@@ -113,7 +117,23 @@ dkv_status dkv_map_pattern(const dkv_layout* layout, const uint8_t* pattern, uin
   p.uniform_width = W;
   if (W == 0)
     for (int32_t k = 0; k <= L.num_bins; ++k) p.edges[k] = e[k];
+  p.unit_len = unit_len;
   return hip_status(dkv::launch_map_pattern(p, (int)nseg, (hipStream_t)stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+dkv_status dkv_map_pattern(const dkv_layout* layout, const uint8_t* pattern, uint8_t* kv_mask,
+                           int32_t* kv_len, uint8_t* q_mask, void* stream) {
+  return map_pattern(layout, nullptr, pattern, kv_mask, kv_len, q_mask, stream);
+}
+
+dkv_status dkv_map_pattern_ragged(const dkv_layout* layout, const int32_t* unit_len, const uint8_t* pattern,
+                                  uint8_t* kv_mask, int32_t* kv_len, uint8_t* q_mask, void* stream) {
+  if (layout != nullptr && layout->num_units > 0 && unit_len == nullptr) return DKV_ERR_INVALID_ARG;
+  return map_pattern(layout, unit_len, pattern, kv_mask, kv_len, q_mask, stream);
 }
 
 size_t dkv_compact_workspace_bytes(const dkv_layout* layout) {

@@ -16,6 +16,7 @@ struct MapParams {
   uint8_t* kv_mask;        // [N][Hkv][T]
   int32_t* kv_len;         // [N*Hkv]
   uint8_t* q_mask;         // [N][Hq][T] or null
+  const int32_t* unit_len; // [N] context length of each unit, or null (all T)
   int32_t T, S, R, D, Hq, Hkv, G;
   int32_t uniform_width;   // > 0: edges are E[k] = uniform_width * k
   int32_t edges[DKV_MAX_GENERAL_BINS + 1];

@@ -9,7 +9,9 @@
 // bin up (a division for uniform edges, a binary search over the edges in LDS
 // otherwise), and writes 16 mask bytes with one 16-byte store when the row
 // is 16-byte aligned.  The retained count is reduced in the block and written
-// once, so kv_len needs no atomics and no pre-clearing.
+// once, so kv_len needs no atomics and no pre-clearing.  In a ragged batch a
+// unit's context is the first unit_len[n] positions of its row: distances
+// count from its end and the rest of the row is not retained.
 
 #include "dkv_device.hpp"
 #include "dkv_launch.hpp"
@@ -60,6 +62,12 @@ __global__ __launch_bounds__(kMapThreads) void map_pattern_kernel(MapParams p) {
 
   const uint32_t all_heads = (1u << G) - 1u;
   const bool aligned_rows = (T & 15) == 0;
+  // this unit's context length (clamped into the row)
+  int32_t Tn = T;
+  if (p.unit_len != nullptr) {
+    Tn = p.unit_len[unit];
+    Tn = Tn < 0 ? 0 : (Tn > T ? T : Tn);
+  }
   uint8_t* kv_row = p.kv_mask + (int64_t)seg * T;
   int64_t count = 0;
 
@@ -69,8 +77,8 @@ __global__ __launch_bounds__(kMapThreads) void map_pattern_kernel(MapParams p) {
     for (int e = 0; e < kMapPerThread; ++e) {
       const int64_t j = j0 + e;
       uint32_t bits = 0;
-      if (j < T) {
-        const int32_t delta = T - 1 - (int32_t)j;
+      if (j < Tn) {
+        const int32_t delta = Tn - 1 - (int32_t)j;
         if (j < p.S || delta < p.R) {
           bits = all_heads;
         } else {

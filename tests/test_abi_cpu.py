@@ -298,6 +298,16 @@ def test_paged_decode_validation():
     assert call(B=0, q=NUL, out=NUL, kp=NUL, vp=NUL) == d.DKV_OK
 
 
+def test_ragged_map_validation():
+    lib = d.library()
+    lay = _lay()
+    f = lib.dkv_map_pattern_ragged
+    assert f(ctypes.byref(lay), NUL, A, A, A, NUL, NUL) == d.DKV_ERR_INVALID_ARG   # unit_len required
+    assert f(NUL, A, A, A, A, NUL, NUL) == d.DKV_ERR_INVALID_ARG
+    assert f(ctypes.byref(lay), A, A, MIS, A, NUL, NUL) == d.DKV_ERR_MISALIGNED
+    assert f(ctypes.byref(_lay(N=0)), NUL, NUL, NUL, NUL, NUL, NUL) == d.DKV_OK
+
+
 def test_budget_and_topk_validation():
     lib = d.library()
     assert d.dkv_budget_entries(0.2, 32, 32, 1013) == 207462

@@ -685,3 +685,19 @@ def test_retention_report_against_painted_masks():
         assert rep["retained_positions"] == int(km.sum())
         if T:
             assert rep["physical"] == pytest.approx(km.mean())
+
+
+def test_ragged_contexts_map_like_separate_contexts():
+    """Per-unit context lengths: each unit's mask is the brute-force painting
+    of its own context, padded with zeros to the row length."""
+    rng = np.random.default_rng(62)
+    for _ in range(40):
+        T, S, R, edges, n_kv, pattern = random_layout(rng)
+        lens = rng.integers(0, T + 1, size=pattern.shape[0])
+        qm, km, kl = o.map_pattern(pattern, T, S, R, edges, n_kv, unit_len=lens)
+        for n, Tn in enumerate(lens):
+            pq, pk = paint_masks(pattern[n:n + 1], int(Tn), S, R, edges, n_kv)
+            np.testing.assert_array_equal(qm[n, :, :Tn], pq[0])
+            np.testing.assert_array_equal(km[n, :, :Tn], pk[0])
+            assert not qm[n, :, Tn:].any() and not km[n, :, Tn:].any()
+            np.testing.assert_array_equal(kl[n], pk[0].sum(axis=1))
