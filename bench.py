@@ -479,6 +479,85 @@ def main():
         del kc_f, vc_f, g
         torch.cuda.empty_cache()
 
+    # ---------------- ragged batch: contexts of different lengths ----------
+    # The 70B-shaped batch (16 sequences x 64q/8kv, 20% physical budget) once
+    # with every context 32K long and once with per-sequence contexts of
+    # 4K-32K (dkv_map_pattern_ragged); then its 16 decode steps, one fused
+    # append + decode call each, graph-replayed.
+    log("ragged batch")
+    wr = di.workload("llama70b_layer_bs16_32k")
+    Br, Hqr, Hkvr, Tr, capr = wr.batch, wr.num_q_heads, wr.num_kv_heads, wr.context_len, wr.append_cap
+    pat_r, _ = di.make_pattern(wr)
+    kr = torch.empty((Br, Hkvr, Tr, dim), dtype=torch.bfloat16, device=dev)
+    vr = torch.empty_like(kr)
+    for b_ in range(Br):
+        kb_, vb_ = di.kv_unit(wr, b_, device=dev)
+        kr[b_].copy_(kb_)
+        vr[b_].copy_(vb_)
+    del kb_, vb_
+    lay_r = d.make_layout(Br, Hqr, Hkvr, dim, Tr, wr.sink, wr.recent, list(wr.bin_edges))
+    lens_r = di.sequence_lengths(wr, seed=1)
+    q_r = [di.q_step(wr, 0, s_, device=dev) for s_ in range(wr.decode_steps)]
+    new_r = [tuple(t.reshape(Br * Hkvr, 1, dim).contiguous() for t in di.kv_new_step(wr, 0, s_, device=dev))
+             for s_ in range(wr.decode_steps)]
+    ws_r = torch.zeros(d.dkv_decode_workspace_bytes(Br, Hqr, Hkvr, dim), dtype=torch.uint8, device=dev)
+    out_r = torch.empty((Br, Hqr, dim), dtype=torch.float32, device=dev)
+    ragged_res = {"workload": wr.name, "batch": Br, "steps": wr.decode_steps,
+                  "context_lens": {"min": int(lens_r.min()), "max": int(lens_r.max()),
+                                   "mean": round(float(lens_r.mean()), 1)}}
+    for mode in ("uniform", "ragged"):
+        km_r = torch.empty((Br, Hkvr, Tr), dtype=torch.uint8, device=dev)
+        kl_r = torch.empty((Br, Hkvr), dtype=torch.int32, device=dev)
+        pat_rd = torch.from_numpy(pat_r).to(dev)
+        if mode == "ragged":
+            d.dkv_map_pattern_ragged(lay_r, torch.from_numpy(lens_r).to(dev), pat_rd, km_r, kl_r)
+        else:
+            d.dkv_map_pattern(lay_r, pat_rd, km_r, kl_r)
+        kept_r = int(kl_r.sum())
+        rows_r = kept_r + Br * Hkvr * capr
+        kc_r = torch.empty((rows_r, dim), dtype=torch.bfloat16, device=dev)
+        vc_r = torch.empty_like(kc_r)
+        so_r = torch.empty(Br * Hkvr, dtype=torch.int64, device=dev)
+        sl_r = torch.empty(Br * Hkvr, dtype=torch.int32, device=dev)
+        cws_r = torch.empty(d.dkv_compact_workspace_bytes(lay_r), dtype=torch.uint8, device=dev)
+        d.dkv_compact(lay_r, kr, vr, km_r, capr, kc_r, vc_r, so_r, sl_r, cws_r)
+        del km_r
+
+        def step_call(s_, shp):
+            kn_, vn_ = new_r[s_]
+            st_ = lib.dkv_append_decode_attn(d.DKV_BF16, Br, Hqr, Hkvr, dim, Pv(q_r[s_].data_ptr()),
+                                             Pv(kn_.data_ptr()), Pv(vn_.data_ptr()), 1, s_, capr, Pv(kc_r.data_ptr()),
+                                             Pv(vc_r.data_ptr()), Pv(so_r.data_ptr()), Pv(sl_r.data_ptr()),
+                                             wr.sm_scale, kept_r + Br * Hkvr * (s_ + 1), Pv(out_r.data_ptr()),
+                                             Pv(ws_r.data_ptr()), ws_r.numel(), Pv(shp))
+            if st_ != 0:
+                raise d.DkvError("dkv_append_decode_attn", st_)
+        step_call(0, sh)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=fam_stream):
+            for s_ in range(wr.decode_steps):
+                step_call(s_, fam_stream.cuda_stream)
+        for _ in range(args.warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        a.record(stream)
+        for _ in range(args.steps):
+            g.replay()
+        b.record(stream)
+        torch.cuda.synchronize()
+        r_us = a.elapsed_time(b) * 1e3 / args.steps / wr.decode_steps
+        r_bytes = (kept_r + Br * Hkvr * (wr.decode_steps + 1) / 2) * dim * elem * 2 + Br * Hqr * dim * (elem + 4)
+        seg = kl_r.view(-1).to(torch.float64)
+        ragged_res[mode] = {"retained_rows": kept_r, "us_per_step": round(r_us, 2),
+                            "gb_per_s": round(r_bytes / (r_us * 1e-6) / 1e9, 1),
+                            "segment_rows": {"min": int(seg.min()), "max": int(seg.max()),
+                                             "cv": round(float(seg.std() / seg.mean()), 3)}}
+        log(f"{mode} batch: {r_us:.1f} us/step, {ragged_res[mode]['gb_per_s']} GB/s")
+        del kc_r, vc_r, g
+        torch.cuda.empty_cache()
+    del kr, vr
+
     # ---------------- dense comparator cache [L][B*Hkv][T+cap][d] ----------
     t_cap = T + cap
     kd = torch.zeros((N, Hkv, t_cap, dim), dtype=torch.bfloat16, device=dev)
@@ -854,6 +933,7 @@ def main():
         "speedup_vs_dense": round(dms / ms, 3),
         "paged": paged_res,
         "topk_export": topk_res,
+        "ragged_batch": ragged_res,
         "pattern_families": {"workload": "llama8b_stack_128k_paper_bins: the same stack with 128-token bins "
                                          "(1,015), pattern = exact-budget export at rho 0.2, then each family",
                              "step": "per layer: dkv_decode_attn (attend only); HIP-graph replays",
