@@ -283,6 +283,8 @@ def main():
     kv_mask = torch.empty((N, Hkv, T), dtype=torch.uint8, device=dev)
     kv_len = torch.empty((N, Hkv), dtype=torch.int32, device=dev)
     e0, e1, e2 = ev(), ev(), ev()
+    d.dkv_map_pattern(lay, pat_d, kv_mask, kv_len)  # first launch loads the code object
+    torch.cuda.synchronize()
     e0.record(stream)
     d.dkv_map_pattern(lay, pat_d, kv_mask, kv_len)
     e1.record(stream)
@@ -295,6 +297,8 @@ def main():
     seg_off = torch.empty(N * Hkv, dtype=torch.int64, device=dev)
     seg_len = torch.empty(N * Hkv, dtype=torch.int32, device=dev)
     cws = torch.empty(d.dkv_compact_workspace_bytes(lay), dtype=torch.uint8, device=dev)
+    d.dkv_compact(lay, k, v, kv_mask, cap, k_c, v_c, seg_off, seg_len, cws)  # loads the code objects
+    torch.cuda.synchronize()
     e1.record(stream)
     d.dkv_compact(lay, k, v, kv_mask, cap, k_c, v_c, seg_off, seg_len, cws)
     e2.record(stream)

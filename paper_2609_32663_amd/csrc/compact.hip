@@ -8,10 +8,13 @@
 //   scan    one workgroup turns tile counts into each tile's first rank within
 //           its segment, the segment lengths, and the segment offsets
 //           (running sum of length + append capacity, unit-major);
-//   gather  each tile rebuilds its ranks with a block scan, lists its retained
-//           positions in rank order in LDS, and copies the rows: LPR lanes
-//           move one row with 16-byte loads and stores (LPR = row bytes / 16),
-//           so a wave moves 64/LPR whole rows per instruction.
+//   gather  two workgroups per tile, one for K and one for V, each rebuild
+//           the tile's ranks with a block scan, list its retained positions
+//           in rank order in LDS, and copy the rows: LPR lanes move one row
+//           with 16-byte loads and stores (LPR = row bytes / 16), so a wave
+//           moves 64/LPR whole rows per instruction, 8 rows per lane group in
+//           flight.  (One workgroup copying both K and V ran 6% slower: four
+//           interleaved streams per workgroup instead of two.)
 // All row arithmetic is 64-bit: a whole-stack cache has more than 2^31 elements.
 
 #include "dkv_device.hpp"
@@ -73,11 +76,12 @@ __global__ __launch_bounds__(kScanThreads) void compact_scan_kernel(CompactParam
 template <int LPR>
 __global__ __launch_bounds__(kThreads) void compact_gather_kernel(CompactParams p) {
   constexpr int kRowsPerPass = kThreads / LPR;
-  constexpr int kUnroll = 4;
+  constexpr int kUnroll = 8;
   __shared__ uint16_t list[kCompactTile];
   __shared__ int64_t red[kThreads / kWave + 1];
 
-  const int tile = blockIdx.x;
+  const int tile = blockIdx.x >> 1;
+  const int which = blockIdx.x & 1;  // 0: K rows (and source positions), 1: V rows
   const int seg = blockIdx.y;
   const int tid = threadIdx.x;
   const uint8_t* mrow = p.mask + (int64_t)seg * p.T;
@@ -95,13 +99,11 @@ __global__ __launch_bounds__(kThreads) void compact_gather_kernel(CompactParams 
   const int64_t src0 = (int64_t)seg * p.T + jt;
   const int lane = tid % LPR;
   const int64_t stride16 = p.row_bytes / 16;  // == LPR
-  const u32x4* ks = reinterpret_cast<const u32x4*>(p.k);
-  const u32x4* vs = reinterpret_cast<const u32x4*>(p.v);
-  u32x4* kd = reinterpret_cast<u32x4*>(p.k_out);
-  u32x4* vd = reinterpret_cast<u32x4*>(p.v_out);
+  const u32x4* src = reinterpret_cast<const u32x4*>(which ? p.v : p.k);
+  u32x4* dst = reinterpret_cast<u32x4*>(which ? p.v_out : p.k_out);
 
   for (int r0 = tid / LPR; r0 < kept; r0 += kRowsPerPass * kUnroll) {
-    u32x4 kb[kUnroll], vb[kUnroll];
+    u32x4 rb[kUnroll];
     int64_t drow[kUnroll];
     bool ok[kUnroll];
 #pragma unroll
@@ -109,18 +111,13 @@ __global__ __launch_bounds__(kThreads) void compact_gather_kernel(CompactParams 
       const int r = r0 + u * kRowsPerPass;
       drow[u] = dst0 + r;
       ok[u] = r < kept && drow[u] < p.out_rows;
-      if (ok[u]) {
-        const int64_t srow = src0 + list[r];
-        kb[u] = ks[srow * stride16 + lane];
-        vb[u] = vs[srow * stride16 + lane];
-      }
+      if (ok[u]) rb[u] = src[(src0 + list[r]) * stride16 + lane];
     }
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       if (ok[u]) {
-        kd[drow[u] * stride16 + lane] = kb[u];
-        vd[drow[u] * stride16 + lane] = vb[u];
-        if (lane == 0 && p.src_pos != nullptr)
+        dst[drow[u] * stride16 + lane] = rb[u];
+        if (which == 0 && lane == 0 && p.src_pos != nullptr)
           p.src_pos[drow[u]] = (int32_t)(jt + list[r0 + u * kRowsPerPass]);
       }
     }
@@ -157,10 +154,11 @@ hipError_t launch_compact(const CompactParams& p, hipStream_t stream) {
   }
   hipLaunchKernelGGL(compact_scan_kernel, dim3(1), dim3(kScanThreads), 0, stream, p);
   if (p.ntiles > 0) {
+    const dim3 ggrid(2 * p.ntiles, p.nseg);  // a K and a V workgroup per tile
     switch (p.row_bytes) {
-      case 128: hipLaunchKernelGGL(compact_gather_kernel<8>, grid, dim3(kThreads), 0, stream, p); break;
-      case 256: hipLaunchKernelGGL(compact_gather_kernel<16>, grid, dim3(kThreads), 0, stream, p); break;
-      case 512: hipLaunchKernelGGL(compact_gather_kernel<32>, grid, dim3(kThreads), 0, stream, p); break;
+      case 128: hipLaunchKernelGGL(compact_gather_kernel<8>, ggrid, dim3(kThreads), 0, stream, p); break;
+      case 256: hipLaunchKernelGGL(compact_gather_kernel<16>, ggrid, dim3(kThreads), 0, stream, p); break;
+      case 512: hipLaunchKernelGGL(compact_gather_kernel<32>, ggrid, dim3(kThreads), 0, stream, p); break;
       default: return hipErrorInvalidValue;
     }
   }

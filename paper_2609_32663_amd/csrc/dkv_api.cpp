@@ -99,7 +99,8 @@ dkv_status map_pattern(const dkv_layout* layout, const int32_t* unit_len, const 
     return DKV_ERR_INVALID_ARG;
   if (!aligned16(kv_mask) || (q_mask != nullptr && !aligned16(q_mask))) return DKV_ERR_MISALIGNED;
   const int64_t nseg = (int64_t)L.num_units * L.num_kv_heads;
-  if (nseg > 0x7FFFFFFF) return DKV_ERR_UNSUPPORTED;
+  // the dispatch's work-item count (workgroups x 256) must fit 32 bits
+  if (nseg > 0x7FFFFFFF || dkv::map_blocks(L.context_len, nseg) > 0xFFFFFFFFLL / 256) return DKV_ERR_UNSUPPORTED;
 
   dkv::MapParams p;
   std::memset(&p, 0, sizeof(p));

@@ -21,6 +21,7 @@ struct MapParams {
   int32_t uniform_width;   // > 0: edges are E[k] = uniform_width * k
   int32_t edges[DKV_MAX_GENERAL_BINS + 1];
 };
+int64_t map_blocks(int32_t T, int64_t num_segments);  // workgroups of one launch
 hipError_t launch_map_pattern(const MapParams& p, int num_segments, hipStream_t stream);
 
 // ---------------------------------------------------------------- compaction

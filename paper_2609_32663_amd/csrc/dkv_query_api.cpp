@@ -19,11 +19,12 @@ dkv_status check_query_shape(int32_t batch, int32_t hq, int32_t hkv, int32_t d, 
   if (batch < 0 || hq <= 0 || hkv <= 0 || hq % hkv != 0 || n_q < 0) return DKV_ERR_INVALID_ARG;
   if (hq / hkv > DKV_MAX_GROUP || (d != 64 && d != 128)) return DKV_ERR_UNSUPPORTED;
   if ((int64_t)batch * hkv > DKV_MAX_SEGMENTS) return DKV_ERR_UNSUPPORTED;
-  // query rows per segment and the grid must fit 31 bits
+  // query rows per segment must fit 31 bits
   const int64_t rows = (int64_t)n_q * (hq / hkv);
   const int64_t wgs = (int64_t)batch * hkv * ((rows + dkv::kQueryRowsPerWG - 1) / dkv::kQueryRowsPerWG) *
                       dkv::kQueryMaxSplit;
-  if (rows > INT32_MAX || wgs > INT32_MAX) return DKV_ERR_UNSUPPORTED;
+  // the dispatch's work-item count (workgroups x 512 threads) must fit 32 bits
+  if (rows > INT32_MAX || wgs > 0xFFFFFFFFLL / 512) return DKV_ERR_UNSUPPORTED;
   return DKV_OK;
 }
 

@@ -1,17 +1,19 @@
 // Pattern -> per-KV-head keep mask (Distance-KV, Sec. 3.4, Eq. (4)-(5) and the
 // GQA union).
 //
-// One workgroup per (unit, KV head) segment.  The group's G pattern rows are
-// folded into one G-bit word per bin in LDS (bit h = query head g*G+h keeps
-// the bin), so the union over the group is "word != 0" and the per-head
-// decision is one bit.  Each thread then owns 16 consecutive positions per
-// sweep: it classifies each as sink / recent / binned / uncovered, looks the
-// bin up (a division for uniform edges, a binary search over the edges in LDS
-// otherwise), and writes 16 mask bytes with one 16-byte store when the row
-// is 16-byte aligned.  The retained count is reduced in the block and written
-// once, so kv_len needs no atomics and no pre-clearing.  In a ragged batch a
-// unit's context is the first unit_len[n] positions of its row: distances
-// count from its end and the rest of the row is not retained.
+// One workgroup per (unit, KV head) segment and chunk of kMapChunk positions
+// (a 128K context is 8 chunks, so the grid fills the chip).  The group's G
+// pattern rows are folded into one G-bit word per bin in LDS (bit h = query
+// head g*G+h keeps the bin), so the union over the group is "word != 0" and
+// the per-head decision is one bit.  Each thread then owns 16 consecutive
+// positions per sweep: it classifies each as sink / recent / binned /
+// uncovered, looks the bin up (a division for uniform edges, a binary search
+// over the edges in LDS otherwise), and writes 16 mask bytes with one 16-byte
+// store when the row is 16-byte aligned.  The chunk's retained count is
+// reduced in the block and added to kv_len with one integer atomic (a first
+// kernel clears kv_len), so the result does not depend on timing.  In a
+// ragged batch a unit's context is the first unit_len[n] positions of its
+// row: distances count from its end and the rest of the row is not retained.
 
 #include "dkv_device.hpp"
 #include "dkv_launch.hpp"
@@ -22,6 +24,7 @@ namespace {
 
 constexpr int kMapThreads = 256;
 constexpr int kMapPerThread = 16;
+constexpr int kMapChunk = 4 * kMapThreads * kMapPerThread;  // positions per workgroup
 
 __device__ __forceinline__ int find_bin(int32_t u, const int32_t* edges, int D, int uniform_w) {
   if (uniform_w > 0) {
@@ -41,7 +44,10 @@ __global__ __launch_bounds__(kMapThreads) void map_pattern_kernel(MapParams p) {
   extern __shared__ __align__(16) uint8_t smem[];
   __shared__ int64_t red[kMapThreads / kWave + 1];
 
-  const int seg = blockIdx.x;
+  const int chunks = (int)(((int64_t)p.T + kMapChunk - 1) / kMapChunk);
+  const int seg = (int)(blockIdx.x / chunks);
+  const int64_t chunk0 = (int64_t)(blockIdx.x - (int64_t)seg * chunks) * kMapChunk;
+  const int64_t chunk1 = chunk0 + kMapChunk < p.T ? chunk0 + kMapChunk : p.T;
   const int unit = seg / p.Hkv;
   const int g = seg - unit * p.Hkv;
   const int tid = threadIdx.x;
@@ -71,7 +77,8 @@ __global__ __launch_bounds__(kMapThreads) void map_pattern_kernel(MapParams p) {
   uint8_t* kv_row = p.kv_mask + (int64_t)seg * T;
   int64_t count = 0;
 
-  for (int64_t j0 = (int64_t)tid * kMapPerThread; j0 < T; j0 += (int64_t)kMapThreads * kMapPerThread) {
+  for (int64_t j0 = chunk0 + (int64_t)tid * kMapPerThread; j0 < chunk1;
+       j0 += (int64_t)kMapThreads * kMapPerThread) {
     uint32_t hb[kMapPerThread];
 #pragma unroll
     for (int e = 0; e < kMapPerThread; ++e) {
@@ -126,15 +133,27 @@ __global__ __launch_bounds__(kMapThreads) void map_pattern_kernel(MapParams p) {
 
   int64_t total;
   block_exclusive_scan<kMapThreads>(count, red, &total);
-  if (tid == 0) p.kv_len[seg] = (int32_t)total;
+  if (tid == 0 && total > 0) atomicAdd(&p.kv_len[seg], (int32_t)total);
+}
+
+__global__ __launch_bounds__(kMapThreads) void map_clear_kernel(int32_t* kv_len, int n) {
+  const int i = blockIdx.x * kMapThreads + threadIdx.x;
+  if (i < n) kv_len[i] = 0;
 }
 
 }  // namespace
 
+int64_t map_blocks(int32_t T, int64_t num_segments) {
+  return ((int64_t)T + kMapChunk - 1) / kMapChunk * num_segments;
+}
+
 hipError_t launch_map_pattern(const MapParams& p, int num_segments, hipStream_t stream) {
   size_t lds = ((size_t)p.D * 2 + 15) & ~(size_t)15;
   if (p.uniform_width == 0) lds += (size_t)(p.D + 1) * 4;
-  hipLaunchKernelGGL(map_pattern_kernel, dim3(num_segments), dim3(kMapThreads), lds, stream, p);
+  hipLaunchKernelGGL(map_clear_kernel, dim3((num_segments + kMapThreads - 1) / kMapThreads), dim3(kMapThreads), 0,
+                     stream, p.kv_len, num_segments);
+  const int64_t blocks = map_blocks(p.T, num_segments);
+  if (blocks > 0) hipLaunchKernelGGL(map_pattern_kernel, dim3((uint32_t)blocks), dim3(kMapThreads), lds, stream, p);
   return hipGetLastError();
 }
 
