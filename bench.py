@@ -51,9 +51,10 @@ def parse():
                     help="skip the oracle timing (for profiler runs)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 1 GiB device copy (HBM-counter calibration)")
-    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+    ap.add_argument("--pmc-summary", nargs=3, metavar=("FETCH_CSV", "WRITE_CSV", "BENCH_LOG"),
                     help="summarise two rocprofv3 --pmc runs of this script (FETCH_SIZE, then "
-                         "WRITE_SIZE, each with --copy-probe --no-cpu-baseline) into the traffic file")
+                         "WRITE_SIZE, each with --copy-probe --no-cpu-baseline) and the JSON line one of "
+                         "them printed into the traffic file")
     ap.add_argument("--trace-summary", nargs=2, metavar=("TRACE_DIR", "BENCH_LOG"),
                     help="summarise a rocprofv3 --kernel-trace --stats run of this script (csv output "
                          "named run_*) and its JSON line into the kernel-trace profile")
@@ -70,6 +71,20 @@ def kernel_hash():
         with open(path, "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
+
+
+def timed_calls_per_mode(b):
+    """Decode calls one timed mode (packed or dense) issues: a warm step, the
+    graph replays and the eager steps, one call per layer each."""
+    return b["config"]["layers"] * (1 + 2 * (b["warmup"] + b["steps"]))
+
+
+def last_json(path):
+    b = None
+    for line in open(path):
+        if line.startswith("{"):
+            b = json.loads(line)
+    return b
 
 
 def is_paged_kernel(name):
@@ -112,10 +127,7 @@ def trace_summary(trace_dir, bench_log, command):
     stats = list(csv.DictReader(open(os.path.join(trace_dir, "run_kernel_stats.csv"))))
     rows = sorted(csv.DictReader(open(os.path.join(trace_dir, "run_kernel_trace.csv"))),
                   key=lambda r: int(r["Start_Timestamp"]))
-    b = None
-    for line in open(bench_log):
-        if line.startswith("{"):
-            b = json.loads(line)
+    b = last_json(bench_log)
     pairs, paged = [], []
     for i in range(len(rows) - 1):
         a, m = rows[i], rows[i + 1]
@@ -124,10 +136,12 @@ def trace_summary(trace_dir, bench_log, command):
             s1, e1 = int(m["Start_Timestamp"]), int(m["End_Timestamp"])
             (paged if is_paged_kernel(a["Kernel_Name"]) else pairs).append(
                 ((e0 - s0) / 1e3, (e1 - s1) / 1e3, (e1 - s0) / 1e3))
-    # with the oracle baseline, one parity call per layer precedes the timing
+    # with the oracle baseline, one parity call per layer precedes the timing;
+    # then the packed and the dense calls, equally many (later sections of
+    # the run make other decode calls)
     front = b["config"]["layers"] if b.get("parity_layer0") else 0
-    timed_pairs = pairs[front:]
-    packed, dense = timed_pairs[: len(timed_pairs) // 2], timed_pairs[len(timed_pairs) // 2:]
+    m = timed_calls_per_mode(b)
+    packed, dense = pairs[front:front + m], pairs[front + m:front + 2 * m]
     lines = [f"# rocprofv3 kernel trace of bench.py ({WORKLOAD}: 32 layers x 32q/8kv x d128, "
              f"T=131072, {b['config']['retained_fraction'] * 100:.1f}% retained)",
              f"# command: {command}",
@@ -190,16 +204,17 @@ def trace_summary(trace_dir, bench_log, command):
         print("\n".join(ql))
 
 
-def pmc_summary(fetch_csv, write_csv, command):
+def pmc_summary(fetch_csv, write_csv, bench_log, command):
     """HBM traffic of one packed attention call from FETCH_SIZE / WRITE_SIZE
     (KiB per dispatch).  Each counter is scaled by what it reads for the
     1 GiB device copy run at the end (which reads and writes exactly 1 GiB),
-    and the packed calls are the first half of the non-paged decode/combine
-    dispatch pairs (the script times the packed path before the dense one);
-    the paged calls, told apart by the kernel's template flag, are averaged
-    on their own."""
+    and the packed calls are the first non-paged decode/combine dispatch pairs
+    of the run (the script times the packed path first; their number follows
+    from the steps of the JSON line); the paged calls, told apart by the
+    kernel's template flag, are averaged on their own."""
     import statistics
     res = {"kernel_sha256_16": kernel_hash(), "command": command, "unit": "bytes per call"}
+    m = timed_calls_per_mode(last_json(bench_log))
     per_call, per_paged = {}, {}
     for key, path, counter in (("fetch", fetch_csv, "FETCH_SIZE"), ("write", write_csv, "WRITE_SIZE")):
         rows = pmc_per_dispatch(path, counter)
@@ -208,7 +223,7 @@ def pmc_summary(fetch_csv, write_csv, command):
         pairs = [(is_paged_kernel(rows[i][0]), rows[i][1] + rows[i + 1][1]) for i in range(len(rows) - 1)
                  if "decode_kernel" in rows[i][0] and "decode_merge_kernel" in rows[i + 1][0]]
         calls = [v for pg, v in pairs if not pg]
-        packed = calls[: len(calls) // 2]
+        packed = calls[:m]
         paged = [v for pg, v in pairs if pg]
         per_call[key] = statistics.mean(packed) * 1024.0 * calib
         res[f"{key}_calibration"] = round(calib, 4)
@@ -383,193 +398,12 @@ def main():
         parity = {"layers": L, "max_rel_err": worst, "seg_len_equal": same_pack}
         log(f"oracle {cpu_s:.2f} s, worst parity err {worst:.2e}")
 
-    # ---------------- exact-budget export and the ablation families -------
-    # The paper's own bin layout (128-token bins: 1,015 at 131,072 tokens) on
-    # the same 8B-shaped stack and the same K/V: the pattern is the
-    # exact-budget export (K = round(0.2 L H D)) of stand-in retention
-    # probabilities, then each ablation family of it; every pattern is mapped,
-    # packed and decoded (32 layers, attend only) like the headline.
-    log("exact-budget export and pattern families")
-    wp = di.workload("llama8b_stack_128k_paper_bins")
-    Lp, Hp, Dp = wp.num_layers, wp.num_q_heads, wp.num_bins
-    probs = di.retention_probs(Lp, Hp, wp.num_kv_heads, Dp, seed=wp.cfg_id)
-    k_budget = d.dkv_budget_entries(wp.rho, Lp, Hp, Dp)
-    probs_d = torch.from_numpy(probs).to(dev)
-    pat_x = torch.empty((Lp, Hp, Dp), dtype=torch.uint8, device=dev)
-    tk_ws = torch.empty(d.dkv_topk_workspace_bytes(Lp, Hp, Dp), dtype=torch.uint8, device=dev)
-    d.dkv_topk_pattern(probs_d, k_budget, pat_x, tk_ws)
-    torch.cuda.synchronize()
-    a, b = ev(), ev()
-    a.record(stream)
-    for _ in range(20):
-        d.dkv_topk_pattern(probs_d, k_budget, pat_x, tk_ws)
-    b.record(stream)
-    torch.cuda.synchronize()
-    topk_us = a.elapsed_time(b) * 1e3 / 20
-    exported = pat_x.cpu().numpy()
-    n_entries = Lp * Hp * Dp
-    # bytes one export reads and writes: six passes over the probabilities
-    # (four digit rounds, tie count, write) and the pattern
-    topk_bytes = 6 * 4 * n_entries + n_entries
-    topk_res = {"entries": n_entries, "k": int(k_budget), "rho": wp.rho, "us": round(topk_us, 1),
-                "gb_per_s": round(topk_bytes / (topk_us * 1e-6) / 1e9, 1),
-                "launches": 11, "ones": int(exported.sum()), "cpu_baseline": None, "equal_to_oracle": None}
-    if not args.no_cpu_baseline:
-        t0 = time.perf_counter()
-        want_pat = o.topk_mask(probs, o.budget_entries(wp.rho, Lp, Hp, Dp))
-        topk_cpu = time.perf_counter() - t0
-        topk_res["equal_to_oracle"] = bool(np.array_equal(exported, want_pat))
-        topk_res["cpu_baseline"] = {"value": round(topk_cpu * 1e3, 2), "unit": "ms", "cores": 1, "kind": "oracle",
-                                    "sample": "the whole export (NumPy lexsort, one thread)"}
-    log(f"topk export {topk_us:.1f} us for {n_entries} entries")
-    lay_p = d.make_layout(N, Hq, Hkv, dim, T, wp.sink, wp.recent, list(wp.bin_edges))
-    fam_res = {}
-    fam_ws = torch.zeros(d.dkv_decode_workspace_bytes(B, Hq, Hkv, dim), dtype=torch.uint8, device=dev)
-    fam_out = torch.empty((B, Hq, dim), dtype=torch.float32, device=dev)
-    fam_stream = torch.cuda.Stream()
-    Pv = ctypes.c_void_p
-    for kind in ("exported",) + di.PATTERN_FAMILIES:
-        pat_f = exported if kind == "exported" else di.pattern_family(exported, kind, Hkv, seed=wp.cfg_id)
-        km_f = torch.empty((N, Hkv, T), dtype=torch.uint8, device=dev)
-        kl_f = torch.empty((N, Hkv), dtype=torch.int32, device=dev)
-        d.dkv_map_pattern(lay_p, torch.from_numpy(np.ascontiguousarray(pat_f)).to(dev), km_f, kl_f)
-        lens_f = kl_f.cpu().to(torch.int64)
-        rows_f = int(lens_f.sum())
-        kc_f = torch.empty((rows_f, dim), dtype=torch.bfloat16, device=dev)
-        vc_f = torch.empty_like(kc_f)
-        so_f = torch.empty(N * Hkv, dtype=torch.int64, device=dev)
-        sl_f = torch.empty(N * Hkv, dtype=torch.int32, device=dev)
-        cws_f = torch.empty(d.dkv_compact_workspace_bytes(lay_p), dtype=torch.uint8, device=dev)
-        d.dkv_compact(lay_p, k, v, km_f, 0, kc_f, vc_f, so_f, sl_f, cws_f)
-        del km_f
-        hints = [int(lens_f[layer * B:(layer + 1) * B].sum()) for layer in range(L)]
-
-        def fam_calls(shp):
-            for layer in range(L):
-                off = layer * nseg_layer
-                st_ = lib.dkv_decode_attn(d.DKV_BF16, B, Hq, Hkv, dim, Pv(q_layers[layer].data_ptr()),
-                                          Pv(kc_f.data_ptr()), Pv(vc_f.data_ptr()), Pv(so_f.data_ptr() + 8 * off),
-                                          Pv(sl_f.data_ptr() + 4 * off), 0, w.sm_scale, hints[layer],
-                                          Pv(fam_out.data_ptr()), Pv(fam_ws.data_ptr()), fam_ws.numel(), Pv(shp))
-                if st_ != 0:
-                    raise d.DkvError("dkv_decode_attn", st_)
-        fam_calls(sh)
-        torch.cuda.synchronize()
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g, stream=fam_stream):
-            fam_calls(fam_stream.cuda_stream)
-        for _ in range(args.warmup):
-            g.replay()
-        torch.cuda.synchronize()
-        a.record(stream)
-        for _ in range(args.steps):
-            g.replay()
-        b.record(stream)
-        torch.cuda.synchronize()
-        f_ms = a.elapsed_time(b) / args.steps
-        f_bytes = rows_f * dim * elem * 2 + L * B * Hq * dim * (elem + 4) + L * nseg_layer * 12
-        per_head = lens_f.view(-1).to(torch.float64)
-        fam_res[kind] = {"logical": round(float(pat_f.mean()), 4),
-                         "physical": round(rows_f / float(N * Hkv * T), 4),
-                         "ms_per_step": round(f_ms, 4), "us_per_layer": round(f_ms * 1e3 / L, 2),
-                         "gb_per_s": round(f_bytes / (f_ms * 1e-3) / 1e9, 1),
-                         "segment_rows": {"min": int(per_head.min()), "max": int(per_head.max()),
-                                          "cv": round(float(per_head.std() / per_head.mean()), 3)},
-                         "lengths_equal_oracle": None}
-        if not args.no_cpu_baseline:
-            olen = o.closed_form_lengths(pat_f, T, wp.sink, wp.recent, wp.bin_edges, Hkv)
-            fam_res[kind]["lengths_equal_oracle"] = bool(np.array_equal(lens_f.numpy(), olen))
-        log(f"pattern {kind}: physical {fam_res[kind]['physical']}, {f_ms * 1e3 / L:.1f} us/layer")
-        del kc_f, vc_f, g
-        torch.cuda.empty_cache()
-
-    # ---------------- ragged batch: contexts of different lengths ----------
-    # The 70B-shaped batch (16 sequences x 64q/8kv, 20% physical budget) once
-    # with every context 32K long and once with per-sequence contexts of
-    # 4K-32K (dkv_map_pattern_ragged); then its 16 decode steps, one fused
-    # append + decode call each, graph-replayed.
-    log("ragged batch")
-    wr = di.workload("llama70b_layer_bs16_32k")
-    Br, Hqr, Hkvr, Tr, capr = wr.batch, wr.num_q_heads, wr.num_kv_heads, wr.context_len, wr.append_cap
-    pat_r, _ = di.make_pattern(wr)
-    kr = torch.empty((Br, Hkvr, Tr, dim), dtype=torch.bfloat16, device=dev)
-    vr = torch.empty_like(kr)
-    for b_ in range(Br):
-        kb_, vb_ = di.kv_unit(wr, b_, device=dev)
-        kr[b_].copy_(kb_)
-        vr[b_].copy_(vb_)
-    del kb_, vb_
-    lay_r = d.make_layout(Br, Hqr, Hkvr, dim, Tr, wr.sink, wr.recent, list(wr.bin_edges))
-    lens_r = di.sequence_lengths(wr, seed=1)
-    q_r = [di.q_step(wr, 0, s_, device=dev) for s_ in range(wr.decode_steps)]
-    new_r = [tuple(t.reshape(Br * Hkvr, 1, dim).contiguous() for t in di.kv_new_step(wr, 0, s_, device=dev))
-             for s_ in range(wr.decode_steps)]
-    ws_r = torch.zeros(d.dkv_decode_workspace_bytes(Br, Hqr, Hkvr, dim), dtype=torch.uint8, device=dev)
-    out_r = torch.empty((Br, Hqr, dim), dtype=torch.float32, device=dev)
-    ragged_res = {"workload": wr.name, "batch": Br, "steps": wr.decode_steps,
-                  "context_lens": {"min": int(lens_r.min()), "max": int(lens_r.max()),
-                                   "mean": round(float(lens_r.mean()), 1)}}
-    for mode in ("uniform", "ragged"):
-        km_r = torch.empty((Br, Hkvr, Tr), dtype=torch.uint8, device=dev)
-        kl_r = torch.empty((Br, Hkvr), dtype=torch.int32, device=dev)
-        pat_rd = torch.from_numpy(pat_r).to(dev)
-        if mode == "ragged":
-            d.dkv_map_pattern_ragged(lay_r, torch.from_numpy(lens_r).to(dev), pat_rd, km_r, kl_r)
-        else:
-            d.dkv_map_pattern(lay_r, pat_rd, km_r, kl_r)
-        kept_r = int(kl_r.sum())
-        rows_r = kept_r + Br * Hkvr * capr
-        kc_r = torch.empty((rows_r, dim), dtype=torch.bfloat16, device=dev)
-        vc_r = torch.empty_like(kc_r)
-        so_r = torch.empty(Br * Hkvr, dtype=torch.int64, device=dev)
-        sl_r = torch.empty(Br * Hkvr, dtype=torch.int32, device=dev)
-        cws_r = torch.empty(d.dkv_compact_workspace_bytes(lay_r), dtype=torch.uint8, device=dev)
-        d.dkv_compact(lay_r, kr, vr, km_r, capr, kc_r, vc_r, so_r, sl_r, cws_r)
-        del km_r
-
-        def step_call(s_, shp):
-            kn_, vn_ = new_r[s_]
-            st_ = lib.dkv_append_decode_attn(d.DKV_BF16, Br, Hqr, Hkvr, dim, Pv(q_r[s_].data_ptr()),
-                                             Pv(kn_.data_ptr()), Pv(vn_.data_ptr()), 1, s_, capr, Pv(kc_r.data_ptr()),
-                                             Pv(vc_r.data_ptr()), Pv(so_r.data_ptr()), Pv(sl_r.data_ptr()),
-                                             wr.sm_scale, kept_r + Br * Hkvr * (s_ + 1), Pv(out_r.data_ptr()),
-                                             Pv(ws_r.data_ptr()), ws_r.numel(), Pv(shp))
-            if st_ != 0:
-                raise d.DkvError("dkv_append_decode_attn", st_)
-        step_call(0, sh)
-        torch.cuda.synchronize()
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g, stream=fam_stream):
-            for s_ in range(wr.decode_steps):
-                step_call(s_, fam_stream.cuda_stream)
-        for _ in range(args.warmup):
-            g.replay()
-        torch.cuda.synchronize()
-        a.record(stream)
-        for _ in range(args.steps):
-            g.replay()
-        b.record(stream)
-        torch.cuda.synchronize()
-        r_us = a.elapsed_time(b) * 1e3 / args.steps / wr.decode_steps
-        r_bytes = (kept_r + Br * Hkvr * (wr.decode_steps + 1) / 2) * dim * elem * 2 + Br * Hqr * dim * (elem + 4)
-        seg = kl_r.view(-1).to(torch.float64)
-        ragged_res[mode] = {"retained_rows": kept_r, "us_per_step": round(r_us, 2),
-                            "gb_per_s": round(r_bytes / (r_us * 1e-6) / 1e9, 1),
-                            "segment_rows": {"min": int(seg.min()), "max": int(seg.max()),
-                                             "cv": round(float(seg.std() / seg.mean()), 3)}}
-        log(f"{mode} batch: {r_us:.1f} us/step, {ragged_res[mode]['gb_per_s']} GB/s")
-        del kc_r, vc_r, g
-        torch.cuda.empty_cache()
-    del kr, vr
-
     # ---------------- dense comparator cache [L][B*Hkv][T+cap][d] ----------
     t_cap = T + cap
     kd = torch.zeros((N, Hkv, t_cap, dim), dtype=torch.bfloat16, device=dev)
     vd = torch.zeros_like(kd)
     kd[:, :, :T].copy_(k)
     vd[:, :, :T].copy_(v)
-    del k, v  # the dense input is no longer needed once packed
-    torch.cuda.empty_cache()
     dseg_off = torch.arange(N * Hkv, dtype=torch.int64, device=dev) * t_cap
     dseg_len = torch.full((N * Hkv,), T, dtype=torch.int32, device=dev)
 
@@ -771,6 +605,188 @@ def main():
     }
     log(f"paged: {pms:.3f} ms/step ({pms * 1e3 / L:.1f} us/layer), select {select_us:.0f} us, "
         f"pages used {paged_res['kv_cache_gib']['pages_used']} GiB")
+
+    # ---------------- exact-budget export and the ablation families -------
+    # The paper's own bin layout (128-token bins: 1,015 at 131,072 tokens) on
+    # the same 8B-shaped stack and the same K/V: the pattern is the
+    # exact-budget export (K = round(0.2 L H D)) of stand-in retention
+    # probabilities, then each ablation family of it; every pattern is mapped,
+    # packed and decoded (32 layers, attend only) like the headline.
+    log("exact-budget export and pattern families")
+    wp = di.workload("llama8b_stack_128k_paper_bins")
+    Lp, Hp, Dp = wp.num_layers, wp.num_q_heads, wp.num_bins
+    probs = di.retention_probs(Lp, Hp, wp.num_kv_heads, Dp, seed=wp.cfg_id)
+    k_budget = d.dkv_budget_entries(wp.rho, Lp, Hp, Dp)
+    probs_d = torch.from_numpy(probs).to(dev)
+    pat_x = torch.empty((Lp, Hp, Dp), dtype=torch.uint8, device=dev)
+    tk_ws = torch.empty(d.dkv_topk_workspace_bytes(Lp, Hp, Dp), dtype=torch.uint8, device=dev)
+    d.dkv_topk_pattern(probs_d, k_budget, pat_x, tk_ws)
+    torch.cuda.synchronize()
+    a, b = ev(), ev()
+    a.record(stream)
+    for _ in range(20):
+        d.dkv_topk_pattern(probs_d, k_budget, pat_x, tk_ws)
+    b.record(stream)
+    torch.cuda.synchronize()
+    topk_us = a.elapsed_time(b) * 1e3 / 20
+    exported = pat_x.cpu().numpy()
+    n_entries = Lp * Hp * Dp
+    # bytes one export reads and writes: six passes over the probabilities
+    # (four digit rounds, tie count, write) and the pattern
+    topk_bytes = 6 * 4 * n_entries + n_entries
+    topk_res = {"entries": n_entries, "k": int(k_budget), "rho": wp.rho, "us": round(topk_us, 1),
+                "gb_per_s": round(topk_bytes / (topk_us * 1e-6) / 1e9, 1),
+                "launches": 11, "ones": int(exported.sum()), "cpu_baseline": None, "equal_to_oracle": None}
+    if not args.no_cpu_baseline:
+        t0 = time.perf_counter()
+        want_pat = o.topk_mask(probs, o.budget_entries(wp.rho, Lp, Hp, Dp))
+        topk_cpu = time.perf_counter() - t0
+        topk_res["equal_to_oracle"] = bool(np.array_equal(exported, want_pat))
+        topk_res["cpu_baseline"] = {"value": round(topk_cpu * 1e3, 2), "unit": "ms", "cores": 1, "kind": "oracle",
+                                    "sample": "the whole export (NumPy lexsort, one thread)"}
+    log(f"topk export {topk_us:.1f} us for {n_entries} entries")
+    lay_p = d.make_layout(N, Hq, Hkv, dim, T, wp.sink, wp.recent, list(wp.bin_edges))
+    fam_res = {}
+    fam_ws = torch.zeros(d.dkv_decode_workspace_bytes(B, Hq, Hkv, dim), dtype=torch.uint8, device=dev)
+    fam_out = torch.empty((B, Hq, dim), dtype=torch.float32, device=dev)
+    fam_stream = torch.cuda.Stream()
+    Pv = ctypes.c_void_p
+    for kind in ("exported",) + di.PATTERN_FAMILIES:
+        pat_f = exported if kind == "exported" else di.pattern_family(exported, kind, Hkv, seed=wp.cfg_id)
+        km_f = torch.empty((N, Hkv, T), dtype=torch.uint8, device=dev)
+        kl_f = torch.empty((N, Hkv), dtype=torch.int32, device=dev)
+        d.dkv_map_pattern(lay_p, torch.from_numpy(np.ascontiguousarray(pat_f)).to(dev), km_f, kl_f)
+        lens_f = kl_f.cpu().to(torch.int64)
+        rows_f = int(lens_f.sum())
+        kc_f = torch.empty((rows_f, dim), dtype=torch.bfloat16, device=dev)
+        vc_f = torch.empty_like(kc_f)
+        so_f = torch.empty(N * Hkv, dtype=torch.int64, device=dev)
+        sl_f = torch.empty(N * Hkv, dtype=torch.int32, device=dev)
+        cws_f = torch.empty(d.dkv_compact_workspace_bytes(lay_p), dtype=torch.uint8, device=dev)
+        d.dkv_compact(lay_p, k, v, km_f, 0, kc_f, vc_f, so_f, sl_f, cws_f)
+        del km_f
+        hints = [int(lens_f[layer * B:(layer + 1) * B].sum()) for layer in range(L)]
+
+        def fam_calls(shp):
+            for layer in range(L):
+                off = layer * nseg_layer
+                st_ = lib.dkv_decode_attn(d.DKV_BF16, B, Hq, Hkv, dim, Pv(q_layers[layer].data_ptr()),
+                                          Pv(kc_f.data_ptr()), Pv(vc_f.data_ptr()), Pv(so_f.data_ptr() + 8 * off),
+                                          Pv(sl_f.data_ptr() + 4 * off), 0, w.sm_scale, hints[layer],
+                                          Pv(fam_out.data_ptr()), Pv(fam_ws.data_ptr()), fam_ws.numel(), Pv(shp))
+                if st_ != 0:
+                    raise d.DkvError("dkv_decode_attn", st_)
+        fam_calls(sh)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=fam_stream):
+            fam_calls(fam_stream.cuda_stream)
+        for _ in range(args.warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        a.record(stream)
+        for _ in range(args.steps):
+            g.replay()
+        b.record(stream)
+        torch.cuda.synchronize()
+        f_ms = a.elapsed_time(b) / args.steps
+        f_bytes = rows_f * dim * elem * 2 + L * B * Hq * dim * (elem + 4) + L * nseg_layer * 12
+        per_head = lens_f.view(-1).to(torch.float64)
+        fam_res[kind] = {"logical": round(float(pat_f.mean()), 4),
+                         "physical": round(rows_f / float(N * Hkv * T), 4),
+                         "ms_per_step": round(f_ms, 4), "us_per_layer": round(f_ms * 1e3 / L, 2),
+                         "gb_per_s": round(f_bytes / (f_ms * 1e-3) / 1e9, 1),
+                         "segment_rows": {"min": int(per_head.min()), "max": int(per_head.max()),
+                                          "cv": round(float(per_head.std() / per_head.mean()), 3)},
+                         "lengths_equal_oracle": None}
+        if not args.no_cpu_baseline:
+            olen = o.closed_form_lengths(pat_f, T, wp.sink, wp.recent, wp.bin_edges, Hkv)
+            fam_res[kind]["lengths_equal_oracle"] = bool(np.array_equal(lens_f.numpy(), olen))
+        log(f"pattern {kind}: physical {fam_res[kind]['physical']}, {f_ms * 1e3 / L:.1f} us/layer")
+        del kc_f, vc_f, g
+        torch.cuda.empty_cache()
+
+    del k, v  # the dense input is no longer needed
+    torch.cuda.empty_cache()
+
+    # ---------------- ragged batch: contexts of different lengths ----------
+    # The 70B-shaped batch (16 sequences x 64q/8kv, 20% physical budget) once
+    # with every context 32K long and once with per-sequence contexts of
+    # 4K-32K (dkv_map_pattern_ragged); then its 16 decode steps, one fused
+    # append + decode call each, graph-replayed.
+    log("ragged batch")
+    wr = di.workload("llama70b_layer_bs16_32k")
+    Br, Hqr, Hkvr, Tr, capr = wr.batch, wr.num_q_heads, wr.num_kv_heads, wr.context_len, wr.append_cap
+    pat_r, _ = di.make_pattern(wr)
+    kr = torch.empty((Br, Hkvr, Tr, dim), dtype=torch.bfloat16, device=dev)
+    vr = torch.empty_like(kr)
+    for b_ in range(Br):
+        kb_, vb_ = di.kv_unit(wr, b_, device=dev)
+        kr[b_].copy_(kb_)
+        vr[b_].copy_(vb_)
+    del kb_, vb_
+    lay_r = d.make_layout(Br, Hqr, Hkvr, dim, Tr, wr.sink, wr.recent, list(wr.bin_edges))
+    lens_r = di.sequence_lengths(wr, seed=1)
+    q_r = [di.q_step(wr, 0, s_, device=dev) for s_ in range(wr.decode_steps)]
+    new_r = [tuple(t.reshape(Br * Hkvr, 1, dim).contiguous() for t in di.kv_new_step(wr, 0, s_, device=dev))
+             for s_ in range(wr.decode_steps)]
+    ws_r = torch.zeros(d.dkv_decode_workspace_bytes(Br, Hqr, Hkvr, dim), dtype=torch.uint8, device=dev)
+    out_r = torch.empty((Br, Hqr, dim), dtype=torch.float32, device=dev)
+    ragged_res = {"workload": wr.name, "batch": Br, "steps": wr.decode_steps,
+                  "context_lens": {"min": int(lens_r.min()), "max": int(lens_r.max()),
+                                   "mean": round(float(lens_r.mean()), 1)}}
+    for mode in ("uniform", "ragged"):
+        km_r = torch.empty((Br, Hkvr, Tr), dtype=torch.uint8, device=dev)
+        kl_r = torch.empty((Br, Hkvr), dtype=torch.int32, device=dev)
+        pat_rd = torch.from_numpy(pat_r).to(dev)
+        if mode == "ragged":
+            d.dkv_map_pattern_ragged(lay_r, torch.from_numpy(lens_r).to(dev), pat_rd, km_r, kl_r)
+        else:
+            d.dkv_map_pattern(lay_r, pat_rd, km_r, kl_r)
+        kept_r = int(kl_r.sum())
+        rows_r = kept_r + Br * Hkvr * capr
+        kc_r = torch.empty((rows_r, dim), dtype=torch.bfloat16, device=dev)
+        vc_r = torch.empty_like(kc_r)
+        so_r = torch.empty(Br * Hkvr, dtype=torch.int64, device=dev)
+        sl_r = torch.empty(Br * Hkvr, dtype=torch.int32, device=dev)
+        cws_r = torch.empty(d.dkv_compact_workspace_bytes(lay_r), dtype=torch.uint8, device=dev)
+        d.dkv_compact(lay_r, kr, vr, km_r, capr, kc_r, vc_r, so_r, sl_r, cws_r)
+        del km_r
+
+        def step_call(s_, shp):
+            kn_, vn_ = new_r[s_]
+            st_ = lib.dkv_append_decode_attn(d.DKV_BF16, Br, Hqr, Hkvr, dim, Pv(q_r[s_].data_ptr()),
+                                             Pv(kn_.data_ptr()), Pv(vn_.data_ptr()), 1, s_, capr, Pv(kc_r.data_ptr()),
+                                             Pv(vc_r.data_ptr()), Pv(so_r.data_ptr()), Pv(sl_r.data_ptr()),
+                                             wr.sm_scale, kept_r + Br * Hkvr * (s_ + 1), Pv(out_r.data_ptr()),
+                                             Pv(ws_r.data_ptr()), ws_r.numel(), Pv(shp))
+            if st_ != 0:
+                raise d.DkvError("dkv_append_decode_attn", st_)
+        step_call(0, sh)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=fam_stream):
+            for s_ in range(wr.decode_steps):
+                step_call(s_, fam_stream.cuda_stream)
+        for _ in range(args.warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        a.record(stream)
+        for _ in range(args.steps):
+            g.replay()
+        b.record(stream)
+        torch.cuda.synchronize()
+        r_us = a.elapsed_time(b) * 1e3 / args.steps / wr.decode_steps
+        r_bytes = (kept_r + Br * Hkvr * (wr.decode_steps + 1) / 2) * dim * elem * 2 + Br * Hqr * dim * (elem + 4)
+        seg = kl_r.view(-1).to(torch.float64)
+        ragged_res[mode] = {"retained_rows": kept_r, "us_per_step": round(r_us, 2),
+                            "gb_per_s": round(r_bytes / (r_us * 1e-6) / 1e9, 1),
+                            "segment_rows": {"min": int(seg.min()), "max": int(seg.max()),
+                                             "cv": round(float(seg.std() / seg.mean()), 3)}}
+        log(f"{mode} batch: {r_us:.1f} us/step, {ragged_res[mode]['gb_per_s']} GB/s")
+        del kc_r, vc_r, g
+        torch.cuda.empty_cache()
+    del kr, vr
 
     # ---------------- query-block attention, all layers ------------------
     log("timing query-block attention")
