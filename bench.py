@@ -170,15 +170,17 @@ def trace_summary(trace_dir, bench_log, command):
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
 
-    # query-block attention: attention kernel (+ combine) per layer call
+    # query-block attention: (plan +) attention kernel (+ combine) per layer call
     qpairs = []
     for i, r in enumerate(rows):
         if "query_attn_kernel" in r["Kernel_Name"]:
             s0, e0 = int(r["Start_Timestamp"]), int(r["End_Timestamp"])
-            e1 = e0
+            sp, e1 = s0, e0
+            if i > 0 and "query_plan_kernel" in rows[i - 1]["Kernel_Name"]:
+                sp = int(rows[i - 1]["Start_Timestamp"])
             if i + 1 < len(rows) and "query_merge_kernel" in rows[i + 1]["Kernel_Name"]:
                 e1 = int(rows[i + 1]["End_Timestamp"])
-            qpairs.append(((e0 - s0) / 1e3, (e1 - e0) / 1e3, (e1 - s0) / 1e3))
+            qpairs.append(((e0 - s0) / 1e3, (e1 - e0) / 1e3, (e1 - sp) / 1e3, (s0 - sp) / 1e3))
     if qpairs and b.get("query_block"):
         qb = b["query_block"]
         ql = [f"# rocprofv3 kernel trace of bench.py, query-block attention ({WORKLOAD}: {qb['n_q']} tokens after "
@@ -191,7 +193,8 @@ def trace_summary(trace_dir, bench_log, command):
                 nm = r["Name"].replace("(anonymous namespace)::", "").replace("dkv::", "")
                 ql.append(f"{nm[:58]:58s} {r['Calls']:>6s} {float(r['AverageNs']) / 1e3:9.2f} "
                           f"{float(r['MinNs']) / 1e3:9.2f} {float(r['MaxNs']) / 1e3:9.2f}")
-        ql += [f"calls {len(qpairs)}: query_attn_kernel mean {st.mean(x[0] for x in qpairs):8.2f}  "
+        ql += [f"calls {len(qpairs)}: plan (start to start) mean {st.mean(x[3] for x in qpairs):6.2f}  "
+               f"query_attn_kernel mean {st.mean(x[0] for x in qpairs):8.2f}  "
                f"combine (end to end) mean {st.mean(x[1] for x in qpairs):6.2f}  call mean "
                f"{st.mean(x[2] for x in qpairs):8.2f} us",
                "",
@@ -832,7 +835,8 @@ def main():
                  "roofline": {"bound": "mfma", "achieved": round(q_tflops, 1), "peak": PEAK_BF16_TFLOPS,
                               "unit": "TFLOP/s", "frac": round(q_tflops / PEAK_BF16_TFLOPS, 4),
                               "traffic": None,
-                              "kernel": "dkv_query_attn call: query_attn_kernel<128> + query_merge_kernel"},
+                              "kernel": "dkv_query_attn call: query_plan_kernel + query_attn_kernel<128> + "
+                                        "query_merge_kernel"},
                  "cpu_baseline": None, "parity_layer0": None}
     if not args.no_cpu_baseline:
         import oracle as o

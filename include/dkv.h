@@ -289,11 +289,15 @@ size_t dkv_query_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t num
  * rows_hint (host) total rows the call attends, sum over segments of
  *          seg_len + n_tail + n_q (0 = unknown); it sizes the split of the key
  *          ranges and must equal the value given to dkv_query_workspace_bytes.
- * workspace  dkv_query_workspace_bytes(...) bytes for per-range partial
- *          results (no initial contents required), or NULL when that is 0.
+ *          A wrong hint changes the split (and the speed), never the result.
+ * workspace  dkv_query_workspace_bytes(...) bytes for the split's plan and
+ *          per-range partial results (no initial contents required), or NULL
+ *          when that is 0 (keys too few to split).
  * Only DKV_BF16 is supported (DKV_ERR_UNSUPPORTED otherwise); head_dim 64 or
- * 128.  The call enqueues the attention kernel and, when the keys are split
- * into several ranges, a combine kernel.
+ * 128; DKV_ERR_UNSUPPORTED also when a dispatch would exceed 2^32 work-items
+ * (512 per workgroup).  When the keys are split the call enqueues a one-workgroup plan
+ * kernel, the attention kernel and a combine kernel; otherwise the attention
+ * kernel alone.
  */
 dkv_status dkv_query_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_heads,
                           int32_t num_kv_heads, int32_t head_dim, int32_t n_q, const void *q,

@@ -20,11 +20,16 @@ dkv_status check_query_shape(int32_t batch, int32_t hq, int32_t hkv, int32_t d, 
   if (hq / hkv > DKV_MAX_GROUP || (d != 64 && d != 128)) return DKV_ERR_UNSUPPORTED;
   if ((int64_t)batch * hkv > DKV_MAX_SEGMENTS) return DKV_ERR_UNSUPPORTED;
   // query rows per segment must fit 31 bits
-  const int64_t rows = (int64_t)n_q * (hq / hkv);
-  const int64_t wgs = (int64_t)batch * hkv * ((rows + dkv::kQueryRowsPerWG - 1) / dkv::kQueryRowsPerWG) *
-                      dkv::kQueryMaxSplit;
-  // the dispatch's work-item count (workgroups x 512 threads) must fit 32 bits
-  if (rows > INT32_MAX || wgs > 0xFFFFFFFFLL / 512) return DKV_ERR_UNSUPPORTED;
+  if ((int64_t)n_q * (hq / hkv) > INT32_MAX) return DKV_ERR_UNSUPPORTED;
+  return DKV_OK;
+}
+
+// The split of a call; DKV_ERR_UNSUPPORTED when its dispatches would not fit
+// 32-bit work-item counts (workgroups x 512 threads) or the items 31 bits.
+dkv_status query_plan(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t n_q, int64_t rows_hint,
+                      dkv::QueryPlanShape* sh) {
+  *sh = dkv::query_plan_shape(batch * hkv, n_q * (hq / hkv), d, rows_hint);
+  if (sh->max_items > 0xFFFFFFFFLL / 512 || sh->max_items > INT32_MAX / 2) return DKV_ERR_UNSUPPORTED;
   return DKV_OK;
 }
 
@@ -36,8 +41,9 @@ size_t dkv_query_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t num
                                  int32_t head_dim, int32_t n_q, int64_t rows_hint) {
   if (check_query_shape(batch, num_q_heads, num_kv_heads, head_dim, n_q) != DKV_OK) return 0;
   if (batch == 0 || n_q == 0) return 0;
-  return dkv::query_workspace_bytes(batch * num_kv_heads, n_q * (num_q_heads / num_kv_heads), head_dim,
-                                    rows_hint);
+  dkv::QueryPlanShape sh;
+  if (query_plan(batch, num_q_heads, num_kv_heads, head_dim, n_q, rows_hint, &sh) != DKV_OK) return 0;
+  return sh.plan_bytes + sh.rec_bytes;
 }
 
 dkv_status dkv_query_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
@@ -56,10 +62,10 @@ dkv_status dkv_query_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_heads, i
       seg_len == nullptr)
     return DKV_ERR_INVALID_ARG;
   if (!aligned16(q) || !aligned16(k_c) || !aligned16(v_c) || !aligned16(out)) return DKV_ERR_MISALIGNED;
-  const int32_t nseg = batch * num_kv_heads;
-  const int32_t G = num_q_heads / num_kv_heads;
-  const int32_t rows = n_q * G;
-  const size_t need = dkv::query_workspace_bytes(nseg, rows, head_dim, rows_hint);
+  dkv::QueryPlanShape sh;
+  st = query_plan(batch, num_q_heads, num_kv_heads, head_dim, n_q, rows_hint, &sh);
+  if (st != DKV_OK) return st;
+  const size_t need = sh.plan_bytes + sh.rec_bytes;
   if (need > 0 && (workspace == nullptr || !aligned16(workspace) || workspace_bytes < need))
     return DKV_ERR_WORKSPACE;
   dkv::QueryParams p;
@@ -71,17 +77,22 @@ dkv_status dkv_query_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_heads, i
   p.seg_len = seg_len;
   p.n_tail = n_tail;
   p.n_q = n_q;
-  p.nseg = nseg;
+  p.nseg = batch * num_kv_heads;
   p.Hkv = num_kv_heads;
   p.Hq = num_q_heads;
-  p.G = G;
-  p.rows = rows;
-  p.qtiles = (rows + dkv::kQueryRowsPerWG - 1) / dkv::kQueryRowsPerWG;
-  p.nsplit = dkv::query_split_count(nseg, rows, rows_hint);
+  p.G = num_q_heads / num_kv_heads;
+  p.rows = n_q * p.G;
+  p.qtiles = sh.qtiles;
+  p.tiles_per_range = (int32_t)sh.tiles_per_range;
+  p.max_items = (int32_t)sh.max_items;
   p.scale_log2 = sm_scale * 1.4426950408889634f;
   p.out = out;
-  p.rec = static_cast<float*>(workspace);
-  return dkv::launch_query_attn(p, head_dim, (hipStream_t)stream) == hipSuccess ? DKV_OK : DKV_ERR_HIP;
+  if (sh.plan_bytes > 0) {
+    p.plan = static_cast<int32_t*>(workspace);
+    p.rec = reinterpret_cast<float*>(static_cast<char*>(workspace) + sh.plan_bytes);
+  }
+  return dkv::launch_query_attn(p, head_dim, sh.max_items, (hipStream_t)stream) == hipSuccess ? DKV_OK
+                                                                                               : DKV_ERR_HIP;
 }
 
 }  // extern "C"

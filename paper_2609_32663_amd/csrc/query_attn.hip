@@ -2,37 +2,52 @@
 // the one-time compaction the query tokens attend to the compressed context,
 // while their own K/V are appended like every new token and kept).
 //
-// Rows and work split.  Segment s = (sequence b, KV head g) has
-// R = n_q * G query rows; row r is token r / G of query head g * G + r % G
-// and sees the segment's first seg_len + n_tail + r / G + 1 rows (the packed
-// context, the tokens appended before the block, and the block causally up
-// to its own token).  A workgroup takes 128 query rows (8 waves of 16) of one
-// segment and one of `nsplit` equal key ranges.  With one range it writes the
-// output; with several, each range writes (max, sum, unnormalised output)
-// per row and a combine kernel folds the ranges in order.
+// Rows.  Segment s = (sequence b, KV head g) has R = n_q * G query rows; row
+// r is token r / G of query head g * G + r % G and sees the segment's first
+// seg_len + n_tail + r / G + 1 rows (the packed context, the tokens appended
+// before the block, and the block causally up to its own token).
 //
-// Per 64-key tile (K and V staged through LDS by the whole workgroup; the
-// next tile's global loads are in flight while the current one is computed):
+// Work split.  A workgroup (8 waves of 32 rows) takes one item: 256 query
+// rows (a query tile) of one segment and one key range.  Each segment's
+// keys are cut into max(1, round(tiles / C)) near-equal ranges of whole
+// 64-key tiles, C the same for every segment, so items are about equally
+// long however unequal the segments are.  A one-workgroup plan kernel counts
+// the ranges and lays the items out segment by segment, range by range,
+// query tile fastest; the workgroups of one hardware L2 domain (ids equal
+// mod 8) take consecutive items, so the query tiles of a key range read it
+// through the same L2.  With one range a workgroup writes the output; with
+// several, each range writes (max, sum, unnormalised output) per row and a
+// combine kernel folds the ranges in order.  When the keys are too few to
+// split at all there is no plan: one workgroup per (segment, query tile).
+//
+// Per 64-key tile, K and V go from memory straight into LDS (16 bytes per
+// lane, two buffers per matrix, a whole tile ahead); every wave then works
+// on 32-key halves:
 //   * S^T = K Q^T with v_mfma_f32_16x16x32_bf16: 16 K rows from LDS are the
-//     A operand, the wave's 16 query rows (registers) the B operand, so lane
-//     (query n, group kg) receives the scores of keys 4kg..4kg+3 of each
+//     A operand, the wave's two 16-row groups (registers) two B operands, so
+//     lane (query n, group kg) receives the scores of keys 4kg..4kg+3 of each
 //     16-key block.
-//   * Online softmax per query row: max over the lane's 16 scores, then over
-//     the row's 4 lanes (permlane swaps); probabilities stay fp32 until the
-//     product.
+//   * Online softmax per query row: max over the lane's scores, then over the
+//     row's 4 lanes (permlane swaps); probabilities 2^(c s - m) stay fp32
+//     until the product.  The reference max m moves only when a half's max
+//     exceeds it by more than 2^8, so the accumulators are rarely rescaled.
 //   * O += P V with v_mfma_f32_16x16x32_bf16 per 32 keys: the probabilities
 //     are the A operand as the scores sit in the lanes (lane (query n, kg)
 //     holds keys 4kg..4kg+3 of two 16-key blocks: its eight K slots), split
 //     into a bf16 high part and a bf16 remainder (two products, ~16
 //     significant bits kept).  The B operand needs, per lane, the same eight
 //     keys of one V column; two ds_read_b64_tr_b16 transpose reads fetch them
-//     from the row-major V tile in LDS (within each 16-lane group, lanes
-//     4r..4r+3 address row r of a 4 x 16 block and lane i receives its column
-//     i).
-// Attention here is a dense contraction (G * n_q query rows against every
-// key), so it is MFMA work, unlike the one-query decode step.
+//     (within each 16-lane group, lanes 4r..4r+3 address row r of a 4 x 16
+//     block and lane i receives its column i).
+// The P V products of one half run beside the softmax of the next, the
+// score products of the half after that beside the bf16 split, so the
+// matrix and the vector units of a SIMD work at once.  Attention here is a
+// dense contraction (G * n_q query rows against every key), so it is MFMA
+// work, unlike the one-query decode step.
 
 #include <hip/hip_runtime.h>
+
+#include <type_traits>
 
 #include "dkv_device.hpp"
 #include "dkv_query.hpp"
@@ -42,9 +57,12 @@ namespace dkv {
 namespace {
 
 constexpr int kQThreads = 512;
-constexpr int kQRows = kQueryRowsPerWG;  // 16 query rows per wave
-constexpr int kQDepth = 2;               // register stages: key tiles whose global loads are in flight
+constexpr int kRG = 2;                   // 16-row groups per wave
+constexpr int kQRows = kQueryRowsPerWG;  // query rows per workgroup
+static_assert(kQRows == kQThreads / kWave * 16 * kRG, "rows per workgroup");
 constexpr int kQKeys = 64;               // keys per tile
+constexpr float kLazy = 8.f;             // log2 headroom of the lazy running max
+constexpr int kPlanThreads = 1024;
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
@@ -54,13 +72,12 @@ typedef float f32x2 __attribute__((ext_vector_type(2)));
 template <int D>
 struct QCfg {
   static constexpr int kRowBytes = D * 2;
-  static constexpr int kKStride = D + 8;   // bf16 per K row in LDS (rows 16-byte aligned)
-  static constexpr int kVStride = D + 16;  // bf16 per V row in LDS (16-byte rows, stride = 32 B mod 128)
-  static constexpr int kChunks = D / 32;   // 16-byte chunks of a row per lane (QK)
-  static constexpr int kBlocks = D / 16;   // 16-column output blocks per lane
-  static constexpr int kRowChunks = D / 8; // 16-byte chunks per row
-  static constexpr int kStage = kQKeys * kRowChunks / kQThreads;  // chunks per thread per matrix
-  static constexpr int kRec = D + 2;       // floats per partial record row
+  static constexpr int kChunks = D / 32;    // 16-byte chunks of a row per lane (QK)
+  static constexpr int kBlocks = D / 16;    // 16-column output blocks per lane
+  static constexpr int kRowChunks = D / 8;  // 16-byte chunks per row
+  static constexpr int kDma = kQKeys * kRowChunks / kWave / (kQThreads / kWave);  // loads per wave per matrix
+  static constexpr int kRec = D + 2;        // floats per partial record row
+  static_assert(kDma >= 1, "a tile needs one direct load per wave at least");
 };
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t q_rsrc(const char* base, uint32_t bytes) {
@@ -95,302 +112,491 @@ __device__ __forceinline__ float row4_max(float x) {
   return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
+// Key tiles of segment s for its last query row (the most any row sees).
+__device__ __forceinline__ int64_t seg_tiles(const QueryParams& p, int s) {
+  return ((int64_t)p.seg_len[s] + p.n_tail + p.n_q + kQKeys - 1) / kQKeys;
+}
+
+__device__ __forceinline__ int64_t seg_ranges(int64_t tiles, int64_t c) {
+  const int64_t r = (tiles + c / 2) / c;
+  return r < 1 ? 1 : r;
+}
+
+// Plan of the split: with C tiles per range (raised if the ranges would not
+// fit the records the workspace holds), ranges per segment and the first
+// item of every segment.
+__global__ __launch_bounds__(kPlanThreads) void query_plan_kernel(QueryParams p) {
+  __shared__ int64_t red[kPlanThreads / kWave + 1];
+  const int tid = threadIdx.x;
+  int64_t part = 0;
+  for (int s = tid; s < p.nseg; s += kPlanThreads) part += seg_tiles(p, s);
+  int64_t total_tiles;
+  block_exclusive_scan<kPlanThreads>(part, red, &total_tiles);
+  // qtiles * sum_s max(1, round(T_s / C)) <= qtiles * (total / C + nseg) <= max_items
+  const int64_t room = p.max_items / p.qtiles - p.nseg;  // >= 1 (host)
+  int64_t c = p.tiles_per_range;
+  const int64_t cmin = (total_tiles + room - 1) / room;
+  if (c < cmin) c = cmin;
+  int64_t base = 0;
+  for (int s0 = 0; s0 < p.nseg; s0 += kPlanThreads) {
+    const int s = s0 + tid;
+    const int64_t r = s < p.nseg ? seg_ranges(seg_tiles(p, s), c) : 0;
+    int64_t sum;
+    const int64_t ex = block_exclusive_scan<kPlanThreads>(r, red, &sum);
+    if (s < p.nseg) p.plan[kQueryPlanHead + s] = (int32_t)((base + ex) * p.qtiles);
+    base += sum;
+  }
+  if (tid == 0) {
+    p.plan[kQueryPlanHead + p.nseg] = (int32_t)(base * p.qtiles);
+    p.plan[0] = (int32_t)(base * p.qtiles);
+    p.plan[1] = (int32_t)c;
+  }
+}
+
 template <int D>
 __global__ __launch_bounds__(kQThreads) void query_attn_kernel(QueryParams p) {
   using C = QCfg<D>;
-  __shared__ __align__(16) uint16_t ks_lds[2][kQKeys * C::kKStride];
-  __shared__ __align__(16) uint16_t vs_lds[2][kQKeys * C::kVStride];
+  // two tile buffers per matrix (separate arrays: the compiler then tells the
+  // direct loads into one apart from the reads of the other)
+  __shared__ __align__(1024) uint16_t k0[kQKeys * D], k1[kQKeys * D];
+  __shared__ __align__(1024) uint16_t v0[kQKeys * D], v1[kQKeys * D];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int n16 = lane & 15;
   const int kg = lane >> 4;
-  const int slot = blockIdx.x;  // (segment, query tile, key range), range fastest
-  const int ks = slot % p.nsplit;
-  const int qt = (slot / p.nsplit) % p.qtiles;
-  const int s = slot / p.nsplit / p.qtiles;
+
+  // ---- this workgroup's item: segment, query tile, key tiles ---------------
+  int item, s, qt;
+  bool single;             // the segment has one range: write the output
+  int64_t t_lo, t_hi;      // key tiles [t_lo, t_hi) of the range
+  if (p.plan == nullptr) {
+    item = blockIdx.x;
+    s = item / p.qtiles;
+    qt = item - s * p.qtiles;
+    single = true;
+    t_lo = 0;
+    t_hi = seg_tiles(p, s);
+  } else {
+    // the grid is a multiple of 8 and at least the items, so every item
+    // i = x * per + y (x < 8, y < per) has its workgroup 8y + x
+    const int total = p.plan[0];
+    const int per = (total + 7) / 8;  // items per L2 domain
+    const int b = blockIdx.x;
+    if (b / 8 >= per) return;
+    item = (b % 8) * per + b / 8;
+    if (item >= total) return;
+    // the segment: the last s with first item <= item
+    int lo = 0, hi = p.nseg;
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (p.plan[kQueryPlanHead + mid] <= item) lo = mid;
+      else hi = mid;
+    }
+    s = lo;
+    const int first = p.plan[kQueryPlanHead + s];
+    const int nr = (p.plan[kQueryPlanHead + s + 1] - first) / p.qtiles;
+    const int r = (item - first) / p.qtiles;
+    qt = item - first - r * p.qtiles;
+    single = nr == 1;
+    const int64_t tiles = seg_tiles(p, s);
+    t_lo = (int64_t)r * tiles / nr;
+    t_hi = (int64_t)(r + 1) * tiles / nr;
+  }
   const int bseq = s / p.Hkv;
   const int g = s - bseq * p.Hkv;
   const int64_t base_len = q_uniform64((int64_t)p.seg_len[s] + p.n_tail);  // rows every query row sees
   const int64_t row0 = q_uniform64(p.seg_off[s]);
 
-  // this lane's query row in the score layout, and the keys it sees
-  const int r = qt * kQRows + wave * 16 + n16;
-  const bool row_ok = r < p.rows;
-  const int tok = row_ok ? r / p.G : 0;
-  const int64_t limit = base_len + tok + 1;
-  // this workgroup's key range
+  // this lane's query rows (one per row group) in the score layout, and the keys they see
+  int r[kRG], tok[kRG];
+  bool row_ok[kRG];
+  int64_t limit[kRG];
+#pragma unroll
+  for (int q = 0; q < kRG; ++q) {
+    r[q] = qt * kQRows + wave * 16 * kRG + 16 * q + n16;
+    row_ok[q] = r[q] < p.rows;
+    tok[q] = row_ok[q] ? r[q] / p.G : 0;
+    limit[q] = base_len + tok[q] + 1;
+  }
+  // this workgroup's keys: the range, up to what its last row sees
+  // (all workgroup-uniform; readfirstlane keeps them in scalar registers)
   const int r_last = min(p.rows - 1, qt * kQRows + kQRows - 1);
   const int64_t lim_max = base_len + r_last / p.G + 1;
-  // (all workgroup-uniform; readfirstlane keeps them in scalar registers)
-  const int64_t chunk = ((lim_max + p.nsplit - 1) / p.nsplit + kQKeys - 1) / kQKeys * kQKeys;
-  const int64_t k_lo = q_uniform64((int64_t)ks * chunk);
-  const int64_t k_hi = q_uniform64(k_lo + chunk < lim_max ? k_lo + chunk : lim_max);
-  const int64_t cut = limit < k_hi ? limit : k_hi;  // keys [k_lo, cut) count for this row
+  const int64_t k_lo = q_uniform64(t_lo * kQKeys);
+  const int64_t k_end = t_hi * kQKeys < lim_max ? t_hi * kQKeys : lim_max;
+  const int64_t k_hi = q_uniform64(k_end > k_lo ? k_end : k_lo);
+  int32_t cut[kRG];  // keys [k_lo, k_lo + cut) count for the row (cut <= the range length)
+#pragma unroll
+  for (int q = 0; q < kRG; ++q) cut[q] = (int32_t)((limit[q] < k_hi ? limit[q] : k_hi) - k_lo);
   // every row of the workgroup sees all keys below this one
   const int64_t all_see = q_uniform64(base_len + 1 < k_hi ? base_len + 1 : k_hi);
 
+  // Scores are taken with |scale| (a negative scale negates the queries,
+  // exactly); a zero scale becomes the smallest normal float, so masked keys
+  // (-inf) stay at -inf after scaling.
+  const bool qneg = p.scale_log2 < 0.f;
+  const float cpos = fmaxf(fabsf(p.scale_log2), 1.17549435e-38f);
   // B operand of QK: query row r, dims 32u + 8kg .. +7
-  u32x4 qb[C::kChunks];
-  {
-    const int hh = r - tok * p.G;
+  u32x4 qb[kRG][C::kChunks];
+#pragma unroll
+  for (int q = 0; q < kRG; ++q) {
+    const int hh = r[q] - tok[q] * p.G;
     const char* qrow = reinterpret_cast<const char*>(p.q) +
-                       (((int64_t)bseq * p.n_q + tok) * p.Hq + (int64_t)g * p.G + (row_ok ? hh : 0)) * C::kRowBytes;
+                       (((int64_t)bseq * p.n_q + tok[q]) * p.Hq + (int64_t)g * p.G + (row_ok[q] ? hh : 0)) *
+                           C::kRowBytes;
 #pragma unroll
     for (int u = 0; u < C::kChunks; ++u) {
       const u32x4 z = {0u, 0u, 0u, 0u};
-      qb[u] = row_ok ? *reinterpret_cast<const u32x4*>(qrow + 64 * u + 16 * kg) : z;
+      qb[q][u] = row_ok[q] ? *reinterpret_cast<const u32x4*>(qrow + 64 * u + 16 * kg) : z;
+      if (qneg) qb[q][u] ^= u32x4{0x80008000u, 0x80008000u, 0x80008000u, 0x80008000u};
     }
   }
 
-  f32x4 o[C::kBlocks];
+  // output accumulators as scalars: a rescale in a branch then updates them
+  // in place instead of in a second set of registers
+  float o[kRG][C::kBlocks][4];
+  float m[kRG], l[kRG];  // reference max of query row n16 (log2 units), this lane's share of its sum
 #pragma unroll
-  for (int b = 0; b < C::kBlocks; ++b) o[b] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m = -INFINITY;  // running max of query row n16 (log2 units)
-  float l = 0.f;        // this lane's share of the row's sum
+  for (int q = 0; q < kRG; ++q) {
+#pragma unroll
+    for (int b = 0; b < C::kBlocks; ++b) o[q][b][0] = o[q][b][1] = o[q][b][2] = o[q][b][3] = 0.f;
+    m[q] = -INFINITY;
+    l[q] = 0.f;
+  }
 
   const char* kbase = reinterpret_cast<const char*>(p.k) + row0 * C::kRowBytes;
   const char* vbase = reinterpret_cast<const char*>(p.v) + row0 * C::kRowBytes;
-  // A ring of kQDepth register stages: while one tile is computed, the
-  // global loads of the next kQDepth tiles are in flight.
-  u32x4 kreg[kQDepth][C::kStage], vreg[kQDepth][C::kStage];
-  // Global -> registers for the tile at key kt: chunk c of the tile is key
-  // c / kRowChunks, bytes 16 * (c % kRowChunks).  Keys past k_hi (a whole
-  // tile past it included) read zeros without touching memory, so the loads
-  // can be issued unconditionally.
-  auto load_stage = [&](u32x4 (&kreg)[C::kStage], u32x4 (&vreg)[C::kStage], int64_t kt) {
+  // LDS layouts (16-byte chunk units; chunk c of key row R is bytes 16c..16c+15):
+  //   K: ((R / 16) * kRowChunks + c) * 16 + R % 16   -- 16 rows of one chunk column together
+  //   V: ((R / 8) * kRowChunks / 2 + c / 2) * 16 + (R % 8) * 2 + c % 2
+  //      -- 8 rows of one 32-byte column pair together
+  // The score product's lanes then read 16 consecutive chunks (K) and the
+  // transpose reads 32 consecutive 8-byte halves (V): no bank conflicts, and
+  // every read is a per-lane base plus a constant.  One wave instruction of
+  // the direct loads fills 64 consecutive chunks (lane l chunk l).
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  // byte offsets of this lane's chunk within a tile for the wave's first
+  // instruction; instruction i covers the chunks 1 KiB x (waves) x i further
+  // on in both layouts, in LDS and in memory alike (the layouts are made of
+  // whole 16-row / 8-row blocks)
+  uint32_t koff, voff;
+  {
+    const int qk_ = 4 * wave + (lane >> 4);  // K: (R / 16) * kRowChunks + c
+    const int rk = 16 * (qk_ / C::kRowChunks) + (lane & 15);
+    koff = (uint32_t)(rk * C::kRowBytes + 16 * (qk_ % C::kRowChunks));
+    const int qv = 4 * wave + (lane >> 4);  // V: (R / 8) * kRowChunks / 2 + c / 2
+    const int rv = 8 * (qv / (C::kRowChunks / 2)) + ((lane >> 1) & 7);
+    voff = (uint32_t)(rv * C::kRowBytes + 16 * (2 * (qv % (C::kRowChunks / 2)) + (lane & 1)));
+  }
+  // Global -> LDS: K or V rows [kt, kt + kQKeys) of the segment into a tile
+  // buffer.  Keys past k_hi (a whole tile past it included) read zeros
+  // without touching memory, so the loads are issued unconditionally.
+  auto issue = [&](const char* base, uint32_t off, int64_t kt, uint16_t* buf) __attribute__((always_inline)) {
     const int64_t left = k_hi - kt;
     const uint32_t nk = (uint32_t)(left <= 0 ? 0 : (left < kQKeys ? left : kQKeys));
-    const __amdgpu_buffer_rsrc_t kr = q_rsrc(kbase + kt * C::kRowBytes, nk * C::kRowBytes);
-    const __amdgpu_buffer_rsrc_t vr = q_rsrc(vbase + kt * C::kRowBytes, nk * C::kRowBytes);
+    const __amdgpu_buffer_rsrc_t rs = q_rsrc(base + kt * C::kRowBytes, nk * C::kRowBytes);
 #pragma unroll
-    for (int i = 0; i < C::kStage; ++i) {
-      const int c = i * kQThreads + tid;
-      const uint32_t off = (uint32_t)((c / C::kRowChunks) * C::kRowBytes + (c % C::kRowChunks) * 16);
-      kreg[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(kr, off, 0, 0));
-      vreg[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(vr, off, 0, 0));
+    for (int i = 0; i < C::kDma; ++i) {
+      const int mi = i * (kQThreads / kWave) + wave_u;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)(buf + 512 * mi), 16, off,
+                                               1024 * (kQThreads / kWave) * i, 0, 0);
     }
   };
 
-  // ---- scores S^T[key][query] of the tile at key kt (K in LDS at kb) --------
-  auto qk = [&](const uint16_t* kb, int64_t kt, float (&sc)[4][4]) {
+  // Scores S^T = K Q^T of half h (keys 32h .. 32h + 31) of the tile in kb:
+  // lane (n16, kg) reads K row 16j + n16, chunk 4u + kg, i.e. chunk index
+  // (j * kRowChunks + 4u + kg) * 16 + n16 = lane + 16 (j kRowChunks + 4u).
+  // Four independent accumulation chains (two key blocks x two row groups).
+  auto qk = [&](const uint16_t* kb, int h, float (&sc)[kRG][2][4]) __attribute__((always_inline)) {
+    f32x4 acc[2][kRG];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int jj = 0; jj < 2; ++jj)
 #pragma unroll
-      for (int u = 0; u < C::kChunks; ++u) {
-        const u32x4 a = *reinterpret_cast<const u32x4*>(&kb[(16 * j + n16) * C::kKStride + 32 * u + 8 * kg]);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, qb[u]),
-                                                      acc, 0, 0, 0);
+      for (int q = 0; q < kRG; ++q) acc[jj][q] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int u = 0; u < C::kChunks; ++u)
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj) {
+        const int j = 2 * h + jj;
+        const u32x4 a = *reinterpret_cast<const u32x4*>(&kb[8 * (lane + 16 * (j * C::kRowChunks + 4 * u))]);
+#pragma unroll
+        for (int q = 0; q < kRG; ++q)
+          acc[jj][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                               __builtin_bit_cast(bf16x8, qb[q][u]), acc[jj][q], 0, 0, 0);
       }
 #pragma unroll
-      for (int v = 0; v < 4; ++v) sc[j][v] = acc[v];
+    for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+      for (int q = 0; q < kRG; ++q)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) sc[q][jj][v] = acc[jj][q][v];
+  };
+
+  // Online softmax of a half whose first key is kh: the raw scores become
+  // the probabilities 2^(c s - m), m and l move on, alpha is each row's
+  // rescale factor.  The reference max m is lazy: it moves only when a
+  // half's max exceeds it by more than kLazy (log2 units), so probabilities
+  // stay below 2^kLazy and the accumulators are rescaled only then.
+  auto softmax = [&](auto masked, float (&sc)[kRG][2][4], int64_t kh, float (&alpha)[kRG])
+                     __attribute__((always_inline)) {
+#pragma unroll
+    for (int q = 0; q < kRG; ++q) {
+      // keys past a row's causal limit or past the range: only in the
+      // halves that reach min over rows of that limit
+      if (decltype(masked)::value && kh + 32 > all_see) {
+        const int32_t lim = cut[q] - (int32_t)(kh - k_lo);  // keys [0, lim) of this half count
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+            if (16 * jj + 4 * kg + v >= lim) sc[q][jj][v] = -INFINITY;
+      }
+      float mx = sc[q][0][0];
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) mx = fmaxf(mx, sc[q][jj][v]);
+      mx = row4_max(mx) * cpos;
+      const bool grow = mx > m[q] + kLazy;
+      alpha[q] = fast_exp2(grow ? m[q] - mx : 0.f);
+      m[q] = grow ? mx : m[q];
+      const float m_use = m[q] == -INFINITY ? 0.f : m[q];
+      float ps = 0.f;
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          sc[q][jj][v] = fast_exp2(__builtin_fmaf(sc[q][jj][v], cpos, -m_use));
+          ps += sc[q][jj][v];
+        }
+      l[q] = l[q] * alpha[q] + ps;
     }
   };
 
-  // ---- softmax of the tile's scores and O += P V (V in LDS at vb) ---------
-  auto softmax_pv = [&](float (&sc)[4][4], const uint16_t* vb, int64_t kt) {
+  // O *= alpha per row.  Output rows of this lane are queries 4kg + v of the
+  // group: their factors live in the lanes of those rows.  The wave skips
+  // the rescale unless a factor differs from 1.
+  auto rescale = [&](const float (&alpha)[kRG]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int q = 0; q < kRG; ++q) {
+      if (__builtin_amdgcn_ballot_w64(alpha[q] != 1.f)) {
 #pragma unroll
-      for (int v = 0; v < 4; ++v) sc[j][v] *= p.scale_log2;
-    // keys past a row's causal limit or past the range: only in the tiles
-    // that reach min over rows of that limit
-    if (kt + kQKeys > all_see) {
-      const int64_t lim = cut - kt;  // keys [0, lim) of this tile count for the row
+        for (int v = 0; v < 4; ++v) {
+          const float av = __shfl(alpha[q], 4 * kg + v, 64);
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int v = 0; v < 4; ++v)
-          if (16 * j + 4 * kg + v >= lim) sc[j][v] = -INFINITY;
-    }
-
-    // online softmax of row n16
-    float mx = sc[0][0];
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) mx = fmaxf(mx, sc[j][v]);
-    mx = row4_max(mx);
-    const float m_new = fmaxf(m, mx);
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = fast_exp2(m - m_use);
-    float ps = 0.f;
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        sc[j][v] = fast_exp2(sc[j][v] - m_use);
-        ps += sc[j][v];
-      }
-    l = l * alpha + ps;
-    m = m_new;
-    // output rows of this lane are queries 4kg + v: their factors live in
-    // the lanes of those rows.  Once the maxima settle every factor is 1 and
-    // the wave skips the rescale.
-    if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const float av = __shfl(alpha, 4 * kg + v, 64);
-#pragma unroll
-        for (int b = 0; b < C::kBlocks; ++b) o[b][v] *= av;
+          for (int b = 0; b < C::kBlocks; ++b) o[q][b][v] *= av;
+        }
       }
     }
+  };
 
-    // O += P V, 32 keys per product.  K slot e of lane group kg is key
-    // 32h + 4kg + e (e < 4) or 32h + 16 + 4kg + (e - 4): the lane's scores of
-    // blocks 2h and 2h + 1.
+  // Probabilities of a half as the A operand of P V: K slot e of lane group
+  // kg is key 4kg + e (e < 4) or 16 + 4kg + (e - 4) of the half, the lane's
+  // scores of its two 16-key blocks; high part and remainder.
+  auto split = [&](const float (&sc)[kRG][2][4], u32x4 (&ph)[kRG], u32x4 (&pl)[kRG]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      u32x4 ph, pl;
+    for (int q = 0; q < kRG; ++q)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        uint32_t a, b;
-        bf16_split(sc[2 * h + (e >> 1)][2 * (e & 1)], sc[2 * h + (e >> 1)][2 * (e & 1) + 1], a, b);
-        ph[e] = a;
-        pl[e] = b;
+        uint32_t x, y;
+        bf16_split(sc[q][e >> 1][2 * (e & 1)], sc[q][e >> 1][2 * (e & 1) + 1], x, y);
+        ph[q][e] = x;
+        pl[q][e] = y;
       }
-      // transpose-read addresses: lane 4r + q of group kg reads row
-      // 32h + 4kg + r (and the row 16 below), columns 16b + 4q .. +3
-      const uint16_t* v0 = &vb[(32 * h + 4 * kg + (n16 >> 2)) * C::kVStride + 4 * (n16 & 3)];
+  };
+
+  // O += P V over half h of the tile whose V is in vb; each V fragment
+  // serves both row groups.  Transpose-read addresses: lane 4r + q of group
+  // kg reads row R = 32h + 4kg + r (and R + 16), columns 16b + 4q .. +3, i.e.
+  // chunk c = 2b + q / 2, half q % 2: chunk index
+  // ((4h + kg / 2) * kRowChunks / 2 + b) * 16 + (4 (kg % 2) + r) * 2 + q / 2.
+  // Two V blocks at a time: the high parts of both, then the remainders, so
+  // a product never waits for the one just before it.
+  auto pv = [&](const uint16_t* vb, int h, const u32x4 (&ph)[kRG], const u32x4 (&pl)[kRG])
+                __attribute__((always_inline)) {
+    const uint16_t* vr0 = &vb[8 * ((4 * h + (kg >> 1)) * (C::kRowChunks / 2) * 16 + (4 * (kg & 1) + (n16 >> 2)) * 2 +
+                                   ((n16 >> 1) & 1)) + 4 * (n16 & 1)];
 #pragma unroll
-      for (int b = 0; b < C::kBlocks; ++b) {
-        const s16x4 t0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(v0 + 16 * b));
-        const s16x4 t1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(v0 + 16 * C::kVStride + 16 * b));
+    for (int b0 = 0; b0 < C::kBlocks; b0 += 2) {
+      u32x4 vbo[2];
+#pragma unroll
+      for (int bb = 0; bb < 2; ++bb) {
+        const int b = b0 + bb;
+        const s16x4 t0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vr0 + 8 * 16 * b));
+        const s16x4 t1 =
+            __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vr0 + 8 * 16 * (2 * (C::kRowChunks / 2) + b)));
         const uint2 w0 = __builtin_bit_cast(uint2, t0);
         const uint2 w1 = __builtin_bit_cast(uint2, t1);
-        const u32x4 vbo = {w0.x, w0.y, w1.x, w1.y};
-        o[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ph), __builtin_bit_cast(bf16x8, vbo),
-                                                       o[b], 0, 0, 0);
-        o[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, pl), __builtin_bit_cast(bf16x8, vbo),
-                                                       o[b], 0, 0, 0);
+        vbo[bb] = u32x4{w0.x, w0.y, w1.x, w1.y};
       }
-    }
-  };
-
-  auto store_tile = [&](const u32x4 (&kr)[C::kStage], const u32x4 (&vr)[C::kStage], uint16_t* kb, uint16_t* vb) {
 #pragma unroll
-    for (int c0 = 0; c0 < C::kStage; ++c0) {
-      const int c = c0 * kQThreads + tid;
-      const int key = c / C::kRowChunks;
-      const int part = c % C::kRowChunks;
-      *reinterpret_cast<u32x4*>(&kb[key * C::kKStride + part * 8]) = kr[c0];
-      *reinterpret_cast<u32x4*>(&vb[key * C::kVStride + part * 8]) = vr[c0];
+      for (int part = 0; part < 2; ++part)
+#pragma unroll
+        for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+          for (int q = 0; q < kRG; ++q) {
+            const int b = b0 + bb;
+            f32x4 c = {o[q][b][0], o[q][b][1], o[q][b][2], o[q][b][3]};
+            c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, part ? pl[q] : ph[q]),
+                                                        __builtin_bit_cast(bf16x8, vbo[bb]), c, 0, 0, 0);
+            o[q][b][0] = c[0];
+            o[q][b][1] = c[1];
+            o[q][b][2] = c[2];
+            o[q][b][3] = c[3];
+          }
     }
   };
 
-  // Software pipeline over key tiles.  Tile t sits in LDS buffer t % 2; the
-  // global loads of tiles t + 1 and t + 2 are in flight in the two register
-  // stages.  Iteration t stores tile t + 1 into the other buffer, issues the
-  // score products of tile t + 1 and then does the softmax and P V of tile t,
-  // so the matrix unit works on tile t + 1 while the vector unit works on
-  // tile t.  Loads are issued in ring order (scheduling barriers keep them
-  // there), so every store waits only for its own stage.  Tiles past k_hi
-  // hold zeros and all their keys are masked, so they change nothing.
-  load_stage(kreg[0], vreg[0], k_lo);
-  __builtin_amdgcn_sched_barrier(0);
-  load_stage(kreg[1], vreg[1], k_lo + kQKeys);
-  __builtin_amdgcn_sched_barrier(0);
-  store_tile(kreg[0], vreg[0], ks_lds[0], vs_lds[0]);
+  // Software pipeline over 32-key halves, in each wave: the P V products of
+  // half g - 1 run beside the softmax of half g, the score products of half
+  // g + 1 beside the bf16 split of half g.  K and V have two tile buffers
+  // each.  Once per tile t, between the score products of its second half
+  // and the P V products of its first, the waves meet: by then every wave
+  // has finished reading K of tile t and V of tile t - 1, so K of tile t + 2
+  // and V of tile t + 1 are loaded into those buffers; they have a whole
+  // tile of work to land before the next meeting, where each wave waits for
+  // its own loads first.  Tiles past k_hi hold zeros and all their keys are
+  // masked, so they change nothing.
+  uint16_t* const kbuf[2] = {k0, k1};
+  uint16_t* const vbuf[2] = {v0, v1};
+  issue(kbase, koff, k_lo, kbuf[0]);
+  issue(vbase, voff, k_lo, vbuf[0]);
+  issue(kbase, koff, k_lo + kQKeys, kbuf[1]);
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
   __syncthreads();
-  load_stage(kreg[0], vreg[0], k_lo + 2 * kQKeys);
-  float sc[2][4][4];
-  qk(ks_lds[0], k_lo, sc[0]);
+  float sa[kRG][2][4], sb[kRG][2][4], al[kRG];
+  u32x4 ph[kRG], pl[kRG];
+  qk(kbuf[0], 0, sa);
+  softmax(std::true_type{}, sa, k_lo, al);
   const int64_t ntile = k_hi > k_lo ? (k_hi - k_lo + kQKeys - 1) / kQKeys : 0;
   const int64_t nround = q_uniform64((ntile + 1) / 2);
+  // pairs of tiles whose halves (up to 32 keys past the pair) all lie below
+  // every row's limit need no masking
+  const int64_t clear = all_see - k_lo - 5 * 32;
+  int64_t nclear = clear >= 0 ? clear / (2 * kQKeys) + 1 : 0;
+  nclear = q_uniform64(nclear < nround ? nclear : nround);
   int64_t kt = k_lo;
-  for (int64_t rd = 0; rd < nround; ++rd) {
+  auto tile_pair = [&](auto masked) __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      __syncthreads();  // every wave is done with tile t - 1 (buffer 1 - i)
-      store_tile(kreg[1 - i], vreg[1 - i], ks_lds[1 - i], vs_lds[1 - i]);
+      qk(kbuf[i], 1, sb);  // half 2t + 1 (tile t)
+      split(sa, ph, pl);   // half 2t
+      __builtin_amdgcn_s_waitcnt(0x0F70);
       __syncthreads();
-      load_stage(kreg[1 - i], vreg[1 - i], kt + 3 * kQKeys);
-      qk(ks_lds[1 - i], kt + kQKeys, sc[1 - i]);
-      softmax_pv(sc[i], vs_lds[i], kt);
+      issue(kbase, koff, kt + 2 * kQKeys, kbuf[i]);
+      issue(vbase, voff, kt + kQKeys, vbuf[1 - i]);
+      pv(vbuf[i], 0, ph, pl);  // half 2t
+      softmax(masked, sb, kt + 32, al);
+      rescale(al);
+      qk(kbuf[1 - i], 0, sa);  // half 2t + 2 (tile t + 1)
+      split(sb, ph, pl);       // half 2t + 1
+      pv(vbuf[i], 1, ph, pl);  // half 2t + 1
+      softmax(masked, sa, kt + kQKeys, al);
+      rescale(al);
       kt += kQKeys;
     }
-  }
+  };
+  for (int64_t rd = 0; rd < nclear; ++rd) tile_pair(std::false_type{});
+  for (int64_t rd = nclear; rd < nround; ++rd) tile_pair(std::true_type{});
+  // no direct load may still be writing LDS when the workgroup ends
+  __builtin_amdgcn_s_waitcnt(0x0F70);
 
   // ---- row totals; write the output or this range's record ------------------
-  l = lane_xor_sum<16>(l);
-  float* rec = p.rec + (int64_t)slot * kQRows * C::kRec;
+  float* rec = p.rec + (int64_t)item * kQRows * C::kRec;
 #pragma unroll
-  for (int v = 0; v < 4; ++v) {
-    const int rr = wave * 16 + 4 * kg + v;  // row within the tile
-    const int rq = qt * kQRows + rr;
-    const float lq = __shfl(l, 4 * kg + v, 64);
-    const float mq = __shfl(m, 4 * kg + v, 64);
-    if (rq < p.rows) {
-      if (p.nsplit == 1) {
-        const int tq = rq / p.G;
-        float* orow = p.out + (((int64_t)bseq * p.n_q + tq) * p.Hq + (int64_t)g * p.G + (rq - tq * p.G)) * D;
-        const float inv = lq > 0.f ? 1.f / lq : 0.f;
+  for (int q = 0; q < kRG; ++q) {
+    l[q] = lane_xor_sum<16>(l[q]);
 #pragma unroll
-        for (int b = 0; b < C::kBlocks; ++b) orow[16 * b + n16] = o[b][v] * inv;
-      } else {
-        float* rrow = rec + (int64_t)rr * C::kRec;
-        if (n16 == 0) {
-          rrow[0] = mq;
-          rrow[1] = lq;
+    for (int v = 0; v < 4; ++v) {
+      const int rr = wave * 16 * kRG + 16 * q + 4 * kg + v;  // row within the tile
+      const int rq = qt * kQRows + rr;
+      const float lq = __shfl(l[q], 4 * kg + v, 64);
+      const float mq = __shfl(m[q], 4 * kg + v, 64);
+      if (rq < p.rows) {
+        if (single) {
+          const int tq = rq / p.G;
+          float* orow = p.out + (((int64_t)bseq * p.n_q + tq) * p.Hq + (int64_t)g * p.G + (rq - tq * p.G)) * D;
+          const float inv = lq > 0.f ? 1.f / lq : 0.f;
+#pragma unroll
+          for (int b = 0; b < C::kBlocks; ++b) orow[16 * b + n16] = o[q][b][v] * inv;
+        } else {
+          float* rrow = rec + (int64_t)rr * C::kRec;
+          if (n16 == 0) {
+            rrow[0] = mq;
+            rrow[1] = lq;
+          }
+#pragma unroll
+          for (int b = 0; b < C::kBlocks; ++b) rrow[2 + 16 * b + n16] = o[q][b][v];
         }
-#pragma unroll
-        for (int b = 0; b < C::kBlocks; ++b) rrow[2 + 16 * b + n16] = o[b][v];
       }
     }
   }
 }
 
 // Combine kernel: thread item (row, 4 columns) of one (segment, query tile);
-// kMergeThreads items per workgroup.  A thread loads the row's max and sum
-// and its 4 columns from every key range at once (one memory round trip),
-// then folds the ranges in order:
+// kMergeThreads items per workgroup.  Segments with one range were written
+// by the attention kernel.  A thread loads the row's max, sum and 4 columns
+// from eight ranges at once (one memory round trip per eight), then folds
+// them in range order into
 //   M = max_k m_k,  out = sum_k 2^(m_k - M) o_k / sum_k 2^(m_k - M) l_k.
 constexpr int kMergeThreads = 256;
+constexpr int kMergeBatch = 8;
 
 template <int D>
 __global__ __launch_bounds__(kMergeThreads) void query_merge_kernel(QueryParams p) {
   using C = QCfg<D>;
-  constexpr int kItems = kQRows * (D / 4);                 // items per query tile
-  constexpr int kParts = kItems / kMergeThreads;           // workgroups per query tile
-  const int tile = blockIdx.x / kParts;                    // s * qtiles + qt
-  const int item = (blockIdx.x - tile * kParts) * kMergeThreads + threadIdx.x;
+  constexpr int kItems = kQRows * (D / 4);        // items per query tile
+  constexpr int kParts = kItems / kMergeThreads;  // workgroups per query tile
+  const int tile = blockIdx.x / kParts;           // s * qtiles + qt
+  const int it = (blockIdx.x - tile * kParts) * kMergeThreads + threadIdx.x;
   const int s = tile / p.qtiles;
   const int qt = tile - s * p.qtiles;
-  const int rr = item / (D / 4);
-  const int c4 = item - rr * (D / 4);
+  const int rr = it / (D / 4);
+  const int c4 = it - rr * (D / 4);
   const int rq = qt * kQRows + rr;
   if (rq >= p.rows) return;
+  const int first = p.plan[kQueryPlanHead + s];
+  const int nr = (p.plan[kQueryPlanHead + s + 1] - first) / p.qtiles;
+  if (nr <= 1) return;
   const int bseq = s / p.Hkv;
   const int g = s - bseq * p.Hkv;
-  const float* recs = p.rec + (int64_t)tile * p.nsplit * kQRows * C::kRec + (int64_t)rr * C::kRec;
-  float mk[kQueryMaxSplit], lk[kQueryMaxSplit];
-  f32x4 ak[kQueryMaxSplit];
-#pragma unroll
-  for (int k = 0; k < kQueryMaxSplit; ++k) {
-    if (k < p.nsplit) {
-      const float* r = recs + (int64_t)k * kQRows * C::kRec;
-      mk[k] = r[0];
-      lk[k] = r[1];
-      ak[k] = *reinterpret_cast<const f32x4*>(r + 2 + 4 * c4);
-    } else {
-      mk[k] = -INFINITY;
-      lk[k] = 0.f;
-      ak[k] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
-  }
-  float M = -INFINITY;
-#pragma unroll
-  for (int k = 0; k < kQueryMaxSplit; ++k) M = fmaxf(M, mk[k]);
-  const float Mu = M == -INFINITY ? 0.f : M;
-  float L = 0.f;
+  // record of range k: item first + k * qtiles + qt
+  const float* recs = p.rec + ((int64_t)first + qt) * kQRows * C::kRec + (int64_t)rr * C::kRec;
+  const int64_t stride = (int64_t)p.qtiles * kQRows * C::kRec;
+  float M = -INFINITY, L = 0.f;
   f32x4 A = {0.f, 0.f, 0.f, 0.f};
+  for (int k0 = 0; k0 < nr; k0 += kMergeBatch) {
+    float mk[kMergeBatch], lk[kMergeBatch];
+    f32x4 ak[kMergeBatch];
 #pragma unroll
-  for (int k = 0; k < kQueryMaxSplit; ++k) {
-    const float f = fast_exp2(mk[k] - Mu);
-    L += f * lk[k];
-    A += f * ak[k];
+    for (int k = 0; k < kMergeBatch; ++k) {
+      if (k0 + k < nr) {
+        const float* r = recs + (int64_t)(k0 + k) * stride;
+        mk[k] = r[0];
+        lk[k] = r[1];
+        ak[k] = *reinterpret_cast<const f32x4*>(r + 2 + 4 * c4);
+      } else {
+        mk[k] = -INFINITY;
+        lk[k] = 0.f;
+        ak[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+    float Mn = M;
+#pragma unroll
+    for (int k = 0; k < kMergeBatch; ++k) Mn = fmaxf(Mn, mk[k]);
+    const float Mu = Mn == -INFINITY ? 0.f : Mn;
+    const float fo = fast_exp2(M - Mu);
+    L *= fo;
+    A *= fo;
+#pragma unroll
+    for (int k = 0; k < kMergeBatch; ++k) {
+      const float f = fast_exp2(mk[k] - Mu);
+      L += f * lk[k];
+      A += f * ak[k];
+    }
+    M = Mn;
   }
   const float inv = L > 0.f ? 1.f / L : 0.f;
   const int tq = rq / p.G;
@@ -399,42 +605,48 @@ __global__ __launch_bounds__(kMergeThreads) void query_merge_kernel(QueryParams 
 }
 
 template <int D>
-hipError_t launch_d(const QueryParams& p, hipStream_t stream) {
-  const int64_t wgs = (int64_t)p.nseg * p.qtiles * p.nsplit;
-  hipLaunchKernelGGL((query_attn_kernel<D>), dim3((unsigned)wgs), dim3(kQThreads), 0, stream, p);
-  if (p.nsplit > 1) {
+hipError_t launch_d(const QueryParams& p, int64_t grid, hipStream_t stream) {
+  if (p.plan != nullptr) hipLaunchKernelGGL(query_plan_kernel, dim3(1), dim3(kPlanThreads), 0, stream, p);
+  hipLaunchKernelGGL((query_attn_kernel<D>), dim3((unsigned)grid), dim3(kQThreads), 0, stream, p);
+  if (p.plan != nullptr) {
     const int64_t parts = (int64_t)kQRows * (D / 4) / kMergeThreads;
-    hipLaunchKernelGGL((query_merge_kernel<D>), dim3((unsigned)(p.nseg * p.qtiles * parts)), dim3(kMergeThreads), 0,
-                       stream, p);
+    hipLaunchKernelGGL((query_merge_kernel<D>), dim3((unsigned)((int64_t)p.nseg * p.qtiles * parts)),
+                       dim3(kMergeThreads), 0, stream, p);
   }
   return hipGetLastError();
 }
 
 }  // namespace
 
-int32_t query_split_count(int32_t nseg, int32_t rows, int64_t rows_hint) {
-  // about two workgroups per compute unit of a 256-CU part
-  constexpr int64_t kTargetWG = 512;
-  const int64_t qtiles = (rows + kQRows - 1) / kQRows;
-  const int64_t base = (int64_t)nseg * qtiles;
-  int64_t n = (kTargetWG + base - 1) / base;
-  // each range keeps at least 8 key tiles
-  const int64_t keys = rows_hint > 0 ? rows_hint / (nseg > 0 ? nseg : 1) : (int64_t)1 << 30;
-  const int64_t by_keys = keys / (8 * kQKeys);
-  if (n > by_keys) n = by_keys;
-  if (n > kQueryMaxSplit) n = kQueryMaxSplit;
-  return (int32_t)(n < 1 ? 1 : n);
+QueryPlanShape query_plan_shape(int32_t nseg, int32_t rows, int32_t head_dim, int64_t rows_hint) {
+  QueryPlanShape sh;
+  sh.qtiles = (rows + kQRows - 1) / kQRows;
+  const int64_t units = (int64_t)nseg * sh.qtiles;
+  // key tiles of all segments: the hint's rows, or (unknown) a long context
+  const int64_t hint = rows_hint < ((int64_t)1 << 40) ? rows_hint : ((int64_t)1 << 40);
+  const int64_t tiles = hint > 0 ? (hint + kQKeys - 1) / kQKeys + nseg : (int64_t)nseg * kQueryUnknownTiles;
+  sh.tiles_per_range = (sh.qtiles * tiles + kQueryTargetItems - 1) / kQueryTargetItems;
+  if (sh.tiles_per_range < kQueryMinTiles) sh.tiles_per_range = kQueryMinTiles;
+  if (sh.tiles_per_range > ((int64_t)1 << 30)) sh.tiles_per_range = (int64_t)1 << 30;
+  // segments of fewer than two ranges' worth of keys on average: no split
+  if (tiles < (int64_t)nseg * 2 * kQueryMinTiles) {
+    sh.max_items = units;
+    sh.plan_bytes = 0;
+    sh.rec_bytes = 0;
+    return sh;
+  }
+  // sum_s max(1, round(T_s / C)) <= tiles / C + nseg for the hinted tiles;
+  // the plan kernel raises C if the real keys would need more
+  // (launched as a multiple of 8 workgroups: items are dealt to the 8 L2
+  // domains in runs of ceil(items / 8))
+  sh.max_items = (sh.qtiles * (tiles / sh.tiles_per_range + nseg + 1) + 7) / 8 * 8;
+  sh.plan_bytes = ((size_t)(kQueryPlanHead + nseg + 1) * sizeof(int32_t) + 255) / 256 * 256;
+  sh.rec_bytes = (size_t)sh.max_items * kQRows * (head_dim + 2) * sizeof(float);
+  return sh;
 }
 
-size_t query_workspace_bytes(int32_t nseg, int32_t rows, int32_t head_dim, int64_t rows_hint) {
-  const int32_t n = query_split_count(nseg, rows, rows_hint);
-  if (n <= 1) return 0;
-  const int64_t qtiles = (rows + kQRows - 1) / kQRows;
-  return (size_t)nseg * qtiles * n * kQRows * (head_dim + 2) * sizeof(float);
-}
-
-hipError_t launch_query_attn(const QueryParams& p, int head_dim, hipStream_t stream) {
-  return head_dim == 64 ? launch_d<64>(p, stream) : launch_d<128>(p, stream);
+hipError_t launch_query_attn(const QueryParams& p, int head_dim, int64_t grid, hipStream_t stream) {
+  return head_dim == 64 ? launch_d<64>(p, grid, stream) : launch_d<128>(p, grid, stream);
 }
 
 }  // namespace dkv

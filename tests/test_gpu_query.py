@@ -62,7 +62,8 @@ def _run(d, rng, B, Hkv, G, T, dim, keep, n_tail, n_q, cap=None, sm_scale=None, 
                      cap, k_c, v_c, seg_off, seg_len)
     d.dkv_append(kb.reshape(B * Hkv, n_q, dim).to(DEV), vb.reshape(B * Hkv, n_q, dim).to(DEV), n_tail, cap,
                  k_c, v_c, seg_off, seg_len)
-    rows_hint = int(mask.sum()) + B * Hkv * (n_tail + n_q) if hint == "exact" else hint
+    exact = int(mask.sum()) + B * Hkv * (n_tail + n_q)
+    rows_hint = exact if hint == "exact" else (hint(exact) if callable(hint) else hint)
     wsb = d.dkv_query_workspace_bytes(B, Hq, Hkv, dim, n_q, rows_hint)
     ws = torch.empty(wsb, dtype=torch.uint8, device=DEV) if wsb else None
     out = torch.full((B, n_q, Hq, dim), float("nan"), dtype=torch.float32, device=DEV)
@@ -105,6 +106,32 @@ def test_query_split_key_ranges(d, G, n_q):
     assert err <= ATTN_TOL, err
 
 
+@pytest.mark.parametrize("hint", ["exact", "third", "twentieth", "twenty_times", "none"])
+def test_query_unequal_segments_and_wrong_hints(d, hint):
+    """Segments from empty to fully kept: the split cuts each into its own
+    number of equal ranges.  A hint below the true rows (the plan widens the
+    ranges to fit the records), far below it (no split), far above it (fewer,
+    longer ranges) or missing changes the split, never the result."""
+    rng = np.random.default_rng(905)
+    B, Hkv = 2, 4
+    keep = rng.permutation(np.array([0.0, 0.001, 0.01, 0.05, 0.2, 0.5, 0.9, 1.0])).reshape(B, Hkv, 1)
+    h = {"exact": "exact", "third": lambda x: x // 3, "twentieth": lambda x: x // 20,
+         "twenty_times": lambda x: 20 * x, "none": 0}[hint]
+    got, want = _run(d, rng, B, Hkv, 4, 20000, 128, keep, 1, 40, hint=h)
+    assert np.isfinite(got).all()
+    err = row_rel_err(got.reshape(-1, 128), want.reshape(-1, 128))
+    assert err <= ATTN_TOL, (hint, err)
+
+
+def test_query_more_segments_than_one_plan_pass(d):
+    """1,200 segments: the plan scans them in two passes of its workgroup,
+    and the items are dealt to the L2 domains in runs."""
+    rng = np.random.default_rng(906)
+    got, want = _run(d, rng, 300, 4, 1, 1100, 64, 1.0, 0, 2)
+    err = row_rel_err(got.reshape(-1, 64), want.reshape(-1, 64))
+    assert err <= ATTN_TOL, err
+
+
 def test_query_unknown_rows_hint_and_empty_context(d):
     """rows_hint 0 (split sized for long segments) with several segments that
     hold no context at all: those rows see only the tokens after it."""
@@ -117,6 +144,16 @@ def test_query_unknown_rows_hint_and_empty_context(d):
 def test_query_large_logits(d):
     rng = np.random.default_rng(902)
     got, want = _run(d, rng, 1, 2, 4, 2000, 128, 0.5, 0, 20, sm_scale=3.0)
+    assert np.isfinite(got).all()
+    assert row_rel_err(got.reshape(-1, 128), want.reshape(-1, 128)) <= ATTN_TOL
+
+
+@pytest.mark.parametrize("scale", [-0.7, 0.0])
+def test_query_negative_and_zero_scale(d, scale):
+    """The kernel scores with |scale| and negated queries for a negative
+    scale; a zero scale is uniform attention over the visible keys."""
+    rng = np.random.default_rng(907)
+    got, want = _run(d, rng, 1, 2, 4, 3000, 128, 0.5, 1, 24, sm_scale=scale)
     assert np.isfinite(got).all()
     assert row_rel_err(got.reshape(-1, 128), want.reshape(-1, 128)) <= ATTN_TOL
 
