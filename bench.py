@@ -63,6 +63,26 @@ def parse():
     return ap.parse_args()
 
 
+def host_info():
+    """The host the oracle ran on: CPU model, cores this process may use, NumPy's BLAS."""
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    blas = None
+    try:
+        from threadpoolctl import threadpool_info
+        blas = [f"{i.get('internal_api')} {i.get('version')} ({i.get('num_threads')} threads)"
+                for i in threadpool_info() if i.get("user_api") == "blas"]
+    except Exception:
+        pass
+    return {"cpu_model": model, "cores_available": len(os.sched_getaffinity(0)), "blas": blas}
+
+
 def kernel_hash():
     """Hash of the decode kernels' sources (the kernel file and the headers it
     includes): stored counter results apply only to the code they measured."""
@@ -349,6 +369,7 @@ def main():
 
     # ---------------- CPU oracle baseline + parity sample (layer 0) --------
     cpu = None
+    cpu_all = None
     parity = None
     dws = torch.zeros(d.dkv_decode_workspace_bytes(B, Hq, Hkv, dim), dtype=torch.uint8, device=dev)
     out = torch.empty((B, Hq, dim), dtype=torch.float32, device=dev)
@@ -360,6 +381,8 @@ def main():
         def bits_of(t):
             return t.cpu().view(torch.int16).numpy().view(np.uint16)
         cpu_s, sample_bytes, worst, same_pack = 0.0, 0, 0.0, True
+        all_cores = len(os.sched_getaffinity(0))
+        all_s, all_bytes, all_layers = 0.0, 0, min(4, L)
         for layer in range(L):
             units = slice(layer * B, (layer + 1) * B)
             segs = slice(layer * nseg_layer, (layer + 1) * nseg_layer)
@@ -380,6 +403,13 @@ def main():
                                      w.sm_scale, Hkv, o.BF16)
                 cpu_s += time.perf_counter() - t0
             sample_bytes += int(ref["seg_len"].sum()) * dim * elem * 2 + B * Hq * dim * (elem + 4)
+            if layer < all_layers:  # the same step with every host core the process may use
+                with threadpool_limits(all_cores):
+                    t0 = time.perf_counter()
+                    o.decode_attn(qb, ref["k_c"], ref["v_c"], ref["seg_off"], ref["seg_len"], 0, w.sm_scale, Hkv,
+                                  o.BF16)
+                    all_s += time.perf_counter() - t0
+                all_bytes += int(ref["seg_len"].sum()) * dim * elem * 2 + B * Hq * dim * (elem + 4)
             # second step of the sample: the step's token appended, then attend
             kn, vn = (bits_of(t).reshape(B, Hkv, 1, dim) for t in new_kv[layer])
             k1, v1 = o.append(ref["k_c"], ref["v_c"], ref["seg_off"], ref["seg_len"], kn, vn, 0)
@@ -399,7 +429,10 @@ def main():
                          f"with the step's appended token) by the fp64 NumPy oracle with 1 BLAS "
                          f"thread: {cpu_s:.2f} s for {sample_bytes / 1e9:.2f} GB of packed K/V"}
         parity = {"layers": L, "max_rel_err": worst, "seg_len_equal": same_pack}
-        log(f"oracle {cpu_s:.2f} s, worst parity err {worst:.2e}")
+        cpu_all = {"value": round(all_bytes / all_s / 1e9, 4), "unit": "GB/s", "cores": all_cores, "kind": "oracle",
+                   "sample": f"the first decode step of layers 0-{all_layers - 1} by the same oracle with "
+                             f"{all_cores} BLAS threads: {all_s:.2f} s for {all_bytes / 1e9:.2f} GB"}
+        log(f"oracle {cpu_s:.2f} s, worst parity err {worst:.2e}; all {all_cores} cores {all_s:.2f} s")
 
     # ---------------- dense comparator cache [L][B*Hkv][T+cap][d] ----------
     t_cap = T + cap
@@ -947,6 +980,8 @@ def main():
                      "avg_launch_us": round(launch_ms * 1e3, 2),
                      "bytes_per_launch": int(per_launch_bytes)},
         "cpu_baseline": cpu,
+        "cpu_baseline_all_cores": cpu_all,
+        "host": host_info(),
         "achievable_read": achievable,
         "query_block": query_res,
         "us_per_step": round(ms * 1e3, 1),
