@@ -998,7 +998,12 @@ def main():
                              "step": "per layer: dkv_decode_attn (attend only); HIP-graph replays",
                              **fam_res},
         "one_time": {"map_us": round(map_us, 1), "compact_us": round(compact_us, 1),
-                     "compact_gb_per_s": round(compact_bytes / (compact_us * 1e-6) / 1e9, 1)},
+                     "compact_gb_per_s": round(compact_bytes / (compact_us * 1e-6) / 1e9, 1),
+                     # the same time priced as a pass that reads the whole dense cache and
+                     # writes the retained rows (what a non-gathering pack would move)
+                     "compact_dense_read_gb_per_s": round(
+                         (2 * N * Hkv * T * dim * elem + 2 * retained * dim * elem + N * Hkv * T)
+                         / (compact_us * 1e-6) / 1e9, 1)},
         "kv_cache_gib": {"dense": round(N * Hkv * T * dim * elem * 2 / 2 ** 30, 3),
                          "packed": round(retained * dim * elem * 2 / 2 ** 30, 3)},
         "parity_layer0": parity,

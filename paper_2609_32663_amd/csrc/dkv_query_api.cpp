@@ -30,6 +30,10 @@ dkv_status query_plan(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t
                       dkv::QueryPlanShape* sh) {
   *sh = dkv::query_plan_shape(batch * hkv, n_q * (hq / hkv), d, rows_hint);
   if (sh->max_items > 0xFFFFFFFFLL / 512 || sh->max_items > INT32_MAX / 2) return DKV_ERR_UNSUPPORTED;
+  // the combine kernel: one work-item per (segment, query row, 4 columns)
+  if (sh->plan_bytes > 0 &&
+      (int64_t)batch * hkv * sh->qtiles * dkv::kQueryRowsPerWG * (d / 4) > 0xFFFFFFFFLL)
+    return DKV_ERR_UNSUPPORTED;
   return DKV_OK;
 }
 

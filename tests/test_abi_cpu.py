@@ -222,6 +222,9 @@ def test_query_validation():
     need = d.dkv_query_workspace_bytes(1, 32, 8, 128, 256, big)
     assert call(n_q=256, cap=256, hint=big, ws=NUL) == d.DKV_ERR_WORKSPACE
     assert call(n_q=256, cap=256, hint=big, ws_bytes=need - 1) == d.DKV_ERR_WORKSPACE
+    # a split whose combine dispatch would pass 2^32 work-items
+    assert call(B=256, Hq=128, Hkv=8, n_q=131072, cap=131072, hint=1 << 36) == d.DKV_ERR_UNSUPPORTED
+    assert d.dkv_query_workspace_bytes(256, 128, 8, 128, 131072, 1 << 36) == 0
     assert call(n_q=0, q=NUL, out=NUL) == d.DKV_OK
     assert call(B=0, q=NUL, out=NUL) == d.DKV_OK
 
