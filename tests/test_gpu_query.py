@@ -31,7 +31,7 @@ def _bf16(rng, shape, scale=1.0):
 
 
 def _run(d, rng, B, Hkv, G, T, dim, keep, n_tail, n_q, cap=None, sm_scale=None, hint="exact",
-         empty_segments=0):
+         empty_segments=0, inspect=None):
     """One case; returns (gpu out [B][n_q][Hq][d], oracle out)."""
     Hq = Hkv * G
     cap = n_tail + n_q if cap is None else cap
@@ -70,6 +70,8 @@ def _run(d, rng, B, Hkv, G, T, dim, keep, n_tail, n_q, cap=None, sm_scale=None, 
     d.dkv_query_attn(q.to(DEV), n_tail, cap, k_c, v_c, seg_off, seg_len, sm_scale, out, ws, Hkv,
                      rows_hint=rows_hint)
     torch.cuda.synchronize()
+    if inspect is not None:
+        inspect(ws, seg_len.cpu().numpy(), rows_hint, wsb)
 
     # oracle on its own
     ref = o.compact(bits(k), bits(v), mask, cap)
@@ -121,6 +123,59 @@ def test_query_unequal_segments_and_wrong_hints(d, hint):
     assert np.isfinite(got).all()
     err = row_rel_err(got.reshape(-1, 128), want.reshape(-1, 128))
     assert err <= ATTN_TOL, (hint, err)
+
+
+# The split's plan, computed independently from its definition: 256-row query
+# tiles; C tiles per range from the hint (about 512 items, at least 8 tiles);
+# no split when the segments average under 16 tiles; records for
+# qtiles * (tiles / C + nseg + 1) items rounded up to 8; C widened on the GPU
+# until qtiles * sum_s max(1, round(T_s / C)) fits them.
+def _plan_shape(nseg, rows, dim, hint):
+    qtiles = -(-rows // 256)
+    tiles = (min(hint, 1 << 40) + 63) // 64 + nseg if hint > 0 else nseg * 512
+    c = min(max(8, -(-(qtiles * tiles) // 512)), 1 << 30)
+    if tiles < nseg * 16:
+        return qtiles, c, nseg * qtiles, 0, 0
+    max_items = -(-(qtiles * (tiles // c + nseg + 1)) // 8) * 8
+    plan_bytes = -(-((4 + nseg + 1) * 4) // 256) * 256
+    return qtiles, c, max_items, plan_bytes, max_items * 256 * (dim + 2) * 4
+
+
+def _plan_expect(seg_tiles, qtiles, c, max_items):
+    nseg = len(seg_tiles)
+    room = max_items // qtiles - nseg
+    c = max(c, -(-int(sum(seg_tiles)) // room))
+    ranges = [max(1, (int(t) + c // 2) // c) for t in seg_tiles]
+    return c, np.concatenate([[0], np.cumsum(ranges)]).astype(np.int64) * qtiles
+
+
+@pytest.mark.parametrize("hint", ["exact", "third", "none"])
+def test_query_plan_bit_exact(d, hint):
+    """The plan kernel's words (items, tiles per range, first item of every
+    segment) equal the split computed from its definition, including the
+    widening a too-small hint forces, and the workspace size matches."""
+    rng = np.random.default_rng(908)
+    B, Hkv, G, T, dim, n_tail, n_q = 2, 4, 4, 20000, 128, 1, 300
+    keep = rng.permutation(np.array([0.0, 0.01, 0.05, 0.2, 0.4, 0.6, 0.9, 1.0])).reshape(B, Hkv, 1)
+    h = {"exact": "exact", "third": lambda x: x // 3, "none": 0}[hint]
+    seen = {}
+
+    def inspect(ws, seg_len, rows_hint, wsb):
+        qtiles, c, max_items, plan_bytes, rec_bytes = _plan_shape(B * Hkv, n_q * G, dim, rows_hint)
+        assert wsb == plan_bytes + rec_bytes
+        assert plan_bytes > 0, "the case must split"
+        words = ws[:plan_bytes].cpu().view(torch.int32).numpy()
+        seg_tiles = (seg_len.astype(np.int64) + n_tail + n_q + 63) // 64
+        c_want, first = _plan_expect(seg_tiles, qtiles, c, max_items)
+        assert int(words[0]) == int(first[-1]) <= max_items
+        assert int(words[1]) == c_want
+        np.testing.assert_array_equal(words[4:4 + B * Hkv + 1].astype(np.int64), first)
+        seen["c"], seen["c_host"] = c_want, c
+
+    got, want = _run(d, rng, B, Hkv, G, T, dim, keep, n_tail, n_q, hint=h, inspect=inspect)
+    assert row_rel_err(got.reshape(-1, dim), want.reshape(-1, dim)) <= ATTN_TOL
+    if hint == "third":
+        assert seen["c"] > seen["c_host"], "a too-small hint must widen the ranges"
 
 
 def test_query_more_segments_than_one_plan_pass(d):
