@@ -36,6 +36,7 @@ WORKLOAD = "llama8b_stack_128k"
 PEAK_HBM_GBPS = 8000.0
 PEAK_BF16_TFLOPS = 2500.0  # dense bf16 matrix peak
 QUERY_TOKENS = 256
+MT_TURNS, MT_STEPS = 4, 16  # multi-turn row: query rounds over one pack, tokens generated per round
 PAGE_ROWS = 128  # rows per page of the zero-copy paged variant
 PMC_FILE = os.path.join(ROOT, "profiles", "decode_attn_llama8b_stack_128k_pmc.json")
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2609_32663_amd", "csrc", f)
@@ -352,19 +353,21 @@ def main():
     # answer) are appended to every segment and attend to the packed context
     # and causally to themselves.
     NQ = QUERY_TOKENS
-    rows_q = int((lens + NQ).sum())
+    cap_q = NQ + MT_STEPS  # room for the block and the tokens generated after it
+    rows_q = int((lens + cap_q).sum())
     k_q = torch.empty((rows_q, dim), dtype=torch.bfloat16, device=dev)
     v_q = torch.empty_like(k_q)
     seg_off_q = torch.empty(N * Hkv, dtype=torch.int64, device=dev)
     seg_len_q = torch.empty(N * Hkv, dtype=torch.int32, device=dev)
-    d.dkv_compact(lay, k, v, kv_mask, NQ, k_q, v_q, seg_off_q, seg_len_q, cws)
-    q_blocks = []
+    d.dkv_compact(lay, k, v, kv_mask, cap_q, k_q, v_q, seg_off_q, seg_len_q, cws)
+    q_blocks, kv_blocks = [], []
     for layer in range(L):
         qb, kb, vb = di.query_block(w, layer, NQ, device=dev)
         segs = slice(layer * nseg_layer, (layer + 1) * nseg_layer)
-        d.dkv_append(kb.reshape(nseg_layer, NQ, dim).contiguous(), vb.reshape(nseg_layer, NQ, dim).contiguous(),
-                     0, NQ, k_q, v_q, seg_off_q[segs], seg_len_q[segs])
+        kb, vb = kb.reshape(nseg_layer, NQ, dim).contiguous(), vb.reshape(nseg_layer, NQ, dim).contiguous()
+        d.dkv_append(kb, vb, 0, cap_q, k_q, v_q, seg_off_q[segs], seg_len_q[segs])
         q_blocks.append(qb.contiguous())
+        kv_blocks.append((kb, vb))
     torch.cuda.synchronize()
 
     # ---------------- CPU oracle baseline + parity sample (layer 0) --------
@@ -833,7 +836,7 @@ def main():
 
     def query_call(layer, shp):
         off = layer * nseg_layer
-        st_ = lib.dkv_query_attn(d.DKV_BF16, B, Hq, Hkv, dim, NQ, P(q_blocks[layer].data_ptr()), 0, NQ,
+        st_ = lib.dkv_query_attn(d.DKV_BF16, B, Hq, Hkv, dim, NQ, P(q_blocks[layer].data_ptr()), 0, cap_q,
                                  P(k_q.data_ptr()), P(v_q.data_ptr()), P(seg_off_q.data_ptr() + 8 * off),
                                  P(seg_len_q.data_ptr() + 4 * off), w.sm_scale, q_hints[layer],
                                  P(q_out.data_ptr()), P(q_ws.data_ptr()), q_ws.numel(), P(shp))
@@ -898,6 +901,94 @@ def main():
         query_res["parity_layer0"] = {"tokens": nqs, "max_rel_err": err}
         log(f"query oracle {cpu_q:.2f} s, parity err {err:.2e}")
     log(f"query block {q_ms * 1e3 / L:.1f} us/layer, {q_tflops:.1f} TFLOP/s")
+
+    # ---------------- multi-turn reuse of one compaction ------------------
+    # Several query rounds over one packed cache: each turn writes a new
+    # 256-token block into the append region (n_tail back to 0), attends it
+    # over every layer (append + query attention per layer), then generates
+    # MT_STEPS tokens (one fused append + decode per layer and token).  The
+    # turn is captured once and replayed; contents do not change the cost.
+    log("timing multi-turn reuse")
+    mt_q = [di.q_step(w, layer, 0, device=dev).contiguous() for layer in range(L)]
+    mt_new = []
+    for layer in range(L):
+        kn_, vn_ = di.kv_new_step(w, layer, 0, device=dev)
+        mt_new.append((kn_.reshape(nseg_layer, 1, dim).contiguous(), vn_.reshape(nseg_layer, 1, dim).contiguous()))
+    mt_out = torch.empty((L, B, Hq, dim), dtype=torch.float32, device=dev)
+
+    def mt_prefill(shp):
+        for layer in range(L):
+            off = layer * nseg_layer
+            kb_, vb_ = kv_blocks[layer]
+            st_ = lib.dkv_append(d.DKV_BF16, nseg_layer, dim, P(kb_.data_ptr()), P(vb_.data_ptr()), NQ, 0, cap_q,
+                                 P(k_q.data_ptr()), P(v_q.data_ptr()), P(seg_off_q.data_ptr() + 8 * off),
+                                 P(seg_len_q.data_ptr() + 4 * off), P(shp))
+            if st_ != 0:
+                raise d.DkvError("dkv_append", st_)
+            query_call(layer, shp)
+
+    def mt_decode(shp):
+        for s_ in range(MT_STEPS):
+            for layer in range(L):
+                off = layer * nseg_layer
+                kn_, vn_ = mt_new[layer]
+                st_ = lib.dkv_append_decode_attn(
+                    d.DKV_BF16, B, Hq, Hkv, dim, P(mt_q[layer].data_ptr()), P(kn_.data_ptr()), P(vn_.data_ptr()), 1,
+                    NQ + s_, cap_q, P(k_q.data_ptr()), P(v_q.data_ptr()), P(seg_off_q.data_ptr() + 8 * off),
+                    P(seg_len_q.data_ptr() + 4 * off), w.sm_scale, q_hints[layer] + nseg_layer * (s_ + 1),
+                    P(mt_out[layer].data_ptr()), P(dws.data_ptr()), dws.numel(), P(shp))
+                if st_ != 0:
+                    raise d.DkvError("dkv_append_decode_attn", st_)
+
+    mt_prefill(sh)
+    mt_decode(sh)
+    torch.cuda.synchronize()
+    gp, gd = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+    with torch.cuda.graph(gp, stream=cap_stream):
+        mt_prefill(cap_stream.cuda_stream)
+    with torch.cuda.graph(gd, stream=cap_stream):
+        mt_decode(cap_stream.cuda_stream)
+    for _ in range(max(1, args.warmup)):
+        gp.replay()
+        gd.replay()
+    torch.cuda.synchronize()
+    ev3 = [ev() for _ in range(2 * MT_TURNS + 1)]
+    ev3[0].record(stream)
+    for t_ in range(MT_TURNS):
+        gp.replay()
+        ev3[2 * t_ + 1].record(stream)
+        gd.replay()
+        ev3[2 * t_ + 2].record(stream)
+    torch.cuda.synchronize()
+    pre_ms = [ev3[2 * t_].elapsed_time(ev3[2 * t_ + 1]) for t_ in range(MT_TURNS)]
+    dec_ms = [ev3[2 * t_ + 1].elapsed_time(ev3[2 * t_ + 2]) for t_ in range(MT_TURNS)]
+    turn_ms = ev3[0].elapsed_time(ev3[-1]) / MT_TURNS
+    mt_res = {"turns": MT_TURNS, "block_tokens": NQ, "tokens_generated_per_turn": MT_STEPS,
+              "ms_per_turn": round(turn_ms, 3), "prefill_ms": round(float(np.median(pre_ms)), 3),
+              "decode_ms_per_token": round(float(np.median(dec_ms)) / MT_STEPS, 4),
+              "compaction_ms": round(compact_us / 1e3, 3),
+              "compaction_share": round(compact_us / 1e3 / (compact_us / 1e3 + MT_TURNS * turn_ms), 4),
+              "step": "turn = per layer (append 256-token block + dkv_query_attn), then 16 x per layer "
+                      "dkv_append_decode_attn; HIP-graph replays", "parity_layer0_last_token": None}
+    if not args.no_cpu_baseline:
+        import oracle as o
+        # the last token of the last turn on layer 0: packed context, the block and 16 generated tokens
+        ref = o.compact(k0_bits, v0_bits, okm0, cap_q)
+        kb0_, vb0_ = kv_blocks[0]
+        to_bits = lambda t_: t_.cpu().view(torch.int16).numpy().view(np.uint16)
+        kc, vc = o.append(ref["k_c"], ref["v_c"], ref["seg_off"], ref["seg_len"],
+                          to_bits(kb0_).reshape(B, Hkv, NQ, dim), to_bits(vb0_).reshape(B, Hkv, NQ, dim), 0)
+        kn0 = np.repeat(to_bits(mt_new[0][0]).reshape(B, Hkv, 1, dim), MT_STEPS, axis=2)
+        vn0 = np.repeat(to_bits(mt_new[0][1]).reshape(B, Hkv, 1, dim), MT_STEPS, axis=2)
+        kc, vc = o.append(kc, vc, ref["seg_off"], ref["seg_len"], kn0, vn0, NQ)
+        want = o.decode_attn(to_bits(mt_q[0]), kc, vc, ref["seg_off"], ref["seg_len"], NQ + MT_STEPS, w.sm_scale,
+                             Hkv, o.BF16)
+        got = mt_out[0].cpu().numpy().astype(np.float64)
+        mt_res["parity_layer0_last_token"] = float(
+            (np.abs(got - want).max(-1) / np.maximum(np.abs(want).max(-1), 1e-30)).max())
+    log(f"multi-turn {turn_ms:.2f} ms/turn (prefill {mt_res['prefill_ms']} ms, "
+        f"{mt_res['decode_ms_per_token']} ms/token), parity {mt_res['parity_layer0_last_token']}")
+    del gp, gd
 
     # ---------------- achievable read bandwidth at this launch size -------
     # The streaming-read probe (same 16-byte non-temporal buffer loads as the
@@ -984,6 +1075,7 @@ def main():
         "host": host_info(),
         "achievable_read": achievable,
         "query_block": query_res,
+        "multi_turn": mt_res,
         "us_per_step": round(ms * 1e3, 1),
         "dense": {"ms_per_step": round(dms, 4), "eager_ms_per_step": round(deager_ms, 4),
                   "gb_per_s": round(dbytes / (dms * 1e-3) / 1e9, 2),
