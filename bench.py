@@ -96,8 +96,10 @@ def kernel_hash():
 
 def timed_calls_per_mode(b):
     """Decode calls one timed mode (packed or dense) issues: a warm step, the
-    graph replays and the eager steps, one call per layer each."""
-    return b["config"]["layers"] * (1 + 2 * (b["warmup"] + b["steps"]))
+    graph replays, the replays of the per-step spread pass (when the line
+    reports one) and the eager steps, one call per layer each."""
+    spread = b["steps"] if b.get("step_ms_spread") else 0
+    return b["config"]["layers"] * (1 + 2 * (b["warmup"] + b["steps"]) + spread)
 
 
 def last_json(path):
@@ -497,6 +499,8 @@ def main():
 
     cap_stream = torch.cuda.Stream()
 
+    timed_spread = {}
+
     def timed(mode, steps, warmup):
         """Step time as HIP-graph replays (one graph per step: each keeps its
         own append slot), plus the same steps launched eagerly."""
@@ -518,6 +522,17 @@ def main():
         b.record(stream)
         torch.cuda.synchronize()
         ms = a.elapsed_time(b) / steps
+        # the spread of single steps: the same replays again, one event pair
+        # per step (a pass of its own, so the timed region above is untouched)
+        evs = [ev() for _ in range(steps + 1)]
+        evs[0].record(stream)
+        for i, s in enumerate(range(warmup, warmup + steps)):
+            graphs[s].replay()
+            evs[i + 1].record(stream)
+        torch.cuda.synchronize()
+        per_step = [evs[i].elapsed_time(evs[i + 1]) for i in range(steps)]
+        spread = {"median": round(float(np.median(per_step)), 4), "p10": round(float(np.percentile(per_step, 10)), 4),
+                  "p90": round(float(np.percentile(per_step, 90)), 4), "reps": steps}
         plans = [step_args(s, mode, sh) for s in range(warmup + steps)]
         for s in range(warmup):
             run(plans[s])
@@ -529,6 +544,7 @@ def main():
         torch.cuda.synchronize()
         eager_ms = a.elapsed_time(b) / steps
         nbytes = sum(decode_bytes(s, mode) for s in range(warmup, warmup + steps)) / steps
+        timed_spread[mode] = spread
         return ms, eager_ms, nbytes
 
     paged_state = {}
@@ -1053,6 +1069,7 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
         "eager_ms_per_step": round(eager_ms, 4),
+        "step_ms_spread": timed_spread.get("packed"),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -1078,6 +1095,7 @@ def main():
         "multi_turn": mt_res,
         "us_per_step": round(ms * 1e3, 1),
         "dense": {"ms_per_step": round(dms, 4), "eager_ms_per_step": round(deager_ms, 4),
+                  "step_ms_spread": timed_spread.get("dense"),
                   "gb_per_s": round(dbytes / (dms * 1e-3) / 1e9, 2),
                   "avg_launch_us": round(dlaunch_ms * 1e3, 2),
                   "launch_frac_of_peak": round(dbytes / L / (dlaunch_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)},
