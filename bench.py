@@ -41,6 +41,8 @@ PAGE_ROWS = 128  # rows per page of the zero-copy paged variant
 PMC_FILE = os.path.join(ROOT, "profiles", "decode_attn_llama8b_stack_128k_pmc.json")
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2609_32663_amd", "csrc", f)
                for f in ("decode_attn.hip", "dkv_device.hpp", "dkv_launch.hpp")]
+QUERY_SRCS = [os.path.join(ROOT, "paper_2609_32663_amd", "csrc", f)
+              for f in ("query_attn.hip", "dkv_device.hpp", "dkv_query.hpp")]
 
 
 def parse():
@@ -84,11 +86,12 @@ def host_info():
     return {"cpu_model": model, "cores_available": len(os.sched_getaffinity(0)), "blas": blas}
 
 
-def kernel_hash():
+def kernel_hash(srcs=None):
     """Hash of the decode kernels' sources (the kernel file and the headers it
-    includes): stored counter results apply only to the code they measured."""
+    includes; or of other sources): stored counter results apply only to the
+    code they measured."""
     h = hashlib.sha256()
-    for path in KERNEL_SRCS:
+    for path in (KERNEL_SRCS if srcs is None else srcs):
         with open(path, "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -259,6 +262,21 @@ def pmc_summary(fetch_csv, write_csv, bench_log, command):
             per_paged[key] = statistics.mean(paged) * 1024.0 * calib
             res[f"paged_{key}_bytes_per_call"] = int(per_paged[key])
     res["traffic_bytes_per_launch"] = int(per_call["fetch"] + per_call["write"])
+    # query-block calls: plan + attention (d 128) + combine dispatches in a row
+    res["query_kernel_sha256_16"] = kernel_hash(QUERY_SRCS)
+    q_bytes = {}
+    for key, path, counter in (("fetch", fetch_csv, "FETCH_SIZE"), ("write", write_csv, "WRITE_SIZE")):
+        rows = pmc_per_dispatch(path, counter)
+        calib = res[f"{key}_calibration"]
+        calls = [rows[i][1] + rows[i + 1][1] + rows[i + 2][1] for i in range(len(rows) - 2)
+                 if "query_plan_kernel" in rows[i][0] and "query_attn_kernel<128>" in rows[i + 1][0]
+                 and "query_merge_kernel" in rows[i + 2][0]]
+        if calls:
+            q_bytes[key] = statistics.mean(calls) * 1024.0 * calib
+            res[f"query_{key}_bytes_per_call"] = int(q_bytes[key])
+            res["query_calls_counted"] = len(calls)
+    if len(q_bytes) == 2:
+        res["query_traffic_bytes_per_call"] = int(q_bytes["fetch"] + q_bytes["write"])
     if len(per_paged) == 2:
         res["paged_traffic_bytes_per_launch"] = int(per_paged["fetch"] + per_paged["write"])
     with open(PMC_FILE, "w") as f:
@@ -884,6 +902,9 @@ def main():
     q_tflops = q_flops / (q_ms * 1e-3) / 1e12
     query_res = {"n_q": NQ, "ms_per_step": round(q_ms, 4), "us_per_layer": round(q_ms * 1e3 / L, 1),
                  "tflop_per_step": round(q_flops / 1e12, 3),
+                 # K/V rows a call attends (every row once), next to the counters' traffic
+                 "kv_bytes_per_call": int(np.mean([(layer_rows[layer] + nseg_layer * NQ) * dim * elem * 2
+                                                   for layer in range(L)])),
                  "roofline": {"bound": "mfma", "achieved": round(q_tflops, 1), "peak": PEAK_BF16_TFLOPS,
                               "unit": "TFLOP/s", "frac": round(q_tflops / PEAK_BF16_TFLOPS, 4),
                               "traffic": None,
@@ -1059,6 +1080,8 @@ def main():
         if pmc.get("kernel_sha256_16") == kernel_hash():
             traffic = pmc.get("traffic_bytes_per_launch")
             paged_res["traffic"] = pmc.get("paged_traffic_bytes_per_launch")
+        if pmc.get("query_kernel_sha256_16") == kernel_hash(QUERY_SRCS):
+            query_res["roofline"]["traffic"] = pmc.get("query_traffic_bytes_per_call")
 
     res = {
         "metric": METRIC,
