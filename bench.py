@@ -393,6 +393,7 @@ def main():
     # ---------------- CPU oracle baseline + parity sample (layer 0) --------
     cpu = None
     cpu_all = None
+    cpu_pack = None
     parity = None
     dws = torch.zeros(d.dkv_decode_workspace_bytes(B, Hq, Hkv, dim), dtype=torch.uint8, device=dev)
     out = torch.empty((B, Hq, dim), dtype=torch.float32, device=dev)
@@ -406,6 +407,7 @@ def main():
         cpu_s, sample_bytes, worst, same_pack = 0.0, 0, 0.0, True
         all_cores = len(os.sched_getaffinity(0))
         all_s, all_bytes, all_layers = 0.0, 0, min(4, L)
+        pack_s, pack_bytes = 0.0, 0
         for layer in range(L):
             units = slice(layer * B, (layer + 1) * B)
             segs = slice(layer * nseg_layer, (layer + 1) * nseg_layer)
@@ -419,7 +421,11 @@ def main():
             _, okm, _ = o.map_pattern(pattern[units], T, w.sink, w.recent, w.bin_edges, Hkv)
             if layer == 0:  # kept for the query-block oracle sample
                 k0_bits, v0_bits, okm0 = kb, vb, okm
-            ref = o.compact(kb, vb, okm, cap)
+            with threadpool_limits(1):
+                t0 = time.perf_counter()
+                ref = o.compact(kb, vb, okm, cap)
+                pack_s += time.perf_counter() - t0
+            pack_bytes += 2 * 2 * int(okm.sum()) * dim * elem + int(okm.size)
             with threadpool_limits(1):
                 t0 = time.perf_counter()
                 want = o.decode_attn(qb, ref["k_c"], ref["v_c"], ref["seg_off"], ref["seg_len"], 0,
@@ -455,7 +461,11 @@ def main():
         cpu_all = {"value": round(all_bytes / all_s / 1e9, 4), "unit": "GB/s", "cores": all_cores, "kind": "oracle",
                    "sample": f"the first decode step of layers 0-{all_layers - 1} by the same oracle with "
                              f"{all_cores} BLAS threads: {all_s:.2f} s for {all_bytes / 1e9:.2f} GB"}
-        log(f"oracle {cpu_s:.2f} s, worst parity err {worst:.2e}; all {all_cores} cores {all_s:.2f} s")
+        cpu_pack = {"value": round(pack_bytes / pack_s / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+                    "sample": f"the oracle's compaction of all {L} layers (retained K/V read + written, mask "
+                              f"read) with 1 BLAS thread: {pack_s:.2f} s for {pack_bytes / 1e9:.2f} GB"}
+        log(f"oracle {cpu_s:.2f} s, worst parity err {worst:.2e}; all {all_cores} cores {all_s:.2f} s; "
+            f"pack {pack_s:.2f} s")
 
     # ---------------- dense comparator cache [L][B*Hkv][T+cap][d] ----------
     t_cap = T + cap
@@ -1112,6 +1122,7 @@ def main():
                      "bytes_per_launch": int(per_launch_bytes)},
         "cpu_baseline": cpu,
         "cpu_baseline_all_cores": cpu_all,
+        "cpu_baseline_compaction": cpu_pack,
         "host": host_info(),
         "achievable_read": achievable,
         "query_block": query_res,
