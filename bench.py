@@ -243,7 +243,9 @@ def pmc_summary(fetch_csv, write_csv, bench_log, command):
     kernel's template flag, are averaged on their own."""
     import statistics
     res = {"kernel_sha256_16": kernel_hash(), "command": command, "unit": "bytes per call"}
-    m = timed_calls_per_mode(last_json(bench_log))
+    b = last_json(bench_log)
+    m = timed_calls_per_mode(b)
+    front = b["config"]["layers"] if b.get("parity_layer0") else 0  # parity calls of an oracle run
     per_call, per_paged = {}, {}
     for key, path, counter in (("fetch", fetch_csv, "FETCH_SIZE"), ("write", write_csv, "WRITE_SIZE")):
         rows = pmc_per_dispatch(path, counter)
@@ -252,7 +254,7 @@ def pmc_summary(fetch_csv, write_csv, bench_log, command):
         pairs = [(is_paged_kernel(rows[i][0]), rows[i][1] + rows[i + 1][1]) for i in range(len(rows) - 1)
                  if "decode_kernel" in rows[i][0] and "decode_merge_kernel" in rows[i + 1][0]]
         calls = [v for pg, v in pairs if not pg]
-        packed = calls[:m]
+        packed = calls[front:front + m]
         paged = [v for pg, v in pairs if pg]
         per_call[key] = statistics.mean(packed) * 1024.0 * calib
         res[f"{key}_calibration"] = round(calib, 4)
