@@ -101,6 +101,8 @@ dkv_status map_pattern(const dkv_layout* layout, const int32_t* unit_len, const 
   const int64_t nseg = (int64_t)L.num_units * L.num_kv_heads;
   // the dispatch's work-item count (workgroups x 256) must fit 32 bits
   if (nseg > 0x7FFFFFFF || dkv::map_blocks(L.context_len, nseg) > 0xFFFFFFFFLL / 256) return DKV_ERR_UNSUPPORTED;
+  // the kernel sweeps runs of 16 positions in 32-bit arithmetic
+  if (L.context_len > INT32_MAX - 16) return DKV_ERR_UNSUPPORTED;
 
   dkv::MapParams p;
   std::memset(&p, 0, sizeof(p));

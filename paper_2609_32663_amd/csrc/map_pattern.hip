@@ -77,32 +77,110 @@ __global__ __launch_bounds__(kMapThreads) void map_pattern_kernel(MapParams p) {
   uint8_t* kv_row = p.kv_mask + (int64_t)seg * T;
   int64_t count = 0;
 
-  for (int64_t j0 = chunk0 + (int64_t)tid * kMapPerThread; j0 < chunk1;
-       j0 += (int64_t)kMapThreads * kMapPerThread) {
+  const int32_t e_end = p.uniform_width > 0 ? 0 : edges[D];  // general edges: the covered span
+  // positions fit 31 bits (T is an int32): the sweep runs in 32-bit arithmetic
+  const int32_t c0 = (int32_t)chunk0, c1 = (int32_t)chunk1;
+  for (int32_t j0 = c0 + tid * kMapPerThread; j0 < c1; j0 += kMapThreads * kMapPerThread) {
     uint32_t hb[kMapPerThread];
+    // Most runs lie in one region (sink, recent window, one bin, uncovered, or
+    // past the context): classify the run once and give every position the
+    // same bits.  Runs across a boundary take the per-position path below.
+    const int32_t jl = j0 + kMapPerThread - 1;
+    bool one = false;
+    uint32_t rb = 0;
+    if (j0 >= Tn) {
+      one = true;  // past this unit's context: nothing retained
+    } else if (jl < Tn) {
+      const int32_t d0 = Tn - 1 - j0, dl = Tn - 1 - jl;  // d0 > dl
+      if (jl < p.S || d0 < p.R) {
+        one = true;
+        rb = all_heads;
+      } else if (j0 >= p.S && dl >= p.R) {
+        const int32_t u0 = d0 - p.R, ul = dl - p.R;  // u0 > ul >= 0
+        if (p.uniform_width > 0) {
+          const int32_t k0 = u0 / p.uniform_width;
+          if (k0 == ul / p.uniform_width) {
+            one = true;
+            rb = k0 < D ? qbits[k0] : 0u;
+          }
+        } else if (ul >= e_end) {
+          one = true;  // past the last edge: uncovered
+        } else if (u0 < e_end) {
+          const int k0 = find_bin(u0, edges, D, 0);
+          if (ul >= edges[k0]) {
+            one = true;
+            rb = qbits[k0];
+          }
+        }
+      }
+    }
+    if (__builtin_amdgcn_ballot_w64(!one) == 0) {
+      // the wave's runs are all uniform
+      const uint32_t wb = rb != 0u ? 0x01010101u : 0u;
+      const u32x4 w = {wb, wb, wb, wb};
+      count += rb != 0u ? kMapPerThread : 0;
+      if (aligned_rows) {
+        *reinterpret_cast<u32x4*>(kv_row + j0) = w;
+      } else {
+#pragma unroll
+        for (int e = 0; e < kMapPerThread; ++e)
+          if (j0 + e < T) kv_row[j0 + e] = rb != 0u ? 1 : 0;
+      }
+      if (p.q_mask != nullptr) {
+        for (int h = 0; h < G; ++h) {
+          uint8_t* q_row = p.q_mask + ((int64_t)unit * p.Hq + (int64_t)g * G + h) * T;
+          const uint8_t qb = (uint8_t)((rb >> h) & 1u);
+          if (aligned_rows) {
+            const uint32_t x = qb ? 0x01010101u : 0u;
+            *reinterpret_cast<u32x4*>(q_row + j0) = u32x4{x, x, x, x};
+          } else {
+#pragma unroll
+            for (int e = 0; e < kMapPerThread; ++e)
+              if (j0 + e < T) q_row[j0 + e] = qb;
+          }
+        }
+      }
+      continue;
+    }
+    // General edges: along the run u = delta - R falls by one per position,
+    // so the bin only moves down.  One binary search for the first covered
+    // position, then a walk down the edges (usually no step: bins are wider
+    // than the run) keeps LDS traffic to about one load per run.
+    int kb = -1;       // bin of the previous covered position of the run
+    int32_t eb = 0;    // its lower edge
 #pragma unroll
     for (int e = 0; e < kMapPerThread; ++e) {
-      const int64_t j = j0 + e;
+      const int32_t j = j0 + e;
       uint32_t bits = 0;
       if (j < Tn) {
-        const int32_t delta = Tn - 1 - (int32_t)j;
+        const int32_t delta = Tn - 1 - j;
         if (j < p.S || delta < p.R) {
           bits = all_heads;
-        } else {
+        } else if (p.uniform_width > 0) {
           const int k = find_bin(delta - p.R, edges, D, p.uniform_width);
           if (k >= 0) bits = qbits[k];
+        } else {
+          const int32_t u = delta - p.R;
+          if (u < e_end) {
+            if (kb < 0) {
+              kb = find_bin(u, edges, D, 0);
+              eb = edges[kb];
+            }
+            while (u < eb) eb = edges[--kb];
+            bits = qbits[kb];
+          }
         }
       }
       hb[e] = bits;
-      count += bits != 0u ? 1 : 0;
+    }
+    u32x4 w;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      w[q] = (hb[4 * q] != 0u ? 1u : 0u) | (hb[4 * q + 1] != 0u ? 1u : 0u) << 8 |
+             (hb[4 * q + 2] != 0u ? 1u : 0u) << 16 | (hb[4 * q + 3] != 0u ? 1u : 0u) << 24;
+      count += __popc(w[q]);  // bytes are 0 or 1
     }
     if (aligned_rows) {
-      u32x4 w;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        w[q] = (hb[4 * q] != 0u ? 1u : 0u) | (hb[4 * q + 1] != 0u ? 1u : 0u) << 8 |
-               (hb[4 * q + 2] != 0u ? 1u : 0u) << 16 | (hb[4 * q + 3] != 0u ? 1u : 0u) << 24;
-      }
       *reinterpret_cast<u32x4*>(kv_row + j0) = w;
     } else {
 #pragma unroll
