@@ -99,12 +99,13 @@ def test_query_random_shapes(d, dim):
         assert err <= ATTN_TOL, (trial, B, Hkv, G, T, n_q, n_tail, err)
 
 
-@pytest.mark.parametrize("G,n_q", [(1, 64), (4, 64), (4, 100), (7, 40), (8, 128)])
-def test_query_split_key_ranges(d, G, n_q):
+@pytest.mark.parametrize("G,n_q,dim", [(1, 64, 128), (4, 64, 128), (4, 100, 128), (7, 40, 128), (8, 128, 128),
+                                       (4, 64, 64), (8, 100, 64)])
+def test_query_split_key_ranges(d, G, n_q, dim):
     """Long contexts: the keys are split into several ranges and combined."""
-    rng = np.random.default_rng(800 + G * 1000 + n_q)
-    got, want = _run(d, rng, 1, 2, G, 12000, 128, 0.4, 2, n_q)
-    err = row_rel_err(got.reshape(-1, 128), want.reshape(-1, 128))
+    rng = np.random.default_rng(800 + G * 1000 + n_q + dim)
+    got, want = _run(d, rng, 1, 2, G, 12000, dim, 0.4, 2, n_q)
+    err = row_rel_err(got.reshape(-1, dim), want.reshape(-1, dim))
     assert err <= ATTN_TOL, err
 
 
