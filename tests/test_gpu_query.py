@@ -100,7 +100,7 @@ def test_query_random_shapes(d, dim):
 
 
 @pytest.mark.parametrize("G,n_q,dim", [(1, 64, 128), (4, 64, 128), (4, 100, 128), (7, 40, 128), (8, 128, 128),
-                                       (4, 64, 64), (8, 100, 64)])
+                                       (4, 64, 64), (8, 100, 64), (16, 33, 128)])
 def test_query_split_key_ranges(d, G, n_q, dim):
     """Long contexts: the keys are split into several ranges and combined."""
     rng = np.random.default_rng(800 + G * 1000 + n_q + dim)
