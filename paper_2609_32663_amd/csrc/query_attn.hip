@@ -39,11 +39,17 @@
 //     keys of one V column; two ds_read_b64_tr_b16 transpose reads fetch them
 //     (within each 16-lane group, lanes 4r..4r+3 address row r of a 4 x 16
 //     block and lane i receives its column i).
-// The P V products of one half run beside the softmax of the next, the
-// score products of the half after that beside the bf16 split, so the
+// The two waves on a SIMD play ping-pong: while one issues the products of
+// its half, the other runs the softmax and bf16 split of its own, so the
 // matrix and the vector units of a SIMD work at once.  Attention here is a
 // dense contraction (G * n_q query rows against every key), so it is MFMA
 // work, unlike the one-query decode step.
+//
+// This file is compiled with IEEE mode off and no NaN semantics
+// (-mno-amdgpu-ieee -fno-honor-nans): the maxima then need no NaN
+// canonicalisation.  With finite inputs no NaN arises anywhere (masked keys
+// are -inf and every -inf - x difference feeds a factor of 0 or 1); for NaN
+// inputs the outputs are unspecified.
 
 #include <hip/hip_runtime.h>
 
@@ -372,6 +378,10 @@ __global__ __launch_bounds__(kQThreads) void query_attn_kernel(QueryParams p) {
           ps += sc[q][jj][v];
         }
       l[q] = l[q] * alpha[q] + ps;
+      // an empty operand barrier: the sum is formed here, in the vector
+      // phase, instead of being sunk into a later one (which unbalances the
+      // phases and keeps the probabilities alive across them)
+      asm volatile("" : "+v"(l[q]));
     }
   };
 
@@ -449,27 +459,50 @@ __global__ __launch_bounds__(kQThreads) void query_attn_kernel(QueryParams p) {
     }
   };
 
-  // Software pipeline over 32-key halves, in each wave: the P V products of
-  // half g - 1 run beside the softmax of half g, the score products of half
-  // g + 1 beside the bf16 split of half g.  K and V have two tile buffers
-  // each.  Once per tile t, between the score products of its second half
-  // and the P V products of its first, the waves meet: by then every wave
-  // has finished reading K of tile t and V of tile t - 1, so K of tile t + 2
-  // and V of tile t + 1 are loaded into those buffers; they have a whole
-  // tile of work to land before the next meeting, where each wave waits for
-  // its own loads first.  Tiles past k_hi hold zeros and all their keys are
-  // masked, so they change nothing.
+  // Ping-pong over 32-key halves.  Each wave alternates a product phase
+  // (P V products of half g, then score products of half g + 1) with a
+  // vector phase (softmax, rescale and bf16 split of half g + 1), and the
+  // waves meet after every phase.  Waves w and w + 4 share a SIMD (waves are
+  // dealt to the four SIMDs in turn); waves 0-3 (lead) run one phase ahead
+  // of waves 4-7 (follow), so on every SIMD one wave issues matrix products
+  // while the other does vector work, and the product wave runs at raised
+  // priority.  A meeting is a bare s_barrier that nothing is scheduled
+  // across: LDS reads of a phase are consumed by its own products before the
+  // meeting, and tile loads are made visible by each wave's own vmcnt wait
+  // before the meeting that precedes their first reader (a workgroup fence
+  // here would wait for every direct load in flight, including the tile
+  // just issued).
+  auto meet = [&]() __attribute__((always_inline)) {
+    __builtin_amdgcn_sched_barrier(0);
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_sched_barrier(0);
+  };
   uint16_t* const kbuf[2] = {k0, k1};
   uint16_t* const vbuf[2] = {v0, v1};
+  const bool lead = __builtin_amdgcn_readfirstlane(wave < 4 ? 1 : 0) != 0;
   issue(kbase, koff, k_lo, kbuf[0]);
   issue(vbase, voff, k_lo, vbuf[0]);
   issue(kbase, koff, k_lo + kQKeys, kbuf[1]);
   __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
   __syncthreads();
-  float sa[kRG][2][4], sb[kRG][2][4], al[kRG];
+  float sc[kRG][2][4], al[kRG];
   u32x4 ph[kRG], pl[kRG];
-  qk(kbuf[0], 0, sa);
-  softmax(std::true_type{}, sa, k_lo, al);
+  constexpr int kWaitOne = 0x0F70 | C::kDma;  // vmcnt(kDma): the younger of two tiles may still be in flight
+  auto vphase = [&](auto masked, int64_t kh) __attribute__((always_inline)) {
+    softmax(masked, sc, kh, al);
+    rescale(al);
+    split(sc, ph, pl);
+  };
+  // P V first: the probabilities are dead before the new scores are formed
+  auto mphase = [&](const uint16_t* kb, int hk, const uint16_t* vb, int hv, bool do_pv) __attribute__((always_inline)) {
+    __builtin_amdgcn_s_setprio(1);
+    if (do_pv) pv(vb, hv, ph, pl);
+    __builtin_amdgcn_sched_barrier(0);
+    qk(kb, hk, sc);
+    __builtin_amdgcn_s_setprio(0);
+  };
   const int64_t ntile = k_hi > k_lo ? (k_hi - k_lo + kQKeys - 1) / kQKeys : 0;
   const int64_t nround = q_uniform64((ntile + 1) / 2);
   // pairs of tiles whose halves (up to 32 keys past the pair) all lie below
@@ -478,28 +511,52 @@ __global__ __launch_bounds__(kQThreads) void query_attn_kernel(QueryParams p) {
   int64_t nclear = clear >= 0 ? clear / (2 * kQKeys) + 1 : 0;
   nclear = q_uniform64(nclear < nround ? nclear : nround);
   int64_t kt = k_lo;
-  auto tile_pair = [&](auto masked) __attribute__((always_inline)) {
+  // Tile t (K in kbuf[i], V in vbuf[i]) takes phases 4t + 1 .. 4t + 4.  K of
+  // tile t is read in phases 4t .. 4t + 3 and V in 4t + 2 .. 4t + 5; V of
+  // tile t + 1 is loaded from phase 4t + 2 on and K of tile t + 2 from
+  // 4t + 4 on, each a whole tile before its first reader.  Each group runs
+  // its own copy of the loop, so no phase branches on the group (a branch
+  // gave the accumulators a second register set).  Both groups meet equally
+  // often: every wave passes the same number of barriers.
+  auto tile_pair = [&](auto masked, auto leadc) __attribute__((always_inline)) {
+    constexpr bool L = decltype(leadc)::value;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      qk(kbuf[i], 1, sb);  // half 2t + 1 (tile t)
-      split(sa, ph, pl);   // half 2t
-      __builtin_amdgcn_s_waitcnt(0x0F70);
-      __syncthreads();
-      issue(kbase, koff, kt + 2 * kQKeys, kbuf[i]);
+      // 4t + 1: lead: vector phase of half 2t; follow: P V of half 2t - 1, scores of 2t
+      if (L) vphase(masked, kt);
+      else mphase(kbuf[i], 0, vbuf[1 - i], 1, i == 1 || kt != k_lo);
+      __builtin_amdgcn_s_waitcnt(kWaitOne);  // V of tile t
+      meet();
+      // 4t + 2: lead: P V of 2t, scores of 2t + 1; follow: vector phase of 2t
       issue(vbase, voff, kt + kQKeys, vbuf[1 - i]);
-      pv(vbuf[i], 0, ph, pl);  // half 2t
-      softmax(masked, sb, kt + 32, al);
-      rescale(al);
-      qk(kbuf[1 - i], 0, sa);  // half 2t + 2 (tile t + 1)
-      split(sb, ph, pl);       // half 2t + 1
-      pv(vbuf[i], 1, ph, pl);  // half 2t + 1
-      softmax(masked, sa, kt + kQKeys, al);
-      rescale(al);
+      if (L) mphase(kbuf[i], 1, vbuf[i], 0, true);
+      else vphase(masked, kt);
+      meet();
+      // 4t + 3: lead: vector phase of 2t + 1; follow: P V of 2t, scores of 2t + 1
+      if (L) vphase(masked, kt + 32);
+      else mphase(kbuf[i], 1, vbuf[i], 0, true);
+      __builtin_amdgcn_s_waitcnt(kWaitOne);  // K of tile t + 1
+      meet();
+      // 4t + 4: lead: P V of 2t + 1, scores of 2t + 2; follow: vector phase of 2t + 1
+      issue(kbase, koff, kt + 2 * kQKeys, kbuf[i]);
+      if (L) mphase(kbuf[1 - i], 0, vbuf[i], 1, true);
+      else vphase(masked, kt + 32);
+      meet();
       kt += kQKeys;
     }
   };
-  for (int64_t rd = 0; rd < nclear; ++rd) tile_pair(std::false_type{});
-  for (int64_t rd = nclear; rd < nround; ++rd) tile_pair(std::true_type{});
+  auto run = [&](auto leadc) __attribute__((always_inline)) {
+    constexpr bool L = decltype(leadc)::value;
+    if (L) mphase(kbuf[0], 0, vbuf[0], 0, false);  // scores of half 0
+    meet();
+    for (int64_t rd = 0; rd < nclear; ++rd) tile_pair(std::false_type{}, leadc);
+    for (int64_t rd = nclear; rd < nround; ++rd) tile_pair(std::true_type{}, leadc);
+    // the follow group's P V products of the last half (tiles past k_hi hold
+    // zeros and all their keys are masked, so the lead's last scores are unused)
+    if (!L && nround > 0) pv(vbuf[1], 1, ph, pl);
+  };
+  if (lead) run(std::true_type{});
+  else run(std::false_type{});
   // no direct load may still be writing LDS when the workgroup ends
   __builtin_amdgcn_s_waitcnt(0x0F70);
 
