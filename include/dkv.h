@@ -285,6 +285,8 @@ size_t dkv_query_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t num
  * [seg_off[s], seg_off[s] + seg_len[s] + n_tail + i + 1): everything before
  * the block, and the block causally up to itself.
  * out      [B][n_q][Hq][d] fp32, softmax(sm_scale * K q) V over those rows.
+ *          q, K, V and sm_scale must be finite: outputs for NaN or infinite
+ *          inputs are unspecified (the kernels run without NaN semantics).
  * append_cap  free rows reserved per segment; n_tail + n_q <= append_cap.
  * rows_hint (host) total rows the call attends, sum over segments of
  *          seg_len + n_tail + n_q (0 = unknown); it sizes the split of the key
