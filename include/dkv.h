@@ -150,12 +150,18 @@ size_t dkv_compact_workspace_bytes(const dkv_layout *layout);
  *            in original token order, followed by append_cap free rows that
  *            this call does not touch.
  * out_rows   capacity of k_out / v_out in rows.  The layout needs
- *            sum_s (kv_len[s] + append_cap) rows; rows that would fall at or
- *            beyond out_rows are not written (their segments are then
- *            incomplete), and the true requirement is reported in
- *            *rows_needed so that the caller can check it.
+ *            sum_s (kv_len[s] + append_cap) rows.  A segment whose retained
+ *            rows and append room would not lie wholly below out_rows is not
+ *            packed: nothing of it is written, its seg_len is set to -1 and
+ *            its seg_off is clamped to out_rows, so no offset points past
+ *            the buffer.  Every call that reads seg_len (dkv_append, the
+ *            decode calls, dkv_query_attn) treats a negative length as a
+ *            segment with no rows and no room: nothing is appended to it and
+ *            its attention outputs are zeros.  *rows_needed reports the true
+ *            requirement.
  * seg_off    out, int64 [N*Hkv], row offset of each segment (unit-major).
- * seg_len    out, int32 [N*Hkv], retained rows of each segment.
+ * seg_len    out, int32 [N*Hkv], retained rows of each segment (-1: not
+ *            packed, see out_rows).
  * src_pos    out, optional int32 [out_rows]: original position j of every
  *            packed row (free rows untouched).
  * rows_needed out, optional int64 [1]: sum_s (seg_len[s] + append_cap).
@@ -204,7 +210,11 @@ size_t dkv_decode_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t nu
  *          [seg_off[s], seg_off[s] + seg_len[s] + n_tail).
  * Every query head of group g attends to all rows of segment (b, g): the
  * union of its group (Sec. 3.4).  out[b][h][:] = softmax(sm_scale * K q) V
- * over those rows, fp32 [B][Hq][d]; a segment with no rows gives zeros.
+ * over those rows, fp32 [B][Hq][d]; a segment with no rows (or seg_len < 0)
+ * gives zeros.
+ * sm_scale   any value with sm_scale * log2(e) finite in fp32 (negative and
+ *          zero included); others return DKV_ERR_INVALID_ARG.  The same rule
+ *          holds for every attention call of this library.
  * rows_hint (host) expected total rows of the call (0 = unknown); it only
  * sizes the split, never the result's correctness.
  * workspace  at least dkv_decode_workspace_bytes(...) bytes of scratch for

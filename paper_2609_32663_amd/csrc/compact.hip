@@ -60,12 +60,21 @@ __global__ __launch_bounds__(kScanThreads) void compact_scan_kernel(CompactParam
         run += c;
       }
       len = run;
-      p.seg_len[s] = run;
     }
     const int64_t need = s < p.nseg ? len + p.cap : 0;
     int64_t chunk_total;
     const int64_t excl = block_exclusive_scan<kScanThreads>(need, red, &chunk_total);
-    if (s < p.nseg) p.seg_off[s] = carry + excl;
+    if (s < p.nseg) {
+      // A segment whose rows and append room do not fit below out_rows is
+      // not packed: its length becomes the marker -1 (every call that reads
+      // lengths treats it as a segment with no rows and no room) and its
+      // offset is clamped to out_rows, so no offset handed out points past
+      // the buffer.
+      const int64_t off = carry + excl;
+      const bool fits = off + need <= p.out_rows;
+      p.seg_off[s] = fits ? off : (off < p.out_rows ? off : p.out_rows);
+      p.seg_len[s] = fits ? (int32_t)len : -1;
+    }
     __syncthreads();
     if (threadIdx.x == 0) carry += chunk_total;
     __syncthreads();
@@ -84,6 +93,7 @@ __global__ __launch_bounds__(kThreads) void compact_gather_kernel(CompactParams 
   const int which = blockIdx.x & 1;  // 0: K rows (and source positions), 1: V rows
   const int seg = blockIdx.y;
   const int tid = threadIdx.x;
+  if (p.seg_len[seg] < 0) return;  // not packed: it does not fit below out_rows
   const uint8_t* mrow = p.mask + (int64_t)seg * p.T;
   const int64_t jt = (int64_t)tile * kCompactTile;
   const u32x4 w = load_mask16(mrow, jt + tid * kPerThread, p.T);
@@ -110,7 +120,7 @@ __global__ __launch_bounds__(kThreads) void compact_gather_kernel(CompactParams 
     for (int u = 0; u < kUnroll; ++u) {
       const int r = r0 + u * kRowsPerPass;
       drow[u] = dst0 + r;
-      ok[u] = r < kept && drow[u] < p.out_rows;
+      ok[u] = r < kept;
       if (ok[u]) rb[u] = src[(src0 + list[r]) * stride16 + lane];
     }
 #pragma unroll
@@ -132,6 +142,7 @@ __global__ __launch_bounds__(kThreads) void append_kernel(AppendParams p) {
   if (row_id >= (int64_t)p.nseg * p.n_new) return;
   const int64_t s = row_id / p.n_new;
   const int64_t t = row_id - s * p.n_new;
+  if (p.seg_len[s] < 0) return;  // a segment dkv_compact could not pack has no room
   const int64_t drow = p.seg_off[s] + p.seg_len[s] + p.n_tail + t;
   const u32x4* ks = reinterpret_cast<const u32x4*>(p.k_new);
   const u32x4* vs = reinterpret_cast<const u32x4*>(p.v_new);

@@ -282,7 +282,11 @@ __device__ __forceinline__ int64_t segment_rows(const DecodeParams& p, int s) {
     const int32_t n = p.n_entries[s];
     return (int64_t)(n < 0 ? 0 : (n > p.max_entries ? p.max_entries : n)) * p.page_rows;
   }
-  return (p.seg_len == nullptr ? p.dense_len : (int64_t)p.seg_len[s] + p.n_tail) + p.n_new;
+  if (p.seg_len == nullptr) return (int64_t)p.dense_len + p.n_new;
+  // a negative length marks a segment dkv_compact could not pack: no rows
+  // and no room to append
+  const int32_t len = p.seg_len[s];
+  return len < 0 ? 0 : (int64_t)len + p.n_tail + p.n_new;
 }
 
 // Flat prefix of work units over the call's segments: pre[s] = units of

@@ -48,7 +48,7 @@ dkv_status check_decode_common(int dtype, int32_t batch, int32_t hq, int32_t hkv
                                const void* ws, size_t ws_bytes, float sm_scale) {
   if (!dtype_ok(dtype)) return DKV_ERR_INVALID_ARG;
   if (batch < 0 || hq <= 0 || hkv <= 0 || hq % hkv != 0) return DKV_ERR_INVALID_ARG;
-  if (!std::isfinite(sm_scale)) return DKV_ERR_INVALID_ARG;
+  if (!dkv::scale_in_range(sm_scale)) return DKV_ERR_INVALID_ARG;
   if (hq / hkv > DKV_MAX_GROUP || !head_dim_ok(d)) return DKV_ERR_UNSUPPORTED;
   if ((int64_t)batch * hkv > DKV_MAX_SEGMENTS) return DKV_ERR_UNSUPPORTED;
   if (batch == 0) return DKV_OK;
@@ -232,7 +232,7 @@ size_t dkv_decode_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t nu
 
 namespace {
 
-// Packed-cache attention, optionally appending n_new tokens first.
+// Packed-cache attention, optionally appending n_new tokens first. 
 dkv_status decode_packed(dkv_dtype dtype, int32_t batch, int32_t hq, int32_t hkv, int32_t d, const void* q,
                          const void* k_new, const void* v_new, int32_t n_new, int32_t n_tail,
                          int32_t append_cap, const void* k_c, const void* v_c, const int64_t* seg_off,

@@ -6,9 +6,17 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <cmath>
+
 #include "../../include/dkv.h"
 
 namespace dkv {
+
+// The attention kernels take the softmax scale as sm_scale * log2(e) in
+// fp32; a scale is accepted when it and that product are finite.
+inline bool scale_in_range(float sm_scale) {
+  return std::isfinite(sm_scale) && std::isfinite(sm_scale * 1.4426950408889634f);
+}
 
 // --------------------------------------------------------------- map pattern
 struct MapParams {

@@ -34,7 +34,7 @@ dkv_status paged_decode(dkv_dtype dtype, int32_t batch, int32_t hq, int32_t hkv,
                         float sm_scale, int64_t rows_hint, float* out, void* ws, size_t ws_bytes, void* stream) {
   if (dtype != DKV_BF16 && dtype != DKV_F32) return DKV_ERR_INVALID_ARG;
   if (batch < 0 || hq <= 0 || hkv <= 0 || hq % hkv != 0) return DKV_ERR_INVALID_ARG;
-  if (!std::isfinite(sm_scale) || n_tail < 0 || n_new < 0 || context_len < 0 || max_entries < 0 ||
+  if (!dkv::scale_in_range(sm_scale) || n_tail < 0 || n_new < 0 || context_len < 0 || max_entries < 0 ||
       num_pages < 0)
     return DKV_ERR_INVALID_ARG;
   if (hq / hkv > DKV_MAX_GROUP || (d != 64 && d != 128)) return DKV_ERR_UNSUPPORTED;

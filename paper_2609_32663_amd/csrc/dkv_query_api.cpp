@@ -8,6 +8,7 @@
 #include <cstring>
 
 #include "../../include/dkv.h"
+#include "dkv_launch.hpp"
 #include "dkv_query.hpp"
 
 namespace {
@@ -59,7 +60,7 @@ dkv_status dkv_query_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_heads, i
   dkv_status st = check_query_shape(batch, num_q_heads, num_kv_heads, head_dim, n_q);
   if (st != DKV_OK) return st;
   if (dtype != DKV_BF16) return DKV_ERR_UNSUPPORTED;
-  if (!std::isfinite(sm_scale) || n_tail < 0 || append_cap < 0) return DKV_ERR_INVALID_ARG;
+  if (!dkv::scale_in_range(sm_scale) || n_tail < 0 || append_cap < 0) return DKV_ERR_INVALID_ARG;
   if ((int64_t)n_tail + n_q > append_cap) return DKV_ERR_CAPACITY;
   if (batch == 0 || n_q == 0) return DKV_OK;
   if (q == nullptr || k_c == nullptr || v_c == nullptr || out == nullptr || seg_off == nullptr ||

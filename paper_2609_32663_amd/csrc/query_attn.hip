@@ -119,8 +119,10 @@ __device__ __forceinline__ float row4_max(float x) {
 }
 
 // Key tiles of segment s for its last query row (the most any row sees).
+// A negative length marks a segment dkv_compact could not pack: no tiles.
 __device__ __forceinline__ int64_t seg_tiles(const QueryParams& p, int s) {
-  return ((int64_t)p.seg_len[s] + p.n_tail + p.n_q + kQKeys - 1) / kQKeys;
+  const int32_t len = p.seg_len[s];
+  return len < 0 ? 0 : ((int64_t)len + p.n_tail + p.n_q + kQKeys - 1) / kQKeys;
 }
 
 __device__ __forceinline__ int64_t seg_ranges(int64_t tiles, int64_t c) {
@@ -212,6 +214,17 @@ __global__ __launch_bounds__(kQThreads) void query_attn_kernel(QueryParams p) {
   }
   const int bseq = s / p.Hkv;
   const int g = s - bseq * p.Hkv;
+  if (p.seg_len[s] < 0) {
+    // a segment dkv_compact could not pack (one range, so this workgroup
+    // owns its query tile's output): no rows to attend, zeros
+    for (int i = tid; i < kQRows * D; i += kQThreads) {
+      const int rq = qt * kQRows + i / D;
+      if (rq >= p.rows) break;
+      const int tq = rq / p.G;
+      p.out[(((int64_t)bseq * p.n_q + tq) * p.Hq + (int64_t)g * p.G + (rq - tq * p.G)) * D + i % D] = 0.f;
+    }
+    return;
+  }
   const int64_t base_len = q_uniform64((int64_t)p.seg_len[s] + p.n_tail);  // rows every query row sees
   const int64_t row0 = q_uniform64(p.seg_off[s]);
 

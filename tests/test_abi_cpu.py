@@ -135,6 +135,14 @@ def test_decode_validation():
     assert _decode(B=300, Hkv=8, Hq=8) == d.DKV_ERR_UNSUPPORTED
     assert _decode(scale=float("nan")) == d.DKV_ERR_INVALID_ARG
     assert _decode(scale=float("inf")) == d.DKV_ERR_INVALID_ARG
+    # the kernels take sm_scale * log2(e) in fp32: a finite scale whose product
+    # overflows is refused, the largest that does not is accepted (the call then
+    # fails later, on the workspace)
+    assert _decode(scale=3e38) == d.DKV_ERR_INVALID_ARG
+    assert _decode(scale=-3e38) == d.DKV_ERR_INVALID_ARG
+    assert _decode(scale=2e38, ws=NUL) == d.DKV_ERR_WORKSPACE
+    assert _decode(scale=-2e38, ws=NUL) == d.DKV_ERR_WORKSPACE
+    assert _decode(scale=0.0, ws=NUL) == d.DKV_ERR_WORKSPACE
     assert _decode(dtype=5) == d.DKV_ERR_INVALID_ARG
     assert _decode(q=NUL) == d.DKV_ERR_INVALID_ARG
     assert _decode(so=NUL) == d.DKV_ERR_INVALID_ARG
@@ -214,6 +222,8 @@ def test_query_validation():
     assert call(n_tail=-1) == d.DKV_ERR_INVALID_ARG
     assert call(n_q=5, n_tail=4, cap=8) == d.DKV_ERR_CAPACITY
     assert call(scale=float("nan")) == d.DKV_ERR_INVALID_ARG
+    assert call(scale=-3e38) == d.DKV_ERR_INVALID_ARG
+    assert call(scale=-2e38, q=NUL) == d.DKV_ERR_INVALID_ARG  # scale accepted, then the null query
     assert call(q=NUL) == d.DKV_ERR_INVALID_ARG
     assert call(sl=NUL) == d.DKV_ERR_INVALID_ARG
     assert call(out=MIS) == d.DKV_ERR_MISALIGNED
@@ -286,6 +296,8 @@ def test_paged_decode_validation():
     assert call(max_e=-1) == d.DKV_ERR_INVALID_ARG
     assert call(n_pages=-1) == d.DKV_ERR_INVALID_ARG
     assert call(scale=float("inf")) == d.DKV_ERR_INVALID_ARG
+    assert call(scale=3e38) == d.DKV_ERR_INVALID_ARG
+    assert call(scale=2e38, w=NUL) == d.DKV_ERR_WORKSPACE
     assert call(q=NUL) == d.DKV_ERR_INVALID_ARG
     assert call(kp=NUL) == d.DKV_ERR_INVALID_ARG
     assert call(ne=NUL) == d.DKV_ERR_INVALID_ARG

@@ -202,6 +202,86 @@ def test_compact_respects_out_rows(d):
                                   ref["k_c"][:ref["seg_len"][0]])
 
 
+def test_truncated_compaction_is_safe_downstream(d):
+    """A pack that does not fit out_rows: segments that fit are packed whole,
+    the others get seg_len -1 and an offset clamped to out_rows; append,
+    decode (plain and fused) and query attention then write nothing at or
+    past out_rows, skip those segments and give zeros for them."""
+    rng = np.random.default_rng(206)
+    B, Hkv, G, T, dim, cap, n_q = 1, 3, 2, 2000, 128, 8, 4
+    Hq = Hkv * G
+    mask = (rng.uniform(size=(B, Hkv, T)) < 0.5).astype(np.uint8)
+    lens = mask.reshape(-1, T).sum(-1).astype(np.int64)
+    k = _rand_kv(rng, (B, Hkv, T, dim), torch.bfloat16)
+    v = _rand_kv(rng, (B, Hkv, T, dim), torch.bfloat16)
+    need = int(lens.sum()) + Hkv * cap
+    out_rows = int(lens[0]) + cap + int(lens[1]) // 2  # segment 0 fits, 1 and 2 do not
+    big_k = torch.full((need + 64, dim), 3.0, dtype=torch.bfloat16, device=DEV)
+    big_v = torch.full((need + 64, dim), 3.0, dtype=torch.bfloat16, device=DEV)
+    k_c, v_c = big_k[:out_rows], big_v[:out_rows]
+    lay = _layout(d, B, Hq, Hkv, dim, T, 0, 0, [0, T])
+    seg_off = torch.empty(Hkv, dtype=torch.int64, device=DEV)
+    seg_len = torch.empty(Hkv, dtype=torch.int32, device=DEV)
+    rn = torch.empty(1, dtype=torch.int64, device=DEV)
+    src = torch.full((need + 64,), -7, dtype=torch.int32, device=DEV)
+    ws = torch.empty(d.dkv_compact_workspace_bytes(lay), dtype=torch.uint8, device=DEV)
+    d.dkv_compact(lay, k, v, torch.from_numpy(mask).to(DEV), cap, k_c, v_c, seg_off, seg_len, ws,
+                  src_pos=src[:out_rows], rows_needed=rn)
+    torch.cuda.synchronize()
+    assert int(rn.item()) == need
+    assert seg_len.cpu().tolist() == [int(lens[0]), -1, -1]
+    assert seg_off.cpu().tolist() == [0, int(lens[0]) + cap, out_rows]
+
+    def guard_intact():
+        torch.cuda.synchronize()
+        return bool((big_k[out_rows:].float() == 3.0).all() and (big_v[out_rows:].float() == 3.0).all()
+                    and (src[out_rows:] == -7).all()) and bool((src[lens[0]:out_rows] == -7).all())
+    assert guard_intact()
+    ref = o.compact(bits(k), bits(v), mask, cap)
+    n0 = int(lens[0])
+    np.testing.assert_array_equal(bits(k_c)[:n0], ref["k_c"][:n0])
+    np.testing.assert_array_equal(bits(v_c)[:n0], ref["v_c"][:n0])
+    # rows of the unpacked segments below out_rows are not written either
+    assert (big_k[n0 + cap:out_rows].float() == 3.0).all()
+
+    # append two tokens, then a fused append + decode of a third
+    kn = _rand_kv(rng, (Hkv, 3, dim), torch.bfloat16)
+    vn = _rand_kv(rng, (Hkv, 3, dim), torch.bfloat16)
+    d.dkv_append(kn[:, :2].contiguous(), vn[:, :2].contiguous(), 0, cap, k_c, v_c, seg_off, seg_len)
+    assert guard_intact() and (big_k[n0 + cap:out_rows].float() == 3.0).all()
+    q = _rand_kv(rng, (B, Hq, dim), torch.bfloat16)
+    out = torch.full((B, Hq, dim), float("nan"), dtype=torch.float32, device=DEV)
+    dws = torch.empty(d.dkv_decode_workspace_bytes(B, Hq, Hkv, dim), dtype=torch.uint8, device=DEV)
+    d.dkv_append_decode_attn(q, kn[:, 2:].contiguous(), vn[:, 2:].contiguous(), 2, cap, k_c, v_c, seg_off,
+                             seg_len, 0.09, out, dws, Hkv, rows_hint=need)
+    assert guard_intact() and (big_k[n0 + cap:out_rows].float() == 3.0).all()
+    kc_ref, vc_ref = o.append(ref["k_c"], ref["v_c"], ref["seg_off"], ref["seg_len"],
+                              bits(kn).reshape(B, Hkv, 3, dim), bits(vn).reshape(B, Hkv, 3, dim), 0)
+    want = o.decode_attn(bits(q), kc_ref, vc_ref, ref["seg_off"], ref["seg_len"], 3, 0.09, Hkv, o.BF16)
+    got = out.cpu().numpy()
+    assert row_rel_err(got[:, :G], want[:, :G]) <= ATTN_TOL
+    assert (got[:, G:] == 0).all()
+    np.testing.assert_array_equal(bits(k_c)[n0:n0 + 3], bits(kn)[0])
+
+    # query attention of a 4-token block appended after the three tokens
+    kb = _rand_kv(rng, (Hkv, n_q, dim), torch.bfloat16)
+    vb = _rand_kv(rng, (Hkv, n_q, dim), torch.bfloat16)
+    d.dkv_append(kb, vb, 3, cap, k_c, v_c, seg_off, seg_len)
+    qb = _rand_kv(rng, (B, n_q, Hq, dim), torch.bfloat16)
+    qout = torch.full((B, n_q, Hq, dim), float("nan"), dtype=torch.float32, device=DEV)
+    for hint in (0, need):
+        wsb = d.dkv_query_workspace_bytes(B, Hq, Hkv, dim, n_q, hint)
+        qws = torch.empty(wsb, dtype=torch.uint8, device=DEV) if wsb else None
+        d.dkv_query_attn(qb, 3, cap, k_c, v_c, seg_off, seg_len, 0.09, qout, qws, Hkv, rows_hint=hint)
+        assert guard_intact()
+        kc2, vc2 = o.append(kc_ref, vc_ref, ref["seg_off"], ref["seg_len"], bits(kb).reshape(B, Hkv, n_q, dim),
+                            bits(vb).reshape(B, Hkv, n_q, dim), 3)
+        qwant = o.query_attn(bits(qb), kc2, vc2, ref["seg_off"], ref["seg_len"], 3, 0.09, Hkv, o.BF16)
+        qgot = qout.cpu().numpy()
+        assert row_rel_err(qgot[:, :, :G].reshape(-1, dim), qwant[:, :, :G].reshape(-1, dim)) <= ATTN_TOL
+        assert (qgot[:, :, G:] == 0).all()
+
+
 def test_append_matches_oracle(d):
     rng = np.random.default_rng(204)
     for dtype, dim in ((torch.bfloat16, 128), (torch.float32, 64), (torch.bfloat16, 64)):
@@ -414,6 +494,60 @@ def test_append_decode_graph_replays_match_eager(d):
         scratch = torch.empty_like(out)  # eager work between replays
         d.dkv_decode_attn(q, k_c, v_c, seg_off, seg_len, 0, scale, scratch, dws, Hkv)
         torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("scale", [-0.7, 0.0])
+@pytest.mark.parametrize("dtype,dim,G", [(torch.bfloat16, 128, 4), (torch.float32, 64, 2),
+                                         (torch.bfloat16, 64, 8)])
+def test_decode_negative_and_zero_scale(d, scale, dtype, dim, G):
+    """A negative scale turns the softmax towards the keys least aligned with
+    the query; a zero scale is uniform attention over every attended row.
+    Both the attend-only and the fused append + decode call, split over many
+    workgroups and in one."""
+    rng = np.random.default_rng(350 + dim + G + int(scale == 0.0))
+    B, Hkv, T, cap = 2, 3, 4000, 8
+    Hq = Hkv * G
+    mask = (rng.uniform(size=(B, Hkv, T)) < 0.4).astype(np.uint8)
+    k = _rand_kv(rng, (B, Hkv, T, dim), dtype)
+    v = _rand_kv(rng, (B, Hkv, T, dim), dtype)
+    q = _rand_kv(rng, (B, Hq, dim), dtype)
+    kn = _rand_kv(rng, (B * Hkv, 3, dim), dtype)
+    vn = _rand_kv(rng, (B * Hkv, 3, dim), dtype)
+    lay = _layout(d, B, Hq, Hkv, dim, T, 0, 0, [0, T])
+    rows = int(mask.sum()) + B * Hkv * cap
+    k_c = torch.empty((rows, dim), dtype=dtype, device=DEV)
+    v_c = torch.empty_like(k_c)
+    seg_off = torch.empty(B * Hkv, dtype=torch.int64, device=DEV)
+    seg_len = torch.empty(B * Hkv, dtype=torch.int32, device=DEV)
+    ws = torch.empty(d.dkv_compact_workspace_bytes(lay), dtype=torch.uint8, device=DEV)
+    d.dkv_compact(lay, k, v, torch.from_numpy(mask).to(DEV), cap, k_c, v_c, seg_off, seg_len, ws)
+    d.dkv_append(kn[:, :2].contiguous(), vn[:, :2].contiguous(), 0, cap, k_c, v_c, seg_off, seg_len)
+    dws = torch.empty(d.dkv_decode_workspace_bytes(B, Hq, Hkv, dim), dtype=torch.uint8, device=DEV)
+    ref = o.compact(bits(k), bits(v), mask, cap)
+    kc_ref, vc_ref = o.append(ref["k_c"], ref["v_c"], ref["seg_off"], ref["seg_len"],
+                              bits(kn).reshape(B, Hkv, 3, dim), bits(vn).reshape(B, Hkv, 3, dim), 0)
+    want2 = o.decode_attn(bits(q), kc_ref, vc_ref, ref["seg_off"], ref["seg_len"], 2, scale, Hkv, odt(q))
+    want3 = o.decode_attn(bits(q), kc_ref, vc_ref, ref["seg_off"], ref["seg_len"], 3, scale, Hkv, odt(q))
+    if scale == 0.0:  # uniform weights: the mean of the attended V rows
+        vr = o.widen(vc_ref, odt(q))
+        for s in range(B * Hkv):
+            lo, n = int(ref["seg_off"][s]), int(ref["seg_len"][s]) + 3
+            np.testing.assert_allclose(want3[s // Hkv, (s % Hkv) * G:(s % Hkv + 1) * G],
+                                       np.broadcast_to(vr[lo:lo + n].mean(0), (G, dim)), rtol=1e-12, atol=1e-12)
+    for hint in (0, 1):  # the flat split over every workgroup, and one workgroup
+        out = torch.full((B, Hq, dim), float("nan"), dtype=torch.float32, device=DEV)
+        d.dkv_decode_attn(q, k_c, v_c, seg_off, seg_len, 2, scale, out, dws, Hkv, rows_hint=hint)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy()
+        assert np.isfinite(got).all()
+        assert row_rel_err(got, want2) <= ATTN_TOL, (hint, row_rel_err(got, want2))
+        fused = torch.full((B, Hq, dim), float("nan"), dtype=torch.float32, device=DEV)
+        d.dkv_append_decode_attn(q, kn[:, 2:].contiguous(), vn[:, 2:].contiguous(), 2, cap, k_c, v_c, seg_off,
+                                 seg_len, scale, fused, dws, Hkv, rows_hint=hint)
+        torch.cuda.synchronize()
+        got = fused.cpu().numpy()
+        assert np.isfinite(got).all()
+        assert row_rel_err(got, want3) <= ATTN_TOL, (hint, row_rel_err(got, want3))
 
 
 def test_decode_large_logits_are_stable(d):
