@@ -253,6 +253,31 @@ dkv_status dkv_append_decode_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_
                                   size_t workspace_bytes, void *stream);
 
 /*
+ * dkv_append_decode_attn_noalloc -- dkv_append_decode_attn for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc): the same arguments without the
+ * workspace, the same kernels and the same result bit for bit.
+ *
+ * The split's scratch is a static array of DKV_NOALLOC_SCRATCH_BYTES that
+ * the library keeps on every GPU it runs on until the process ends; the call
+ * itself allocates and frees nothing.  Shapes whose workspace
+ * (dkv_decode_workspace_bytes) exceeds that size return DKV_ERR_UNSUPPORTED.
+ * The first call on a device looks the array's address up (DKV_ERR_HIP if
+ * that fails).  Every call on one GPU shares that GPU's array: two calls that
+ * may overlap on one GPU (different streams, or different host threads)
+ * race and must be ordered by the caller.  The array needs no initial
+ * contents and keeps whatever the last call left.
+ */
+#define DKV_NOALLOC_SCRATCH_BYTES (16u << 20)
+dkv_status dkv_append_decode_attn_noalloc(dkv_dtype dtype, int32_t batch, int32_t num_q_heads,
+                                          int32_t num_kv_heads, int32_t head_dim, const void *q,
+                                          const void *k_new, const void *v_new, int32_t n_new,
+                                          int32_t n_tail, int32_t append_cap, void *k_c, void *v_c,
+                                          const int64_t *seg_off, const int32_t *seg_len,
+                                          float sm_scale, int64_t rows_hint, float *out,
+                                          void *stream);
+
+/*
  * dkv_dense_decode_attn -- the same attention over an uncompressed cache
  * k, v [B][Hkv][t_cap][d]; every segment attends rows [0, n_valid),
  * n_valid <= t_cap.  Same workspace rules as dkv_decode_attn.

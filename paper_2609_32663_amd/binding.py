@@ -18,7 +18,8 @@ __all__ = [
     "DkvError", "Layout", "make_layout", "library", "library_path", "dtype_code",
     "dkv_map_pattern", "dkv_compact_workspace_bytes", "dkv_compact", "dkv_append",
     "dkv_decode_workspace_bytes", "dkv_decode_attn", "dkv_dense_decode_attn",
-    "dkv_append_decode_attn", "dkv_dense_append_decode_attn",
+    "dkv_append_decode_attn", "dkv_append_decode_attn_noalloc", "dkv_dense_append_decode_attn",
+    "DKV_NOALLOC_SCRATCH_BYTES",
     "dkv_status_string", "dkv_probe_stream_read", "dkv_query_workspace_bytes", "dkv_query_attn",
     "dkv_page_select_workspace_bytes", "dkv_page_entries_bound", "dkv_page_select",
     "dkv_paged_decode_attn", "dkv_paged_append_decode_attn", "dkv_budget_entries",
@@ -28,6 +29,7 @@ __all__ = [
 (DKV_OK, DKV_ERR_INVALID_ARG, DKV_ERR_UNSUPPORTED, DKV_ERR_MISALIGNED, DKV_ERR_CAPACITY,
  DKV_ERR_WORKSPACE, DKV_ERR_HIP) = range(7)
 DKV_BF16, DKV_F32 = 0, 1
+DKV_NOALLOC_SCRATCH_BYTES = 16 << 20  # include/dkv.h: scratch of dkv_append_decode_attn_noalloc
 
 library_path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdkv.so")
 
@@ -92,6 +94,8 @@ def library():
                                         SZ, VP]),
         "dkv_append_decode_attn": (I32, [I32, I32, I32, I32, I32, VP, VP, VP, I32, I32, I32, VP, VP,
                                          VP, VP, F32, I64, VP, VP, SZ, VP]),
+        "dkv_append_decode_attn_noalloc": (I32, [I32, I32, I32, I32, I32, VP, VP, VP, I32, I32, I32, VP,
+                                                 VP, VP, VP, F32, I64, VP, VP]),
         "dkv_dense_append_decode_attn": (I32, [I32, I32, I32, I32, I32, VP, VP, VP, I32, VP, VP, I64,
                                                I32, F32, VP, VP, SZ, VP]),
         "dkv_status_string": (ctypes.c_char_p, [I32]),
@@ -218,6 +222,18 @@ def dkv_append_decode_attn(q, k_new, v_new, n_tail, append_cap, k_c, v_c, seg_of
         _dev(v_c, "v_c"), _dev(seg_off, "seg_off"), _dev(seg_len, "seg_len"), float(sm_scale),
         int(rows_hint), _dev(out, "out"), _dev(workspace, "workspace"),
         workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def dkv_append_decode_attn_noalloc(q, k_new, v_new, n_tail, append_cap, k_c, v_c, seg_off, seg_len,
+                                   sm_scale, out, num_kv_heads, rows_hint=0, stream=None):
+    """dkv_append_decode_attn without a workspace (the library's static scratch)."""
+    B, Hq, d = q.shape
+    n_new = k_new.shape[1]
+    _check("dkv_append_decode_attn_noalloc", library().dkv_append_decode_attn_noalloc(
+        dtype_code(q.dtype), B, Hq, int(num_kv_heads), d, _dev(q, "q"), _dev(k_new, "k_new"),
+        _dev(v_new, "v_new"), n_new, int(n_tail), int(append_cap), _dev(k_c, "k_c"),
+        _dev(v_c, "v_c"), _dev(seg_off, "seg_off"), _dev(seg_len, "seg_len"), float(sm_scale),
+        int(rows_hint), _dev(out, "out"), _stream(stream)))
 
 
 def dkv_dense_append_decode_attn(q, k_new, v_new, k, v, n_valid, sm_scale, out, workspace,

@@ -872,7 +872,32 @@ hipError_t launch_d(const DecodeParams& p, int GP, int64_t rows_hint, hipStream_
   }
 }
 
+// Scratch of the allocation-free entry point (dkv_append_decode_attn_noalloc):
+// the split's partial records and segment metadata, in a file-scope array
+// that every GPU the library runs on holds until the process ends.  Host code
+// never passes the array's name to a kernel (on the host it is a stand-in,
+// not a device address); it passes the address hipGetSymbolAddress returns
+// for the current device.  The records need no initial contents.
+static __device__ __align__(256) unsigned char scratch[DKV_NOALLOC_SCRATCH_BYTES];
+
 }  // namespace
+
+hipError_t decode_static_scratch(void** ptr) {
+  static std::atomic<void*> addr[kMaxDevices];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  void* a = addr[dev].load(std::memory_order_acquire);
+  if (a == nullptr) {
+    // once per device, with that device current: each GPU holds its own copy
+    e = hipGetSymbolAddress(&a, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || a == nullptr) return e != hipSuccess ? e : hipErrorInvalidSymbol;
+    addr[dev].store(a, std::memory_order_release);
+  }
+  *ptr = a;
+  return hipSuccess;
+}
 
 int decode_group_pad(int G) { return G <= 4 ? 4 : (G <= 8 ? 8 : 16); }
 

@@ -43,9 +43,11 @@ int32_t uniform_width(const int32_t* e, int32_t D) {
   return W;
 }
 
+// Workspace checks are skipped for the allocation-free entry point, whose
+// scratch is the library's own (check_ws = false).
 dkv_status check_decode_common(int dtype, int32_t batch, int32_t hq, int32_t hkv, int32_t d,
                                const void* q, const void* k, const void* v, const float* out,
-                               const void* ws, size_t ws_bytes, float sm_scale) {
+                               const void* ws, size_t ws_bytes, float sm_scale, bool check_ws = true) {
   if (!dtype_ok(dtype)) return DKV_ERR_INVALID_ARG;
   if (batch < 0 || hq <= 0 || hkv <= 0 || hq % hkv != 0) return DKV_ERR_INVALID_ARG;
   if (!dkv::scale_in_range(sm_scale)) return DKV_ERR_INVALID_ARG;
@@ -54,6 +56,7 @@ dkv_status check_decode_common(int dtype, int32_t batch, int32_t hq, int32_t hkv
   if (batch == 0) return DKV_OK;
   if (q == nullptr || k == nullptr || v == nullptr || out == nullptr) return DKV_ERR_INVALID_ARG;
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return DKV_ERR_MISALIGNED;
+  if (!check_ws) return DKV_OK;
   if (ws == nullptr || !aligned16(ws)) return DKV_ERR_WORKSPACE;
   if (ws_bytes < dkv_decode_workspace_bytes(batch, hq, hkv, d)) return DKV_ERR_WORKSPACE;
   return DKV_OK;
@@ -232,13 +235,16 @@ size_t dkv_decode_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t nu
 
 namespace {
 
-// Packed-cache attention, optionally appending n_new tokens first. 
+// Packed-cache attention, optionally appending n_new tokens first.  With
+// static_ws the split's scratch is the library's own per-device array (ws
+// and ws_bytes are ignored): the allocation-free entry point.
 dkv_status decode_packed(dkv_dtype dtype, int32_t batch, int32_t hq, int32_t hkv, int32_t d, const void* q,
                          const void* k_new, const void* v_new, int32_t n_new, int32_t n_tail,
                          int32_t append_cap, const void* k_c, const void* v_c, const int64_t* seg_off,
                          const int32_t* seg_len, float sm_scale, int64_t rows_hint, float* out, void* ws,
-                         size_t ws_bytes, void* stream) {
-  dkv_status st = check_decode_common(dtype, batch, hq, hkv, d, q, k_c, v_c, out, ws, ws_bytes, sm_scale);
+                         size_t ws_bytes, void* stream, bool static_ws = false) {
+  dkv_status st =
+      check_decode_common(dtype, batch, hq, hkv, d, q, k_c, v_c, out, ws, ws_bytes, sm_scale, !static_ws);
   if (st != DKV_OK) return st;
   if (n_tail < 0 || n_new < 0) return DKV_ERR_INVALID_ARG;
   if (n_new > 0 && (int64_t)n_tail + n_new > append_cap) return DKV_ERR_CAPACITY;
@@ -246,6 +252,12 @@ dkv_status decode_packed(dkv_dtype dtype, int32_t batch, int32_t hq, int32_t hkv
   if (seg_off == nullptr || seg_len == nullptr) return DKV_ERR_INVALID_ARG;
   if (n_new > 0 && (k_new == nullptr || v_new == nullptr)) return DKV_ERR_INVALID_ARG;
   if (n_new > 0 && (!aligned16(k_new) || !aligned16(v_new))) return DKV_ERR_MISALIGNED;
+  if (static_ws) {
+    if (dkv_decode_workspace_bytes(batch, hq, hkv, d) > (size_t)DKV_NOALLOC_SCRATCH_BYTES)
+      return DKV_ERR_UNSUPPORTED;
+    if (dkv::decode_static_scratch(&ws) != hipSuccess) return DKV_ERR_HIP;
+    ws_bytes = DKV_NOALLOC_SCRATCH_BYTES;
+  }
   dkv::DecodeParams p;
   std::memset(&p, 0, sizeof(p));
   p.q = q;
@@ -325,6 +337,16 @@ dkv_status dkv_append_decode_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_
   return decode_packed(dtype, batch, num_q_heads, num_kv_heads, head_dim, q, k_new, v_new, n_new, n_tail,
                        append_cap, k_c, v_c, seg_off, seg_len, sm_scale, rows_hint, out, workspace,
                        workspace_bytes, stream);
+}
+
+dkv_status dkv_append_decode_attn_noalloc(dkv_dtype dtype, int32_t batch, int32_t num_q_heads,
+                                          int32_t num_kv_heads, int32_t head_dim, const void* q, const void* k_new,
+                                          const void* v_new, int32_t n_new, int32_t n_tail, int32_t append_cap,
+                                          void* k_c, void* v_c, const int64_t* seg_off, const int32_t* seg_len,
+                                          float sm_scale, int64_t rows_hint, float* out, void* stream) {
+  return decode_packed(dtype, batch, num_q_heads, num_kv_heads, head_dim, q, k_new, v_new, n_new, n_tail,
+                       append_cap, k_c, v_c, seg_off, seg_len, sm_scale, rows_hint, out, nullptr, 0, stream,
+                       /*static_ws=*/true);
 }
 
 dkv_status dkv_dense_decode_attn(dkv_dtype dtype, int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,

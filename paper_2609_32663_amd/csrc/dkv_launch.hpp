@@ -130,5 +130,8 @@ size_t decode_workspace_bytes(int nseg, int G, int head_dim);  // records + segm
 // rows_hint: expected total rows of the call (0 = unknown); sizes the split.
 hipError_t launch_decode(const DecodeParams& p, dkv_dtype dtype, int head_dim, int64_t rows_hint,
                          hipStream_t stream);
+// Device address of the allocation-free entry point's scratch array
+// (DKV_NOALLOC_SCRATCH_BYTES) on the current device, looked up once per device.
+hipError_t decode_static_scratch(void** ptr);
 
 }  // namespace dkv

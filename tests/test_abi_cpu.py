@@ -371,3 +371,25 @@ def test_binding_rejects_host_tensors():
         d.dkv_map_pattern(lay, torch.zeros(1, 8, 3, dtype=torch.uint8),
                           torch.zeros(1, 2, 1024, dtype=torch.uint8),
                           torch.zeros(1, 2, dtype=torch.int32))
+
+
+def test_noalloc_validation():
+    """The allocation-free call checks its arguments like the workspace call,
+    and refuses shapes whose workspace exceeds its static scratch, all on the
+    host before the scratch is looked up."""
+    lib = d.library()
+
+    def call(B=1, Hq=32, Hkv=8, dim=128, q=A, kn=A, vn=A, n_new=1, n_tail=0, cap=4, kc=A, vc=A, so=A, sl=A,
+             scale=1.0, out=A):
+        return lib.dkv_append_decode_attn_noalloc(d.DKV_BF16, B, Hq, Hkv, dim, q, kn, vn, n_new, n_tail, cap, kc,
+                                                  vc, so, sl, scale, 0, out, NUL)
+
+    assert d.dkv_decode_workspace_bytes(128, 128, 8, 128) > d.DKV_NOALLOC_SCRATCH_BYTES
+    assert call(B=128, Hq=128, Hkv=8) == d.DKV_ERR_UNSUPPORTED
+    assert call(n_new=2, n_tail=3) == d.DKV_ERR_CAPACITY
+    assert call(q=NUL) == d.DKV_ERR_INVALID_ARG
+    assert call(sl=NUL) == d.DKV_ERR_INVALID_ARG
+    assert call(scale=float("inf")) == d.DKV_ERR_INVALID_ARG
+    assert call(out=MIS) == d.DKV_ERR_MISALIGNED
+    assert call(dim=96) == d.DKV_ERR_UNSUPPORTED
+    assert call(B=0, q=NUL, out=NUL) == d.DKV_OK
