@@ -141,6 +141,7 @@ def pmc_per_dispatch(path, counter):
 
 TRACE_FILE = os.path.join(ROOT, "profiles", "decode_attn_llama8b_stack_128k.txt")
 QUERY_TRACE_FILE = os.path.join(ROOT, "profiles", "query_attn_llama8b_stack_128k.txt")
+CONFIGS_TRACE_FILE = os.path.join(ROOT, "profiles", "decode_attn_other_configs.txt")
 
 
 def trace_summary(trace_dir, bench_log, command):
@@ -171,6 +172,8 @@ def trace_summary(trace_dir, bench_log, command):
     lines = [f"# rocprofv3 kernel trace of bench.py ({WORKLOAD}: 32 layers x 32q/8kv x d128, "
              f"T=131072, {b['config']['retained_fraction'] * 100:.1f}% retained)",
              f"# command: {command}",
+             f"# sources measured: decode kernel sha256/16 {kernel_hash()} (decode_attn.hip, dkv_device.hpp, "
+             f"dkv_launch.hpp)",
              "# per-kernel statistics (rocprofv3 --stats, dkv kernels only; us):",
              f"{'kernel':58s} {'calls':>6s} {'avg':>9s} {'min':>9s} {'max':>9s}"]
     for r in stats:
@@ -212,6 +215,8 @@ def trace_summary(trace_dir, bench_log, command):
         ql = [f"# rocprofv3 kernel trace of bench.py, query-block attention ({WORKLOAD}: {qb['n_q']} tokens after "
               f"the context, every layer)",
               f"# command: {command}",
+              f"# sources measured: query kernel sha256/16 {kernel_hash(QUERY_SRCS)} (query_attn.hip, "
+              f"dkv_device.hpp, dkv_query.hpp)",
               "# per-kernel statistics (rocprofv3 --stats; us):",
               f"{'kernel':58s} {'calls':>6s} {'avg':>9s} {'min':>9s} {'max':>9s}"]
         for r in stats:
@@ -231,6 +236,36 @@ def trace_summary(trace_dir, bench_log, command):
         with open(QUERY_TRACE_FILE, "w") as f:
             f.write("\n".join(ql) + "\n")
         print("\n".join(ql))
+
+    # the other configurations: their decode calls are the run's last
+    # non-paged ones, issued in the order the JSON line lists them
+    seq = b.get("configs_decode_calls")
+    if seq:
+        n = sum(c for _, c in seq)
+        tail = pairs[len(pairs) - n:]
+        cl = ["# rocprofv3 kernel trace of bench.py, the other configurations (decode calls in issue order: "
+              "the eager call, warm-up and timed graph replays of each row)",
+              f"# command: {command}",
+              f"# sources measured: decode kernel sha256/16 {kernel_hash()}",
+              f"{'row':34s} {'calls':>6s} {'decode_kernel':>14s} {'merge':>8s} {'call':>9s}  (means, us)"]
+        i = 0
+        for label, c in seq:
+            ps = tail[i:i + c]
+            i += c
+            cl.append(f"{label:34s} {len(ps):6d} {st.mean(p[0] for p in ps):14.2f} {st.mean(p[1] for p in ps):8.2f} "
+                      f"{st.mean(p[2] for p in ps):9.2f}")
+        cl += ["", "# JSON rows of the same run (timed region = HIP-graph replays; the profiler adds overhead):"]
+        for name, r in b["configs"].items():
+            keep = {k: r[k] for k in r if k in ("us_per_step", "gb_per_s", "frac_of_peak", "speedup_vs_dense",
+                                                "dense", "parity", "one_time")}
+            for k, r2 in r.items():
+                if k.startswith("budget_"):
+                    keep[k] = {k2: r2[k2] for k2 in ("us_per_step", "gb_per_s", "frac_of_peak", "speedup_vs_dense",
+                                                      "parity", "one_time")}
+            cl.append(f"{name} {json.dumps(keep)}")
+        with open(CONFIGS_TRACE_FILE, "w") as f:
+            f.write("\n".join(cl) + "\n")
+        print("\n".join(cl))
 
 
 def pmc_summary(fetch_csv, write_csv, bench_log, command):
@@ -285,6 +320,408 @@ def pmc_summary(fetch_csv, write_csv, bench_log, command):
         json.dump(res, f, indent=1)
         f.write("\n")
     print(json.dumps(res))
+
+
+def rel_err(got, want):
+    """Max over output rows of |got - want|_inf / max(|want|_inf, 1e-30)."""
+    import numpy as np
+    got = np.asarray(got, np.float64)
+    want = np.asarray(want, np.float64)
+    return float((np.abs(got - want).max(-1) / np.maximum(np.abs(want).max(-1), 1e-30)).max())
+
+
+def bench_configs(ctx):
+    """The other configurations of the measurement plan, one row each: the
+    8B-shaped layer at 32K, the 70B-shaped batch at each budget and the
+    Qwen-shaped stack.  Every row times the packed step and the same build's
+    dense decode, the one-time compaction, checks a sample of outputs against
+    the oracle and (with the oracle baseline on) times the oracle on the same
+    sample.  Caches whose step reads less than 1 GiB are rotated over
+    copies, so no timed call finds its bytes in the 256 MB last-level cache
+    from the call before.  Returns the rows and the decode calls they issued,
+    in order (for the kernel-trace summary)."""
+    import ctypes
+    import numpy as np
+    import torch
+
+    import dkv_inputs as di
+    d, lib, dev, stream, args = ctx["d"], ctx["lib"], ctx["dev"], ctx["stream"], ctx["args"]
+    o = ctx.get("oracle")
+    P = ctypes.c_void_p
+    elem = 2
+    gstream = torch.cuda.Stream()
+    calls = []  # (label, decode calls issued), in issue order
+
+    def ev():
+        return torch.cuda.Event(enable_timing=True)
+
+    def check(fn, *a):
+        st = fn(*a)
+        if st != 0:
+            raise d.DkvError(fn.__name__, st)
+
+    def replay_ms(g, reps, warm):
+        for _ in range(warm):
+            g.replay()
+        torch.cuda.synchronize()
+        a, b = ev(), ev()
+        a.record(stream)
+        for _ in range(reps):
+            g.replay()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    def capture(fn):
+        fn(stream.cuda_stream)  # eager once: code objects loaded, results defined
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=gstream):
+            fn(gstream.cuda_stream)
+        return g
+
+    def timed_event(fn, reps=3):
+        fn()  # warm
+        torch.cuda.synchronize()
+        a, b = ev(), ev()
+        a.record(stream)
+        for _ in range(reps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e3 / reps
+
+    def pack(w, pattern, k, v, cap, lay):
+        N, Hkv, T = w.num_units, w.num_kv_heads, w.context_len
+        km = torch.empty((N, Hkv, T), dtype=torch.uint8, device=dev)
+        kl = torch.empty((N, Hkv), dtype=torch.int32, device=dev)
+        pat = torch.from_numpy(np.ascontiguousarray(pattern)).to(dev)
+        map_us = timed_event(lambda: d.dkv_map_pattern(lay, pat, km, kl))
+        lens = kl.cpu().to(torch.int64)
+        rows = int((lens + cap).sum())
+        k_c = torch.empty((rows, w.head_dim), dtype=torch.bfloat16, device=dev)
+        v_c = torch.empty_like(k_c)
+        so = torch.empty(N * Hkv, dtype=torch.int64, device=dev)
+        sl = torch.empty(N * Hkv, dtype=torch.int32, device=dev)
+        ws = torch.empty(d.dkv_compact_workspace_bytes(lay), dtype=torch.uint8, device=dev)
+        c_us = timed_event(lambda: d.dkv_compact(lay, k, v, km, cap, k_c, v_c, so, sl, ws), reps=2)
+        retained = int(lens.sum())
+        c_bytes = 2 * 2 * retained * w.head_dim * elem + N * Hkv * T
+        one_time = {"map_us": round(map_us, 1), "compact_us": round(c_us, 1),
+                    "compact_gb_per_s": round(c_bytes / (c_us * 1e-6) / 1e9, 1),
+                    "map_write_gb_per_s": round(N * Hkv * T / (map_us * 1e-6) / 1e9, 1)}
+        return dict(km=km, lens=lens, rows=rows, k_c=k_c, v_c=v_c, so=so, sl=sl, retained=retained,
+                    one_time=one_time)
+
+    def bits(t):
+        return t.cpu().view(torch.int16).numpy().view(np.uint16)
+
+    def copies_for(step_bytes):
+        # enough copies that a call's bytes were last read >= 1 GiB earlier
+        return max(1, -(-(1 << 30) // max(1, int(step_bytes))))
+
+    rows = {}
+
+    # ---------------- 8B-shaped layer at 32K ------------------------------
+    w = di.workload("llama8b_layer_32k")
+    B, Hq, Hkv, dim, T, cap = w.batch, w.num_q_heads, w.num_kv_heads, w.head_dim, w.context_len, w.append_cap
+    nseg = B * Hkv
+    pattern, pinfo = di.make_pattern(w)
+    ku, vu = di.kv_unit(w, 0, device=dev)
+    k, v = ku[None].contiguous(), vu[None].contiguous()
+    del ku, vu
+    lay = d.make_layout(1, Hq, Hkv, dim, T, w.sink, w.recent, list(w.bin_edges))
+    pk = pack(w, pattern, k, v, cap, lay)
+    q = di.q_step(w, 0, 0, device=dev).contiguous()
+    kn, vn = (t.reshape(nseg, 1, dim).contiguous() for t in di.kv_new_step(w, 0, 0, device=dev))
+    out = torch.empty((B, Hq, dim), dtype=torch.float32, device=dev)
+    dws = torch.empty(d.dkv_decode_workspace_bytes(B, Hq, Hkv, dim), dtype=torch.uint8, device=dev)
+    p_bytes = (pk["retained"] + nseg) * dim * elem * 2 + B * Hq * dim * (elem + 4) + nseg * 12
+    d_bytes = nseg * (T + 1) * dim * elem * 2 + B * Hq * dim * (elem + 4)
+    Rp, Rd = copies_for(p_bytes), copies_for(d_bytes)
+    kcs = [pk["k_c"]] + [pk["k_c"].clone() for _ in range(Rp - 1)]
+    vcs = [pk["v_c"]] + [pk["v_c"].clone() for _ in range(Rp - 1)]
+    kds, vds = [], []
+    for _ in range(Rd):
+        kd_ = torch.zeros((B, Hkv, T + cap, dim), dtype=torch.bfloat16, device=dev)
+        vd_ = torch.zeros_like(kd_)
+        kd_[:, :, :T].copy_(k)
+        vd_[:, :, :T].copy_(v)
+        kds.append(kd_)
+        vds.append(vd_)
+    hint = pk["retained"] + nseg
+
+    def packed_calls(shp):
+        for r in range(Rp):
+            check(lib.dkv_append_decode_attn, d.DKV_BF16, B, Hq, Hkv, dim, P(q.data_ptr()), P(kn.data_ptr()),
+                  P(vn.data_ptr()), 1, 0, cap, P(kcs[r].data_ptr()), P(vcs[r].data_ptr()),
+                  P(pk["so"].data_ptr()), P(pk["sl"].data_ptr()), w.sm_scale, hint, P(out.data_ptr()),
+                  P(dws.data_ptr()), dws.numel(), P(shp))
+
+    def dense_calls(shp):
+        for r in range(Rd):
+            check(lib.dkv_dense_append_decode_attn, d.DKV_BF16, B, Hq, Hkv, dim, P(q.data_ptr()),
+                  P(kn.data_ptr()), P(vn.data_ptr()), 1, P(kds[r].data_ptr()), P(vds[r].data_ptr()), T + cap, T,
+                  w.sm_scale, P(out.data_ptr()), P(dws.data_ptr()), dws.numel(), P(shp))
+
+    g = capture(packed_calls)
+    p_us = replay_ms(g, args.steps, args.warmup) * 1e3 / Rp
+    calls.append(("llama8b_layer_32k packed", Rp * (1 + args.warmup + args.steps)))
+    got = out.cpu().numpy()
+    del g
+    g = capture(dense_calls)
+    dn_us = replay_ms(g, args.steps, args.warmup) * 1e3 / Rd
+    calls.append(("llama8b_layer_32k dense", Rd * (1 + args.warmup + args.steps)))
+    del g
+    row = {"workload": w.name, "step": "one dkv_append_decode_attn (append 1 token, attend); HIP-graph replays "
+                                      f"cycling over {Rp} copies of the packed cache ({Rd} of the dense one)",
+           "retained_fraction": round(pk["retained"] / float(nseg * T), 4),
+           "us_per_step": round(p_us, 2), "gb_per_s": round(p_bytes / (p_us * 1e-6) / 1e9, 1),
+           "frac_of_peak": round(p_bytes / (p_us * 1e-6) / 1e9 / ctx["peak_hbm"], 4), "bytes_per_step": int(p_bytes),
+           "dense": {"us_per_step": round(dn_us, 2), "gb_per_s": round(d_bytes / (dn_us * 1e-6) / 1e9, 1)},
+           "speedup_vs_dense": round(dn_us / p_us, 3), "copies": {"packed": Rp, "dense": Rd},
+           "one_time": pk["one_time"], "parity": None, "cpu_baseline": None}
+    if o is not None:
+        from threadpoolctl import threadpool_limits
+        kb, vb = bits(k), bits(v)
+        _, okm, _ = o.map_pattern(pattern, T, w.sink, w.recent, w.bin_edges, Hkv)
+        with threadpool_limits(1):
+            t0 = time.perf_counter()
+            ref = o.compact(kb, vb, okm, cap)
+            t_pack = time.perf_counter() - t0
+            kc1, vc1 = o.append(ref["k_c"], ref["v_c"], ref["seg_off"], ref["seg_len"],
+                                bits(kn).reshape(B, Hkv, 1, dim), bits(vn).reshape(B, Hkv, 1, dim), 0)
+            t0 = time.perf_counter()
+            want = o.decode_attn(bits(q), kc1, vc1, ref["seg_off"], ref["seg_len"], 1, w.sm_scale, Hkv, o.BF16)
+            t_dec = time.perf_counter() - t0
+        # the retained rows and the appended token of every segment (the rest
+        # of the append room is never written)
+        live = np.concatenate([np.arange(int(ref["seg_off"][s_]), int(ref["seg_off"][s_] + ref["seg_len"][s_]) + 1)
+                               for s_ in range(nseg)])
+        row["parity"] = {"max_rel_err": rel_err(got, want),
+                         "seg_len_equal": bool(np.array_equal(pk["sl"].cpu().numpy(), ref["seg_len"])),
+                         "packed_rows_equal": bool(np.array_equal(bits(pk["k_c"])[live], kc1[live]))}
+        row["cpu_baseline"] = {"value": round(p_bytes / t_dec / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+                               "sample": f"the whole step (one decode over the packed layer plus the appended token) "
+                                         f"by the fp64 NumPy oracle, 1 BLAS thread: {t_dec:.3f} s",
+                               "compaction_s": round(t_pack, 3)}
+        del kb, vb, ref, kc1, vc1
+    rows[w.name] = row
+    del kcs, vcs, kds, vds, k, v, pk
+    torch.cuda.empty_cache()
+
+    # ---------------- 70B-shaped batch at each budget ---------------------
+    w = di.workload("llama70b_layer_bs16_32k")
+    B, Hq, Hkv, dim, T, cap, S = (w.batch, w.num_q_heads, w.num_kv_heads, w.head_dim, w.context_len,
+                                  w.append_cap, w.decode_steps)
+    nseg = B * Hkv
+    k = torch.empty((B, Hkv, T, dim), dtype=torch.bfloat16, device=dev)
+    v = torch.empty_like(k)
+    for b_ in range(B):
+        ku, vu = di.kv_unit(w, b_, device=dev)
+        k[b_].copy_(ku)
+        v[b_].copy_(vu)
+    del ku, vu
+    lay = d.make_layout(B, Hq, Hkv, dim, T, w.sink, w.recent, list(w.bin_edges))
+    qs = [di.q_step(w, 0, s_, device=dev).contiguous() for s_ in range(S)]
+    news = [tuple(t.reshape(nseg, 1, dim).contiguous() for t in di.kv_new_step(w, 0, s_, device=dev))
+            for s_ in range(S)]
+    k_all = torch.cat([kn_ for kn_, _ in news], dim=1).contiguous()  # [nseg][S][d]
+    v_all = torch.cat([vn_ for _, vn_ in news], dim=1).contiguous()
+    out = torch.empty((B, Hq, dim), dtype=torch.float32, device=dev)
+    dws = torch.empty(d.dkv_decode_workspace_bytes(B, Hq, Hkv, dim), dtype=torch.uint8, device=dev)
+    kd = torch.zeros((B, Hkv, T + cap, dim), dtype=torch.bfloat16, device=dev)
+    vd = torch.zeros_like(kd)
+    kd[:, :, :T].copy_(k)
+    vd[:, :, :T].copy_(v)
+    d_bytes = sum(nseg * (T + s_ + 1) * dim * elem * 2 for s_ in range(S)) / S + B * Hq * dim * (elem + 4)
+
+    def dense_steps(shp):
+        for s_ in range(S):
+            kn_, vn_ = news[s_]
+            check(lib.dkv_dense_append_decode_attn, d.DKV_BF16, B, Hq, Hkv, dim, P(qs[s_].data_ptr()),
+                  P(kn_.data_ptr()), P(vn_.data_ptr()), 1, P(kd.data_ptr()), P(vd.data_ptr()), T + cap, T + s_,
+                  w.sm_scale, P(out.data_ptr()), P(dws.data_ptr()), dws.numel(), P(shp))
+
+    g = capture(dense_steps)
+    dn_us = replay_ms(g, max(1, args.steps // 4), 1) * 1e3 / S
+    calls.append(("llama70b dense", S * (1 + 1 + max(1, args.steps // 4))))
+    del g, kd, vd
+    torch.cuda.empty_cache()
+    brow = {"workload": w.name, "steps": S, "step": "one dkv_append_decode_attn per step (append 1 token, attend "
+                                                      "the whole batch); the 16 steps as one HIP graph",
+            "dense": {"us_per_step": round(dn_us, 2), "gb_per_s": round(d_bytes / (dn_us * 1e-6) / 1e9, 1),
+                      "frac_of_peak": round(d_bytes / (dn_us * 1e-6) / 1e9 / ctx["peak_hbm"], 4)}}
+    for budget in w.budgets:
+        pattern, pinfo = di.make_pattern(w, budget=budget)
+        pk = pack(w, pattern, k, v, cap, lay)
+        # every step's token written once up front (untimed), so each copy
+        # holds what the sequential steps would have appended before it
+        d.dkv_append(k_all, v_all, 0, cap, pk["k_c"], pk["v_c"], pk["so"], pk["sl"])
+        p_bytes = (sum((pk["retained"] + nseg * (s_ + 1)) for s_ in range(S)) / S * dim * elem * 2
+                   + B * Hq * dim * (elem + 4) + nseg * 12)
+        R = copies_for(p_bytes)
+        kcs = [pk["k_c"]] + [pk["k_c"].clone() for _ in range(R - 1)]
+        vcs = [pk["v_c"]] + [pk["v_c"].clone() for _ in range(R - 1)]
+
+        def packed_steps(shp):
+            for s_ in range(S):
+                kn_, vn_ = news[s_]
+                r = s_ % R
+                check(lib.dkv_append_decode_attn, d.DKV_BF16, B, Hq, Hkv, dim, P(qs[s_].data_ptr()),
+                      P(kn_.data_ptr()), P(vn_.data_ptr()), 1, s_, cap, P(kcs[r].data_ptr()), P(vcs[r].data_ptr()),
+                      P(pk["so"].data_ptr()), P(pk["sl"].data_ptr()), w.sm_scale, pk["retained"] + nseg * (s_ + 1),
+                      P(out.data_ptr()), P(dws.data_ptr()), dws.numel(), P(shp))
+
+        g = capture(packed_steps)
+        p_us = replay_ms(g, args.steps, args.warmup) * 1e3 / S
+        calls.append((f"llama70b packed {budget}", S * (1 + args.warmup + args.steps)))
+        got = out.cpu().numpy()  # the last step: every sequence, all 16 tokens appended
+        del g
+        seg = pk["lens"].view(-1).to(torch.float64)
+        r_ = {"retained_fraction": round(pk["retained"] / float(nseg * T), 4),
+              "us_per_step": round(p_us, 2), "gb_per_s": round(p_bytes / (p_us * 1e-6) / 1e9, 1),
+              "frac_of_peak": round(p_bytes / (p_us * 1e-6) / 1e9 / ctx["peak_hbm"], 4),
+              "bytes_per_step": int(p_bytes), "speedup_vs_dense": round(dn_us / p_us, 3), "copies": R,
+              "segment_rows": {"min": int(seg.min()), "max": int(seg.max()),
+                               "cv": round(float(seg.std() / seg.mean()), 3)},
+              "one_time": pk["one_time"], "parity": None, "cpu_baseline": None}
+        if o is not None:
+            from threadpoolctl import threadpool_limits
+            ns = 2  # sample: the first two sequences, at the last step
+            _, okm, _ = o.map_pattern(pattern[:ns], T, w.sink, w.recent, w.bin_edges, Hkv)
+            with threadpool_limits(1):
+                t0 = time.perf_counter()
+                ref = o.compact(bits(k[:ns]), bits(v[:ns]), okm, cap)
+                t_pack = time.perf_counter() - t0
+                kc1, vc1 = o.append(ref["k_c"], ref["v_c"], ref["seg_off"], ref["seg_len"],
+                                    bits(k_all[:ns * Hkv]).reshape(ns, Hkv, S, dim),
+                                    bits(v_all[:ns * Hkv]).reshape(ns, Hkv, S, dim), 0)
+                t0 = time.perf_counter()
+                want = o.decode_attn(bits(qs[S - 1][:ns]), kc1, vc1, ref["seg_off"], ref["seg_len"], S, w.sm_scale,
+                                     Hkv, o.BF16)
+                t_dec = time.perf_counter() - t0
+            s_bytes = (int(ref["seg_len"].sum()) + ns * Hkv * S) * dim * elem * 2
+            r_["parity"] = {"sequences": ns, "step": S - 1, "max_rel_err": rel_err(got[:ns], want),
+                            "seg_len_equal": bool(np.array_equal(pk["sl"].cpu().numpy()[:ns * Hkv], ref["seg_len"]))}
+            r_["cpu_baseline"] = {"value": round(s_bytes / t_dec / 1e9, 4), "unit": "GB/s", "cores": 1,
+                                  "kind": "oracle",
+                                  "sample": f"the last decode step of sequences 0-{ns - 1} by the fp64 NumPy oracle, "
+                                            f"1 BLAS thread: {t_dec:.3f} s", "compaction_s_sample": round(t_pack, 3)}
+        brow[f"budget_{budget}"] = r_
+        del kcs, vcs, pk
+        torch.cuda.empty_cache()
+    rows[w.name] = brow
+    del k, v, k_all, v_all
+    torch.cuda.empty_cache()
+
+    # ---------------- Qwen-shaped stack, batch 4, 128K --------------------
+    w = di.workload("qwen7b_stack_bs4_128k")
+    L, B, Hq, Hkv, dim, T, cap = (w.num_layers, w.batch, w.num_q_heads, w.num_kv_heads, w.head_dim, w.context_len,
+                                  w.append_cap)
+    N, S, nsl = w.num_units, w.decode_steps, B * Hkv
+    k = torch.empty((N, Hkv, T, dim), dtype=torch.bfloat16, device=dev)
+    v = torch.empty_like(k)
+    for u in range(N):
+        ku, vu = di.kv_unit(w, u, device=dev)
+        k[u].copy_(ku)
+        v[u].copy_(vu)
+        del ku, vu
+    pattern, pinfo = di.make_pattern(w)
+    lay = d.make_layout(N, Hq, Hkv, dim, T, w.sink, w.recent, list(w.bin_edges))
+    pk = pack(w, pattern, k, v, cap, lay)
+    qs = [di.q_step(w, layer, 0, device=dev).contiguous() for layer in range(L)]
+    news = [tuple(t.reshape(nsl, 1, dim).contiguous() for t in di.kv_new_step(w, layer, 0, device=dev))
+            for layer in range(L)]
+    outs = torch.empty((L, B, Hq, dim), dtype=torch.float32, device=dev)
+    dws = torch.empty(d.dkv_decode_workspace_bytes(B, Hq, Hkv, dim), dtype=torch.uint8, device=dev)
+    lrows = [int(pk["lens"][layer * B:(layer + 1) * B].sum()) for layer in range(L)]
+
+    def gen_steps(shp):  # all 256 steps of the generation, 28 layers each
+        for s_ in range(S):
+            for layer in range(L):
+                off = layer * nsl
+                kn_, vn_ = news[layer]
+                check(lib.dkv_append_decode_attn, d.DKV_BF16, B, Hq, Hkv, dim, P(qs[layer].data_ptr()),
+                      P(kn_.data_ptr()), P(vn_.data_ptr()), 1, s_, cap, P(pk["k_c"].data_ptr()),
+                      P(pk["v_c"].data_ptr()), P(pk["so"].data_ptr() + 8 * off), P(pk["sl"].data_ptr() + 4 * off),
+                      w.sm_scale, lrows[layer] + nsl * (s_ + 1), P(outs[layer].data_ptr()), P(dws.data_ptr()),
+                      dws.numel(), P(shp))
+
+    g = capture(gen_steps)
+    reps = max(1, args.steps // 10)
+    p_us = replay_ms(g, reps, 1) * 1e3 / S
+    calls.append(("qwen packed", S * L * (1 + 1 + reps)))
+    got_last = outs[0].cpu().numpy()  # layer 0 after the last of the 256 steps
+    del g
+    p_bytes = (sum(pk["retained"] + N * Hkv * (s_ + 1) for s_ in range(S)) / S * dim * elem * 2
+               + L * B * Hq * dim * (elem + 4) + N * Hkv * 12)
+
+    def dense_step(shp):  # attend-only over the dense cache (no room to append in it)
+        for layer in range(L):
+            u = slice(layer * B, (layer + 1) * B)
+            check(lib.dkv_dense_decode_attn, d.DKV_BF16, B, Hq, Hkv, dim, P(qs[layer].data_ptr()),
+                  P(k[u].data_ptr()), P(v[u].data_ptr()), T, T, w.sm_scale, P(outs[layer].data_ptr()),
+                  P(dws.data_ptr()), dws.numel(), P(shp))
+
+    g = capture(dense_step)
+    dreps = max(2, args.steps // 4)
+    dn_us = replay_ms(g, dreps, 1) * 1e3
+    calls.append(("qwen dense", L * (1 + 1 + dreps)))
+    del g
+    d_bytes = N * Hkv * T * dim * elem * 2 + L * B * Hq * dim * (elem + 4)
+    seg = pk["lens"].view(-1).to(torch.float64)
+    qrow = {"workload": w.name, "layers": L, "batch": B, "steps": S,
+            "step": "per layer one dkv_append_decode_attn (append 1 token per sequence, attend); the 256 steps of "
+                    "the generation as one HIP graph",
+            "retained_fraction": round(pk["retained"] / float(N * Hkv * T), 4),
+            "us_per_step": round(p_us, 1), "us_per_layer": round(p_us / L, 2),
+            "gb_per_s": round(p_bytes / (p_us * 1e-6) / 1e9, 1),
+            "frac_of_peak": round(p_bytes / (p_us * 1e-6) / 1e9 / ctx["peak_hbm"], 4),
+            "bytes_per_step": int(p_bytes),
+            "dense": {"us_per_step": round(dn_us, 1), "gb_per_s": round(d_bytes / (dn_us * 1e-6) / 1e9, 1),
+                      "frac_of_peak": round(d_bytes / (dn_us * 1e-6) / 1e9 / ctx["peak_hbm"], 4),
+                      "step": "per layer one dkv_dense_decode_attn over the 131,072 context rows (attend only)"},
+            "speedup_vs_dense": round(dn_us / p_us, 3),
+            "segment_rows": {"min": int(seg.min()), "max": int(seg.max()), "cv": round(float(seg.std() / seg.mean()), 3)},
+            "one_time": pk["one_time"], "all_keep_equals_dense": None, "parity": None, "cpu_baseline": None}
+    # all-keep pattern on layer 0: the packed decode must give the dense kernel's result bit for bit
+    lay0 = d.make_layout(B, Hq, Hkv, dim, T, w.sink, w.recent, list(w.bin_edges))
+    wk = di.workload(w.name, num_layers=1)
+    pk1 = pack(wk, np.ones((B, Hq, w.num_bins), np.uint8), k[:B], v[:B], 0, lay0)
+    o_p = torch.empty((B, Hq, dim), dtype=torch.float32, device=dev)
+    o_d = torch.empty_like(o_p)
+    d.dkv_decode_attn(qs[0], pk1["k_c"], pk1["v_c"], pk1["so"], pk1["sl"], 0, w.sm_scale, o_p, dws, Hkv,
+                      rows_hint=pk1["rows"])
+    d.dkv_dense_decode_attn(qs[0], k[:B], v[:B], T, w.sm_scale, o_d, dws)
+    torch.cuda.synchronize()
+    calls.append(("qwen all-keep check", 2))
+    qrow["all_keep_equals_dense"] = bool(torch.equal(o_p, o_d))
+    del pk1
+    if o is not None:
+        from threadpoolctl import threadpool_limits
+        _, okm, _ = o.map_pattern(pattern[:B], T, w.sink, w.recent, w.bin_edges, Hkv)
+        with threadpool_limits(1):
+            t0 = time.perf_counter()
+            ref = o.compact(bits(k[:B]), bits(v[:B]), okm, cap)
+            t_pack = time.perf_counter() - t0
+            kn0 = np.repeat(bits(news[0][0]).reshape(B, Hkv, 1, dim), S, axis=2)
+            vn0 = np.repeat(bits(news[0][1]).reshape(B, Hkv, 1, dim), S, axis=2)
+            kc1, vc1 = o.append(ref["k_c"], ref["v_c"], ref["seg_off"], ref["seg_len"], kn0, vn0, 0)
+            t0 = time.perf_counter()
+            want = o.decode_attn(bits(qs[0]), kc1, vc1, ref["seg_off"], ref["seg_len"], S, w.sm_scale, Hkv, o.BF16)
+            t_dec = time.perf_counter() - t0
+        l_bytes = (int(ref["seg_len"].sum()) + nsl * S) * dim * elem * 2
+        qrow["parity"] = {"layer": 0, "step": S - 1, "max_rel_err": rel_err(got_last, want),
+                          "seg_len_equal": bool(np.array_equal(pk["sl"].cpu().numpy()[:nsl], ref["seg_len"]))}
+        qrow["cpu_baseline"] = {"value": round(l_bytes / t_dec / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+                                "sample": f"the last step of layer 0 (4 sequences) by the fp64 NumPy oracle, 1 BLAS "
+                                          f"thread: {t_dec:.3f} s; a 28-layer step scales to {t_dec * L:.2f} s",
+                                "compaction_s_layer0": round(t_pack, 3)}
+    rows[w.name] = qrow
+    del k, v, pk
+    torch.cuda.empty_cache()
+    return rows, calls
 
 
 def main():
@@ -595,6 +1032,37 @@ def main():
     ms, eager_ms, nbytes = timed("packed", args.steps, args.warmup)
     log("timing dense decode")
     dms, deager_ms, dbytes = timed("dense", args.steps, args.warmup)
+    # the whole generation of the workload: every one of its decode steps
+    # (tails 0 .. decode_steps - 1), one graph per step, replayed in order
+    log("timing the full generation")
+
+    def full_generation(mode):
+        graphs = []
+        for s_ in range(w.decode_steps):
+            g_ = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g_, stream=cap_stream):
+                run(step_args(s_, mode, cap_stream.cuda_stream))
+            graphs.append(g_)
+        for g_ in graphs:
+            g_.replay()
+        torch.cuda.synchronize()
+        a_, b_ = ev(), ev()
+        a_.record(stream)
+        for g_ in graphs:
+            g_.replay()
+        b_.record(stream)
+        torch.cuda.synchronize()
+        n_bytes = sum(decode_bytes(s_, mode) for s_ in range(w.decode_steps))
+        return a_.elapsed_time(b_) / w.decode_steps, n_bytes / w.decode_steps
+
+    fg_ms, fg_bytes = full_generation("packed")
+    fgd_ms, fgd_bytes = full_generation("dense")
+    full_gen = {"steps": w.decode_steps, "ms_per_step": round(fg_ms, 4),
+                "gb_per_s": round(fg_bytes / (fg_ms * 1e-3) / 1e9, 2),
+                "dense_ms_per_step": round(fgd_ms, 4), "speedup_vs_dense": round(fgd_ms / fg_ms, 3),
+                "step": f"all {w.decode_steps} steps of the generation (tails 0-{w.decode_steps - 1}), one graph per "
+                        "step, replayed once in order"}
+    log(f"full generation: {fg_ms:.4f} ms/step packed, {fgd_ms:.4f} dense")
     # A step is exactly one attention call per layer on one stream, so the
     # average duration of a call (split + combine kernel, with the gaps
     # between them) is the timed region's event interval over L calls.
@@ -1039,6 +1507,15 @@ def main():
         f"{mt_res['decode_ms_per_token']} ms/token), parity {mt_res['parity_layer0_last_token']}")
     del gp, gd
 
+    # ---------------- the other configurations ---------------------------
+    log("other configurations: 8B layer at 32K, 70B-shaped batch, Qwen-shaped stack")
+    cfg_rows, cfg_calls = bench_configs({"d": d, "lib": lib, "dev": dev, "stream": stream, "args": args,
+                                         "oracle": None if args.no_cpu_baseline else __import__("oracle"),
+                                         "peak_hbm": PEAK_HBM_GBPS})
+    for name_, r_ in cfg_rows.items():
+        log(f"{name_}: " + json.dumps({k_: r_[k_] for k_ in r_ if k_ in ("us_per_step", "gb_per_s",
+                                                                          "speedup_vs_dense")}))
+
     # ---------------- achievable read bandwidth at this launch size -------
     # The streaming-read probe (same 16-byte non-temporal buffer loads as the
     # decode kernel's K/V stream) over L slices of one decode launch's size,
@@ -1136,6 +1613,9 @@ def main():
                   "avg_launch_us": round(dlaunch_ms * 1e3, 2),
                   "launch_frac_of_peak": round(dbytes / L / (dlaunch_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)},
         "speedup_vs_dense": round(dms / ms, 3),
+        "full_generation": full_gen,
+        "configs": cfg_rows,
+        "configs_decode_calls": cfg_calls,
         "paged": paged_res,
         "topk_export": topk_res,
         "ragged_batch": ragged_res,
