@@ -61,6 +61,9 @@ def parse():
     ap.add_argument("--trace-summary", nargs=2, metavar=("TRACE_DIR", "BENCH_LOG"),
                     help="summarise a rocprofv3 --kernel-trace --stats run of this script (csv output "
                          "named run_*) and its JSON line into the kernel-trace profile")
+    ap.add_argument("--phase-budget", action="store_true",
+                    help="per-phase time budget of the headline call from the phase-stamp build "
+                         "(python paper_2609_32663_amd/build.py --phase-stamps first); writes the profile")
     ap.add_argument("--pmc-command", default="",
                     help="command line recorded by --pmc-summary / --trace-summary")
     return ap.parse_args()
@@ -142,6 +145,8 @@ def pmc_per_dispatch(path, counter):
 TRACE_FILE = os.path.join(ROOT, "profiles", "decode_attn_llama8b_stack_128k.txt")
 QUERY_TRACE_FILE = os.path.join(ROOT, "profiles", "query_attn_llama8b_stack_128k.txt")
 CONFIGS_TRACE_FILE = os.path.join(ROOT, "profiles", "decode_attn_other_configs.txt")
+PHASE_FILE = os.path.join(ROOT, "profiles", "decode_phase_budget_llama8b_stack_128k.txt")
+PHASE_LIB = os.path.join(ROOT, "paper_2609_32663_amd", "libdkv_phase.so")
 
 
 def trace_summary(trace_dir, bench_log, command):
@@ -724,8 +729,237 @@ def bench_configs(ctx):
     return rows, calls
 
 
+def phase_budget(args):
+    """Where the time of one decode call goes, for the headline stack, the
+    70B-shaped batch (20% budget) and the Qwen-shaped stack: their decode
+    steps (fused append + decode calls) captured as graphs through the
+    phase-stamp build and replayed; per-workgroup clock stamps (100 MHz, one
+    clock for the whole chip) give, per call, the prologue, the stream, the
+    tail of the slowest workgroups, the fold, the combine kernel and the gaps
+    between kernels.  The product library's graphs of the same steps are
+    timed in the same run, and so is the streaming-read probe over the same
+    bytes."""
+    import ctypes
+    import numpy as np
+    import torch
+
+    import dkv_inputs as di
+    import paper_2609_32663_amd as d
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    lib = d.library()
+    plib = d.library_at(PHASE_LIB)
+    plib.dkv_phase_stamps.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    plib.dkv_phase_stamps.restype = ctypes.c_int
+    plib.dkv_phase_reset.argtypes = []
+    plib.dkv_phase_reset.restype = None
+    P = ctypes.c_void_p
+    cs = torch.cuda.Stream()
+
+    def ev():
+        return torch.cuda.Event(enable_timing=True)
+
+    def case(name, budget=None):
+        w = di.workload(name)
+        L, B, Hq, Hkv, dim, T, cap, N = (w.num_layers, w.batch, w.num_q_heads, w.num_kv_heads, w.head_dim,
+                                         w.context_len, w.append_cap, w.num_units)
+        nsl = B * Hkv
+        log(f"phase budget: {name}")
+        pattern, _ = di.make_pattern(w, budget=budget)
+        k = torch.empty((N, Hkv, T, dim), dtype=torch.bfloat16, device=dev)
+        v = torch.empty_like(k)
+        for u in range(N):
+            ku, vu = di.kv_unit(w, u, device=dev)
+            k[u].copy_(ku)
+            v[u].copy_(vu)
+            del ku, vu
+        lay = d.make_layout(N, Hq, Hkv, dim, T, w.sink, w.recent, list(w.bin_edges))
+        km = torch.empty((N, Hkv, T), dtype=torch.uint8, device=dev)
+        kl = torch.empty((N, Hkv), dtype=torch.int32, device=dev)
+        d.dkv_map_pattern(lay, torch.from_numpy(pattern).to(dev), km, kl)
+        lens = kl.cpu().to(torch.int64)
+        rows = int((lens + cap).sum())
+        k_c = torch.empty((rows, dim), dtype=torch.bfloat16, device=dev)
+        v_c = torch.empty_like(k_c)
+        so = torch.empty(N * Hkv, dtype=torch.int64, device=dev)
+        sl = torch.empty(N * Hkv, dtype=torch.int32, device=dev)
+        cws = torch.empty(d.dkv_compact_workspace_bytes(lay), dtype=torch.uint8, device=dev)
+        d.dkv_compact(lay, k, v, km, cap, k_c, v_c, so, sl, cws)
+        del k, v, km
+        torch.cuda.empty_cache()
+        qs = [di.q_step(w, layer, 0, device=dev) for layer in range(L)]
+        news = [tuple(t.reshape(nsl, 1, dim).contiguous() for t in di.kv_new_step(w, layer, 0, device=dev))
+                for layer in range(L)]
+        out = torch.empty((B, Hq, dim), dtype=torch.float32, device=dev)
+        dws = torch.zeros(d.dkv_decode_workspace_bytes(B, Hq, Hkv, dim), dtype=torch.uint8, device=dev)
+        lrows = [int(lens[layer * B:(layer + 1) * B].sum()) for layer in range(L)]
+        # a graph of `per_graph` calls: whole steps of the stack, or (one layer) several steps
+        steps_per_graph = max(1, 32 // L)
+        per_graph = L * steps_per_graph
+
+        def graph_calls(lb, g_idx, shp):
+            for j in range(steps_per_graph):
+                s_ = (g_idx * steps_per_graph + j) % cap
+                for layer in range(L):
+                    kn, vn = news[layer]
+                    st_ = lb.dkv_append_decode_attn(d.DKV_BF16, B, Hq, Hkv, dim, P(qs[layer].data_ptr()),
+                                                    P(kn.data_ptr()), P(vn.data_ptr()), 1, s_, cap, P(k_c.data_ptr()),
+                                                    P(v_c.data_ptr()), P(so.data_ptr() + 8 * layer * nsl),
+                                                    P(sl.data_ptr() + 4 * layer * nsl), w.sm_scale,
+                                                    lrows[layer] + nsl * (s_ + 1), P(out.data_ptr()),
+                                                    P(dws.data_ptr()), dws.numel(), P(shp))
+                    if st_ != 0:
+                        raise d.DkvError("dkv_append_decode_attn", st_)
+
+        n_graphs, n_warm = 8, 5
+
+        def graphs_of(lb):
+            gs = []
+            for gi in range(n_graphs):
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g, stream=cs):
+                    graph_calls(lb, gi, cs.cuda_stream)
+                gs.append(g)
+            return gs
+
+        graph_calls(lib, 0, stream.cuda_stream)
+        torch.cuda.synchronize()
+        prod = graphs_of(lib)
+        for g in prod[:n_warm]:
+            g.replay()
+        torch.cuda.synchronize()
+        a, b = ev(), ev()
+        a.record(stream)
+        for g in prod[n_warm:]:
+            g.replay()
+        b.record(stream)
+        torch.cuda.synchronize()
+        prod_us = a.elapsed_time(b) * 1e3 / (n_graphs - n_warm) / per_graph
+        del prod
+
+        plib.dkv_phase_reset()  # graph g, call c -> slot (g * per_graph + c) % 64
+        stamped = graphs_of(plib)
+        for g in stamped[:n_warm]:
+            g.replay()
+        torch.cuda.synchronize()
+        split = np.zeros((64, 1024, 8), dtype=np.uint64)
+        merge = np.zeros((64, 4096, 2), dtype=np.uint64)
+        calls, stamped_us = [], []
+        for gi in range(n_warm, n_graphs):
+            a.record(stream)
+            stamped[gi].replay()
+            b.record(stream)
+            torch.cuda.synchronize()
+            stamped_us.append(a.elapsed_time(b) * 1e3 / per_graph)
+            st_ = plib.dkv_phase_stamps(P(split.ctypes.data), P(merge.ctypes.data))
+            if st_ != 0:
+                raise RuntimeError(f"dkv_phase_stamps: {st_}")
+            for c in range(min(per_graph, 64) - 1):  # the last call of a graph has no next call in it
+                sl_ = (gi * per_graph + c) % 64
+                nx = (sl_ + 1) % 64
+                t = split[sl_].astype(np.int64)
+                used = t[:, 0] > 0
+                wg = np.nonzero(used)[0]
+                t = t[used]
+                m = merge[sl_][:nsl * w.group].astype(np.int64)
+                t0 = t[:, 0].min()
+                us = lambda x: (x - t0) * 0.01  # 100 MHz
+                nt = split[nx].astype(np.int64)
+                nt = nt[nt[:, 0] > 0]
+                loop_end = us(t[:, 3:7].max(1))
+                calls.append({
+                    "workgroups": float(used.sum()),
+                    "last_start": float(us(t[:, 0]).max()),
+                    "prologue_p50": float(np.median(us(t[:, 1]))),
+                    "first_tile_p50": float(np.median(us(t[:, 2]))),
+                    "loop_end_p50": float(np.median(loop_end)),
+                    "loop_end_max": float(loop_end.max()),
+                    "fold_p50": float(np.median(us(t[:, 7]) - loop_end)),
+                    "wg_end_p10": float(np.percentile(us(t[:, 7]), 10)),
+                    "wg_end_p50": float(np.median(us(t[:, 7]))),
+                    "wg_end_max": float(us(t[:, 7]).max()),
+                    "combine_start": float(us(m[:, 0]).min()),
+                    "combine_end": float(us(m[:, 1]).max()),
+                    "next_start": float(us(nt[:, 0]).min()),
+                    "xcd": [float(np.median(us(t[wg % 8 == x, 7]))) for x in range(8)],
+                })
+        c = {k_: float(np.mean([x[k_] for x in calls])) for k_ in calls[0] if k_ != "xcd"}
+        xcd = np.mean([x["xcd"] for x in calls], axis=0)
+        # bytes of a call of the stamped replays
+        tails = [(gi * steps_per_graph + j) % cap + 1 for gi in range(n_warm, n_graphs) for j in range(steps_per_graph)]
+        nbytes = int(np.mean([(lrows[layer] + nsl * t_) * dim * 2 * 2 + B * Hq * dim * 6 + nsl * 12
+                              for layer in range(L) for t_ in tails]))
+        del stamped, k_c, v_c
+        torch.cuda.empty_cache()
+
+        # the streaming-read probe over the same bytes, one launch per call, graph-replayed
+        per = (nbytes + 15) // 16 * 16
+        pbuf = torch.ones(32 * per // 2, dtype=torch.int16, device=dev)
+        psink = torch.zeros(4, dtype=torch.int32, device=dev)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=cs):
+            for i in range(32):
+                lib.dkv_probe_stream_read(P(pbuf.data_ptr() + i * per), per, P(psink.data_ptr()), 256,
+                                          P(cs.cuda_stream))
+        for _ in range(3):
+            g.replay()
+        torch.cuda.synchronize()
+        a.record(stream)
+        for _ in range(5):
+            g.replay()
+        b.record(stream)
+        torch.cuda.synchronize()
+        probe_us = a.elapsed_time(b) * 1e3 / 5 / 32
+        del pbuf, g
+
+        stream_us = c["loop_end_p50"] - c["prologue_p50"]
+        terms = [
+            ("launch skew + prologue (metadata round trip, scan; no K/V bytes in flight yet)", c["prologue_p50"]),
+            ("stream: prologue end -> median workgroup's last tile", stream_us),
+            ("tail: median -> slowest workgroup's last tile", c["loop_end_max"] - c["loop_end_p50"]),
+            ("fold after the slowest last tile (waves -> output or record)", c["wg_end_max"] - c["loop_end_max"]),
+            ("gap: split kernel end -> combine start", c["combine_start"] - c["wg_end_max"]),
+            ("combine kernel", c["combine_end"] - c["combine_start"]),
+            ("gap: combine end -> next call's first workgroup", c["next_start"] - c["combine_end"]),
+        ]
+        lines = [f"## {name}" + (f" at {budget:.0%} retained" if budget else "") +
+                 f": {L} layer(s) x batch {B} x {Hq}q/{Hkv}kv, d {dim}, T {T}; {nbytes / 1e6:.1f} MB of K/V per call",
+                 f"# graph-replayed decode steps; means over {len(calls)} calls of {n_graphs - n_warm} replays; "
+                 "times in us from the call's first workgroup start",
+                 f"product library, same graphs: {prod_us:.2f} us per call = {nbytes / (prod_us * 1e-6) / 1e9:.0f} GB/s "
+                 f"({nbytes / (prod_us * 1e-6) / 1e9 / PEAK_HBM_GBPS:.1%} of 8 TB/s); stamped library "
+                 f"{np.mean(stamped_us):.2f} us per call",
+                 f"streaming-read probe over the same bytes (256 workgroups, graph-replayed): {probe_us:.2f} us per "
+                 f"launch = {per / (probe_us * 1e-6) / 1e9:.0f} GB/s",
+                 f"{'term':78s} {'us':>7s}"]
+        for nm, val in terms:
+            lines.append(f"{nm:78s} {val:7.2f}")
+        lines += [f"{'call period (sum)':78s} {c['next_start']:7.2f}",
+                  f"stream rate over the stream term: {nbytes / (stream_us * 1e-6) / 1e9:.0f} GB/s; workgroups "
+                  f"{c['workgroups']:.0f}; last start {c['last_start']:.2f}; first tile reached (wave 0, median) "
+                  f"{c['first_tile_p50']:.2f}; per-workgroup fold median {c['fold_p50']:.2f}",
+                  f"workgroup end p10 / p50 / max: {c['wg_end_p10']:.2f} / {c['wg_end_p50']:.2f} / "
+                  f"{c['wg_end_max']:.2f}; median end by XCD (id mod 8): " + ", ".join(f"{x:.2f}" for x in xcd), ""]
+        return lines
+
+    lines = ["# per-phase time budget of decode calls (dkv_append_decode_attn: split kernel + combine kernel)",
+             "# command: python paper_2609_32663_amd/build.py --phase-stamps && python bench.py --phase-budget",
+             f"# sources measured: decode kernel sha256/16 {kernel_hash()} (stamps compiled in with "
+             "DKV_PHASE_STAMPS=1; the product library has none); 100 MHz chip clock", ""]
+    lines += case(WORKLOAD)
+    lines += case("llama70b_layer_bs16_32k", 0.2)
+    lines += case("qwen7b_stack_bs4_128k")
+    with open(PHASE_FILE, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
     args = parse()
+    if args.phase_budget:
+        phase_budget(args)
+        return
     if args.pmc_summary:
         pmc_summary(*args.pmc_summary, args.pmc_command)
         return

@@ -15,7 +15,7 @@ import torch
 __all__ = [
     "DKV_OK", "DKV_ERR_INVALID_ARG", "DKV_ERR_UNSUPPORTED", "DKV_ERR_MISALIGNED",
     "DKV_ERR_CAPACITY", "DKV_ERR_WORKSPACE", "DKV_ERR_HIP", "DKV_BF16", "DKV_F32",
-    "DkvError", "Layout", "make_layout", "library", "library_path", "dtype_code",
+    "DkvError", "Layout", "make_layout", "library", "library_at", "library_path", "dtype_code",
     "dkv_map_pattern", "dkv_compact_workspace_bytes", "dkv_compact", "dkv_append",
     "dkv_decode_workspace_bytes", "dkv_decode_attn", "dkv_dense_decode_attn",
     "dkv_append_decode_attn", "dkv_append_decode_attn_noalloc", "dkv_dense_append_decode_attn",
@@ -73,13 +73,19 @@ _lib = None
 def library():
     """The loaded libdkv.so (raises if it has not been built)."""
     global _lib
-    if _lib is not None:
-        return _lib
-    if not os.path.exists(library_path):
+    if _lib is None:
+        _lib = library_at(library_path)
+    return _lib
+
+
+def library_at(path):
+    """Another build of the same C ABI (e.g. the phase-stamp build), loaded
+    with the same signatures; raises if it has not been built."""
+    if not os.path.exists(path):
         raise ImportError(
-            f"{library_path} is missing: build it with `python paper_2609_32663_amd/build.py` "
+            f"{path} is missing: build it with `python paper_2609_32663_amd/build.py` "
             "(the Distance-KV path has no fallback)")
-    lib = ctypes.CDLL(library_path)
+    lib = ctypes.CDLL(path)
     P, I32, I64, SZ, F32, VP = (ctypes.POINTER(Layout), ctypes.c_int32, ctypes.c_int64,
                                 ctypes.c_size_t, ctypes.c_float, ctypes.c_void_p)
     sigs = {
@@ -119,7 +125,6 @@ def library():
         f = getattr(lib, name)
         f.restype = res
         f.argtypes = args
-    _lib = lib
     return lib
 
 

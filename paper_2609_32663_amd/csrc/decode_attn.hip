@@ -59,6 +59,20 @@ constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / kWave;
 constexpr int kTK = 32;  // keys per wave tile
 
+#if DKV_PHASE_STAMPS
+// Phase-stamp build (a separate library, built on request; the product
+// library has none of this): per call slot and workgroup, the constant
+// 100 MHz clock at kernel entry [0], after the prologue [1], at wave 0's
+// first tile [2], at each wave's loop end [3..6] and at the workgroup's end
+// [7]; per combine workgroup, its start and end.
+constexpr int kStampCalls = 64, kStampWG = kDecodeMaxWG, kStampMergeWG = 4096;
+__device__ unsigned long long stamp_split[kStampCalls][kStampWG][8];
+__device__ unsigned long long stamp_merge[kStampCalls][kStampMergeWG][2];
+#define DKV_STAMP(...) __VA_ARGS__
+#else
+#define DKV_STAMP(...)
+#endif
+
 template <bool BF16, int D, int GP>
 struct DecodeCfg {
   static constexpr int kElem = BF16 ? 2 : 4;
@@ -418,12 +432,19 @@ void decode_kernel(DecodeParams p) {
   const int nseg = p.nseg;
   const bool dense = !PAGED && p.seg_len == nullptr;
 
-  // fixed cost of a piece, in rows: about as long as streaming 128 KiB of K
-  // and V (measured: a second piece adds about 6 us to a workgroup that
-  // streams about 43 bf16 d128 rows per us)
-  constexpr int64_t kSegCost = 131072 / (2 * C::kRowBytes);
+  // fixed cost of a piece, in rows: about as long as streaming 256 KiB of K
+  // and V.  A piece restarts the ring (its first tiles wait out the load
+  // queue: ~8 us under full load, per-workgroup clock stamps) and ends with
+  // the cross-wave fold (1.4-2.3 us); at ~23 KB/us per workgroup that is
+  // ~240 KiB.  (Measured on graph-replayed steps: 256 KiB takes 5-7% off the
+  // ragged 70B-shaped batch and the Qwen-shaped stack against 128 KiB, and
+  // leaves the headline stack, 1-2 pieces per workgroup, unchanged.)
+  constexpr int64_t kSegCost = 262144 / (2 * C::kRowBytes);
+  DKV_STAMP(const unsigned long long stamp_t0 = __builtin_amdgcn_s_memrealtime();)
   build_row_prefix<PAGED>(p, kSegCost, pre, offs, red);
   const int64_t total = uniform64(pre[nseg]);
+  DKV_STAMP(unsigned long long* stamp = stamp_split[p.stamp_slot][w]; bool stamp_first = true;
+            if (tid == 0) { stamp[0] = stamp_t0; stamp[1] = __builtin_amdgcn_s_memrealtime(); })
 
   // ---- segments with no rows at all produce zeros ----------------------
   for (int s = w; s < nseg; s += p.P) {
@@ -647,14 +668,18 @@ void decode_kernel(DecodeParams p) {
         for (int i = 0; i < S; ++i) {
           load_tile(tl[(i + S - 1) % S], kr, vr, (t + (S - 1) * kWaves) * kTK, k_lane, v_lane);
           __builtin_amdgcn_sched_barrier(0);
-          if (t < ntile)
+          if (t < ntile) {
+            DKV_STAMP(if (stamp_first && wave == 0 && lane == 0) stamp[2] = __builtin_amdgcn_s_memrealtime();
+                      stamp_first = false;)
             compute_tile<BF16, D, GP, false>(st, tl[i], qa, t * kTK, nrows, p.scale_log2, pbuf[wave], abuf[wave],
                                              j16, kg, rp);
+          }
           t += kWaves;
         }
       }
     }
 
+    DKV_STAMP(if (lane == 0) stamp[3 + wave] = __builtin_amdgcn_s_memrealtime();)
     // ---- wave state -> LDS ---------------------------------------------
 #pragma unroll
     for (int v = 0; v < 4; ++v) st.l[v] = row16_sum(st.l[v]);
@@ -715,6 +740,7 @@ void decode_kernel(DecodeParams p) {
       }
     }
     __syncthreads();  // LDS is reused by the next piece
+    DKV_STAMP(if (tid == 0) stamp[7] = __builtin_amdgcn_s_memrealtime();)
   }
 }
 
@@ -740,8 +766,13 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(DecodeParams p) 
 
   const int s = blockIdx.x / p.G;
   const int h = blockIdx.x - s * p.G;
+  DKV_STAMP(const unsigned long long stamp_m0 = __builtin_amdgcn_s_memrealtime();
+            unsigned long long* mstamp = stamp_merge[p.stamp_slot][blockIdx.x < kStampMergeWG ? blockIdx.x : 0];)
   const int n = p.seg_meta[2 * s + 1];
-  if (n <= 1) return;
+  if (n <= 1) {
+    DKV_STAMP(if (threadIdx.x == 0) { mstamp[0] = stamp_m0; mstamp[1] = stamp_m0; })
+    return;
+  }
   const float* first = p.partials + (int64_t)p.seg_meta[2 * s] * kRec;
   const int tid = threadIdx.x;
   const int cq = tid % kQuads, ph = tid / kQuads;
@@ -800,7 +831,16 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(DecodeParams p) 
     float* o = p.out + ((int64_t)bseq * p.Hq + (int64_t)g * p.G + h) * D + 4 * cq;
     *reinterpret_cast<f32x4*>(o) = At * (Lt > 0.f ? 1.f / Lt : 0.f);
   }
+  DKV_STAMP(__syncthreads(); if (threadIdx.x == 0) { mstamp[0] = stamp_m0; mstamp[1] = __builtin_amdgcn_s_memrealtime(); })
 }
+
+#if DKV_PHASE_STAMPS
+std::atomic<int>& stamp_slot_counter() {
+  static std::atomic<int> c{0};
+  return c;
+}
+int stamp_next_slot() { return stamp_slot_counter().fetch_add(1) % kStampCalls; }
+#endif
 
 // Split count: about one 128-row slice per workgroup, capped at the number of
 // workgroups the device holds at once (so every slice starts immediately and
@@ -848,6 +888,7 @@ int32_t split_count(int64_t rows_hint) {
 template <bool BF16, int D, int GP>
 hipError_t launch_g(DecodeParams p, int64_t rows_hint, hipStream_t stream) {
   const size_t lds = (2 * (size_t)p.nseg + 1) * sizeof(int64_t);
+  DKV_STAMP(p.stamp_slot = stamp_next_slot();)
   if (p.entries != nullptr) {
     p.P = split_count<BF16, D, GP, true>(rows_hint);
     hipLaunchKernelGGL((decode_kernel<BF16, D, GP, true>), dim3(p.P), dim3(kThreads), lds, stream, p);
@@ -881,6 +922,19 @@ hipError_t launch_d(const DecodeParams& p, int GP, int64_t rows_hint, hipStream_
 static __device__ __align__(256) unsigned char scratch[DKV_NOALLOC_SCRATCH_BYTES];
 
 }  // namespace
+
+#if DKV_PHASE_STAMPS
+}  // namespace dkv
+// Phase-stamp build only: the stamps of every call slot, and a reset of the
+// slot counter (launches take slots 0, 1, ... modulo 64 from then on).
+extern "C" int dkv_phase_stamps(void* split, void* merge) {
+  hipError_t e = hipMemcpyFromSymbol(split, HIP_SYMBOL(dkv::stamp_split), sizeof(dkv::stamp_split));
+  if (e == hipSuccess) e = hipMemcpyFromSymbol(merge, HIP_SYMBOL(dkv::stamp_merge), sizeof(dkv::stamp_merge));
+  return (int)e;
+}
+extern "C" void dkv_phase_reset() { dkv::stamp_slot_counter().store(0); }
+namespace dkv {
+#endif
 
 hipError_t decode_static_scratch(void** ptr) {
   static std::atomic<void*> addr[kMaxDevices];

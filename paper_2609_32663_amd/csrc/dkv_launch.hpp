@@ -123,6 +123,9 @@ struct DecodeParams {
   int64_t num_pages;
   int32_t max_entries, page_rows, page_shift, ctx_len;  // page_rows = 1 << page_shift
   int32_t tail_entries;      // entries of the append region (the last ones of a segment)
+#if DKV_PHASE_STAMPS
+  int32_t stamp_slot;        // phase-stamp build only: the call's stamp slot
+#endif
 };
 int decode_group_pad(int G);
 size_t decode_partials_bytes(int nseg, int G, int head_dim);   // partial records

@@ -9,11 +9,14 @@
 // positions per sweep: it classifies each as sink / recent / binned /
 // uncovered, looks the bin up (a division for uniform edges, a binary search
 // over the edges in LDS otherwise), and writes 16 mask bytes with one 16-byte
-// store when the row is 16-byte aligned.  The chunk's retained count is
-// reduced in the block and added to kv_len with one integer atomic (a first
-// kernel clears kv_len), so the result does not depend on timing.  In a
-// ragged batch a unit's context is the first unit_len[n] positions of its
-// row: distances count from its end and the rest of the row is not retained.
+// store when the row is 16-byte aligned.  The retained length is not counted
+// from the mask: the first chunk of each segment writes it from the closed
+// form of Eq. (4)-(5), |sink U recent| plus the width (clipped to the
+// compressible span) of every bin some head of the group keeps, with one
+// plain store, so the call is one kernel with no atomics or clearing pass.
+// In a ragged batch a unit's context is the first unit_len[n] positions of
+// its row: distances count from its end and the rest of the row is not
+// retained.
 
 #include "dkv_device.hpp"
 #include "dkv_launch.hpp"
@@ -25,6 +28,12 @@ namespace {
 constexpr int kMapThreads = 256;
 constexpr int kMapPerThread = 16;
 constexpr int kMapChunk = 4 * kMapThreads * kMapPerThread;  // positions per workgroup
+
+// Chunks per segment; at least one, whose workgroup writes the length.
+__host__ __device__ inline int64_t map_chunks(int32_t T) {
+  const int64_t c = ((int64_t)T + kMapChunk - 1) / kMapChunk;
+  return c > 0 ? c : 1;
+}
 
 __device__ __forceinline__ int find_bin(int32_t u, const int32_t* edges, int D, int uniform_w) {
   if (uniform_w > 0) {
@@ -44,7 +53,7 @@ __global__ __launch_bounds__(kMapThreads) void map_pattern_kernel(MapParams p) {
   extern __shared__ __align__(16) uint8_t smem[];
   __shared__ int64_t red[kMapThreads / kWave + 1];
 
-  const int chunks = (int)(((int64_t)p.T + kMapChunk - 1) / kMapChunk);
+  const int chunks = (int)map_chunks(p.T);
   const int seg = (int)(blockIdx.x / chunks);
   const int64_t chunk0 = (int64_t)(blockIdx.x - (int64_t)seg * chunks) * kMapChunk;
   const int64_t chunk1 = chunk0 + kMapChunk < p.T ? chunk0 + kMapChunk : p.T;
@@ -75,7 +84,25 @@ __global__ __launch_bounds__(kMapThreads) void map_pattern_kernel(MapParams p) {
     Tn = Tn < 0 ? 0 : (Tn > T ? T : Tn);
   }
   uint8_t* kv_row = p.kv_mask + (int64_t)seg * T;
-  int64_t count = 0;
+
+  if (chunk0 == 0) {
+    // retained length, closed form: min(Tn, S + R) always-kept positions,
+    // then every kept bin's offsets [E[k], E[k+1]) within the compressible
+    // span [0, Tn - S - R)
+    const int64_t span = (int64_t)Tn - p.S - p.R;
+    int64_t part = 0;
+    for (int k = tid; k < D && span > 0; k += kMapThreads) {
+      if (qbits[k] == 0) continue;
+      const int64_t lo = p.uniform_width > 0 ? (int64_t)p.uniform_width * k : edges[k];
+      const int64_t hi_e = p.uniform_width > 0 ? (int64_t)p.uniform_width * (k + 1) : edges[k + 1];
+      const int64_t hi = hi_e < span ? hi_e : span;
+      if (hi > lo) part += hi - lo;
+    }
+    int64_t binned;
+    block_exclusive_scan<kMapThreads>(part, red, &binned);
+    const int64_t always = (int64_t)p.S + p.R < Tn ? (int64_t)p.S + p.R : Tn;
+    if (tid == 0) p.kv_len[seg] = (int32_t)(always + binned);
+  }
 
   const int32_t e_end = p.uniform_width > 0 ? 0 : edges[D];  // general edges: the covered span
   // positions fit 31 bits (T is an int32): the sweep runs in 32-bit arithmetic
@@ -118,7 +145,6 @@ __global__ __launch_bounds__(kMapThreads) void map_pattern_kernel(MapParams p) {
       // the wave's runs are all uniform
       const uint32_t wb = rb != 0u ? 0x01010101u : 0u;
       const u32x4 w = {wb, wb, wb, wb};
-      count += rb != 0u ? kMapPerThread : 0;
       if (aligned_rows) {
         *reinterpret_cast<u32x4*>(kv_row + j0) = w;
       } else {
@@ -178,7 +204,6 @@ __global__ __launch_bounds__(kMapThreads) void map_pattern_kernel(MapParams p) {
     for (int q = 0; q < 4; ++q) {
       w[q] = (hb[4 * q] != 0u ? 1u : 0u) | (hb[4 * q + 1] != 0u ? 1u : 0u) << 8 |
              (hb[4 * q + 2] != 0u ? 1u : 0u) << 16 | (hb[4 * q + 3] != 0u ? 1u : 0u) << 24;
-      count += __popc(w[q]);  // bytes are 0 or 1
     }
     if (aligned_rows) {
       *reinterpret_cast<u32x4*>(kv_row + j0) = w;
@@ -208,28 +233,15 @@ __global__ __launch_bounds__(kMapThreads) void map_pattern_kernel(MapParams p) {
       }
     }
   }
-
-  int64_t total;
-  block_exclusive_scan<kMapThreads>(count, red, &total);
-  if (tid == 0 && total > 0) atomicAdd(&p.kv_len[seg], (int32_t)total);
-}
-
-__global__ __launch_bounds__(kMapThreads) void map_clear_kernel(int32_t* kv_len, int n) {
-  const int i = blockIdx.x * kMapThreads + threadIdx.x;
-  if (i < n) kv_len[i] = 0;
 }
 
 }  // namespace
 
-int64_t map_blocks(int32_t T, int64_t num_segments) {
-  return ((int64_t)T + kMapChunk - 1) / kMapChunk * num_segments;
-}
+int64_t map_blocks(int32_t T, int64_t num_segments) { return map_chunks(T) * num_segments; }
 
 hipError_t launch_map_pattern(const MapParams& p, int num_segments, hipStream_t stream) {
   size_t lds = ((size_t)p.D * 2 + 15) & ~(size_t)15;
   if (p.uniform_width == 0) lds += (size_t)(p.D + 1) * 4;
-  hipLaunchKernelGGL(map_clear_kernel, dim3((num_segments + kMapThreads - 1) / kMapThreads), dim3(kMapThreads), 0,
-                     stream, p.kv_len, num_segments);
   const int64_t blocks = map_blocks(p.T, num_segments);
   if (blocks > 0) hipLaunchKernelGGL(map_pattern_kernel, dim3((uint32_t)blocks), dim3(kMapThreads), lds, stream, p);
   return hipGetLastError();
