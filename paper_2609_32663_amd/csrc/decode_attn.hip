@@ -84,7 +84,12 @@ struct DecodeCfg {
   static constexpr int kRPT = kTK / kRP;           // V rows per lane per tile
   static constexpr int kKG = kTK / 16;             // 16-key groups per tile
   static constexpr int kRec = GP * (D + 2);        // floats per partial record
-  static constexpr int kMergeChunk = kWaves * D;   // pieces per merge pass (weights fit in wacc)
+  // Row-phase partial accumulators each wave leaves in LDS for the fold: all
+  // kRP of them, or fewer (summed across lanes first) when the partials of
+  // all waves would pass 64 KiB.
+  static constexpr int kRPK =
+      (kWaves * kRP * GP * D * 4 <= 65536) ? kRP : (kWaves * (kRP / 2) * GP * D * 4 <= 65536 ? kRP / 2 : kRP / 4);
+  static_assert(kRPK >= 1 && kWaves * kRPK * GP * D * 4 <= 65536, "fold partials must fit 64 KiB of LDS");
   static constexpr int64_t kSubRows = (1LL << 30) / kRowBytes;  // rows per buffer descriptor
   static_assert(kTK % kRP == 0, "tile must cover whole row phases");
 };
@@ -116,8 +121,14 @@ __device__ __forceinline__ void widen16(const u32x4& w, float* out) {
 
 // Workgroup that owns flat row x when `total` rows are cut into P slices
 // [floor(w*total/P), floor((w+1)*total/P)).
+// The quotient comes from an fp64 division (the numerator is below 2^53) and
+// is corrected by one where rounding crossed an integer; a 64-bit integer
+// division is a long emulated sequence.
 __device__ __forceinline__ int64_t owner_of(int64_t x, int64_t total, int64_t P) {
-  const int64_t w = ((x + 1) * P - 1) / total;
+  const int64_t num = (x + 1) * P - 1;
+  int64_t w = (int64_t)((double)num / (double)total);
+  if (w * total > num) --w;
+  else if ((w + 1) * total <= num) ++w;
   return w < P - 1 ? w : P - 1;
 }
 
@@ -420,7 +431,7 @@ void decode_kernel(DecodeParams p) {
   int64_t* offs = pre + p.nseg + 1;
   __shared__ __align__(16) float pbuf[kWaves][kTK][GP];   // probabilities per wave tile
   __shared__ __align__(16) float abuf[kWaves][GP];        // rescale factors per wave
-  __shared__ __align__(16) float wacc[kWaves][GP][D];     // per-wave accumulators
+  __shared__ __align__(16) float wacc[kWaves][C::kRPK][GP][D];  // per-wave row-phase partial accumulators
   __shared__ float wm[kWaves][GP];
   __shared__ float wl[kWaves][GP];
   __shared__ int64_t red[kWaves + 1];
@@ -681,19 +692,25 @@ void decode_kernel(DecodeParams p) {
 
     DKV_STAMP(if (lane == 0) stamp[3 + wave] = __builtin_amdgcn_s_memrealtime();)
     // ---- wave state -> LDS ---------------------------------------------
+    // Every lane's accumulators are partial sums over its row phase; they go
+    // to LDS as they are (a cross-lane sum first only where the partials of
+    // all waves would not fit), and the fold below adds them up.  (Summing
+    // all row phases with lane swaps first cost ~0.5 us more per piece.)
 #pragma unroll
     for (int v = 0; v < 4; ++v) st.l[v] = row16_sum(st.l[v]);
-#pragma unroll
-    for (int h = 0; h < GP; ++h)
-#pragma unroll
-      for (int c = 0; c < C::kCPL; ++c) {
-        st.acc[h][c] = lane_xor_sum<C::kLPR>(st.acc[h][c]);
-      }
-    if (rp == 0) {
+    if constexpr (C::kRPK < C::kRP) {
 #pragma unroll
       for (int h = 0; h < GP; ++h)
 #pragma unroll
-        for (int c = 0; c < C::kCPL; ++c) wacc[wave][h][cc * C::kCPL + c] = st.acc[h][c];
+        for (int c = 0; c < C::kCPL; ++c) st.acc[h][c] = lane_xor_sum<C::kRPK * C::kLPR>(st.acc[h][c]);
+    }
+    if (rp < C::kRPK) {
+#pragma unroll
+      for (int h = 0; h < GP; ++h)
+#pragma unroll
+        for (int c4 = 0; c4 < C::kCPL; c4 += 4)
+          *reinterpret_cast<f32x4*>(&wacc[wave][rp][h][cc * C::kCPL + c4]) =
+              f32x4{st.acc[h][c4], st.acc[h][c4 + 1], st.acc[h][c4 + 2], st.acc[h][c4 + 3]};
     }
     if (j16 == 0 && 4 * kg < GP) {
 #pragma unroll
@@ -716,23 +733,28 @@ void decode_kernel(DecodeParams p) {
     }
     float* rec = p.partials + (int64_t)(w + s) * C::kRec;
     float* outp = p.out + ((int64_t)bseq * p.Hq + (int64_t)g * p.G) * D;
-    for (int idx = tid; idx < p.G * D; idx += kThreads) {
-      const int h = idx / D, c = idx - (idx / D) * D;
+    // thread -> (head h, columns 4 c4 .. 4 c4 + 3)
+    for (int idx = tid; idx < p.G * (D / 4); idx += kThreads) {
+      const int h = idx / (D / 4), c = 4 * (idx - h * (D / 4));
       float M = wm[0][h];
 #pragma unroll
       for (int q = 1; q < kWaves; ++q) M = fmaxf(M, wm[q][h]);
       const float Mu = M == -INFINITY ? 0.f : M;
-      float L = 0.f, A = 0.f;
+      float L = 0.f;
+      f32x4 A = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int q = 0; q < kWaves; ++q) {
         const float f = fast_exp2(wm[q][h] - Mu);
         L += f * wl[q][h];
-        A += f * wacc[q][h][c];
+        f32x4 part = *reinterpret_cast<const f32x4*>(&wacc[q][0][h][c]);
+#pragma unroll
+        for (int r = 1; r < C::kRPK; ++r) part += *reinterpret_cast<const f32x4*>(&wacc[q][r][h][c]);
+        A += f * part;
       }
       if (single) {
-        outp[idx] = L > 0.f ? A / L : 0.f;
+        *reinterpret_cast<f32x4*>(outp + h * D + c) = A * (L > 0.f ? 1.f / L : 0.f);
       } else {
-        rec[2 * GP + h * D + c] = A;
+        *reinterpret_cast<f32x4*>(rec + 2 * GP + h * D + c) = A;
         if (c == 0) {
           rec[h] = M;
           rec[GP + h] = L;
