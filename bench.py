@@ -43,6 +43,8 @@ KERNEL_SRCS = [os.path.join(ROOT, "paper_2609_32663_amd", "csrc", f)
                for f in ("decode_attn.hip", "dkv_device.hpp", "dkv_launch.hpp")]
 QUERY_SRCS = [os.path.join(ROOT, "paper_2609_32663_amd", "csrc", f)
               for f in ("query_attn.hip", "dkv_device.hpp", "dkv_query.hpp")]
+COMPACT_SRCS = [os.path.join(ROOT, "paper_2609_32663_amd", "csrc", f)
+                for f in ("compact.hip", "dkv_device.hpp", "dkv_launch.hpp")]
 
 
 def parse():
@@ -64,6 +66,10 @@ def parse():
     ap.add_argument("--phase-budget", action="store_true",
                     help="per-phase time budget of the headline call from the phase-stamp build "
                          "(python paper_2609_32663_amd/build.py --phase-stamps first); writes the profile")
+    ap.add_argument("--query-counters", nargs=3, metavar=("SQ_CSV", "TRACE_DIR", "BENCH_LOG"),
+                    help="summarise a rocprofv3 --pmc run of this script with GRBM_GUI_ACTIVE, "
+                         "SQ_VALU_MFMA_BUSY_CYCLES, SQ_INSTS_VALU_MFMA_MOPS_BF16 and SQ_BUSY_CYCLES, next to a "
+                         "kernel-trace run, into the query kernel's clock and matrix-unit profile")
     ap.add_argument("--pmc-command", default="",
                     help="command line recorded by --pmc-summary / --trace-summary")
     return ap.parse_args()
@@ -321,10 +327,89 @@ def pmc_summary(fetch_csv, write_csv, bench_log, command):
         res["query_traffic_bytes_per_call"] = int(q_bytes["fetch"] + q_bytes["write"])
     if len(per_paged) == 2:
         res["paged_traffic_bytes_per_launch"] = int(per_paged["fetch"] + per_paged["write"])
+    # the headline's timed one-time compaction: the second count / scan /
+    # gather triple of the run (the first is its warm-up call), against its
+    # algorithmic bytes (retained K and V rows read and written, mask read)
+    res["compact_kernel_sha256_16"] = kernel_hash(COMPACT_SRCS)
+    for key, path, counter in (("fetch", fetch_csv, "FETCH_SIZE"), ("write", write_csv, "WRITE_SIZE")):
+        rows = pmc_per_dispatch(path, counter)
+        calib = res[f"{key}_calibration"]
+        triples = [rows[i][1] + rows[i + 1][1] + rows[i + 2][1] for i in range(len(rows) - 2)
+                   if "compact_count_kernel" in rows[i][0] and "compact_scan_kernel" in rows[i + 1][0]
+                   and "compact_gather_kernel" in rows[i + 2][0]]
+        if len(triples) >= 2:
+            res[f"compact_{key}_bytes"] = int(triples[1] * 1024.0 * calib)
+    if "compact_fetch_bytes" in res and "compact_write_bytes" in res:
+        res["compact_traffic_bytes"] = res["compact_fetch_bytes"] + res["compact_write_bytes"]
+        oc = b.get("one_time", {})
+        if oc.get("compact_bytes"):
+            res["compact_algorithmic_bytes"] = oc["compact_bytes"]
+            res["compact_traffic_over_algorithmic"] = round(res["compact_traffic_bytes"] / oc["compact_bytes"], 4)
     with open(PMC_FILE, "w") as f:
         json.dump(res, f, indent=1)
         f.write("\n")
     print(json.dumps(res))
+
+
+QUERY_COUNTERS_FILE = os.path.join(ROOT, "profiles", "query_attn_counters_llama8b_stack_128k.txt")
+
+
+def query_counters(sq_csv, trace_dir, bench_log, command):
+    """Clock and matrix-unit use of the query-block attention kernel (d 128):
+    per dispatch, the GPU's busy cycles (GRBM_GUI_ACTIVE, the largest of its
+    instances), the cycles the matrix units were busy (summed over the 1,024
+    SIMDs) and the bf16 matrix operations issued, next to the kernel's mean
+    duration in a kernel-trace run of the same script."""
+    import csv
+    import statistics as st
+    per = {}
+    with open(sq_csv) as f:
+        for r in csv.DictReader(f):
+            if "query_attn_kernel<128>" not in r["Kernel_Name"]:
+                continue
+            i = int(r["Dispatch_Id"])
+            d_ = per.setdefault(i, {})
+            name, val = r["Counter_Name"], float(r["Counter_Value"])
+            if name.startswith("GRBM"):
+                d_[name] = max(d_.get(name, 0.0), val)
+            else:
+                d_[name] = d_.get(name, 0.0) + val
+    rows = [v for v in per.values() if len(v) == 4]
+    trace = [r for r in csv.DictReader(open(os.path.join(trace_dir, "run_kernel_trace.csv")))
+             if "query_attn_kernel<128>" in r["Kernel_Name"]]
+    dur_us = st.mean((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in trace)
+    b = last_json(bench_log)
+    qb = b["query_block"]
+    alg_flops = qb["tflop_per_step"] * 1e12 / b["config"]["layers"]
+    cyc = st.mean(r["GRBM_GUI_ACTIVE"] for r in rows)
+    mfma_busy = st.mean(r["SQ_VALU_MFMA_BUSY_CYCLES"] for r in rows)
+    sq_busy = st.mean(r["SQ_BUSY_CYCLES"] for r in rows)
+    issued = st.mean(r["SQ_INSTS_VALU_MFMA_MOPS_BF16"] for r in rows) * 512
+    clock = cyc / dur_us / 1e3
+    simds = 1024
+    lines = ["# query-block attention kernel (query_attn_kernel<128>, llama8b_stack_128k: 256 tokens after the "
+             "context, every layer): clock and matrix-unit counters",
+             f"# command: {command}",
+             f"# sources measured: query kernel sha256/16 {kernel_hash(QUERY_SRCS)}",
+             f"dispatches with all four counters: {len(rows)}; kernel-trace dispatches: {len(trace)}",
+             f"mean duration (kernel trace): {dur_us:.2f} us",
+             f"GRBM_GUI_ACTIVE per dispatch: {cyc:.0f} cycles -> effective clock {clock:.3f} GHz "
+             f"(the 2.5 PFLOP/s bf16 peak assumes 2.4 GHz)",
+             f"SQ_VALU_MFMA_BUSY_CYCLES: {mfma_busy:.0f} summed over {simds} SIMDs -> matrix units busy "
+             f"{mfma_busy / (cyc * simds):.1%} of the dispatch's cycles",
+             f"SQ_BUSY_CYCLES: {sq_busy:.0f}",
+             f"bf16 matrix operations issued (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512): {issued / 1e9:.1f} GFLOP per "
+             f"dispatch; algorithmic {alg_flops / 1e9:.1f} GFLOP per call (ratio {issued / alg_flops:.3f}: the bf16 "
+             "remainder products of P and masked key slots)",
+             f"issued rate {issued / (dur_us * 1e-6) / 1e12:.0f} TFLOP/s = {issued / (dur_us * 1e-6) / 1e12 / 2500:.1%} "
+             f"of 2.5 PFLOP/s, {issued / (dur_us * 1e-6) / 1e12 / (2500 * clock / 2.4):.1%} of the peak at the "
+             f"measured clock; algorithmic {alg_flops / (dur_us * 1e-6) / 1e12:.0f} TFLOP/s",
+             "",
+             f"JSON line of the counter run: query_block us_per_layer {qb['us_per_layer']}  roofline "
+             f"{json.dumps(qb['roofline'])}"]
+    with open(QUERY_COUNTERS_FILE, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
 
 
 def rel_err(got, want):
@@ -962,6 +1047,9 @@ def main():
         return
     if args.pmc_summary:
         pmc_summary(*args.pmc_summary, args.pmc_command)
+        return
+    if args.query_counters:
+        query_counters(*args.query_counters, args.pmc_command)
         return
     if args.trace_summary:
         trace_summary(*args.trace_summary, args.pmc_command)
@@ -1858,6 +1946,7 @@ def main():
                              "step": "per layer: dkv_decode_attn (attend only); HIP-graph replays",
                              **fam_res},
         "one_time": {"map_us": round(map_us, 1), "compact_us": round(compact_us, 1),
+                     "compact_bytes": int(compact_bytes),
                      "compact_gb_per_s": round(compact_bytes / (compact_us * 1e-6) / 1e9, 1),
                      # the same time priced as a pass that reads the whole dense cache and
                      # writes the retained rows (what a non-gathering pack would move)
