@@ -54,6 +54,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip the oracle timing (for profiler runs)")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the other configurations' rows (counter runs: rocprofv3 --pmc has crashed on the "
+                         "host in that section)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 1 GiB device copy (HBM-counter calibration)")
     ap.add_argument("--pmc-summary", nargs=3, metavar=("FETCH_CSV", "WRITE_CSV", "BENCH_LOG"),
@@ -66,10 +69,10 @@ def parse():
     ap.add_argument("--phase-budget", action="store_true",
                     help="per-phase time budget of the headline call from the phase-stamp build "
                          "(python paper_2609_32663_amd/build.py --phase-stamps first); writes the profile")
-    ap.add_argument("--query-counters", nargs=3, metavar=("SQ_CSV", "TRACE_DIR", "BENCH_LOG"),
-                    help="summarise a rocprofv3 --pmc run of this script with GRBM_GUI_ACTIVE, "
-                         "SQ_VALU_MFMA_BUSY_CYCLES, SQ_INSTS_VALU_MFMA_MOPS_BF16 and SQ_BUSY_CYCLES, next to a "
-                         "kernel-trace run, into the query kernel's clock and matrix-unit profile")
+    ap.add_argument("--query-counters", nargs=2, metavar=("SQ_DIR", "BENCH_LOG"),
+                    help="summarise a rocprofv3 run of this script with --kernel-trace and --pmc GRBM_GUI_ACTIVE "
+                         "SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_BUSY_CYCLES (csv output named "
+                         "run_*) into the query kernel's clock and matrix-unit profile")
     ap.add_argument("--pmc-command", default="",
                     help="command line recorded by --pmc-summary / --trace-summary")
     return ap.parse_args()
@@ -354,59 +357,56 @@ def pmc_summary(fetch_csv, write_csv, bench_log, command):
 QUERY_COUNTERS_FILE = os.path.join(ROOT, "profiles", "query_attn_counters_llama8b_stack_128k.txt")
 
 
-def query_counters(sq_csv, trace_dir, bench_log, command):
-    """Clock and matrix-unit use of the query-block attention kernel (d 128):
-    per dispatch, the GPU's busy cycles (GRBM_GUI_ACTIVE, the largest of its
-    instances), the cycles the matrix units were busy (summed over the 1,024
-    SIMDs) and the bf16 matrix operations issued, next to the kernel's mean
-    duration in a kernel-trace run of the same script."""
+def query_counters(sq_dir, bench_log, command):
+    """Clock and matrix-unit use of the query-block attention kernel (d 128)
+    from one rocprofv3 run with --pmc GRBM_GUI_ACTIVE SQ_VALU_MFMA_BUSY_CYCLES
+    SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_BUSY_CYCLES and --kernel-trace: per
+    dispatch, the GPU's busy cycles (GRBM_GUI_ACTIVE is reported summed over
+    the XCDs), the matrix units' busy cycles (summed over the SIMDs) and the
+    bf16 matrix operations issued, against the same dispatch's duration."""
     import csv
     import statistics as st
+    agent = next(r for r in csv.DictReader(open(os.path.join(sq_dir, "run_agent_info.csv")))
+                 if r["Agent_Type"] == "GPU")
+    xcc, simds, fmax = int(agent["Num_Xcc"]), int(agent["Simd_Count"]), float(agent["Max_Engine_Clk_Fcompute"])
     per = {}
-    with open(sq_csv) as f:
-        for r in csv.DictReader(f):
-            if "query_attn_kernel<128>" not in r["Kernel_Name"]:
-                continue
-            i = int(r["Dispatch_Id"])
-            d_ = per.setdefault(i, {})
-            name, val = r["Counter_Name"], float(r["Counter_Value"])
-            if name.startswith("GRBM"):
-                d_[name] = max(d_.get(name, 0.0), val)
-            else:
-                d_[name] = d_.get(name, 0.0) + val
-    rows = [v for v in per.values() if len(v) == 4]
-    trace = [r for r in csv.DictReader(open(os.path.join(trace_dir, "run_kernel_trace.csv")))
-             if "query_attn_kernel<128>" in r["Kernel_Name"]]
-    dur_us = st.mean((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in trace)
+    for r in csv.DictReader(open(os.path.join(sq_dir, "run_counter_collection.csv"))):
+        if "query_attn_kernel<128>" in r["Kernel_Name"]:
+            d_ = per.setdefault(int(r["Dispatch_Id"]), {})
+            d_[r["Counter_Name"]] = d_.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    dur = {int(r["Dispatch_Id"]): (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+           for r in csv.DictReader(open(os.path.join(sq_dir, "run_kernel_trace.csv")))
+           if "query_attn_kernel<128>" in r["Kernel_Name"]}
+    rows = [dict(v, us=dur[i]) for i, v in per.items() if len(v) == 4 and i in dur]
     b = last_json(bench_log)
     qb = b["query_block"]
     alg_flops = qb["tflop_per_step"] * 1e12 / b["config"]["layers"]
-    cyc = st.mean(r["GRBM_GUI_ACTIVE"] for r in rows)
-    mfma_busy = st.mean(r["SQ_VALU_MFMA_BUSY_CYCLES"] for r in rows)
-    sq_busy = st.mean(r["SQ_BUSY_CYCLES"] for r in rows)
-    issued = st.mean(r["SQ_INSTS_VALU_MFMA_MOPS_BF16"] for r in rows) * 512
-    clock = cyc / dur_us / 1e3
-    simds = 1024
+    us = st.mean(r["us"] for r in rows)
+    cyc = st.mean(r["GRBM_GUI_ACTIVE"] / xcc for r in rows)  # per XCD
+    clocks = sorted(r["GRBM_GUI_ACTIVE"] / xcc / r["us"] / 1e3 for r in rows)
+    busy = st.mean(r["SQ_VALU_MFMA_BUSY_CYCLES"] / (r["GRBM_GUI_ACTIVE"] / xcc * simds) for r in rows)
+    issued = st.mean(r["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512 for r in rows)
+    clock = st.mean(clocks)
+    rate = issued / (us * 1e-6) / 1e12
     lines = ["# query-block attention kernel (query_attn_kernel<128>, llama8b_stack_128k: 256 tokens after the "
              "context, every layer): clock and matrix-unit counters",
              f"# command: {command}",
              f"# sources measured: query kernel sha256/16 {kernel_hash(QUERY_SRCS)}",
-             f"dispatches with all four counters: {len(rows)}; kernel-trace dispatches: {len(trace)}",
-             f"mean duration (kernel trace): {dur_us:.2f} us",
-             f"GRBM_GUI_ACTIVE per dispatch: {cyc:.0f} cycles -> effective clock {clock:.3f} GHz "
-             f"(the 2.5 PFLOP/s bf16 peak assumes 2.4 GHz)",
-             f"SQ_VALU_MFMA_BUSY_CYCLES: {mfma_busy:.0f} summed over {simds} SIMDs -> matrix units busy "
-             f"{mfma_busy / (cyc * simds):.1%} of the dispatch's cycles",
-             f"SQ_BUSY_CYCLES: {sq_busy:.0f}",
+             f"# device: {xcc} XCDs, {simds} SIMDs, engine clock up to {fmax:.0f} MHz; dispatches with all four "
+             f"counters and a duration: {len(rows)} (counter collection runs the dispatches one at a time)",
+             f"duration per dispatch (same run): {us:.2f} us; GRBM_GUI_ACTIVE per XCD {cyc:.0f} cycles",
+             f"effective clock (busy cycles / duration): mean {clock:.3f} GHz, min {clocks[0]:.3f}, "
+             f"max {clocks[-1]:.3f}",
+             f"matrix units busy (SQ_VALU_MFMA_BUSY_CYCLES / (busy cycles x {simds} SIMDs)): {busy:.1%}",
              f"bf16 matrix operations issued (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512): {issued / 1e9:.1f} GFLOP per "
              f"dispatch; algorithmic {alg_flops / 1e9:.1f} GFLOP per call (ratio {issued / alg_flops:.3f}: the bf16 "
-             "remainder products of P and masked key slots)",
-             f"issued rate {issued / (dur_us * 1e-6) / 1e12:.0f} TFLOP/s = {issued / (dur_us * 1e-6) / 1e12 / 2500:.1%} "
-             f"of 2.5 PFLOP/s, {issued / (dur_us * 1e-6) / 1e12 / (2500 * clock / 2.4):.1%} of the peak at the "
-             f"measured clock; algorithmic {alg_flops / (dur_us * 1e-6) / 1e12:.0f} TFLOP/s",
+             "remainder products of P, and key slots past a row's causal limit)",
+             f"issued rate {rate:.0f} TFLOP/s = {rate / 2500:.1%} of 2.5 PFLOP/s (a {fmax / 1e3:.1f} GHz figure) and "
+             f"{rate / (2500 * clock / (fmax / 1e3)):.1%} of the peak at the measured clock; algorithmic "
+             f"{alg_flops / (us * 1e-6) / 1e12:.0f} TFLOP/s",
              "",
-             f"JSON line of the counter run: query_block us_per_layer {qb['us_per_layer']}  roofline "
-             f"{json.dumps(qb['roofline'])}"]
+             f"JSON line of the counter run (dispatches serialised by counter collection): query_block us_per_layer "
+             f"{qb['us_per_layer']}"]
     with open(QUERY_COUNTERS_FILE, "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
@@ -1830,10 +1830,12 @@ def main():
     del gp, gd
 
     # ---------------- the other configurations ---------------------------
-    log("other configurations: 8B layer at 32K, 70B-shaped batch, Qwen-shaped stack")
-    cfg_rows, cfg_calls = bench_configs({"d": d, "lib": lib, "dev": dev, "stream": stream, "args": args,
-                                         "oracle": None if args.no_cpu_baseline else __import__("oracle"),
-                                         "peak_hbm": PEAK_HBM_GBPS})
+    cfg_rows, cfg_calls = {}, []
+    if not args.no_configs:
+        log("other configurations: 8B layer at 32K, 70B-shaped batch, Qwen-shaped stack")
+        cfg_rows, cfg_calls = bench_configs({"d": d, "lib": lib, "dev": dev, "stream": stream, "args": args,
+                                             "oracle": None if args.no_cpu_baseline else __import__("oracle"),
+                                             "peak_hbm": PEAK_HBM_GBPS})
     for name_, r_ in cfg_rows.items():
         log(f"{name_}: " + json.dumps({k_: r_[k_] for k_ in r_ if k_ in ("us_per_step", "gb_per_s",
                                                                           "speedup_vs_dense")}))
