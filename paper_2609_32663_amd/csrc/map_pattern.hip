@@ -9,7 +9,11 @@
 // positions per sweep: it classifies each as sink / recent / binned /
 // uncovered, looks the bin up (a division for uniform edges, a binary search
 // over the edges in LDS otherwise), and writes 16 mask bytes with one 16-byte
-// store when the row is 16-byte aligned.  The retained length is not counted
+// store when the row is 16-byte aligned.  A run inside one region, or with one
+// bin edge inside it (its first b positions in one bin, the rest in the next),
+// is settled from its two ends; only runs that cross more (a region boundary,
+// or bins narrower than a run) go position by position, and then so does their
+// whole wave.  The retained length is not counted
 // from the mask: the first chunk of each segment writes it from the closed
 // form of Eq. (4)-(5), |sink U recent| plus the width (clipped to the
 // compressible span) of every bin some head of the group keeps, with one
@@ -113,8 +117,10 @@ __global__ __launch_bounds__(kMapThreads) void map_pattern_kernel(MapParams p) {
     // past the context): classify the run once and give every position the
     // same bits.  Runs across a boundary take the per-position path below.
     const int32_t jl = j0 + kMapPerThread - 1;
-    bool one = false;
-    uint32_t rb = 0;
+    bool one = false;   // every position of the run has the bits rb
+    bool two = false;   // one bin edge inside: the first b positions rb, the rest rl
+    uint32_t rb = 0, rl = 0;
+    int32_t b = kMapPerThread;
     if (j0 >= Tn) {
       one = true;  // past this unit's context: nothing retained
     } else if (jl < Tn) {
@@ -125,18 +131,27 @@ __global__ __launch_bounds__(kMapThreads) void map_pattern_kernel(MapParams p) {
       } else if (j0 >= p.S && dl >= p.R) {
         const int32_t u0 = d0 - p.R, ul = dl - p.R;  // u0 > ul >= 0
         if (p.uniform_width > 0) {
-          const int32_t k0 = u0 / p.uniform_width;
-          if (k0 == ul / p.uniform_width) {
+          const int32_t k0 = u0 / p.uniform_width, kl = ul / p.uniform_width;
+          rb = k0 < D ? qbits[k0] : 0u;
+          if (k0 == kl) {
             one = true;
-            rb = k0 < D ? qbits[k0] : 0u;
+          } else if (k0 == kl + 1) {
+            two = true;
+            rl = kl < D ? qbits[kl] : 0u;
+            b = u0 - k0 * p.uniform_width + 1;
           }
         } else if (ul >= e_end) {
           one = true;  // past the last edge: uncovered
         } else if (u0 < e_end) {
           const int k0 = find_bin(u0, edges, D, 0);
-          if (ul >= edges[k0]) {
+          const int32_t e0 = edges[k0];
+          rb = qbits[k0];
+          if (ul >= e0) {
             one = true;
-            rb = qbits[k0];
+          } else if (ul >= edges[k0 - 1]) {  // k0 >= 1 here: edges[0] = 0 <= ul
+            two = true;
+            rl = qbits[k0 - 1];
+            b = u0 - e0 + 1;
           }
         }
       }
@@ -163,6 +178,50 @@ __global__ __launch_bounds__(kMapThreads) void map_pattern_kernel(MapParams p) {
 #pragma unroll
             for (int e = 0; e < kMapPerThread; ++e)
               if (j0 + e < T) q_row[j0 + e] = qb;
+          }
+        }
+      }
+      continue;
+    }
+    if (__builtin_amdgcn_ballot_w64(!(one || two)) == 0) {
+      // every run of the wave has at most one bin edge inside it: the first b
+      // positions take rb, the others rl
+      if (one) {
+        rl = rb;
+        b = kMapPerThread;
+      }
+      u32x4 w;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        uint32_t x = 0;
+#pragma unroll
+        for (int e4 = 0; e4 < 4; ++e4) x |= ((4 * q + e4 < b ? rb : rl) != 0u ? 1u : 0u) << (8 * e4);
+        w[q] = x;
+      }
+      if (aligned_rows) {
+        *reinterpret_cast<u32x4*>(kv_row + j0) = w;
+      } else {
+#pragma unroll
+        for (int e = 0; e < kMapPerThread; ++e)
+          if (j0 + e < T) kv_row[j0 + e] = (e < b ? rb : rl) != 0u ? 1 : 0;
+      }
+      if (p.q_mask != nullptr) {
+        for (int h = 0; h < G; ++h) {
+          uint8_t* q_row = p.q_mask + ((int64_t)unit * p.Hq + (int64_t)g * G + h) * T;
+          if (aligned_rows) {
+            u32x4 wq;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              uint32_t x = 0;
+#pragma unroll
+              for (int e4 = 0; e4 < 4; ++e4) x |= (((4 * q + e4 < b ? rb : rl) >> h) & 1u) << (8 * e4);
+              wq[q] = x;
+            }
+            *reinterpret_cast<u32x4*>(q_row + j0) = wq;
+          } else {
+#pragma unroll
+            for (int e = 0; e < kMapPerThread; ++e)
+              if (j0 + e < T) q_row[j0 + e] = (uint8_t)(((e < b ? rb : rl) >> h) & 1u);
           }
         }
       }
