@@ -1836,9 +1836,12 @@ def main():
         cfg_rows, cfg_calls = bench_configs({"d": d, "lib": lib, "dev": dev, "stream": stream, "args": args,
                                              "oracle": None if args.no_cpu_baseline else __import__("oracle"),
                                              "peak_hbm": PEAK_HBM_GBPS})
+    shown = ("us_per_step", "gb_per_s", "speedup_vs_dense")
     for name_, r_ in cfg_rows.items():
-        log(f"{name_}: " + json.dumps({k_: r_[k_] for k_ in r_ if k_ in ("us_per_step", "gb_per_s",
-                                                                          "speedup_vs_dense")}))
+        row_ = {k_: r_[k_] for k_ in r_ if k_ in shown}
+        row_.update({k_: {j_: v_[j_] for j_ in v_ if j_ in shown} for k_, v_ in r_.items()
+                     if k_.startswith("budget_") and isinstance(v_, dict)})
+        log(f"{name_}: " + json.dumps(row_))
 
     # ---------------- achievable read bandwidth at this launch size -------
     # The streaming-read probe (same 16-byte non-temporal buffer loads as the

@@ -74,7 +74,6 @@ struct PageSelectParams {
   uint8_t* page_used;      // [nseg][pages_per_seg] or null
   int32_t* tile_cnt;       // [nseg][ntiles] runs starting in each tile (workspace)
   int32_t* tile_kept;      // [nseg][ntiles] retained positions per tile (workspace)
-  int32_t* tile_base;      // [nseg][ntiles] first entry of each tile (workspace)
   int32_t T, nseg, ntiles, page_rows, pages_per_seg, max_entries, cap;
 };
 size_t page_select_workspace_bytes(int64_t nseg, int64_t T);

@@ -133,7 +133,6 @@ dkv_status dkv_page_select(int32_t num_segments, int32_t context_len, int32_t ap
   p.page_used = page_used;
   p.tile_cnt = static_cast<int32_t*>(workspace);
   p.tile_kept = p.tile_cnt + n;
-  p.tile_base = p.tile_kept + n;
   p.T = context_len;
   p.nseg = num_segments;
   p.ntiles = (int32_t)ntiles;

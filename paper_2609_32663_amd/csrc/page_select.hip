@@ -9,16 +9,20 @@
 // page; decode reads those slots in place.  With the paper's 128-token bins
 // and 128-row pages every context entry is a whole page.
 //
-// Three passes over the (segment, 4096-position tile) grid, like the pack:
+// Two passes over the (segment, 4096-position tile) grid:
 //   count  each thread turns 16 mask bytes into a 16-bit keep mask; a run
 //          starts at a kept position whose predecessor is not kept or that
 //          opens a page; the tile sums its starts and kept positions;
-//   scan   one thread per segment turns tile counts into each tile's first
-//          entry, the segment's retained length and entry count, and writes
-//          the append region's entries (appended tokens are always kept);
-//   emit   each thread writes the entries whose runs start in its 16
-//          positions (page, logical page, lo) and the end slot of the runs
-//          that end there; a run's entry index is its start's rank.
+//   emit   each workgroup adds up the run counts of its segment's earlier
+//          tiles (its first entry), and each thread writes the entries whose
+//          runs start in its 16 positions (page, logical page, lo) and the
+//          end slot of the runs that end there; a run's entry index is its
+//          start's rank.  The segment's last tile also writes the retained
+//          length, the append region's entries (appended tokens are always
+//          kept) and the entry count.
+// (A separate scan pass, one thread per segment walking its tiles, took
+// ~20 us of dependent loads; the prefix inside emit is one round trip.)
+// A context of length 0 has no tile: one small kernel writes those segments.
 // Page sizes are multiples of 16 that divide the tile, so a page boundary is
 // always the boundary of a thread's 16 positions, and every wave's first
 // lane starts a page: neighbouring bits come from the adjacent lane.
@@ -79,22 +83,12 @@ __global__ __launch_bounds__(kThreads) void page_count_kernel(PageSelectParams p
   }
 }
 
-constexpr int kScanThreads = 256;
-
-__global__ __launch_bounds__(kScanThreads) void page_scan_kernel(PageSelectParams p) {
-  const int s = blockIdx.x * kScanThreads + threadIdx.x;
-  if (s >= p.nseg) return;
-  const int64_t base = (int64_t)s * p.ntiles;
-  int32_t run = 0, kept = 0;
-  for (int t = 0; t < p.ntiles; ++t) {
-    p.tile_base[base + t] = run;
-    run += p.tile_cnt[base + t];
-    kept += p.tile_kept[base + t];
-  }
-  p.seg_len[s] = kept;
-  // the append region [T, T + cap), one entry per page it touches
+// The append region [T, T + cap) of segment s: one entry per page it touches,
+// after the segment's n context entries; returns the segment's entry count.
+// Also marks those pages used and clears the flags of pages past the context
+// tiles that the region does not use.  One thread.
+__device__ int32_t finish_segment(const PageSelectParams& p, int s, int32_t n) {
   const int pr = p.page_rows;
-  int32_t n = run;
   if (p.cap > 0) {
     const int64_t first = (int64_t)p.T / pr, last = ((int64_t)p.T + p.cap - 1) / pr;
     for (int64_t lp = first; lp <= last; ++lp, ++n) {
@@ -111,9 +105,6 @@ __global__ __launch_bounds__(kScanThreads) void page_scan_kernel(PageSelectParam
       if (p.page_used != nullptr) p.page_used[(int64_t)s * p.pages_per_seg + lp] = 1;
     }
   }
-  p.n_entries[s] = n;
-  // pages past the count pass's tiles hold no context position: clear the
-  // ones the append region does not use
   if (p.page_used != nullptr) {
     const int64_t covered = (int64_t)p.ntiles * (kCompactTile / pr);
     const int64_t tail0 = p.cap > 0 ? (int64_t)p.T / pr : p.pages_per_seg;
@@ -121,16 +112,29 @@ __global__ __launch_bounds__(kScanThreads) void page_scan_kernel(PageSelectParam
     for (int64_t lp = covered; lp < p.pages_per_seg; ++lp)
       if (lp < tail0 || lp > tail1) p.page_used[(int64_t)s * p.pages_per_seg + lp] = 0;
   }
+  return n;
 }
 
 __global__ __launch_bounds__(kThreads) void page_emit_kernel(PageSelectParams p) {
   __shared__ int64_t red[kThreads / kWave + 1];
   const int tile = blockIdx.x;
   const int seg = blockIdx.y;
+  const bool last_tile = tile == p.ntiles - 1;
+  // runs that start in the segment's earlier tiles (low 32 bits: all its
+  // tiles' runs, needed by the last tile) and its retained positions
+  int64_t packed = 0, kept_part = 0;
+  for (int t = threadIdx.x; t < p.ntiles; t += kThreads) {
+    const int64_t c = p.tile_cnt[(int64_t)seg * p.ntiles + t];
+    packed += (t < tile ? (c << 32) : 0) + c;
+    if (last_tile) kept_part += p.tile_kept[(int64_t)seg * p.ntiles + t];
+  }
+  int64_t sums;
+  block_exclusive_scan<kThreads>(packed, red, &sums);
+  const int64_t before = sums >> 32, runs = sums & 0xFFFFFFFFLL;
   const RunBits r = run_bits(p, seg, tile);
   int64_t total;
   const int64_t rank = block_exclusive_scan<kThreads>(__popc(r.starts), red, &total);
-  const int64_t e0 = p.tile_base[(int64_t)seg * p.ntiles + tile] + rank;  // entry of this thread's first start
+  const int64_t e0 = before + rank;  // entry of this thread's first start
   const int64_t j0 = (int64_t)tile * kCompactTile + threadIdx.x * kPerThread;
   const int pr = p.page_rows;
   int32_t* ent = p.entries + (int64_t)seg * p.max_entries * 4;
@@ -157,23 +161,40 @@ __global__ __launch_bounds__(kThreads) void page_emit_kernel(PageSelectParams p)
     const int64_t j = j0 + b;
     if (idx < p.max_entries) ent[idx * 4 + 3] = (int32_t)(j - (j / pr) * pr + 1);
   }
+  if (last_tile) {
+    int64_t kept;
+    block_exclusive_scan<kThreads>(kept_part, red, &kept);
+    if (threadIdx.x == 0) {
+      p.seg_len[seg] = (int32_t)kept;
+      p.n_entries[seg] = finish_segment(p, seg, (int32_t)runs);
+    }
+  }
+}
+
+// Segments of a context of length 0: no retained position, only the append
+// region.
+__global__ __launch_bounds__(kThreads) void page_empty_kernel(PageSelectParams p) {
+  const int s = blockIdx.x * kThreads + threadIdx.x;
+  if (s >= p.nseg) return;
+  p.seg_len[s] = 0;
+  p.n_entries[s] = finish_segment(p, s, 0);
 }
 
 }  // namespace
 
 size_t page_select_workspace_bytes(int64_t nseg, int64_t T) {
   const int64_t ntiles = (T + kCompactTile - 1) / kCompactTile;
-  return (size_t)(3 * nseg * ntiles) * sizeof(int32_t);
+  return (size_t)(2 * nseg * ntiles) * sizeof(int32_t);
 }
 
 hipError_t launch_page_select(const PageSelectParams& p, hipStream_t stream) {
   if (p.nseg == 0) return hipSuccess;
-  if (p.ntiles > 0)
+  if (p.ntiles > 0) {
     hipLaunchKernelGGL(page_count_kernel, dim3(p.ntiles, p.nseg), dim3(kThreads), 0, stream, p);
-  hipLaunchKernelGGL(page_scan_kernel, dim3((p.nseg + kScanThreads - 1) / kScanThreads), dim3(kScanThreads), 0,
-                     stream, p);
-  if (p.ntiles > 0)
     hipLaunchKernelGGL(page_emit_kernel, dim3(p.ntiles, p.nseg), dim3(kThreads), 0, stream, p);
+  } else {
+    hipLaunchKernelGGL(page_empty_kernel, dim3((p.nseg + kThreads - 1) / kThreads), dim3(kThreads), 0, stream, p);
+  }
   return hipGetLastError();
 }
 

@@ -241,7 +241,7 @@ def test_query_validation():
 
 def test_page_select_validation():
     lib = d.library()
-    assert d.dkv_page_select_workspace_bytes(256, 131072) == 3 * 4 * 256 * 32
+    assert d.dkv_page_select_workspace_bytes(256, 131072) == 2 * 4 * 256 * 32
     assert d.dkv_page_select_workspace_bytes(-1, 10) == 0
     lay = _lay(T=131072, S=128, R=1024, edges=tuple(128 * k for k in range(1016)))
     # 1024 context pages + 1015 bins + sink + recent, and one page of the append region
@@ -269,7 +269,7 @@ def test_page_select_validation():
     assert call(mask=MIS) == d.DKV_ERR_MISALIGNED
     assert call(ent=MIS) == d.DKV_ERR_MISALIGNED
     assert call(ws=NUL) == d.DKV_ERR_WORKSPACE
-    assert call(ws_bytes=3 * 4 * 4 - 1) == d.DKV_ERR_WORKSPACE
+    assert call(ws_bytes=2 * 4 * 4 - 1) == d.DKV_ERR_WORKSPACE
     assert call(nseg=0, mask=NUL, table=NUL, ent=NUL, ne=NUL, sl=NUL, ws=NUL) == d.DKV_OK
 
 
