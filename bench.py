@@ -931,6 +931,7 @@ def phase_budget(args):
         split = np.zeros((64, 1024, 8), dtype=np.uint64)
         merge = np.zeros((64, 4096, 2), dtype=np.uint64)
         calls, stamped_us = [], []
+        rel_by_layer = {}  # layer -> per-call arrays of each workgroup's last tile minus the call's median
         for gi in range(n_warm, n_graphs):
             a.record(stream)
             stamped[gi].replay()
@@ -953,6 +954,9 @@ def phase_budget(args):
                 nt = split[nx].astype(np.int64)
                 nt = nt[nt[:, 0] > 0]
                 loop_end = us(t[:, 3:7].max(1))
+                rel = np.full(split.shape[1], np.nan)
+                rel[wg] = loop_end - np.median(loop_end)
+                rel_by_layer.setdefault(c % L, []).append(rel)
                 calls.append({
                     "workgroups": float(used.sum()),
                     "last_start": float(us(t[:, 0]).max()),
@@ -970,6 +974,10 @@ def phase_budget(args):
                     "xcd": [float(np.median(us(t[wg % 8 == x, 7]))) for x in range(8)],
                 })
         c = {k_: float(np.mean([x[k_] for x in calls])) for k_ in calls[0] if k_ != "xcd"}
+        # spread of the workgroups' last tiles within a call, and the part of it
+        # that stays with a workgroup over calls of the same layer
+        within = float(np.mean([np.nanstd(r) for v in rel_by_layer.values() for r in v]))
+        persist = float(np.mean([np.nanstd(np.nanmean(np.array(v), 0)) for v in rel_by_layer.values() if len(v) > 1]))
         xcd = np.mean([x["xcd"] for x in calls], axis=0)
         # bytes of a call of the stamped replays
         tails = [(gi * steps_per_graph + j) % cap + 1 for gi in range(n_warm, n_graphs) for j in range(steps_per_graph)]
@@ -1025,7 +1033,9 @@ def phase_budget(args):
                   f"{c['workgroups']:.0f}; last start {c['last_start']:.2f}; first tile reached (wave 0, median) "
                   f"{c['first_tile_p50']:.2f}; per-workgroup fold median {c['fold_p50']:.2f}",
                   f"workgroup end p10 / p50 / max: {c['wg_end_p10']:.2f} / {c['wg_end_p50']:.2f} / "
-                  f"{c['wg_end_max']:.2f}; median end by XCD (id mod 8): " + ", ".join(f"{x:.2f}" for x in xcd), ""]
+                  f"{c['wg_end_max']:.2f}; median end by XCD (id mod 8): " + ", ".join(f"{x:.2f}" for x in xcd),
+                  f"workgroups' last tiles within a call: std {within:.2f}; of which persistent (std over workgroups "
+                  f"of their mean over calls of the same layer): {persist:.2f}", ""]
         return lines
 
     lines = ["# per-phase time budget of decode calls (dkv_append_decode_attn: split kernel + combine kernel)",
