@@ -1516,12 +1516,12 @@ def main():
     topk_us = a.elapsed_time(b) * 1e3 / 20
     exported = pat_x.cpu().numpy()
     n_entries = Lp * Hp * Dp
-    # bytes one export reads and writes: six passes over the probabilities
-    # (four digit rounds, tie count, write) and the pattern
-    topk_bytes = 6 * 4 * n_entries + n_entries
+    # bytes one export reads and writes: four passes over the probabilities
+    # (three digit rounds, write) and the pattern
+    topk_bytes = 4 * 4 * n_entries + n_entries
     topk_res = {"entries": n_entries, "k": int(k_budget), "rho": wp.rho, "us": round(topk_us, 1),
                 "gb_per_s": round(topk_bytes / (topk_us * 1e-6) / 1e9, 1),
-                "launches": 11, "ones": int(exported.sum()), "cpu_baseline": None, "equal_to_oracle": None}
+                "launches": 5, "ones": int(exported.sum()), "cpu_baseline": None, "equal_to_oracle": None}
     if not args.no_cpu_baseline:
         t0 = time.perf_counter()
         want_pat = o.topk_mask(probs, o.budget_entries(wp.rho, Lp, Hp, Dp))

@@ -373,7 +373,7 @@ size_t dkv_topk_workspace_bytes(int32_t num_layers, int32_t num_q_heads, int32_t
  *          contents required (DKV_ERR_WORKSPACE otherwise).
  * Ties at the k-th value go to the lowest flat (layer, head, bin) indices, so
  * the result is unique and deterministic.  L * Hq * D < 2^31.  A radix
- * select of eleven small launches; nothing is read back to the host.
+ * select of five small launches; nothing is read back to the host.
  */
 dkv_status dkv_topk_pattern(int32_t num_layers, int32_t num_q_heads, int32_t num_bins,
                             const float *probs, int64_t k, uint8_t *pattern, void *workspace,

@@ -83,7 +83,7 @@ hipError_t launch_page_select(const PageSelectParams& p, hipStream_t stream);
 struct TopkParams {
   const float* probs;  // [n] retention probabilities
   uint8_t* pattern;    // [n] out
-  uint32_t* state;     // workspace: prefix, count still to take, histogram, per-chunk tie counts
+  uint32_t* state;     // workspace: selected prefixes, per-round histograms, per-chunk last-round counts
   int64_t n;           // entries, < 2^31
   int64_t k;           // 0 <= k <= n
   int64_t chunk;       // entries per workgroup (set by the launcher)

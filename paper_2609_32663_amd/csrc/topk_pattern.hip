@@ -3,16 +3,21 @@
 // probabilities become the pattern's ones, all other entries zeros.
 //
 // A radix select over the whole grid.  Every entry gets a 32-bit key that
-// orders like its value (NaN lowest, -0 equal to +0).  Four rounds of 8-bit
-// digits, most significant first, each a histogram kernel (every workgroup
-// counts the keys of its contiguous chunk that match the prefix found so far
-// in LDS and adds its 256 counts to a global histogram) and a one-workgroup
-// select kernel (the digit whose bucket holds the K-th largest key; the
-// prefix grows by it), find the K-th largest key v and how many entries equal
-// to v must be kept.  Ties go to the lowest flat indices: a count kernel
-// gives every chunk its number of entries equal to v, and the write kernel
-// ranks its ties after those of the earlier chunks, in index order.
-// State lives in a caller-provided workspace; no launch depends on the host.
+// orders like its value (NaN lowest, -0 equal to +0).  Three rounds of
+// digits (11, 11 and 10 bits, most significant first) find the K-th largest
+// key v and how many entries equal to v must be kept.  In a round every
+// workgroup counts the keys of its contiguous chunk that match the prefix
+// found so far (one LDS histogram per wave) and adds its counts to the
+// round's global histogram.  The digit of a round -- the one whose bucket
+// holds the K-th largest key -- is picked at the start of the next launch by
+// every workgroup from that histogram (the kernel boundary publishes it; no
+// device-scope fence, which costs an L2 write-back per workgroup, and no
+// counters); workgroup 0 also stores the grown prefix for the launch after.
+// Ties go to the lowest flat indices: in the last round every workgroup also
+// stores its own histogram, so the write pass ranks its chunk's ties after
+// the earlier chunks' (their count of the final digit), in index order.
+// Five launches (clear, three rounds, write); no launch depends on the host.
+// State lives in a caller-provided workspace.
 
 #include "dkv_device.hpp"
 #include "dkv_launch.hpp"
@@ -26,8 +31,18 @@ constexpr int kTkWaves = kTkThreads / kWave;
 constexpr int kTkStep = kTkThreads * 4;     // entries per workgroup iteration (one quadruple per thread)
 constexpr int kTkMinChunk = 4 * kTkStep;    // entries per workgroup at least
 constexpr int kTkMaxBlocks = 1024;
-// workspace (uint32): prefix, entries still to take within it, histogram, per-chunk tie counts
-constexpr int kTkPrefix = 0, kTkNeed = 1, kTkHist = 2, kTkTies = kTkHist + 256;
+constexpr int kTkRounds = 3;
+constexpr int kTkShift[kTkRounds] = {21, 10, 0};
+constexpr int kTkBits[kTkRounds] = {11, 11, 10};
+constexpr int kTkMaxBins = 2048;
+constexpr int kTkLastBins = 1 << 10;
+// workspace (uint32): the prefix and the entries still to take within it
+// after the digits of rounds 0 and 1 (two slots: a launch reads one and
+// stores the next), one histogram per round, then the last round's histogram
+// of every workgroup
+constexpr int kTkSel = 0;  // round r's result: kTkSel + 2r (prefix), + 1 (need)
+constexpr int kTkHist = 4;
+constexpr int kTkWgHist = kTkHist + kTkRounds * kTkMaxBins;
 
 __device__ __forceinline__ uint32_t order_key(float x) {
   if (x != x) return 0u;  // NaN below every number
@@ -62,21 +77,69 @@ __device__ __forceinline__ void chunk_of(const TopkParams& p, int b, int64_t& c0
 }
 
 __global__ __launch_bounds__(kTkThreads) void topk_init_kernel(TopkParams p) {
-  for (int i = threadIdx.x; i < 256; i += kTkThreads) p.state[kTkHist + i] = 0u;
-  if (threadIdx.x == 0) {
-    p.state[kTkPrefix] = 0u;
-    p.state[kTkNeed] = (uint32_t)p.k;
-  }
+  for (int i = threadIdx.x; i < kTkWgHist; i += kTkThreads) p.state[i] = 0u;
 }
 
-__global__ __launch_bounds__(kTkThreads) void topk_hist_kernel(TopkParams p, int shift) {
-  __shared__ uint32_t hist[kTkWaves][256];
+// The digit of round R: with the keys of round R's global histogram that
+// match `prefix` counted per digit, the largest digit whose bucket holds the
+// need-th largest of them.  Thread t takes the bins NB - 1 - per t down to
+// NB - per (t + 1); its exclusive scan is the count above its first bin and
+// the one thread whose bins cross `need` finds the digit.  Every thread gets
+// the grown prefix and what is still to take within it.
+template <int R>
+__device__ __forceinline__ void select_digit(const TopkParams& p, uint32_t& prefix, uint32_t& need, int64_t* red,
+                                             uint32_t* out) {
+  constexpr int NB = 1 << kTkBits[R];
+  constexpr int per = NB / kTkThreads;
+  static_assert(NB % kTkThreads == 0, "bins spread evenly over the threads");
+  const uint32_t* g = p.state + kTkHist + R * kTkMaxBins;
+  uint32_t h[per];
+  int64_t mine = 0;
+#pragma unroll
+  for (int j = 0; j < per; ++j) {
+    h[j] = g[NB - 1 - (per * threadIdx.x + j)];
+    mine += h[j];
+  }
+  int64_t all;
+  int64_t above = block_exclusive_scan<kTkThreads>(mine, red, &all);
+#pragma unroll
+  for (int j = 0; j < per; ++j) {
+    if (above < (int64_t)need && above + h[j] >= (int64_t)need) {
+      out[0] = prefix | ((uint32_t)(NB - 1 - (per * threadIdx.x + j)) << kTkShift[R]);
+      out[1] = need - (uint32_t)above;
+    }
+    above += h[j];
+  }
+  __syncthreads();
+  prefix = out[0];
+  need = out[1];
+}
+
+// Round R: the previous round's digit (R > 0), then this round's counts.
+template <int R>
+__global__ __launch_bounds__(kTkThreads) void topk_round_kernel(TopkParams p) {
+  constexpr int shift = kTkShift[R];
+  constexpr int NB = 1 << kTkBits[R];
+  __shared__ uint32_t hist[kTkWaves][NB];
+  __shared__ int64_t red[kTkWaves + 1];
+  __shared__ uint32_t sel[2];
   const int tid = threadIdx.x;
   const int wave = tid / kWave;
-  for (int i = tid; i < kTkWaves * 256; i += kTkThreads) (&hist[0][0])[i] = 0u;
+  for (int i = tid; i < kTkWaves * NB; i += kTkThreads) (&hist[0][0])[i] = 0u;
+  uint32_t prefix = 0u, need = (uint32_t)p.k;
+  if constexpr (R > 0) {
+    if constexpr (R > 1) {
+      prefix = p.state[kTkSel + 2 * (R - 2)];
+      need = p.state[kTkSel + 2 * (R - 2) + 1];
+    }
+    select_digit<R - 1>(p, prefix, need, red, sel);
+    if (blockIdx.x == 0 && tid == 0) {
+      p.state[kTkSel + 2 * (R - 1)] = prefix;
+      p.state[kTkSel + 2 * (R - 1) + 1] = need;
+    }
+  }
   __syncthreads();
-  const uint32_t prefix = p.state[kTkPrefix];
-  const uint32_t mask = shift == 24 ? 0u : 0xFFFFFFFFu << (shift + 8);
+  const uint32_t mask = R == 0 ? 0u : 0xFFFFFFFFu << ((shift + kTkBits[R]) & 31);
   int64_t c0, c1;
   chunk_of(p, blockIdx.x, c0, c1);
   for (int64_t i = c0 + tid * 4; i < c1; i += kTkStep) {
@@ -84,62 +147,36 @@ __global__ __launch_bounds__(kTkThreads) void topk_hist_kernel(TopkParams p, int
     const uint32_t valid = load_keys(p.probs, i, c1, key);
 #pragma unroll
     for (int e = 0; e < 4; ++e)
-      if (((valid >> e) & 1u) && (key[e] & mask) == prefix) atomicAdd(&hist[wave][(key[e] >> shift) & 255u], 1u);
+      if (((valid >> e) & 1u) && (key[e] & mask) == prefix) atomicAdd(&hist[wave][(key[e] >> shift) & (NB - 1)], 1u);
   }
   __syncthreads();
-  if (tid < 256) {
+  uint32_t* g = p.state + kTkHist + R * kTkMaxBins;
+  for (int i = tid; i < NB; i += kTkThreads) {
     uint32_t c = 0;
 #pragma unroll
-    for (int w = 0; w < kTkWaves; ++w) c += hist[w][tid];
-    if (c) atomicAdd(&p.state[kTkHist + tid], c);
+    for (int w = 0; w < kTkWaves; ++w) c += hist[w][i];
+    if (R == kTkRounds - 1) p.state[kTkWgHist + (int64_t)blockIdx.x * kTkLastBins + i] = c;
+    if (c) atomicAdd(&g[i], c);
   }
-}
-
-__global__ __launch_bounds__(kTkThreads) void topk_select_kernel(TopkParams p, int shift) {
-  __shared__ uint32_t h[256];
-  const int tid = threadIdx.x;
-  h[tid] = p.state[kTkHist + tid];
-  p.state[kTkHist + tid] = 0u;  // ready for the next round
-  __syncthreads();
-  if (tid == 0) {
-    // largest digit first: the bucket that holds the remaining K-th key
-    const uint32_t need = p.state[kTkNeed];
-    uint32_t above = 0;
-    int dgt = 255;
-    for (; dgt > 0; --dgt) {
-      if (above + h[dgt] >= need) break;
-      above += h[dgt];
-    }
-    p.state[kTkPrefix] |= (uint32_t)dgt << shift;
-    p.state[kTkNeed] = need - above;
-  }
-}
-
-__global__ __launch_bounds__(kTkThreads) void topk_ties_kernel(TopkParams p) {
-  __shared__ int64_t red[kTkWaves + 1];
-  const uint32_t thr = p.state[kTkPrefix];
-  int64_t c0, c1;
-  chunk_of(p, blockIdx.x, c0, c1);
-  uint32_t ties = 0;
-  for (int64_t i = c0 + threadIdx.x * 4; i < c1; i += kTkStep) {
-    uint32_t key[4];
-    const uint32_t valid = load_keys(p.probs, i, c1, key);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) ties += ((valid >> e) & 1u) && key[e] == thr ? 1u : 0u;
-  }
-  int64_t total;
-  block_exclusive_scan<kTkThreads>(ties, red, &total);
-  if (threadIdx.x == 0) p.state[kTkTies + blockIdx.x] = (uint32_t)total;
 }
 
 __global__ __launch_bounds__(kTkThreads) void topk_write_kernel(TopkParams p) {
   __shared__ int64_t red[kTkWaves + 1];
+  __shared__ uint32_t sel[2];
   const int tid = threadIdx.x;
-  const uint32_t thr = p.state[kTkPrefix];
-  const uint32_t take = p.k > 0 ? p.state[kTkNeed] : 0u;  // entries equal to thr that are kept
-  // ties in the chunks before this one
+  // the last digit: thr is the K-th largest key, take the entries equal to
+  // it that are kept
+  uint32_t thr = 0u, take = 0u;
+  if (p.k > 0) {
+    thr = p.state[kTkSel + 2 * (kTkRounds - 2)];
+    take = p.state[kTkSel + 2 * (kTkRounds - 2) + 1];
+    select_digit<kTkRounds - 1>(p, thr, take, red, sel);
+  }
+  // entries equal to thr in the chunks before this one
   uint32_t before = 0;
-  for (int j = tid; j < (int)blockIdx.x; j += kTkThreads) before += p.state[kTkTies + j];
+  if (p.k > 0)
+    for (int j = tid; j < (int)blockIdx.x; j += kTkThreads)
+      before += p.state[kTkWgHist + (int64_t)j * kTkLastBins + (thr & (kTkLastBins - 1))];
   int64_t rank;  // the block's total
   block_exclusive_scan<kTkThreads>(before, red, &rank);
   int64_t c0, c1;
@@ -179,20 +216,20 @@ int topk_blocks(int64_t n) {
   return (int)(b < 1 ? 1 : (b > kTkMaxBlocks ? kTkMaxBlocks : b));
 }
 
-size_t topk_workspace_bytes(int64_t n) { return (size_t)(kTkTies + topk_blocks(n)) * sizeof(uint32_t); }
+size_t topk_workspace_bytes(int64_t n) {
+  return ((size_t)kTkWgHist + (size_t)topk_blocks(n) * kTkLastBins) * sizeof(uint32_t);
+}
 
 hipError_t launch_topk_pattern(TopkParams p, hipStream_t stream) {
   if (p.n == 0) return hipSuccess;
   const int blocks = topk_blocks(p.n);
   // chunks are whole iterations of the workgroup's quadruples
   p.chunk = ((p.n + blocks - 1) / blocks + kTkStep - 1) / kTkStep * kTkStep;
-  hipLaunchKernelGGL(topk_init_kernel, dim3(1), dim3(kTkThreads), 0, stream, p);
   if (p.k > 0) {
-    for (int shift = 24; shift >= 0; shift -= 8) {
-      hipLaunchKernelGGL(topk_hist_kernel, dim3(blocks), dim3(kTkThreads), 0, stream, p, shift);
-      hipLaunchKernelGGL(topk_select_kernel, dim3(1), dim3(kTkThreads), 0, stream, p, shift);
-    }
-    hipLaunchKernelGGL(topk_ties_kernel, dim3(blocks), dim3(kTkThreads), 0, stream, p);
+    hipLaunchKernelGGL(topk_init_kernel, dim3(1), dim3(kTkThreads), 0, stream, p);
+    hipLaunchKernelGGL(topk_round_kernel<0>, dim3(blocks), dim3(kTkThreads), 0, stream, p);
+    hipLaunchKernelGGL(topk_round_kernel<1>, dim3(blocks), dim3(kTkThreads), 0, stream, p);
+    hipLaunchKernelGGL(topk_round_kernel<2>, dim3(blocks), dim3(kTkThreads), 0, stream, p);
   }
   hipLaunchKernelGGL(topk_write_kernel, dim3(blocks), dim3(kTkThreads), 0, stream, p);
   return hipGetLastError();
