@@ -74,10 +74,11 @@ struct PageSelectParams {
   uint8_t* page_used;      // [nseg][pages_per_seg] or null
   int32_t* tile_cnt;       // [nseg][ntiles] runs starting in each tile (workspace)
   int32_t* tile_kept;      // [nseg][ntiles] retained positions per tile (workspace)
+  int32_t* tile_base;      // [nseg][ntiles] first entry of each tile (workspace; set by the launcher)
   int32_t T, nseg, ntiles, page_rows, pages_per_seg, max_entries, cap;
 };
 size_t page_select_workspace_bytes(int64_t nseg, int64_t T);
-hipError_t launch_page_select(const PageSelectParams& p, hipStream_t stream);
+hipError_t launch_page_select(PageSelectParams p, hipStream_t stream);
 
 // -------------------------------------------------------- exact-budget export
 struct TopkParams {

@@ -22,6 +22,9 @@
 //          kept) and the entry count.
 // (A separate scan pass, one thread per segment walking its tiles, took
 // ~20 us of dependent loads; the prefix inside emit is one round trip.)
+// Contexts of more than kSumTiles tiles (4M positions) keep that scan pass:
+// there every emit workgroup summing all earlier tiles would cost work
+// quadratic in the context length.
 // A context of length 0 has no tile: one small kernel writes those segments.
 // Page sizes are multiples of 16 that divide the tile, so a page boundary is
 // always the boundary of a thread's 16 positions, and every wave's first
@@ -36,6 +39,7 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kPerThread = 16;
+constexpr int kSumTiles = 1024;  // longest context (in tiles) whose emit pass sums tile counts itself
 static_assert(kThreads * kPerThread == kCompactTile, "tile = threads x 16 positions");
 
 // Keep mask of this thread's 16 positions, and the run starts and ends among
@@ -115,22 +119,48 @@ __device__ int32_t finish_segment(const PageSelectParams& p, int s, int32_t n) {
   return n;
 }
 
+// Long contexts: one thread per segment turns tile counts into each tile's
+// first entry, then finishes the segment.
+__global__ __launch_bounds__(kThreads) void page_scan_kernel(PageSelectParams p) {
+  const int s = blockIdx.x * kThreads + threadIdx.x;
+  if (s >= p.nseg) return;
+  const int64_t base = (int64_t)s * p.ntiles;
+  int32_t run = 0, kept = 0;
+  for (int t = 0; t < p.ntiles; ++t) {
+    p.tile_base[base + t] = run;
+    run += p.tile_cnt[base + t];
+    kept += p.tile_kept[base + t];
+  }
+  p.seg_len[s] = kept;
+  p.n_entries[s] = finish_segment(p, s, run);
+}
+
 __global__ __launch_bounds__(kThreads) void page_emit_kernel(PageSelectParams p) {
   __shared__ int64_t red[kThreads / kWave + 1];
   const int tile = blockIdx.x;
   const int seg = blockIdx.y;
-  const bool last_tile = tile == p.ntiles - 1;
-  // runs that start in the segment's earlier tiles (low 32 bits: all its
-  // tiles' runs, needed by the last tile) and its retained positions
-  int64_t packed = 0, kept_part = 0;
-  for (int t = threadIdx.x; t < p.ntiles; t += kThreads) {
-    const int64_t c = p.tile_cnt[(int64_t)seg * p.ntiles + t];
-    packed += (t < tile ? (c << 32) : 0) + c;
-    if (last_tile) kept_part += p.tile_kept[(int64_t)seg * p.ntiles + t];
+  // With tile_base (long contexts) the scan pass gave this tile its first
+  // entry and finished the segment; otherwise the workgroup adds up the runs
+  // that start in the segment's earlier tiles (high 32 bits; low 32 bits:
+  // all its tiles' runs, which the last tile needs) and the last tile sums
+  // the retained positions.
+  const bool summed = p.tile_base == nullptr;
+  const bool last_tile = summed && tile == p.ntiles - 1;
+  int64_t before = 0, runs = 0, kept_part = 0;
+  if (summed) {
+    int64_t packed = 0;
+    for (int t = threadIdx.x; t < p.ntiles; t += kThreads) {
+      const int64_t c = p.tile_cnt[(int64_t)seg * p.ntiles + t];
+      packed += (t < tile ? (c << 32) : 0) + c;
+      if (last_tile) kept_part += p.tile_kept[(int64_t)seg * p.ntiles + t];
+    }
+    int64_t sums;
+    block_exclusive_scan<kThreads>(packed, red, &sums);
+    before = sums >> 32;
+    runs = sums & 0xFFFFFFFFLL;
+  } else {
+    before = p.tile_base[(int64_t)seg * p.ntiles + tile];
   }
-  int64_t sums;
-  block_exclusive_scan<kThreads>(packed, red, &sums);
-  const int64_t before = sums >> 32, runs = sums & 0xFFFFFFFFLL;
   const RunBits r = run_bits(p, seg, tile);
   int64_t total;
   const int64_t rank = block_exclusive_scan<kThreads>(__popc(r.starts), red, &total);
@@ -184,13 +214,17 @@ __global__ __launch_bounds__(kThreads) void page_empty_kernel(PageSelectParams p
 
 size_t page_select_workspace_bytes(int64_t nseg, int64_t T) {
   const int64_t ntiles = (T + kCompactTile - 1) / kCompactTile;
-  return (size_t)(2 * nseg * ntiles) * sizeof(int32_t);
+  return (size_t)((ntiles > kSumTiles ? 3 : 2) * nseg * ntiles) * sizeof(int32_t);
 }
 
-hipError_t launch_page_select(const PageSelectParams& p, hipStream_t stream) {
+hipError_t launch_page_select(PageSelectParams p, hipStream_t stream) {
   if (p.nseg == 0) return hipSuccess;
   if (p.ntiles > 0) {
+    // workspace: tile counts, kept positions, and for long contexts each tile's first entry
+    p.tile_base = p.ntiles > kSumTiles ? p.tile_kept + (int64_t)p.nseg * p.ntiles : nullptr;
     hipLaunchKernelGGL(page_count_kernel, dim3(p.ntiles, p.nseg), dim3(kThreads), 0, stream, p);
+    if (p.tile_base != nullptr)
+      hipLaunchKernelGGL(page_scan_kernel, dim3((p.nseg + kThreads - 1) / kThreads), dim3(kThreads), 0, stream, p);
     hipLaunchKernelGGL(page_emit_kernel, dim3(p.ntiles, p.nseg), dim3(kThreads), 0, stream, p);
   } else {
     hipLaunchKernelGGL(page_empty_kernel, dim3((p.nseg + kThreads - 1) / kThreads), dim3(kThreads), 0, stream, p);

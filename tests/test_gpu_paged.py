@@ -93,6 +93,26 @@ def test_page_select_random_masks(d, page_rows, T):
     _check_select(GpuSelect(d, _mask_tensor(m), table, page_rows, cap, max_e), ref, max_e)
 
 
+@pytest.mark.parametrize("page_rows", [128, 1024])
+def test_page_select_long_context(d, page_rows):
+    """More than 1,024 tiles of 4,096 positions: the selection takes its
+    separate scan pass (each tile's first entry), bit-exact like the short
+    contexts that sum tile counts inside the emit pass."""
+    rng = np.random.default_rng(page_rows)
+    nseg, T, cap = 2, 1025 * 4096 + 777, 40
+    m = np.zeros((nseg, T), np.uint8)
+    pos = 0
+    while pos < T:
+        n = int(rng.integers(1, 3000))
+        m[:, pos:pos + n] = rng.integers(0, 2, size=(nseg, 1))
+        pos += n
+    m[1, :T // 3] = 0  # a long empty stretch in one segment
+    table, _ = di.page_table(nseg, -(-(T + cap) // page_rows) + 2, seed=page_rows, spare=5)
+    ref = o.page_select(m, table, page_rows, cap)
+    max_e = int(ref["n_entries"].max())
+    _check_select(GpuSelect(d, _mask_tensor(m), table, page_rows, cap, max_e), ref, max_e)
+
+
 def test_page_select_overflow_reports_true_counts(d):
     """Entries past max_entries are not written; n_entries still says how
     many there are."""
