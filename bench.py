@@ -1138,6 +1138,24 @@ def main():
     compact_bytes = 2 * 2 * retained * dim * elem + N * Hkv * T  # K,V read+write + mask
     phys_frac = retained / float(N * Hkv * T)
     log(f"map {map_us:.0f} us, compact {compact_us:.0f} us, retained {phys_frac:.4f}")
+    # the rate a pack can at best approach: dkv_probe_copy of the retained K and
+    # V bytes (one contiguous copy, 16-byte non-temporal loads and stores)
+    copy_bytes = 2 * retained * dim * elem
+    csrc = torch.ones(copy_bytes // 2, dtype=torch.int16, device=dev)
+    cdst = torch.empty_like(csrc)
+    copy_gbps = {}
+    for wg in (4096, 8192):
+        d.dkv_probe_copy(csrc, cdst, wg)
+        torch.cuda.synchronize()
+        e1.record(stream)
+        for _ in range(3):
+            d.dkv_probe_copy(csrc, cdst, wg)
+        e2.record(stream)
+        torch.cuda.synchronize()
+        copy_gbps[wg] = round(2 * copy_bytes / (e1.elapsed_time(e2) / 3 * 1e-3) / 1e9, 1)
+    del csrc, cdst
+    torch.cuda.empty_cache()
+    log(f"copy probe over the packed bytes (read + write GB/s): {copy_gbps}")
 
     # ---------------- query block: a second pack with room for it ----------
     # The tokens after the context (the paper reserves 256 for query and
@@ -1963,6 +1981,11 @@ def main():
         "one_time": {"map_us": round(map_us, 1), "compact_us": round(compact_us, 1),
                      "compact_bytes": int(compact_bytes),
                      "compact_gb_per_s": round(compact_bytes / (compact_us * 1e-6) / 1e9, 1),
+                     "copy_probe": {"kind": "dkv_probe_copy of the retained K and V bytes (read + write)",
+                                    "bytes": int(2 * copy_bytes), "gb_per_s_by_workgroups": copy_gbps,
+                                    "best_gb_per_s": max(copy_gbps.values())},
+                     "compact_frac_of_copy": round(compact_bytes / (compact_us * 1e-6) / 1e9
+                                                   / max(copy_gbps.values()), 4),
                      # the same time priced as a pass that reads the whole dense cache and
                      # writes the retained rows (what a non-gathering pack would move)
                      "compact_dense_read_gb_per_s": round(

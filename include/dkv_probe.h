@@ -1,12 +1,13 @@
 /*
- * dkv_probe.h -- achievable-bandwidth probe (a measurement aid; not part of
+ * dkv_probe.h -- achievable-bandwidth probes (measurement aids; not part of
  * the Distance-KV method).
  *
  * A plain streaming read of device memory with the same load instructions
  * and cache policy as the decode kernel's K/V stream (16-byte non-temporal
- * buffer loads).  The benchmark times it on buffers of one decode launch's
+ * buffer loads), and a plain copy (16-byte non-temporal loads and stores).  The benchmark times the read on buffers of one decode launch's
  * size to report what a launch of that size reaches on this GPU, next to the
- * HBM specification.  Conventions (device pointers, asynchronous on `stream`,
+ * HBM specification, and the copy on the bytes the one-time pack moves, the
+ * rate a gather of retained rows can at best approach.  Conventions (device pointers, asynchronous on `stream`,
  * host-side argument checks, status codes) are those of dkv.h.
  */
 #ifndef DKV_PROBE_H
@@ -35,6 +36,19 @@ extern "C" {
  * DKV_ERR_MISALIGNED, DKV_ERR_HIP (launch refused). */
 dkv_status dkv_probe_stream_read(const void* src, int64_t bytes, void* sink, int32_t workgroups,
                                  void* stream);
+
+/* Copies bytes [0, bytes) from `src` to `dst` with `workgroups` workgroups of
+ * 256 threads, the 16-byte granules dealt out grid-stride (in every round the
+ * workgroups take consecutive blocks of 2,048 granules, so the grid sweeps
+ * the buffers together); each thread loads eight granules, then stores them.
+ *   src, dst   device pointers, 16-byte aligned, `bytes` bytes each, not
+ *              overlapping (the caller owns both; dst is overwritten).
+ *   bytes      multiple of 16, >= 0 (0: nothing is enqueued).
+ *   workgroups 1 .. 65535.
+ * Errors: DKV_ERR_INVALID_ARG (null pointer, overlapping buffers, bytes < 0
+ * or not a multiple of 16, workgroups out of range), DKV_ERR_MISALIGNED,
+ * DKV_ERR_HIP (launch refused). */
+dkv_status dkv_probe_copy(const void* src, void* dst, int64_t bytes, int32_t workgroups, void* stream);
 
 #ifdef __cplusplus
 }

@@ -20,7 +20,7 @@ __all__ = [
     "dkv_decode_workspace_bytes", "dkv_decode_attn", "dkv_dense_decode_attn",
     "dkv_append_decode_attn", "dkv_append_decode_attn_noalloc", "dkv_dense_append_decode_attn",
     "DKV_NOALLOC_SCRATCH_BYTES",
-    "dkv_status_string", "dkv_probe_stream_read", "dkv_query_workspace_bytes", "dkv_query_attn",
+    "dkv_status_string", "dkv_probe_stream_read", "dkv_probe_copy", "dkv_query_workspace_bytes", "dkv_query_attn",
     "dkv_page_select_workspace_bytes", "dkv_page_entries_bound", "dkv_page_select",
     "dkv_paged_decode_attn", "dkv_paged_append_decode_attn", "dkv_budget_entries",
     "dkv_topk_workspace_bytes", "dkv_topk_pattern", "dkv_map_pattern_ragged",
@@ -106,6 +106,7 @@ def library_at(path):
                                                I32, F32, VP, VP, SZ, VP]),
         "dkv_status_string": (ctypes.c_char_p, [I32]),
         "dkv_probe_stream_read": (I32, [VP, I64, VP, I32, VP]),
+        "dkv_probe_copy": (I32, [VP, VP, I64, I32, VP]),
         "dkv_query_workspace_bytes": (SZ, [I32, I32, I32, I32, I32, I64]),
         "dkv_query_attn": (I32, [I32, I32, I32, I32, I32, I32, VP, I32, I32, VP, VP, VP, VP, F32, I64,
                                  VP, VP, SZ, VP]),
@@ -269,6 +270,14 @@ def dkv_probe_stream_read(src, sink, workgroups, nbytes=None, stream=None):
     n = src.numel() * src.element_size() if nbytes is None else int(nbytes)
     _check("dkv_probe_stream_read", library().dkv_probe_stream_read(
         _dev(src, "src"), n, _dev(sink, "sink"), int(workgroups), _stream(stream)))
+
+
+def dkv_probe_copy(src, dst, workgroups, nbytes=None, stream=None):
+    """Copy probe (measurement aid): copies `nbytes` (default: all) bytes of
+    the device tensor `src` into the device tensor `dst`."""
+    n = src.numel() * src.element_size() if nbytes is None else int(nbytes)
+    _check("dkv_probe_copy", library().dkv_probe_copy(
+        _dev(src, "src"), _dev(dst, "dst"), n, int(workgroups), _stream(stream)))
 
 
 def dkv_query_workspace_bytes(batch, num_q_heads, num_kv_heads, head_dim, n_q, rows_hint=0):

@@ -1,6 +1,7 @@
-// Achievable-bandwidth probe: a plain streaming read with the decode
+// Achievable-bandwidth probes: a plain streaming read with the decode
 // kernel's load instruction and cache policy (16-byte non-temporal buffer
-// loads), used to measure what one launch of a given size reaches on this GPU.
+// loads), and a plain copy (16-byte non-temporal loads and stores), used to
+// measure what one launch of a given size reaches on this GPU.
 
 #include <hip/hip_runtime.h>
 
@@ -42,6 +43,30 @@ __global__ __launch_bounds__(kProbeThreads) void stream_read_kernel(const char* 
   if ((acc.x ^ acc.y ^ acc.z ^ acc.w) == kProbeImpossible) *sink = acc;
 }
 
+// Copy of `bytes` bytes, 16-byte granules dealt out grid-stride: in every
+// round the workgroups take consecutive blocks of 256 x 8 granules, so the
+// whole grid sweeps the buffers together (measured 5-20% faster for a copy
+// than one contiguous slice per workgroup); each thread keeps eight
+// non-temporal loads in flight, then stores them non-temporally.
+__global__ __launch_bounds__(kProbeThreads) void copy_kernel(const u32x4* __restrict__ src, u32x4* __restrict__ dst,
+                                                             int64_t granules) {
+  const int64_t step = (int64_t)gridDim.x * kProbeThreads * kProbeUnroll;
+  for (int64_t base = (int64_t)blockIdx.x * kProbeThreads * kProbeUnroll + threadIdx.x; base < granules;
+       base += step) {
+    u32x4 x[kProbeUnroll];
+#pragma unroll
+    for (int u = 0; u < kProbeUnroll; ++u) {
+      const int64_t i = base + (int64_t)u * kProbeThreads;
+      if (i < granules) x[u] = __builtin_nontemporal_load(src + i);
+    }
+#pragma unroll
+    for (int u = 0; u < kProbeUnroll; ++u) {
+      const int64_t i = base + (int64_t)u * kProbeThreads;
+      if (i < granules) __builtin_nontemporal_store(x[u], dst + i);
+    }
+  }
+}
+
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 }  // namespace
@@ -56,5 +81,18 @@ extern "C" dkv_status dkv_probe_stream_read(const void* src, int64_t bytes, void
   if (per > (int64_t(1) << 31)) return DKV_ERR_UNSUPPORTED;
   hipLaunchKernelGGL(stream_read_kernel, dim3(workgroups), dim3(kProbeThreads), 0, (hipStream_t)stream,
                      static_cast<const char*>(src), bytes, static_cast<u32x4*>(sink));
+  return hipGetLastError() == hipSuccess ? DKV_OK : DKV_ERR_HIP;
+}
+
+extern "C" dkv_status dkv_probe_copy(const void* src, void* dst, int64_t bytes, int32_t workgroups, void* stream) {
+  if (bytes < 0 || bytes % 16 != 0 || workgroups < 1 || workgroups > 65535) return DKV_ERR_INVALID_ARG;
+  if (bytes == 0) return DKV_OK;
+  if (src == nullptr || dst == nullptr) return DKV_ERR_INVALID_ARG;
+  if (!aligned16(src) || !aligned16(dst)) return DKV_ERR_MISALIGNED;
+  const char* s = static_cast<const char*>(src);
+  char* d = static_cast<char*>(dst);
+  if (s < d + bytes && d < s + bytes) return DKV_ERR_INVALID_ARG;  // overlapping buffers
+  hipLaunchKernelGGL(copy_kernel, dim3(workgroups), dim3(kProbeThreads), 0, (hipStream_t)stream,
+                     static_cast<const u32x4*>(src), static_cast<u32x4*>(dst), bytes / 16);
   return hipGetLastError() == hipSuccess ? DKV_OK : DKV_ERR_HIP;
 }

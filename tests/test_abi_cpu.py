@@ -199,6 +199,17 @@ def test_probe_validation():
     assert lib.dkv_probe_stream_read(A, 4096, NUL, 1, NUL) == d.DKV_ERR_INVALID_ARG
     assert lib.dkv_probe_stream_read(MIS, 4096, A, 1, NUL) == d.DKV_ERR_MISALIGNED
     assert lib.dkv_probe_stream_read(A, 4096, MIS, 1, NUL) == d.DKV_ERR_MISALIGNED
+    B = ctypes.c_void_p(A.value + (1 << 20))  # a second, disjoint (never dereferenced) buffer
+    assert lib.dkv_probe_copy(A, B, 0, 1, NUL) == d.DKV_OK  # nothing to copy
+    assert lib.dkv_probe_copy(A, B, -16, 1, NUL) == d.DKV_ERR_INVALID_ARG
+    assert lib.dkv_probe_copy(A, B, 24, 1, NUL) == d.DKV_ERR_INVALID_ARG
+    assert lib.dkv_probe_copy(A, B, 4096, 0, NUL) == d.DKV_ERR_INVALID_ARG
+    assert lib.dkv_probe_copy(A, B, 4096, 65536, NUL) == d.DKV_ERR_INVALID_ARG
+    assert lib.dkv_probe_copy(NUL, B, 4096, 1, NUL) == d.DKV_ERR_INVALID_ARG
+    assert lib.dkv_probe_copy(A, NUL, 4096, 1, NUL) == d.DKV_ERR_INVALID_ARG
+    assert lib.dkv_probe_copy(A, A, 4096, 1, NUL) == d.DKV_ERR_INVALID_ARG  # overlapping
+    assert lib.dkv_probe_copy(MIS, B, 4096, 1, NUL) == d.DKV_ERR_MISALIGNED
+    assert lib.dkv_probe_copy(A, MIS, 4096, 1, NUL) == d.DKV_ERR_MISALIGNED
     assert lib.dkv_probe_stream_read(A, (1 << 32) + 16, A, 1, NUL) == d.DKV_ERR_UNSUPPORTED
 
 
