@@ -1,4 +1,5 @@
-"""Guard canaries past (and before) every output buffer of every entry point.
+"""Guard canaries past (and before) every output buffer of every entry point,
+and bitwise reproducibility of the calls the other tests do not repeat.
 
 Each output, in-out cache and workspace is carved out of a larger byte buffer
 whose 4 KiB before and after it hold a sentinel; after the call (on small,
@@ -133,6 +134,9 @@ def test_append_and_decode_calls_stay_inside(d):
     ws = _ws(d.dkv_decode_workspace_bytes(1, HQ, HKV, DIM))
     d.dkv_dense_decode_attn(q, kd.t, vd.t, T, 0.1, out.t, ws.t)
     assert out.intact() and ws.intact()
+    first = out.t.clone()
+    d.dkv_dense_decode_attn(q, kd.t, vd.t, T, 0.1, out.t, ws.t)
+    assert torch.equal(out.t, first)  # fixed merge order
     d.dkv_dense_append_decode_attn(q, kn[:HKV, :3].contiguous(), vn[:HKV, :3].contiguous(), kd.t, vd.t, T, 0.1,
                                    out.t, ws.t)
     assert out.intact() and ws.intact() and kd.intact() and vd.intact()
@@ -187,6 +191,9 @@ def test_page_select_and_paged_decode_stay_inside(d, page_rows):
     dws = _ws(d.dkv_decode_workspace_bytes(1, HQ, HKV, DIM))
     d.dkv_paged_decode_attn(q, kp.t, vp.t, ent.t[:HKV], ne.t[:HKV], T, 0, 0.1, out.t, dws.t, HKV)
     assert out.intact() and dws.intact()
+    first = out.t.clone()
+    d.dkv_paged_decode_attn(q, kp.t, vp.t, ent.t[:HKV], ne.t[:HKV], T, 0, 0.1, out.t, dws.t, HKV)
+    assert torch.equal(out.t, first)  # fixed merge order
     d.dkv_paged_append_decode_attn(q, kn, vn, CAP - 2, CAP, kp.t, vp.t, ent.t[:HKV], ne.t[:HKV], T, 0.1, out.t,
                                    dws.t, HKV)
     assert out.intact() and dws.intact() and kp.intact() and vp.intact()
@@ -237,3 +244,6 @@ def test_query_block_split_stays_inside(d):
         ws = _ws(nb)
         d.dkv_query_attn(qb, 0, n_q, kc.t, vc.t, off, ln, 0.1, out.t, ws.t, HKV, rows_hint=hint)
         assert out.intact() and ws.intact()
+        first = out.t.clone()
+        d.dkv_query_attn(qb, 0, n_q, kc.t, vc.t, off, ln, 0.1, out.t, ws.t, HKV, rows_hint=hint)
+        assert torch.equal(out.t, first)  # ranges combined in a fixed order
