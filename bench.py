@@ -497,9 +497,22 @@ def bench_configs(ctx):
         c_us = timed_event(lambda: d.dkv_compact(lay, k, v, km, cap, k_c, v_c, so, sl, ws), reps=2)
         retained = int(lens.sum())
         c_bytes = 2 * 2 * retained * w.head_dim * elem + N * Hkv * T
+        # the block gather from the pattern into a second buffer, checked against it
+        k_b, v_b = torch.empty_like(k_c), torch.empty_like(v_c)
+        so_b, sl_b = torch.empty_like(so), torch.empty_like(sl)
+        bws = torch.empty(d.dkv_compact_bins_workspace_bytes(lay), dtype=torch.uint8, device=dev)
+        b_us = timed_event(lambda: d.dkv_compact_bins(lay, k, v, pat, cap, k_b, v_b, so_b, sl_b, bws), reps=2)
+        b_equal = bool(torch.equal(so_b, so) and torch.equal(sl_b, sl)
+                       and torch.equal(k_b.view(torch.int16), k_c.view(torch.int16))
+                       and torch.equal(v_b.view(torch.int16), v_c.view(torch.int16)))
+        del k_b, v_b, bws
+        b_bytes = 2 * 2 * retained * w.head_dim * elem
         one_time = {"map_us": round(map_us, 1), "compact_us": round(c_us, 1),
                     "compact_gb_per_s": round(c_bytes / (c_us * 1e-6) / 1e9, 1),
-                    "map_write_gb_per_s": round(N * Hkv * T / (map_us * 1e-6) / 1e9, 1)}
+                    "map_write_gb_per_s": round(N * Hkv * T / (map_us * 1e-6) / 1e9, 1),
+                    "compact_bins_us": round(b_us, 1),
+                    "compact_bins_gb_per_s": round(b_bytes / (b_us * 1e-6) / 1e9, 1),
+                    "compact_bins_equal_to_compact": b_equal}
         return dict(km=km, lens=lens, rows=rows, k_c=k_c, v_c=v_c, so=so, sl=sl, retained=retained,
                     one_time=one_time)
 
@@ -1138,21 +1151,45 @@ def main():
     compact_bytes = 2 * 2 * retained * dim * elem + N * Hkv * T  # K,V read+write + mask
     phys_frac = retained / float(N * Hkv * T)
     log(f"map {map_us:.0f} us, compact {compact_us:.0f} us, retained {phys_frac:.4f}")
-    # the rate a pack can at best approach: dkv_probe_copy of the retained K and
-    # V bytes (one contiguous copy, 16-byte non-temporal loads and stores)
+    # the same pack straight from the pattern (block gather: no mask), into a
+    # second buffer, checked bit for bit against dkv_compact's
+    k_b, v_b = torch.empty_like(k_c), torch.empty_like(v_c)
+    seg_off_b, seg_len_b = torch.empty_like(seg_off), torch.empty_like(seg_len)
+    bws = torch.empty(d.dkv_compact_bins_workspace_bytes(lay), dtype=torch.uint8, device=dev)
+    d.dkv_compact_bins(lay, k, v, pat_d, cap, k_b, v_b, seg_off_b, seg_len_b, bws)
+    torch.cuda.synchronize()
+    bins_ms = []
+    for _ in range(3):
+        e1.record(stream)
+        d.dkv_compact_bins(lay, k, v, pat_d, cap, k_b, v_b, seg_off_b, seg_len_b, bws)
+        e2.record(stream)
+        torch.cuda.synchronize()
+        bins_ms.append(e1.elapsed_time(e2))
+    bins_us = min(bins_ms) * 1e3
+    bins_equal = bool(torch.equal(seg_off_b, seg_off) and torch.equal(seg_len_b, seg_len)
+                      and torch.equal(k_b.view(torch.int16), k_c.view(torch.int16))
+                      and torch.equal(v_b.view(torch.int16), v_c.view(torch.int16)))
+    del k_b, v_b, bws
+    torch.cuda.empty_cache()
+    bins_bytes = 2 * 2 * retained * dim * elem
+    log(f"compact_bins {bins_us:.0f} us ({bins_bytes / (bins_us * 1e-6) / 1e9:.0f} GB/s), "
+        f"equal to compact: {bins_equal}")
+    # what a plain copy of the same bytes reaches: dkv_probe_copy of the
+    # retained K and V bytes (one block of 4, 8 or 16 KiB per workgroup,
+    # 16-byte non-temporal loads and stores)
     copy_bytes = 2 * retained * dim * elem
     csrc = torch.ones(copy_bytes // 2, dtype=torch.int16, device=dev)
     cdst = torch.empty_like(csrc)
     copy_gbps = {}
-    for wg in (4096, 8192):
-        d.dkv_probe_copy(csrc, cdst, wg)
+    for g in (1, 2, 4):
+        d.dkv_probe_copy(csrc, cdst, g)
         torch.cuda.synchronize()
         e1.record(stream)
         for _ in range(3):
-            d.dkv_probe_copy(csrc, cdst, wg)
+            d.dkv_probe_copy(csrc, cdst, g)
         e2.record(stream)
         torch.cuda.synchronize()
-        copy_gbps[wg] = round(2 * copy_bytes / (e1.elapsed_time(e2) / 3 * 1e-3) / 1e9, 1)
+        copy_gbps[f"{4 * g}KiB"] = round(2 * copy_bytes / (e1.elapsed_time(e2) / 3 * 1e-3) / 1e9, 1)
     del csrc, cdst
     torch.cuda.empty_cache()
     log(f"copy probe over the packed bytes (read + write GB/s): {copy_gbps}")
@@ -1833,8 +1870,9 @@ def main():
     mt_res = {"turns": MT_TURNS, "block_tokens": NQ, "tokens_generated_per_turn": MT_STEPS,
               "ms_per_turn": round(turn_ms, 3), "prefill_ms": round(float(np.median(pre_ms)), 3),
               "decode_ms_per_token": round(float(np.median(dec_ms)) / MT_STEPS, 4),
-              "compaction_ms": round(compact_us / 1e3, 3),
-              "compaction_share": round(compact_us / 1e3 / (compact_us / 1e3 + MT_TURNS * turn_ms), 4),
+              "compaction_ms": round(bins_us / 1e3, 3),
+              "compaction_share": round(bins_us / 1e3 / (bins_us / 1e3 + MT_TURNS * turn_ms), 4),
+              "compaction_call": "dkv_compact_bins",
               "step": "turn = per layer (append 256-token block + dkv_query_attn), then 16 x per layer "
                       "dkv_append_decode_attn; HIP-graph replays", "parity_layer0_last_token": None}
     if not args.no_cpu_baseline:
@@ -1981,11 +2019,16 @@ def main():
         "one_time": {"map_us": round(map_us, 1), "compact_us": round(compact_us, 1),
                      "compact_bytes": int(compact_bytes),
                      "compact_gb_per_s": round(compact_bytes / (compact_us * 1e-6) / 1e9, 1),
+                     "compact_bins_us": round(bins_us, 1), "compact_bins_bytes": int(bins_bytes),
+                     "compact_bins_gb_per_s": round(bins_bytes / (bins_us * 1e-6) / 1e9, 1),
+                     "compact_bins_equal_to_compact": bins_equal,
                      "copy_probe": {"kind": "dkv_probe_copy of the retained K and V bytes (read + write)",
-                                    "bytes": int(2 * copy_bytes), "gb_per_s_by_workgroups": copy_gbps,
+                                    "bytes": int(2 * copy_bytes), "gb_per_s_by_block": copy_gbps,
                                     "best_gb_per_s": max(copy_gbps.values())},
                      "compact_frac_of_copy": round(compact_bytes / (compact_us * 1e-6) / 1e9
                                                    / max(copy_gbps.values()), 4),
+                     "compact_bins_frac_of_copy": round(bins_bytes / (bins_us * 1e-6) / 1e9
+                                                        / max(copy_gbps.values()), 4),
                      # the same time priced as a pass that reads the whole dense cache and
                      # writes the retained rows (what a non-gathering pack would move)
                      "compact_dense_read_gb_per_s": round(

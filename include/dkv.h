@@ -12,6 +12,8 @@
  *   dkv_map_pattern   pattern -> per-KV-head keep masks and retained lengths
  *                     (dkv_map_pattern_ragged: contexts of different lengths)
  *   dkv_compact       dense K/V + keep mask -> packed K/V, offsets, lengths
+ *                     (dkv_compact_bins: map and pack from the pattern in one
+ *                     call, whole retained bins copied as blocks)
  *   dkv_append        new tokens -> free rows after each packed segment
  *   dkv_decode_attn   one decode step of attention over the packed segments
  *   dkv_query_attn    the query block after the context: attention over the
@@ -175,6 +177,39 @@ dkv_status dkv_compact(const dkv_layout *layout, dkv_dtype dtype, const void *k,
                        void *k_out, void *v_out, int64_t out_rows, int64_t *seg_off,
                        int32_t *seg_len, int32_t *src_pos, int64_t *rows_needed,
                        void *workspace, size_t workspace_bytes, void *stream);
+
+/* Workspace bytes dkv_compact_bins needs for this layout (host, no GPU call);
+ * 0 for a layout it does not accept. */
+size_t dkv_compact_bins_workspace_bytes(const dkv_layout *layout);
+
+/*
+ * dkv_compact_bins -- map and pack in one call, straight from the pattern, as
+ * a block gather.  Under Eq. (4)-(5) and the union of Sec. 3.4 a KV head keeps
+ * its sink, its recent window and every bin that some query head of its group
+ * keeps, and bin k is the contiguous range of positions
+ * [T - recent - min(E[k+1], U), T - recent - E[k]) with U = T - sink - recent
+ * the compressible span (empty when E[k] >= U).  The packed segment is those
+ * ranges in token order, and each is copied as one block of rows (with the
+ * paper's 128-token bins of Appendix A: 128 consecutive rows per kept bin).
+ * No keep mask is read or written.
+ *
+ * pattern   uint8 [N][Hq][D] as for dkv_map_pattern.
+ * Every other argument as dkv_compact, whose outputs this call reproduces
+ * exactly for dkv_map_pattern's kv_mask of the same layout and pattern:
+ * k_out, v_out (the retained rows; free rows untouched), seg_off, seg_len
+ * (with the same -1 marker for segments that do not fit below out_rows),
+ * src_pos and rows_needed.
+ * workspace  at least dkv_compact_bins_workspace_bytes(layout) bytes, no
+ *            initial contents required.
+ * Limits: those of dkv_map_pattern and dkv_compact, N * Hkv <= 65,535 and
+ * N * Hkv * (D + 3) <= 2^27 (the workspace's per-segment block tables);
+ * beyond them DKV_ERR_UNSUPPORTED.  Other errors as dkv_compact's.
+ */
+dkv_status dkv_compact_bins(const dkv_layout *layout, dkv_dtype dtype, const void *k,
+                            const void *v, const uint8_t *pattern, int32_t append_cap,
+                            void *k_out, void *v_out, int64_t out_rows, int64_t *seg_off,
+                            int32_t *seg_len, int32_t *src_pos, int64_t *rows_needed,
+                            void *workspace, size_t workspace_bytes, void *stream);
 
 /*
  * dkv_append -- appended tokens are retained in full (Sec. 3.4).

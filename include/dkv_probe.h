@@ -37,18 +37,19 @@ extern "C" {
 dkv_status dkv_probe_stream_read(const void* src, int64_t bytes, void* sink, int32_t workgroups,
                                  void* stream);
 
-/* Copies bytes [0, bytes) from `src` to `dst` with `workgroups` workgroups of
- * 256 threads, the 16-byte granules dealt out grid-stride (in every round the
- * workgroups take consecutive blocks of 2,048 granules, so the grid sweeps
- * the buffers together); each thread loads eight granules, then stores them.
+/* Copies bytes [0, bytes) from `src` to `dst` in blocks of 256 x G 16-byte
+ * granules (G = granules_per_thread: 4, 8, 16 or 32 KiB), one block per
+ * workgroup of 256 threads: each thread loads its G granules non-temporally,
+ * then stores them, and the grid has one workgroup per block.
  *   src, dst   device pointers, 16-byte aligned, `bytes` bytes each, not
  *              overlapping (the caller owns both; dst is overwritten).
  *   bytes      multiple of 16, >= 0 (0: nothing is enqueued).
- *   workgroups 1 .. 65535.
+ *   granules_per_thread  1, 2, 4 or 8.
  * Errors: DKV_ERR_INVALID_ARG (null pointer, overlapping buffers, bytes < 0
- * or not a multiple of 16, workgroups out of range), DKV_ERR_MISALIGNED,
- * DKV_ERR_HIP (launch refused). */
-dkv_status dkv_probe_copy(const void* src, void* dst, int64_t bytes, int32_t workgroups, void* stream);
+ * or not a multiple of 16, G not one of the four), DKV_ERR_MISALIGNED,
+ * DKV_ERR_UNSUPPORTED (more than 2^31 - 1 blocks), DKV_ERR_HIP (launch
+ * refused). */
+dkv_status dkv_probe_copy(const void* src, void* dst, int64_t bytes, int32_t granules_per_thread, void* stream);
 
 #ifdef __cplusplus
 }

@@ -16,7 +16,8 @@ __all__ = [
     "DKV_OK", "DKV_ERR_INVALID_ARG", "DKV_ERR_UNSUPPORTED", "DKV_ERR_MISALIGNED",
     "DKV_ERR_CAPACITY", "DKV_ERR_WORKSPACE", "DKV_ERR_HIP", "DKV_BF16", "DKV_F32",
     "DkvError", "Layout", "make_layout", "library", "library_at", "library_path", "dtype_code",
-    "dkv_map_pattern", "dkv_compact_workspace_bytes", "dkv_compact", "dkv_append",
+    "dkv_map_pattern", "dkv_compact_workspace_bytes", "dkv_compact", "dkv_compact_bins_workspace_bytes",
+    "dkv_compact_bins", "dkv_append",
     "dkv_decode_workspace_bytes", "dkv_decode_attn", "dkv_dense_decode_attn",
     "dkv_append_decode_attn", "dkv_append_decode_attn_noalloc", "dkv_dense_append_decode_attn",
     "DKV_NOALLOC_SCRATCH_BYTES",
@@ -121,6 +122,8 @@ def library_at(path):
         "dkv_topk_workspace_bytes": (SZ, [I32, I32, I32]),
         "dkv_map_pattern_ragged": (I32, [P, VP, VP, VP, VP, VP, VP]),
         "dkv_topk_pattern": (I32, [I32, I32, I32, VP, I64, VP, VP, SZ, VP]),
+        "dkv_compact_bins_workspace_bytes": (SZ, [P]),
+        "dkv_compact_bins": (I32, [P, I32, VP, VP, VP, I32, VP, VP, I64, VP, VP, VP, VP, VP, SZ, VP]),
     }
     for name, (res, args) in sigs.items():
         f = getattr(lib, name)
@@ -191,6 +194,22 @@ def dkv_compact(layout, k, v, kv_mask, append_cap, k_out, v_out, seg_off, seg_le
         _dev(src_pos, "src_pos", True), _dev(rows_needed, "rows_needed", True),
         _dev(workspace, "workspace"), workspace.numel() * workspace.element_size(),
         _stream(stream)))
+
+
+def dkv_compact_bins_workspace_bytes(layout):
+    return int(library().dkv_compact_bins_workspace_bytes(ctypes.byref(layout)))
+
+
+def dkv_compact_bins(layout, k, v, pattern, append_cap, k_out, v_out, seg_off, seg_len, workspace,
+                     src_pos=None, rows_needed=None, stream=None):
+    """Map and pack from the pattern in one call (the block gather); outputs
+    as dkv_compact's for dkv_map_pattern's mask."""
+    _check("dkv_compact_bins", library().dkv_compact_bins(
+        ctypes.byref(layout), dtype_code(k.dtype), _dev(k, "k"), _dev(v, "v"), _dev(pattern, "pattern"),
+        int(append_cap), _dev(k_out, "k_out"), _dev(v_out, "v_out"), k_out.shape[0],
+        _dev(seg_off, "seg_off"), _dev(seg_len, "seg_len"), _dev(src_pos, "src_pos", True),
+        _dev(rows_needed, "rows_needed", True), _dev(workspace, "workspace"),
+        workspace.numel() * workspace.element_size(), _stream(stream)))
 
 
 def dkv_append(k_new, v_new, n_tail, append_cap, k_c, v_c, seg_off, seg_len, stream=None):
@@ -272,12 +291,13 @@ def dkv_probe_stream_read(src, sink, workgroups, nbytes=None, stream=None):
         _dev(src, "src"), n, _dev(sink, "sink"), int(workgroups), _stream(stream)))
 
 
-def dkv_probe_copy(src, dst, workgroups, nbytes=None, stream=None):
+def dkv_probe_copy(src, dst, granules_per_thread, nbytes=None, stream=None):
     """Copy probe (measurement aid): copies `nbytes` (default: all) bytes of
-    the device tensor `src` into the device tensor `dst`."""
+    the device tensor `src` into the device tensor `dst`, one block of
+    256 x granules_per_thread 16-byte granules per workgroup."""
     n = src.numel() * src.element_size() if nbytes is None else int(nbytes)
     _check("dkv_probe_copy", library().dkv_probe_copy(
-        _dev(src, "src"), _dev(dst, "dst"), n, int(workgroups), _stream(stream)))
+        _dev(src, "src"), _dev(dst, "dst"), n, int(granules_per_thread), _stream(stream)))
 
 
 def dkv_query_workspace_bytes(batch, num_q_heads, num_kv_heads, head_dim, n_q, rows_hint=0):

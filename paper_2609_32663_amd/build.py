@@ -38,7 +38,7 @@ COMMON_FLAGS = [
 # NaN semantics, so its row maxima need no NaN canonicalisation (its kernels
 # form no NaN from finite inputs; see the file's header).
 FILE_FLAGS = {"query_attn.hip": ["-mno-amdgpu-ieee", "-fno-honor-nans"]}
-SOURCES = ["map_pattern.hip", "compact.hip", "decode_attn.hip", "dkv_api.cpp", "bw_probe.hip",
+SOURCES = ["map_pattern.hip", "compact.hip", "compact_bins.hip", "decode_attn.hip", "dkv_api.cpp", "bw_probe.hip",
            "query_attn.hip", "dkv_query_api.cpp", "page_select.hip", "dkv_paged_api.cpp",
            "topk_pattern.hip", "dkv_pattern_api.cpp"]
 

@@ -43,27 +43,26 @@ __global__ __launch_bounds__(kProbeThreads) void stream_read_kernel(const char* 
   if ((acc.x ^ acc.y ^ acc.z ^ acc.w) == kProbeImpossible) *sink = acc;
 }
 
-// Copy of `bytes` bytes, 16-byte granules dealt out grid-stride: in every
-// round the workgroups take consecutive blocks of 256 x 8 granules, so the
-// whole grid sweeps the buffers together (measured 5-20% faster for a copy
-// than one contiguous slice per workgroup); each thread keeps eight
-// non-temporal loads in flight, then stores them non-temporally.
+// Copy of `bytes` bytes in blocks of 256 x G 16-byte granules, one block per
+// workgroup (no grid-stride loop): every thread issues its G non-temporal
+// loads, then its G stores, and the workgroup retires.  Short workgroups are
+// what copies fastest here: with 4-16 KiB per workgroup a copy measured
+// 6.0-6.5 TB/s of reads plus writes, with 32 KiB 4.1-4.3 TB/s, and a
+// grid-stride sweep with 8 granules per thread per round 5.25-5.36 TB/s.
+template <int G>
 __global__ __launch_bounds__(kProbeThreads) void copy_kernel(const u32x4* __restrict__ src, u32x4* __restrict__ dst,
                                                              int64_t granules) {
-  const int64_t step = (int64_t)gridDim.x * kProbeThreads * kProbeUnroll;
-  for (int64_t base = (int64_t)blockIdx.x * kProbeThreads * kProbeUnroll + threadIdx.x; base < granules;
-       base += step) {
-    u32x4 x[kProbeUnroll];
+  const int64_t base = (int64_t)blockIdx.x * kProbeThreads * G + threadIdx.x;
+  u32x4 x[G];
 #pragma unroll
-    for (int u = 0; u < kProbeUnroll; ++u) {
-      const int64_t i = base + (int64_t)u * kProbeThreads;
-      if (i < granules) x[u] = __builtin_nontemporal_load(src + i);
-    }
+  for (int u = 0; u < G; ++u) {
+    const int64_t i = base + (int64_t)u * kProbeThreads;
+    if (i < granules) x[u] = __builtin_nontemporal_load(src + i);
+  }
 #pragma unroll
-    for (int u = 0; u < kProbeUnroll; ++u) {
-      const int64_t i = base + (int64_t)u * kProbeThreads;
-      if (i < granules) __builtin_nontemporal_store(x[u], dst + i);
-    }
+  for (int u = 0; u < G; ++u) {
+    const int64_t i = base + (int64_t)u * kProbeThreads;
+    if (i < granules) __builtin_nontemporal_store(x[u], dst + i);
   }
 }
 
@@ -84,15 +83,29 @@ extern "C" dkv_status dkv_probe_stream_read(const void* src, int64_t bytes, void
   return hipGetLastError() == hipSuccess ? DKV_OK : DKV_ERR_HIP;
 }
 
-extern "C" dkv_status dkv_probe_copy(const void* src, void* dst, int64_t bytes, int32_t workgroups, void* stream) {
-  if (bytes < 0 || bytes % 16 != 0 || workgroups < 1 || workgroups > 65535) return DKV_ERR_INVALID_ARG;
+extern "C" dkv_status dkv_probe_copy(const void* src, void* dst, int64_t bytes, int32_t granules_per_thread,
+                                     void* stream) {
+  const int g = granules_per_thread;
+  if (bytes < 0 || bytes % 16 != 0 || (g != 1 && g != 2 && g != 4 && g != 8)) return DKV_ERR_INVALID_ARG;
   if (bytes == 0) return DKV_OK;
   if (src == nullptr || dst == nullptr) return DKV_ERR_INVALID_ARG;
   if (!aligned16(src) || !aligned16(dst)) return DKV_ERR_MISALIGNED;
   const char* s = static_cast<const char*>(src);
   char* d = static_cast<char*>(dst);
   if (s < d + bytes && d < s + bytes) return DKV_ERR_INVALID_ARG;  // overlapping buffers
-  hipLaunchKernelGGL(copy_kernel, dim3(workgroups), dim3(kProbeThreads), 0, (hipStream_t)stream,
-                     static_cast<const u32x4*>(src), static_cast<u32x4*>(dst), bytes / 16);
+  const int64_t granules = bytes / 16;
+  const int64_t per = (int64_t)kProbeThreads * g;
+  const int64_t blocks = (granules + per - 1) / per;
+  if (blocks > 2147483647LL) return DKV_ERR_UNSUPPORTED;
+  const dim3 grid((unsigned)blocks);
+  const u32x4* s16 = static_cast<const u32x4*>(src);
+  u32x4* d16 = static_cast<u32x4*>(dst);
+  hipStream_t st = (hipStream_t)stream;
+  switch (g) {
+    case 1: hipLaunchKernelGGL(copy_kernel<1>, grid, dim3(kProbeThreads), 0, st, s16, d16, granules); break;
+    case 2: hipLaunchKernelGGL(copy_kernel<2>, grid, dim3(kProbeThreads), 0, st, s16, d16, granules); break;
+    case 4: hipLaunchKernelGGL(copy_kernel<4>, grid, dim3(kProbeThreads), 0, st, s16, d16, granules); break;
+    default: hipLaunchKernelGGL(copy_kernel<8>, grid, dim3(kProbeThreads), 0, st, s16, d16, granules); break;
+  }
   return hipGetLastError() == hipSuccess ? DKV_OK : DKV_ERR_HIP;
 }

@@ -10,6 +10,7 @@
 #include <cstdint>
 #include <cstring>
 
+#include "dkv_bins.hpp"
 #include "dkv_launch.hpp"
 
 namespace {
@@ -83,19 +84,29 @@ const char* dkv_status_string(dkv_status status) {
 
 namespace {
 
-dkv_status map_pattern(const dkv_layout* layout, const int32_t* unit_len, const uint8_t* pattern,
-                       uint8_t* kv_mask, int32_t* kv_len, uint8_t* q_mask, void* stream) {
-  dkv_status st = check_shape(layout);
-  if (st != DKV_OK) return st;
-  const dkv_layout& L = *layout;
+// Bin edges: E[0] = 0 and strictly increasing, within the limits for
+// uniform or general edges.  *W is the uniform width (0: general edges).
+dkv_status check_edges(const dkv_layout& L, int32_t* W) {
   if (L.num_bins < 1 || L.bin_edges == nullptr) return DKV_ERR_INVALID_ARG;
   const int32_t* e = L.bin_edges;
   if (e[0] != 0) return DKV_ERR_INVALID_ARG;
   for (int32_t k = 0; k < L.num_bins; ++k)
     if (!(e[k + 1] > e[k])) return DKV_ERR_INVALID_ARG;
-  const int32_t W = uniform_width(e, L.num_bins);
-  if (W > 0 ? L.num_bins > DKV_MAX_UNIFORM_BINS : L.num_bins > DKV_MAX_GENERAL_BINS)
+  *W = uniform_width(e, L.num_bins);
+  if (*W > 0 ? L.num_bins > DKV_MAX_UNIFORM_BINS : L.num_bins > DKV_MAX_GENERAL_BINS)
     return DKV_ERR_UNSUPPORTED;
+  return DKV_OK;
+}
+
+dkv_status map_pattern(const dkv_layout* layout, const int32_t* unit_len, const uint8_t* pattern,
+                       uint8_t* kv_mask, int32_t* kv_len, uint8_t* q_mask, void* stream) {
+  dkv_status st = check_shape(layout);
+  if (st != DKV_OK) return st;
+  const dkv_layout& L = *layout;
+  int32_t W = 0;
+  st = check_edges(L, &W);
+  if (st != DKV_OK) return st;
+  const int32_t* e = L.bin_edges;
   if (L.num_units == 0) return DKV_OK;
   // With T = 0 there is no mask byte to write, so the mask pointers may be null.
   if (pattern == nullptr || kv_len == nullptr || (kv_mask == nullptr && L.context_len > 0))
@@ -190,6 +201,72 @@ dkv_status dkv_compact(const dkv_layout* layout, dkv_dtype dtype, const void* k,
   p.cap = append_cap;
   p.row_bytes = L.head_dim * elem_bytes(dtype);
   return hip_status(dkv::launch_compact(p, (hipStream_t)stream));
+}
+
+size_t dkv_compact_bins_workspace_bytes(const dkv_layout* layout) {
+  if (layout == nullptr || layout->num_units < 0 || layout->num_kv_heads <= 0 || layout->context_len < 0 ||
+      layout->num_bins < 1)
+    return 0;
+  const int64_t nseg = (int64_t)layout->num_units * layout->num_kv_heads;
+  if (nseg > 65535 || nseg * ((int64_t)layout->num_bins + 3) > (int64_t(1) << 27)) return 0;
+  return dkv::bins_workspace_bytes(nseg, layout->num_bins, layout->context_len);
+}
+
+dkv_status dkv_compact_bins(const dkv_layout* layout, dkv_dtype dtype, const void* k, const void* v,
+                            const uint8_t* pattern, int32_t append_cap, void* k_out, void* v_out,
+                            int64_t out_rows, int64_t* seg_off, int32_t* seg_len, int32_t* src_pos,
+                            int64_t* rows_needed, void* workspace, size_t workspace_bytes, void* stream) {
+  dkv_status st = check_shape(layout);
+  if (st != DKV_OK) return st;
+  const dkv_layout& L = *layout;
+  int32_t W = 0;
+  st = check_edges(L, &W);
+  if (st != DKV_OK) return st;
+  if (!dtype_ok(dtype) || append_cap < 0 || out_rows < 0) return DKV_ERR_INVALID_ARG;
+  if (!head_dim_ok(L.head_dim)) return DKV_ERR_UNSUPPORTED;
+  const int64_t nseg = (int64_t)L.num_units * L.num_kv_heads;
+  if (nseg > 65535 || nseg * ((int64_t)L.num_bins + 3) > (int64_t(1) << 27)) return DKV_ERR_UNSUPPORTED;
+  if (nseg == 0) return DKV_OK;
+  if (k == nullptr || v == nullptr || pattern == nullptr || k_out == nullptr || v_out == nullptr ||
+      seg_off == nullptr || seg_len == nullptr)
+    return DKV_ERR_INVALID_ARG;
+  if (!aligned16(k) || !aligned16(v) || !aligned16(k_out) || !aligned16(v_out)) return DKV_ERR_MISALIGNED;
+  if (workspace == nullptr || workspace_bytes < dkv_compact_bins_workspace_bytes(layout))
+    return DKV_ERR_WORKSPACE;
+
+  dkv::BinsParams p;
+  std::memset(&p, 0, sizeof(p));
+  const int32_t D = L.num_bins;
+  p.pattern = pattern;
+  p.k = k;
+  p.v = v;
+  p.k_out = k_out;
+  p.v_out = v_out;
+  p.item_pos = static_cast<int32_t*>(workspace);
+  p.item_dst = p.item_pos + nseg * (D + 2);
+  p.item_cnt = p.item_dst + nseg * (D + 3);
+  p.lens = p.item_cnt + nseg;
+  p.chunk_first = p.lens + nseg;
+  p.seg_off = seg_off;
+  p.seg_len = seg_len;
+  p.src_pos = src_pos;
+  p.rows_needed = rows_needed;
+  p.out_rows = out_rows;
+  p.T = L.context_len;
+  p.S = L.sink;
+  p.R = L.recent;
+  p.D = D;
+  p.Hq = L.num_q_heads;
+  p.Hkv = L.num_kv_heads;
+  p.G = L.num_q_heads / L.num_kv_heads;
+  p.nseg = (int32_t)nseg;
+  p.cap = append_cap;
+  p.row_bytes = L.head_dim * elem_bytes(dtype);
+  p.nchunks = (int32_t)(((int64_t)L.context_len + dkv::kBinsChunkRows - 1) / dkv::kBinsChunkRows);
+  p.uniform_width = W;
+  if (W == 0)
+    for (int32_t i = 0; i <= D; ++i) p.edges[i] = L.bin_edges[i];
+  return hip_status(dkv::launch_compact_bins(p, (hipStream_t)stream));
 }
 
 dkv_status dkv_append(dkv_dtype dtype, int32_t num_segments, int32_t head_dim, const void* k_new,

@@ -102,6 +102,42 @@ def test_compact_validation():
     assert _compact(_lay(N=0), k=NUL) == d.DKV_OK
 
 
+def _compact_bins(lay, dtype=d.DKV_BF16, k=A, v=A, pattern=A, cap=4, k_out=A, v_out=A, out_rows=100,
+                  seg_off=A, seg_len=A, ws=A, ws_bytes=None):
+    if ws_bytes is None:
+        ws_bytes = d.dkv_compact_bins_workspace_bytes(lay)
+    return d.library().dkv_compact_bins(ctypes.byref(lay), dtype, k, v, pattern, cap, k_out, v_out,
+                                        out_rows, seg_off, seg_len, NUL, NUL, ws, ws_bytes, NUL)
+
+
+def test_compact_bins_validation():
+    ws = d.dkv_compact_bins_workspace_bytes(_lay())
+    # per segment: kept ranges (D + 2), their packed rows (D + 3), count, length, and the
+    # head of every 32-row chunk (T / 32 of them)
+    assert ws == 4 * 2 * ((3 + 2) + (3 + 3) + 1 + 1 + 1024 // 32) + 256
+    assert d.dkv_compact_bins_workspace_bytes(_lay(N=-1)) == 0
+    assert d.dkv_compact_bins_workspace_bytes(_lay(N=40000, Hq=2, Hkv=2)) == 0  # segments
+    assert d.dkv_compact_bins_workspace_bytes(_lay(N=30000, Hq=2, Hkv=2, edges=[3 * k for k in range(3001)])) == 0
+    assert _compact_bins(_lay(dim=96)) == d.DKV_ERR_UNSUPPORTED
+    assert _compact_bins(_lay(), dtype=7) == d.DKV_ERR_INVALID_ARG
+    assert _compact_bins(_lay(), cap=-1) == d.DKV_ERR_INVALID_ARG
+    assert _compact_bins(_lay(), out_rows=-1) == d.DKV_ERR_INVALID_ARG
+    assert _compact_bins(_lay(edges=(0, 9, 5))) == d.DKV_ERR_INVALID_ARG
+    assert _compact_bins(_lay(edges=(1, 5, 9))) == d.DKV_ERR_INVALID_ARG
+    assert _compact_bins(_lay(edges=[0] + [k * k + 1 for k in range(1, 514)])) == d.DKV_ERR_UNSUPPORTED
+    assert _compact_bins(_lay(Hq=6, Hkv=4)) == d.DKV_ERR_INVALID_ARG
+    assert _compact_bins(_lay(), k=NUL) == d.DKV_ERR_INVALID_ARG
+    assert _compact_bins(_lay(), pattern=NUL) == d.DKV_ERR_INVALID_ARG
+    assert _compact_bins(_lay(), seg_len=NUL) == d.DKV_ERR_INVALID_ARG
+    assert _compact_bins(_lay(), v=MIS) == d.DKV_ERR_MISALIGNED
+    assert _compact_bins(_lay(), v_out=MIS) == d.DKV_ERR_MISALIGNED
+    assert _compact_bins(_lay(), ws=NUL) == d.DKV_ERR_WORKSPACE
+    assert _compact_bins(_lay(), ws_bytes=ws - 1) == d.DKV_ERR_WORKSPACE
+    assert _compact_bins(_lay(N=40000, Hq=2, Hkv=2)) == d.DKV_ERR_UNSUPPORTED
+    assert _compact_bins(_lay(N=10000, Hq=2, Hkv=2, edges=list(range(16385)))) == d.DKV_ERR_UNSUPPORTED
+    assert _compact_bins(_lay(N=0), k=NUL, pattern=NUL) == d.DKV_OK
+
+
 def _append(dtype=d.DKV_BF16, nseg=4, dim=128, kn=A, vn=A, n_new=1, n_tail=0, cap=2, kc=A, vc=A,
             so=A, sl=A):
     return d.library().dkv_append(dtype, nseg, dim, kn, vn, n_new, n_tail, cap, kc, vc, so, sl, NUL)
@@ -203,8 +239,10 @@ def test_probe_validation():
     assert lib.dkv_probe_copy(A, B, 0, 1, NUL) == d.DKV_OK  # nothing to copy
     assert lib.dkv_probe_copy(A, B, -16, 1, NUL) == d.DKV_ERR_INVALID_ARG
     assert lib.dkv_probe_copy(A, B, 24, 1, NUL) == d.DKV_ERR_INVALID_ARG
-    assert lib.dkv_probe_copy(A, B, 4096, 0, NUL) == d.DKV_ERR_INVALID_ARG
-    assert lib.dkv_probe_copy(A, B, 4096, 65536, NUL) == d.DKV_ERR_INVALID_ARG
+    for g in (0, 3, 16, -1):
+        assert lib.dkv_probe_copy(A, B, 4096, g, NUL) == d.DKV_ERR_INVALID_ARG
+    assert lib.dkv_probe_copy(A, ctypes.c_void_p(A.value + (1 << 44)), (1 << 31) * 4096 + 16, 1,
+                              NUL) == d.DKV_ERR_UNSUPPORTED  # 2^31 blocks
     assert lib.dkv_probe_copy(NUL, B, 4096, 1, NUL) == d.DKV_ERR_INVALID_ARG
     assert lib.dkv_probe_copy(A, NUL, 4096, 1, NUL) == d.DKV_ERR_INVALID_ARG
     assert lib.dkv_probe_copy(A, A, 4096, 1, NUL) == d.DKV_ERR_INVALID_ARG  # overlapping

@@ -97,6 +97,31 @@ def test_map_and_ragged_map_stay_inside(d):
     assert km.intact() and kl.intact() and qm.intact()
 
 
+@pytest.mark.parametrize("short", [False, True])
+def test_compact_bins_stays_inside(d, short):
+    """The block gather from the pattern, with room for every segment and
+    with out_rows one short of it (some segments marked unpacked)."""
+    lay, pattern, k, v, _ = _setup(d)
+    pk = _pack(d, lay, pattern, k, v)
+    rows = pk["rows"] - (1 if short else 0)
+    gb = {
+        "k": Guarded((rows, DIM), torch.bfloat16, 0), "v": Guarded((rows, DIM), torch.bfloat16, 0),
+        "off": Guarded((N * HKV,), torch.int64), "len": Guarded((N * HKV,), torch.int32),
+        "src": Guarded((rows,), torch.int32), "need": Guarded((1,), torch.int64),
+        "ws": _ws(d.dkv_compact_bins_workspace_bytes(lay)),
+    }
+    d.dkv_compact_bins(lay, k, v, pattern, CAP, gb["k"].t, gb["v"].t, gb["off"].t, gb["len"].t, gb["ws"].t,
+                       src_pos=gb["src"].t, rows_needed=gb["need"].t)
+    for name, gbuf in gb.items():
+        assert gbuf.intact(), f"dkv_compact_bins wrote outside {name}"
+    assert int(gb["need"].t.item()) == pk["rows"]
+    if not short:
+        assert torch.equal(gb["k"].t.view(torch.int16), pk["k"].t.view(torch.int16))
+        assert torch.equal(gb["len"].t, pk["len"].t)
+    else:
+        assert bool((gb["len"].t < 0).any())
+
+
 def test_append_and_decode_calls_stay_inside(d):
     lay, pattern, k, v, g = _setup(d)
     pk = _pack(d, lay, pattern, k, v)

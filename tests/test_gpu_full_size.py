@@ -7,7 +7,8 @@ with the same rows_hint and workspace as the benchmark.  Checked against the
 oracle, layer by layer (dense K/V streamed back one layer at a time):
 
 * packing: lengths, offsets and every packed row bit-exact, and after the
-  last step the appended rows too;
+  last step the appended rows too; the block gather (dkv_compact_bins) of
+  the same stack equal to map + compact's pack in every output;
 * attention: every layer at the first and at the last step, and sampled
   (step, layer) pairs in between: for each intermediate step of the 8B stack
   one layer drawn by a seeded generator, for every 32nd intermediate step of
@@ -68,6 +69,7 @@ class StackRun:
             self.v[u].copy_(vu)
         lay = d.make_layout(N, Hq, Hkv, dim, T, w.sink, w.recent, list(w.bin_edges))
         self.pack = GpuPack(d, lay, self.pattern, self.k, self.v, cap)
+        self.bins_equal = self._bins_pack(d, lay, cap)
         lens = self.pack.kv_len.cpu().to(torch.int64)
         nseg = B * Hkv
         layer_rows = [int(lens[layer * B:(layer + 1) * B].sum()) for layer in range(L)]
@@ -89,6 +91,27 @@ class StackRun:
                     self.outs[(s, layer)] = out.clone()
         torch.cuda.synchronize()
         self._okm = None
+
+    def _bins_pack(self, d, lay, cap):
+        """The same stack packed by the block gather straight from the pattern,
+        compared with map + compact's pack (before any append): offsets,
+        lengths, rows_needed, every source position and every packed row."""
+        pk = self.pack
+        kb, vb = torch.empty_like(pk.k_c), torch.empty_like(pk.v_c)
+        so, sl = torch.empty_like(pk.seg_off), torch.empty_like(pk.seg_len)
+        sp = torch.full_like(pk.src_pos, -7)
+        rn = torch.empty_like(pk.rows_needed)
+        ws = torch.empty(d.dkv_compact_bins_workspace_bytes(lay), dtype=torch.uint8, device=DEV)
+        d.dkv_compact_bins(lay, self.k, self.v, pk.pattern, cap, kb, vb, so, sl, ws, src_pos=sp, rows_needed=rn)
+        kept = pk.src_pos >= 0  # the packed rows (free append rows keep -7)
+        eq = {"seg_off": torch.equal(so, pk.seg_off), "seg_len": torch.equal(sl, pk.seg_len),
+              "rows_needed": torch.equal(rn, pk.rows_needed), "src_pos": torch.equal(sp, pk.src_pos),
+              "k": torch.equal(kb[kept].view(torch.int16), pk.k_c[kept].view(torch.int16)),
+              "v": torch.equal(vb[kept].view(torch.int16), pk.v_c[kept].view(torch.int16)),
+              "packed_rows": int(kept.sum())}
+        del kb, vb, ws
+        torch.cuda.empty_cache()
+        return eq
 
     def _oracle_map(self):
         """The oracle's masks for the whole stack (computed once), after checking
@@ -161,11 +184,26 @@ def test_headline_stack_full_size(headline, chunk):
     headline.check_layers(range(8 * chunk, 8 * chunk + 8))
 
 
+def test_headline_stack_bins_pack(headline):
+    """dkv_compact_bins packs the whole 8B stack exactly as map + compact,
+    whose rows the layer tests compare with the oracle."""
+    eq = headline.bins_equal
+    assert eq["packed_rows"] == int(headline.pack.kv_len.sum())
+    assert all(v for key, v in eq.items() if key != "packed_rows"), eq
+
+
 @pytest.mark.parametrize("chunk", range(7))
 def test_qwen_stack_full_size(qwen, chunk):
     """Qwen-7B-shaped stack at 128K, 28 layers x 4 sequences, 256 steps:
     layers 4*chunk .. 4*chunk+3."""
     qwen.check_layers(range(4 * chunk, 4 * chunk + 4))
+
+
+def test_qwen_stack_bins_pack(qwen):
+    """The same for the Qwen-shaped stack (G = 7, four sequences per layer)."""
+    eq = qwen.bins_equal
+    assert eq["packed_rows"] == int(qwen.pack.kv_len.sum())
+    assert all(v for key, v in eq.items() if key != "packed_rows"), eq
 
 
 def test_qwen_all_keep_layer_equals_dense(d):

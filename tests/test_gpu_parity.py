@@ -683,3 +683,17 @@ def test_probe_stream_read_runs(d):
     for wg in (1, 3, 256, 2048):
         d.dkv_probe_stream_read(src, sink, wg)
     torch.cuda.synchronize()
+
+
+def test_probe_copy_copies(d):
+    """The copy probe copies every byte, with each block size, over lengths
+    that end inside a block, and touches nothing past `nbytes`."""
+    g = torch.Generator(device=DEV).manual_seed(5)
+    src = torch.randint(0, 256, ((1 << 20) + 4096,), dtype=torch.uint8, device=DEV, generator=g)
+    for gpt in (1, 2, 4, 8):
+        for n in (16, 4096 * gpt - 16, 4096 * gpt, (1 << 20) + 48):
+            dst = torch.full_like(src, 0xA5)
+            d.dkv_probe_copy(src, dst, gpt, nbytes=n)
+            torch.cuda.synchronize()
+            assert torch.equal(dst[:n], src[:n]), (gpt, n)
+            assert bool((dst[n:] == 0xA5).all()), (gpt, n)
