@@ -1142,11 +1142,14 @@ def main():
     cws = torch.empty(d.dkv_compact_workspace_bytes(lay), dtype=torch.uint8, device=dev)
     d.dkv_compact(lay, k, v, kv_mask, cap, k_c, v_c, seg_off, seg_len, cws)  # loads the code objects
     torch.cuda.synchronize()
-    e1.record(stream)
-    d.dkv_compact(lay, k, v, kv_mask, cap, k_c, v_c, seg_off, seg_len, cws)
-    e2.record(stream)
-    torch.cuda.synchronize()
-    compact_us = e1.elapsed_time(e2) * 1e3
+    compact_ms = []
+    for _ in range(3):  # best of three single calls (as for dkv_compact_bins below)
+        e1.record(stream)
+        d.dkv_compact(lay, k, v, kv_mask, cap, k_c, v_c, seg_off, seg_len, cws)
+        e2.record(stream)
+        torch.cuda.synchronize()
+        compact_ms.append(e1.elapsed_time(e2))
+    compact_us = min(compact_ms) * 1e3
     retained = int(lens.sum())
     compact_bytes = 2 * 2 * retained * dim * elem + N * Hkv * T  # K,V read+write + mask
     phys_frac = retained / float(N * Hkv * T)
@@ -2017,6 +2020,7 @@ def main():
                              "step": "per layer: dkv_decode_attn (attend only); HIP-graph replays",
                              **fam_res},
         "one_time": {"map_us": round(map_us, 1), "compact_us": round(compact_us, 1),
+                     "compact_timing": "best of 3 single calls, each between synchronisations",
                      "compact_bytes": int(compact_bytes),
                      "compact_gb_per_s": round(compact_bytes / (compact_us * 1e-6) / 1e9, 1),
                      "compact_bins_us": round(bins_us, 1), "compact_bins_bytes": int(bins_bytes),

@@ -1,20 +1,27 @@
 // One-time prune and pack of the KV cache (Distance-KV, Sec. 3.4 / Fig. 2(b)),
 // and the append of new tokens.
 //
-// The pack is an order-preserving stream compaction in three passes over the
-// (segment, 4096-position tile) grid:
-//   count   each tile counts its retained positions (16 mask bytes per lane,
-//           nonzero-byte popcount, block reduction);
+// The pack is an order-preserving stream compaction in three passes:
+//   count   each (segment, 4096-position tile) counts its retained positions
+//           (16 mask bytes per lane, nonzero-byte popcount, block scan) and
+//           records where each of its kCompactSub-position sub-tiles starts
+//           in the tile's rank order;
 //   scan    one workgroup turns tile counts into each tile's first rank within
 //           its segment, the segment lengths, and the segment offsets
 //           (running sum of length + append capacity, unit-major);
-//   gather  two workgroups per tile, one for K and one for V, each rebuild
-//           the tile's ranks with a block scan, list its retained positions
-//           in rank order in LDS, and copy the rows: LPR lanes move one row
-//           with 16-byte loads and stores (LPR = row bytes / 16), so a wave
-//           moves 64/LPR whole rows per instruction, 8 rows per lane group in
-//           flight.  (One workgroup copying both K and V ran 6% slower: four
-//           interleaved streams per workgroup instead of two.)
+//   gather  two workgroups of 256 lanes per sub-tile, one for K and one for
+//           V, each rank the sub-tile's positions with a block scan, list the
+//           retained ones in LDS, and copy the rows: LPR lanes move one row
+//           with 16-byte non-temporal loads and stores (LPR = row bytes / 16),
+//           so a wave moves 64/LPR whole rows per instruction and a lane
+//           group moves at most kCompactSub * LPR / 256 rows.
+// Short workgroups copy fastest.  On the Llama-3.1-8B-shaped 128K stack (35%
+// kept) whole 4096-position tiles per gather workgroup took 2.50-2.55 ms
+// whatever the rows in flight per lane group (1 to 8); sub-tiles of 256, 128,
+// 64 and 32 positions took 2.18, 2.09-2.10, 2.06-2.07 and 2.48-2.50 ms, and
+// on the Qwen-shaped stack 2.78-2.80, 2.65-2.68, 2.81 and 3.72 ms (with 32
+// the launch holds two to four million workgroups).  (One workgroup copying both K
+// and V ran 6% slower: four interleaved streams per workgroup instead of two.)
 // All row arithmetic is 64-bit: a whole-stack cache has more than 2^31 elements.
 
 #include "dkv_device.hpp"
@@ -37,8 +44,12 @@ __global__ __launch_bounds__(kThreads) void compact_count_kernel(CompactParams p
   const u32x4 w = load_mask16(row, j0, p.T);
   const int64_t c = nonzero_bytes(w[0]) + nonzero_bytes(w[1]) + nonzero_bytes(w[2]) + nonzero_bytes(w[3]);
   int64_t total;
-  block_exclusive_scan<kThreads>(c, red, &total);
-  if (threadIdx.x == 0) p.tile_cnt[(int64_t)seg * p.ntiles + tile] = (int32_t)total;
+  const int64_t before = block_exclusive_scan<kThreads>(c, red, &total);
+  const int64_t ti = (int64_t)seg * p.ntiles + tile;
+  if (threadIdx.x == 0) p.tile_cnt[ti] = (int32_t)total;
+  constexpr int kLanesPerSub = kCompactSub / kPerThread;
+  if (threadIdx.x % kLanesPerSub == 0)  // rank of the sub-tile's first position: < 4096
+    p.sub_base[ti * kCompactSubPerTile + threadIdx.x / kLanesPerSub] = (uint16_t)before;
 }
 
 constexpr int kScanThreads = 1024;
@@ -82,53 +93,51 @@ __global__ __launch_bounds__(kScanThreads) void compact_scan_kernel(CompactParam
   if (threadIdx.x == 0 && p.rows_needed != nullptr) *p.rows_needed = carry;
 }
 
-template <int LPR>
-__global__ __launch_bounds__(kThreads) void compact_gather_kernel(CompactParams p) {
-  constexpr int kRowsPerPass = kThreads / LPR;
-  constexpr int kUnroll = 8;
-  __shared__ uint16_t list[kCompactTile];
-  __shared__ int64_t red[kThreads / kWave + 1];
+constexpr int kGatherThreads = 256;  // lanes < kCompactSub each rank one position
+static_assert(kCompactSub <= kGatherThreads && kCompactSub % 16 == 0, "sub-tile fits the workgroup");
 
-  const int tile = blockIdx.x >> 1;
+template <int LPR>
+__global__ __launch_bounds__(kGatherThreads) void compact_gather_kernel(CompactParams p) {
+  constexpr int kRowsPerPass = kGatherThreads / LPR;
+  constexpr int kPasses = (kCompactSub + kRowsPerPass - 1) / kRowsPerPass;
+  constexpr int kUnroll = kPasses < 8 ? kPasses : 8;  // rows per lane group in flight
+  __shared__ uint16_t list[kCompactSub];
+  __shared__ int64_t red[kGatherThreads / kWave + 1];
+
+  const int sub = blockIdx.x >> 1;
   const int which = blockIdx.x & 1;  // 0: K rows (and source positions), 1: V rows
   const int seg = blockIdx.y;
   const int tid = threadIdx.x;
   if (p.seg_len[seg] < 0) return;  // not packed: it does not fit below out_rows
-  const uint8_t* mrow = p.mask + (int64_t)seg * p.T;
-  const int64_t jt = (int64_t)tile * kCompactTile;
-  const u32x4 w = load_mask16(mrow, jt + tid * kPerThread, p.T);
-  const uint32_t bits = nonzero_byte_bits(w);
+  const int64_t js = (int64_t)sub * kCompactSub;
+  const bool keep = tid < kCompactSub && js + tid < p.T && p.mask[(int64_t)seg * p.T + js + tid] != 0;
   int64_t kept;
-  int rank = (int)block_exclusive_scan<kThreads>(__popc(bits), red, &kept);
-#pragma unroll
-  for (int e = 0; e < kPerThread; ++e)
-    if ((bits >> e) & 1u) list[rank++] = (uint16_t)(tid * kPerThread + e);
+  const int rank = (int)block_exclusive_scan<kGatherThreads>(keep ? 1 : 0, red, &kept);
+  if (keep) list[rank] = (uint16_t)tid;
   __syncthreads();
+  if (kept == 0) return;  // (the same for every lane)
 
-  const int64_t dst0 = p.seg_off[seg] + p.tile_base[(int64_t)seg * p.ntiles + tile];
-  const int64_t src0 = (int64_t)seg * p.T + jt;
+  const int tile = sub / kCompactSubPerTile;
+  const int64_t ti = (int64_t)seg * p.ntiles + tile;
+  const int64_t dst0 = p.seg_off[seg] + p.tile_base[ti] + p.sub_base[ti * kCompactSubPerTile + (sub - tile * kCompactSubPerTile)];
+  const int64_t src0 = (int64_t)seg * p.T + js;
   const int lane = tid % LPR;
-  const int64_t stride16 = p.row_bytes / 16;  // == LPR
   const u32x4* src = reinterpret_cast<const u32x4*>(which ? p.v : p.k);
   u32x4* dst = reinterpret_cast<u32x4*>(which ? p.v_out : p.k_out);
 
   for (int r0 = tid / LPR; r0 < kept; r0 += kRowsPerPass * kUnroll) {
     u32x4 rb[kUnroll];
-    int64_t drow[kUnroll];
-    bool ok[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int r = r0 + u * kRowsPerPass;
-      drow[u] = dst0 + r;
-      ok[u] = r < kept;
-      if (ok[u]) rb[u] = src[(src0 + list[r]) * stride16 + lane];
+      if (r < kept) rb[u] = __builtin_nontemporal_load(&src[(src0 + list[r]) * LPR + lane]);
     }
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-      if (ok[u]) {
-        dst[drow[u] * stride16 + lane] = rb[u];
-        if (which == 0 && lane == 0 && p.src_pos != nullptr)
-          p.src_pos[drow[u]] = (int32_t)(jt + list[r0 + u * kRowsPerPass]);
+      const int r = r0 + u * kRowsPerPass;
+      if (r < kept) {
+        __builtin_nontemporal_store(rb[u], &dst[(dst0 + r) * LPR + lane]);
+        if (which == 0 && lane == 0 && p.src_pos != nullptr) p.src_pos[dst0 + r] = (int32_t)(js + list[r]);
       }
     }
   }
@@ -155,7 +164,7 @@ __global__ __launch_bounds__(kThreads) void append_kernel(AppendParams p) {
 size_t compact_workspace_bytes(int64_t nseg, int64_t T) {
   const int64_t ntiles = (T + kCompactTile - 1) / kCompactTile;
   const int64_t n = nseg * (ntiles > 0 ? ntiles : 1);
-  return (size_t)(2 * n * 4 + 256);
+  return (size_t)(2 * n * 4 + n * kCompactSubPerTile * 2 + 256);  // tile counts, tile bases, sub-tile bases
 }
 
 hipError_t launch_compact(const CompactParams& p, hipStream_t stream) {
@@ -165,11 +174,12 @@ hipError_t launch_compact(const CompactParams& p, hipStream_t stream) {
   }
   hipLaunchKernelGGL(compact_scan_kernel, dim3(1), dim3(kScanThreads), 0, stream, p);
   if (p.ntiles > 0) {
-    const dim3 ggrid(2 * p.ntiles, p.nseg);  // a K and a V workgroup per tile
+    const int64_t nsub = ((int64_t)p.T + kCompactSub - 1) / kCompactSub;
+    const dim3 ggrid((uint32_t)(2 * nsub), p.nseg);  // a K and a V workgroup per sub-tile
     switch (p.row_bytes) {
-      case 128: hipLaunchKernelGGL(compact_gather_kernel<8>, ggrid, dim3(kThreads), 0, stream, p); break;
-      case 256: hipLaunchKernelGGL(compact_gather_kernel<16>, ggrid, dim3(kThreads), 0, stream, p); break;
-      case 512: hipLaunchKernelGGL(compact_gather_kernel<32>, ggrid, dim3(kThreads), 0, stream, p); break;
+      case 128: hipLaunchKernelGGL(compact_gather_kernel<8>, ggrid, dim3(kGatherThreads), 0, stream, p); break;
+      case 256: hipLaunchKernelGGL(compact_gather_kernel<16>, ggrid, dim3(kGatherThreads), 0, stream, p); break;
+      case 512: hipLaunchKernelGGL(compact_gather_kernel<32>, ggrid, dim3(kGatherThreads), 0, stream, p); break;
       default: return hipErrorInvalidValue;
     }
   }

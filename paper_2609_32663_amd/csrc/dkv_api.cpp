@@ -190,6 +190,7 @@ dkv_status dkv_compact(const dkv_layout* layout, dkv_dtype dtype, const void* k,
   p.v_out = v_out;
   p.tile_cnt = static_cast<int32_t*>(workspace);
   p.tile_base = p.tile_cnt + nseg * (ntiles > 0 ? ntiles : 1);
+  p.sub_base = reinterpret_cast<uint16_t*>(p.tile_base + nseg * (ntiles > 0 ? ntiles : 1));
   p.seg_off = seg_off;
   p.seg_len = seg_len;
   p.src_pos = src_pos;

@@ -33,7 +33,9 @@ int64_t map_blocks(int32_t T, int64_t num_segments);  // workgroups of one launc
 hipError_t launch_map_pattern(const MapParams& p, int num_segments, hipStream_t stream);
 
 // ---------------------------------------------------------------- compaction
-constexpr int kCompactTile = 4096;  // positions per compaction tile
+constexpr int kCompactTile = 4096;  // positions per compaction tile (count and scan)
+constexpr int kCompactSub = 128;    // positions per gather workgroup
+constexpr int kCompactSubPerTile = kCompactTile / kCompactSub;
 
 struct CompactParams {
   const uint8_t* mask;     // [nseg][T]
@@ -43,6 +45,7 @@ struct CompactParams {
   void* v_out;
   int32_t* tile_cnt;       // [nseg][ntiles] (workspace)
   int32_t* tile_base;      // [nseg][ntiles] (workspace)
+  uint16_t* sub_base;      // [nseg][ntiles][kCompactSubPerTile] rank of a sub-tile's first row in its tile (workspace)
   int64_t* seg_off;        // [nseg]
   int32_t* seg_len;        // [nseg]
   int32_t* src_pos;        // [out_rows] or null
