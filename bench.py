@@ -45,6 +45,8 @@ QUERY_SRCS = [os.path.join(ROOT, "paper_2609_32663_amd", "csrc", f)
               for f in ("query_attn.hip", "dkv_device.hpp", "dkv_query.hpp")]
 COMPACT_SRCS = [os.path.join(ROOT, "paper_2609_32663_amd", "csrc", f)
                 for f in ("compact.hip", "dkv_device.hpp", "dkv_launch.hpp")]
+BINS_SRCS = [os.path.join(ROOT, "paper_2609_32663_amd", "csrc", f)
+             for f in ("compact_bins.hip", "dkv_device.hpp", "dkv_bins.hpp")]
 
 
 def parse():
@@ -348,6 +350,24 @@ def pmc_summary(fetch_csv, write_csv, bench_log, command):
         if oc.get("compact_bytes"):
             res["compact_algorithmic_bytes"] = oc["compact_bytes"]
             res["compact_traffic_over_algorithmic"] = round(res["compact_traffic_bytes"] / oc["compact_bytes"], 4)
+    # the block gather from the pattern: the second plan / scan / copy triple
+    # (the first is its warm-up call), against its algorithmic bytes
+    res["compact_bins_kernel_sha256_16"] = kernel_hash(BINS_SRCS)
+    for key, path, counter in (("fetch", fetch_csv, "FETCH_SIZE"), ("write", write_csv, "WRITE_SIZE")):
+        rows = pmc_per_dispatch(path, counter)
+        calib = res[f"{key}_calibration"]
+        triples = [rows[i][1] + rows[i + 1][1] + rows[i + 2][1] for i in range(len(rows) - 2)
+                   if "bins_plan_kernel" in rows[i][0] and "bins_scan_kernel" in rows[i + 1][0]
+                   and "bins_copy_kernel" in rows[i + 2][0]]
+        if len(triples) >= 2:
+            res[f"compact_bins_{key}_bytes"] = int(triples[1] * 1024.0 * calib)
+    if "compact_bins_fetch_bytes" in res and "compact_bins_write_bytes" in res:
+        res["compact_bins_traffic_bytes"] = res["compact_bins_fetch_bytes"] + res["compact_bins_write_bytes"]
+        oc = b.get("one_time", {})
+        if oc.get("compact_bins_bytes"):
+            res["compact_bins_algorithmic_bytes"] = oc["compact_bins_bytes"]
+            res["compact_bins_traffic_over_algorithmic"] = round(
+                res["compact_bins_traffic_bytes"] / oc["compact_bins_bytes"], 4)
     with open(PMC_FILE, "w") as f:
         json.dump(res, f, indent=1)
         f.write("\n")
@@ -489,8 +509,9 @@ def bench_configs(ctx):
         map_us = timed_event(lambda: d.dkv_map_pattern(lay, pat, km, kl))
         lens = kl.cpu().to(torch.int64)
         rows = int((lens + cap).sum())
-        k_c = torch.empty((rows, w.head_dim), dtype=torch.bfloat16, device=dev)
-        v_c = torch.empty_like(k_c)
+        # zeroed, so the two packs' buffers agree on the free rows neither writes
+        k_c = torch.zeros((rows, w.head_dim), dtype=torch.bfloat16, device=dev)
+        v_c = torch.zeros_like(k_c)
         so = torch.empty(N * Hkv, dtype=torch.int64, device=dev)
         sl = torch.empty(N * Hkv, dtype=torch.int32, device=dev)
         ws = torch.empty(d.dkv_compact_workspace_bytes(lay), dtype=torch.uint8, device=dev)
@@ -498,7 +519,7 @@ def bench_configs(ctx):
         retained = int(lens.sum())
         c_bytes = 2 * 2 * retained * w.head_dim * elem + N * Hkv * T
         # the block gather from the pattern into a second buffer, checked against it
-        k_b, v_b = torch.empty_like(k_c), torch.empty_like(v_c)
+        k_b, v_b = torch.zeros_like(k_c), torch.zeros_like(v_c)
         so_b, sl_b = torch.empty_like(so), torch.empty_like(sl)
         bws = torch.empty(d.dkv_compact_bins_workspace_bytes(lay), dtype=torch.uint8, device=dev)
         b_us = timed_event(lambda: d.dkv_compact_bins(lay, k, v, pat, cap, k_b, v_b, so_b, sl_b, bws), reps=2)
@@ -1135,8 +1156,9 @@ def main():
     map_us = e0.elapsed_time(e1) * 1e3
     lens = kv_len.cpu().to(torch.int64)
     rows = int((lens + cap).sum())
-    k_c = torch.empty((rows, dim), dtype=torch.bfloat16, device=dev)
-    v_c = torch.empty_like(k_c)
+    # zeroed, so the two packs' buffers agree on the free rows neither writes
+    k_c = torch.zeros((rows, dim), dtype=torch.bfloat16, device=dev)
+    v_c = torch.zeros_like(k_c)
     seg_off = torch.empty(N * Hkv, dtype=torch.int64, device=dev)
     seg_len = torch.empty(N * Hkv, dtype=torch.int32, device=dev)
     cws = torch.empty(d.dkv_compact_workspace_bytes(lay), dtype=torch.uint8, device=dev)
@@ -1156,7 +1178,7 @@ def main():
     log(f"map {map_us:.0f} us, compact {compact_us:.0f} us, retained {phys_frac:.4f}")
     # the same pack straight from the pattern (block gather: no mask), into a
     # second buffer, checked bit for bit against dkv_compact's
-    k_b, v_b = torch.empty_like(k_c), torch.empty_like(v_c)
+    k_b, v_b = torch.zeros_like(k_c), torch.zeros_like(v_c)
     seg_off_b, seg_len_b = torch.empty_like(seg_off), torch.empty_like(seg_len)
     bws = torch.empty(d.dkv_compact_bins_workspace_bytes(lay), dtype=torch.uint8, device=dev)
     d.dkv_compact_bins(lay, k, v, pat_d, cap, k_b, v_b, seg_off_b, seg_len_b, bws)
@@ -1958,7 +1980,7 @@ def main():
 
     per_launch_bytes = nbytes / L
     achieved = per_launch_bytes / (launch_ms * 1e-3) / 1e9
-    traffic = None
+    traffic = compact_traffic = bins_traffic = None
     if os.path.exists(PMC_FILE):
         with open(PMC_FILE) as f:
             pmc = json.load(f)
@@ -1967,6 +1989,10 @@ def main():
             paged_res["traffic"] = pmc.get("paged_traffic_bytes_per_launch")
         if pmc.get("query_kernel_sha256_16") == kernel_hash(QUERY_SRCS):
             query_res["roofline"]["traffic"] = pmc.get("query_traffic_bytes_per_call")
+        if pmc.get("compact_kernel_sha256_16") == kernel_hash(COMPACT_SRCS):
+            compact_traffic = pmc.get("compact_traffic_bytes")
+        if pmc.get("compact_bins_kernel_sha256_16") == kernel_hash(BINS_SRCS):
+            bins_traffic = pmc.get("compact_bins_traffic_bytes")
 
     res = {
         "metric": METRIC,
@@ -2026,6 +2052,8 @@ def main():
                      "compact_bins_us": round(bins_us, 1), "compact_bins_bytes": int(bins_bytes),
                      "compact_bins_gb_per_s": round(bins_bytes / (bins_us * 1e-6) / 1e9, 1),
                      "compact_bins_equal_to_compact": bins_equal,
+                     # HBM bytes from FETCH_SIZE + WRITE_SIZE (calibrated) of the same sources, else null
+                     "compact_traffic": compact_traffic, "compact_bins_traffic": bins_traffic,
                      "copy_probe": {"kind": "dkv_probe_copy of the retained K and V bytes (read + write)",
                                     "bytes": int(2 * copy_bytes), "gb_per_s_by_block": copy_gbps,
                                     "best_gb_per_s": max(copy_gbps.values())},
