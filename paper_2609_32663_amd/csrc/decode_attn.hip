@@ -18,7 +18,7 @@
 // last-workgroup-merges scheme avoids device-scope fences, which on this part
 // are whole-L2 write-backs and cost more than the merge itself.
 //
-// Inside a workgroup the 4 waves take 32-key tiles round-robin, with the next
+// Inside a workgroup the 4 waves take 16-key tiles round-robin, with the next
 // tile's loads in flight while the current one is computed.  Per tile:
 //   * K rows go straight from HBM into MFMA operands: lane (j, kg) of a wave
 //     loads 16-byte chunks kg, kg+4, ... of key j (j = lane % 16), which is
@@ -39,7 +39,7 @@
 // Paged addressing (the zero-copy variant): K and V stay in a page pool and a
 // segment's rows are the page_rows slots of each of its entries (page, logical
 // page, lo, hi), so the split, the ring and the combine are the same.  Tiles
-// are aligned to the 32-row grid of that row space and never straddle a page;
+// are aligned to the 16-row grid of that row space and never straddle a page;
 // each tile gets its own buffer descriptor over the page rows from the tile's
 // start to the end of the attended slots, so slots past an entry's end (and
 // past the tokens appended so far) read zeros without touching memory, and the
@@ -57,7 +57,13 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / kWave;
-constexpr int kTK = 32;  // keys per wave tile
+// Keys per wave tile.  With one tile loading while the other is computed a
+// wave keeps 8 KiB of bf16 d128 K/V in flight, 32 KiB per compute unit: on
+// this part a stream with fewer bytes in flight per compute unit runs faster
+// (32-key tiles three deep, 128 KiB per unit: 40.4 us per headline call;
+// two deep, 64 KiB: 38.8; 16-key tiles two deep: 37.7; three or four deep
+// or two workgroups per unit: 38.3-39.2).
+constexpr int kTK = 16;
 
 #if DKV_PHASE_STAMPS
 // Phase-stamp build (a separate library, built on request; the product
@@ -147,7 +153,7 @@ __device__ __forceinline__ float group_sum(float x) {
 }
 
 // K and V registers of one wave tile.  Paged tiles also carry the range
-// [lo, hi) of their 32 rows that is attended.
+// [lo, hi) of their kTK rows that is attended.
 template <bool BF16, int D, int GP>
 struct Tile {
   using C = DecodeCfg<BF16, D, GP>;
@@ -352,18 +358,12 @@ __device__ __forceinline__ void build_row_prefix(const DecodeParams& p, int64_t 
   __syncthreads();
 }
 
-// Register tiles in flight per wave (pipeline depth of the K/V stream).
+// Register tiles per wave (pipeline depth of the K/V stream): the ring keeps
+// S - 1 tiles loading, about 8 KiB per wave (bf16 d64 tiles are half that,
+// fp32 d128 ones twice).
 template <bool BF16, int D, int GP>
 constexpr int decode_stages() {
-  return (!BF16 && D == 128) ? 2 : 3;  // fp32 d128 tiles are twice as large
-}
-
-// Waves per SIMD the register budget is sized for: two only for a two-stage
-// ring small enough to fit 256 VGPRs; otherwise one wave per SIMD with up to
-// 512 registers, relying on the ring's depth for bytes in flight.
-template <bool BF16, int D, int GP>
-constexpr int decode_waves_per_eu() {
-  return (decode_stages<BF16, D, GP>() == 2 && GP == 4 && (BF16 || D == 64)) ? 2 : 1;
+  return (BF16 && D == 64) ? 3 : 2;
 }
 
 constexpr int kEntryChunk = kWave;  // paged entries held per wave (one per lane)
@@ -424,8 +424,7 @@ __device__ __forceinline__ void paged_tile(const DecodeParams& p, const PagedEnt
 }
 
 template <bool BF16, int D, int GP, bool PAGED>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(decode_waves_per_eu<BF16, D, GP>())))
-void decode_kernel(DecodeParams p) {
+__global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
   using C = DecodeCfg<BF16, D, GP>;
   extern __shared__ __align__(16) int64_t pre[];          // [nseg + 1] unit prefix, then [nseg] offsets / rows
   int64_t* offs = pre + p.nseg + 1;
@@ -864,13 +863,12 @@ std::atomic<int>& stamp_slot_counter() {
 int stamp_next_slot() { return stamp_slot_counter().fetch_add(1) % kStampCalls; }
 #endif
 
-// Split count: about one 128-row slice per workgroup, capped at the number of
-// workgroups the device holds at once (so every slice starts immediately and
-// all finish together) and at the workspace bound.
-// The device's compute-unit count and the kernel's resident workgroups per
-// CU are looked up once per (device, kernel) and cached: the queries cost
-// more host time than a launch.  The occupancy is taken with the largest
-// dynamic LDS a call may request, so the cache holds for every call.
+// Split count: about one 128-row slice per workgroup, capped at one workgroup
+// per compute unit (so every slice starts immediately, all finish together,
+// and each unit streams one slice: two resident workgroups per unit doubled
+// the bytes in flight and ran slower) and at the workspace bound.  The
+// device's compute-unit count is looked up once per device and cached: the
+// query costs more host time than a launch.
 constexpr int kMaxDevices = 64;
 
 inline int device_cus(int dev) {
@@ -884,23 +882,10 @@ inline int device_cus(int dev) {
   return c;
 }
 
-// One occupancy cache per kernel instantiation.
-template <bool BF16, int D, int GP, bool PAGED>
 int32_t split_count(int64_t rows_hint) {
-  static std::atomic<int> occ_cache[kMaxDevices];
-  const auto kernel = decode_kernel<BF16, D, GP, PAGED>;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) dev = 0;
-  const int cus = device_cus(dev);
-  int per_cu = occ_cache[dev].load(std::memory_order_relaxed);
-  if (per_cu <= 0) {
-    const size_t lds_max = (2 * (size_t)DKV_MAX_SEGMENTS + 1) * sizeof(int64_t);
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, lds_max) != hipSuccess ||
-        per_cu <= 0)
-      per_cu = 1;
-    occ_cache[dev].store(per_cu, std::memory_order_relaxed);
-  }
-  int64_t cap = (int64_t)cus * per_cu;
+  int64_t cap = device_cus(dev);
   if (cap > kDecodeMaxWG) cap = kDecodeMaxWG;
   if (rows_hint <= 0) return (int32_t)cap;
   int64_t P = (rows_hint + 127) / 128;
@@ -912,10 +897,10 @@ hipError_t launch_g(DecodeParams p, int64_t rows_hint, hipStream_t stream) {
   const size_t lds = (2 * (size_t)p.nseg + 1) * sizeof(int64_t);
   DKV_STAMP(p.stamp_slot = stamp_next_slot();)
   if (p.entries != nullptr) {
-    p.P = split_count<BF16, D, GP, true>(rows_hint);
+    p.P = split_count(rows_hint);
     hipLaunchKernelGGL((decode_kernel<BF16, D, GP, true>), dim3(p.P), dim3(kThreads), lds, stream, p);
   } else {
-    p.P = split_count<BF16, D, GP, false>(rows_hint);
+    p.P = split_count(rows_hint);
     hipLaunchKernelGGL((decode_kernel<BF16, D, GP, false>), dim3(p.P), dim3(kThreads), lds, stream, p);
   }
   // Segments split over several workgroups are finished by the combine
