@@ -1027,7 +1027,7 @@ def phase_budget(args):
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g, stream=cs):
             for i in range(32):
-                lib.dkv_probe_stream_read(P(pbuf.data_ptr() + i * per), per, P(psink.data_ptr()), 256,
+                lib.dkv_probe_stream_read(P(pbuf.data_ptr() + i * per), per, P(psink.data_ptr()), 2,
                                           P(cs.cuda_stream))
         for _ in range(3):
             g.replay()
@@ -1057,7 +1057,7 @@ def phase_budget(args):
                  f"product library, same graphs: {prod_us:.2f} us per call = {nbytes / (prod_us * 1e-6) / 1e9:.0f} GB/s "
                  f"({nbytes / (prod_us * 1e-6) / 1e9 / PEAK_HBM_GBPS:.1%} of 8 TB/s); stamped library "
                  f"{np.mean(stamped_us):.2f} us per call",
-                 f"streaming-read probe over the same bytes (256 workgroups, graph-replayed): {probe_us:.2f} us per "
+                 f"streaming-read probe over the same bytes (8 KiB per workgroup, graph-replayed): {probe_us:.2f} us per "
                  f"launch = {per / (probe_us * 1e-6) / 1e9:.0f} GB/s",
                  f"{'term':78s} {'us':>7s}"]
         for nm, val in terms:
@@ -1936,17 +1936,18 @@ def main():
 
     # ---------------- achievable read bandwidth at this launch size -------
     # The streaming-read probe (same 16-byte non-temporal buffer loads as the
-    # decode kernel's K/V stream) over L slices of one decode launch's size,
-    # one launch per slice, captured and replayed like a decode step.
+    # decode kernel's K/V stream; one block of 4-32 KiB per workgroup) over L
+    # slices of one decode launch's size, one launch per slice, captured and
+    # replayed like a decode step.
     per = (int(nbytes / L) + 15) // 16 * 16
     pbuf = torch.ones(L * per // 2, dtype=torch.int16, device=dev)
     psink = torch.zeros(4, dtype=torch.int32, device=dev)
     probe_gbps = {}
-    for wg in (256, 512, 1024, 2048):
-        def probe_step(shp, wg=wg):
+    for gpt in (1, 2, 4, 8):
+        def probe_step(shp, gpt=gpt):
             for layer in range(L):
                 st_ = lib.dkv_probe_stream_read(P(pbuf.data_ptr() + layer * per), per,
-                                                P(psink.data_ptr()), wg, P(shp))
+                                                P(psink.data_ptr()), gpt, P(shp))
                 if st_ != 0:
                     raise d.DkvError("dkv_probe_stream_read", st_)
         probe_step(sh)
@@ -1963,11 +1964,11 @@ def main():
             g.replay()
         b.record(stream)
         torch.cuda.synchronize()
-        probe_gbps[wg] = round(L * per / (a.elapsed_time(b) / args.steps * 1e-3) / 1e9, 1)
+        probe_gbps[f"{4 * gpt}KiB"] = round(L * per / (a.elapsed_time(b) / args.steps * 1e-3) / 1e9, 1)
     del pbuf
-    achievable = {"kind": "dkv_probe_stream_read: streaming read, one launch per layer-sized slice, "
-                          "HIP-graph replays", "bytes_per_launch": per,
-                  "gb_per_s_by_workgroups": probe_gbps, "best_gb_per_s": max(probe_gbps.values())}
+    achievable = {"kind": "dkv_probe_stream_read: streaming read, one launch per layer-sized slice, one block "
+                          "per workgroup, HIP-graph replays", "bytes_per_launch": per,
+                  "gb_per_s_by_block": probe_gbps, "best_gb_per_s": max(probe_gbps.values())}
     log(f"probe {probe_gbps}")
 
     if args.copy_probe:

@@ -22,19 +22,20 @@
 extern "C" {
 #endif
 
-/* Reads bytes [0, bytes) at `src` with `workgroups` workgroups of 256
- * threads; workgroup w streams the w-th of `workgroups` equal contiguous
- * slices (16-byte granules), each thread keeping eight 16-byte loads in
- * flight.  The loaded data is folded into a value that is stored to `sink`
- * (16 bytes) only if it equals an impossible constant, so the loads cannot be
- * removed; the content of `sink` is unspecified.
+/* Reads bytes [0, bytes) at `src` in blocks of 256 x G 16-byte granules
+ * (G = granules_per_thread: 4, 8, 16 or 32 KiB), one block per workgroup of
+ * 256 threads, with the decode kernel's K/V load (16-byte non-temporal buffer
+ * loads); each thread issues its G loads and the workgroup retires.  The
+ * loaded data is folded into a value that is stored to `sink` (16 bytes) only
+ * if it equals an impossible constant, so the loads cannot be removed; the
+ * content of `sink` is unspecified.
  *   src, sink  device pointers, 16-byte aligned; src holds `bytes` bytes.
  *   bytes      multiple of 16, >= 0 (0: nothing is enqueued).
- *   workgroups 1 .. 65535; a slice may not exceed 2^31 bytes.
+ *   granules_per_thread  1, 2, 4 or 8.
  * Errors: DKV_ERR_INVALID_ARG (null pointer, bytes < 0 or not a multiple of
- * 16, workgroups out of range), DKV_ERR_UNSUPPORTED (slice over 2^31 bytes),
- * DKV_ERR_MISALIGNED, DKV_ERR_HIP (launch refused). */
-dkv_status dkv_probe_stream_read(const void* src, int64_t bytes, void* sink, int32_t workgroups,
+ * 16, G not one of the four), DKV_ERR_UNSUPPORTED (more than 2^31 - 1
+ * blocks), DKV_ERR_MISALIGNED, DKV_ERR_HIP (launch refused). */
+dkv_status dkv_probe_stream_read(const void* src, int64_t bytes, void* sink, int32_t granules_per_thread,
                                  void* stream);
 
 /* Copies bytes [0, bytes) from `src` to `dst` in blocks of 256 x G 16-byte

@@ -283,12 +283,13 @@ def dkv_dense_decode_attn(q, k, v, n_valid, sm_scale, out, workspace, stream=Non
         workspace.numel() * workspace.element_size(), _stream(stream)))
 
 
-def dkv_probe_stream_read(src, sink, workgroups, nbytes=None, stream=None):
+def dkv_probe_stream_read(src, sink, granules_per_thread, nbytes=None, stream=None):
     """Streaming-read probe (measurement aid): reads `nbytes` (default: all)
-    bytes of the device tensor `src`; `sink` is a device tensor of >= 16 bytes."""
+    bytes of the device tensor `src`, one block of 256 x granules_per_thread
+    16-byte granules per workgroup; `sink` is a device tensor of >= 16 bytes."""
     n = src.numel() * src.element_size() if nbytes is None else int(nbytes)
     _check("dkv_probe_stream_read", library().dkv_probe_stream_read(
-        _dev(src, "src"), n, _dev(sink, "sink"), int(workgroups), _stream(stream)))
+        _dev(src, "src"), n, _dev(sink, "sink"), int(granules_per_thread), _stream(stream)))
 
 
 def dkv_probe_copy(src, dst, granules_per_thread, nbytes=None, stream=None):

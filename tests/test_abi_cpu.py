@@ -229,8 +229,8 @@ def test_probe_validation():
     assert lib.dkv_probe_stream_read(A, 0, NUL, 1, NUL) == d.DKV_OK  # nothing to read
     assert lib.dkv_probe_stream_read(A, -16, A, 1, NUL) == d.DKV_ERR_INVALID_ARG
     assert lib.dkv_probe_stream_read(A, 24, A, 1, NUL) == d.DKV_ERR_INVALID_ARG
-    assert lib.dkv_probe_stream_read(A, 4096, A, 0, NUL) == d.DKV_ERR_INVALID_ARG
-    assert lib.dkv_probe_stream_read(A, 4096, A, 65536, NUL) == d.DKV_ERR_INVALID_ARG
+    for g in (0, 3, 16, -1):
+        assert lib.dkv_probe_stream_read(A, 4096, A, g, NUL) == d.DKV_ERR_INVALID_ARG
     assert lib.dkv_probe_stream_read(NUL, 4096, A, 1, NUL) == d.DKV_ERR_INVALID_ARG
     assert lib.dkv_probe_stream_read(A, 4096, NUL, 1, NUL) == d.DKV_ERR_INVALID_ARG
     assert lib.dkv_probe_stream_read(MIS, 4096, A, 1, NUL) == d.DKV_ERR_MISALIGNED
@@ -248,7 +248,7 @@ def test_probe_validation():
     assert lib.dkv_probe_copy(A, A, 4096, 1, NUL) == d.DKV_ERR_INVALID_ARG  # overlapping
     assert lib.dkv_probe_copy(MIS, B, 4096, 1, NUL) == d.DKV_ERR_MISALIGNED
     assert lib.dkv_probe_copy(A, MIS, 4096, 1, NUL) == d.DKV_ERR_MISALIGNED
-    assert lib.dkv_probe_stream_read(A, (1 << 32) + 16, A, 1, NUL) == d.DKV_ERR_UNSUPPORTED
+    assert lib.dkv_probe_stream_read(A, (1 << 31) * 4096 + 16, A, 1, NUL) == d.DKV_ERR_UNSUPPORTED  # 2^31 blocks
 
 
 def test_query_validation():

@@ -676,13 +676,16 @@ def test_path_llama70b_batched_budgets(d, budget):
 
 
 def test_probe_stream_read_runs(d):
-    """The bandwidth probe reads a ragged buffer with several grid shapes
-    (no result to compare: it only must not fail)."""
+    """The bandwidth probe reads a ragged buffer with every block size, over
+    lengths that end inside a block (no result to compare: it only must not
+    fail, and the sink keeps its contents since no fold hits the constant)."""
     src = torch.ones((1 << 20) + 48, dtype=torch.uint8, device=DEV)
     sink = torch.zeros(4, dtype=torch.int32, device=DEV)
-    for wg in (1, 3, 256, 2048):
-        d.dkv_probe_stream_read(src, sink, wg)
+    for g in (1, 2, 4, 8):
+        for n in (16, 4096 * g - 16, (1 << 20) + 48):
+            d.dkv_probe_stream_read(src, sink, g, nbytes=n)
     torch.cuda.synchronize()
+    assert int(sink.abs().sum()) == 0
 
 
 def test_probe_copy_copies(d):
