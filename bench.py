@@ -1154,6 +1154,13 @@ def main():
     e1.record(stream)
     torch.cuda.synchronize()
     map_us = e0.elapsed_time(e1) * 1e3
+    # kernel time: 20 calls back to back (no synchronisation between them)
+    e0.record(stream)
+    for _ in range(20):
+        d.dkv_map_pattern(lay, pat_d, kv_mask, kv_len)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    map_b2b_us = e0.elapsed_time(e1) * 1e3 / 20
     lens = kv_len.cpu().to(torch.int64)
     rows = int((lens + cap).sum())
     # zeroed, so the two packs' buffers agree on the free rows neither writes
@@ -1966,10 +1973,26 @@ def main():
         torch.cuda.synchronize()
         probe_gbps[f"{4 * gpt}KiB"] = round(L * per / (a.elapsed_time(b) / args.steps * 1e-3) / 1e9, 1)
     del pbuf
+    # the same probe over one 4 GiB buffer (a read of the whole device's scale)
+    big = torch.ones(1 << 31, dtype=torch.int16, device=dev)
+    big_gbps = {}
+    for gpt in (1, 2, 4, 8):
+        d.dkv_probe_stream_read(big, psink, gpt)
+        torch.cuda.synchronize()
+        a, b = ev(), ev()
+        a.record(stream)
+        for _ in range(3):
+            d.dkv_probe_stream_read(big, psink, gpt)
+        b.record(stream)
+        torch.cuda.synchronize()
+        big_gbps[f"{4 * gpt}KiB"] = round((1 << 32) / (a.elapsed_time(b) / 3 * 1e-3) / 1e9, 1)
+    del big
+    torch.cuda.empty_cache()
     achievable = {"kind": "dkv_probe_stream_read: streaming read, one launch per layer-sized slice, one block "
                           "per workgroup, HIP-graph replays", "bytes_per_launch": per,
-                  "gb_per_s_by_block": probe_gbps, "best_gb_per_s": max(probe_gbps.values())}
-    log(f"probe {probe_gbps}")
+                  "gb_per_s_by_block": probe_gbps, "best_gb_per_s": max(probe_gbps.values()),
+                  "one_4GiB_launch": {"gb_per_s_by_block": big_gbps, "best_gb_per_s": max(big_gbps.values())}}
+    log(f"probe {probe_gbps}; over 4 GiB {big_gbps}")
 
     if args.copy_probe:
         # an elementwise kernel (not a DMA/blit copy) that reads and writes 1 GiB
@@ -2046,7 +2069,11 @@ def main():
                                          "(1,015), pattern = exact-budget export at rho 0.2, then each family",
                              "step": "per layer: dkv_decode_attn (attend only); HIP-graph replays",
                              **fam_res},
-        "one_time": {"map_us": round(map_us, 1), "compact_us": round(compact_us, 1),
+        "one_time": {"map_us": round(map_us, 1),
+                     "map_back_to_back_us": round(map_b2b_us, 2),
+                     # the masks written (1 byte per position), over the back-to-back time
+                     "map_write_gb_per_s": round(N * Hkv * T / (map_b2b_us * 1e-6) / 1e9, 1),
+                     "compact_us": round(compact_us, 1),
                      "compact_timing": "best of 3 single calls, each between synchronisations",
                      "compact_bytes": int(compact_bytes),
                      "compact_gb_per_s": round(compact_bytes / (compact_us * 1e-6) / 1e9, 1),
