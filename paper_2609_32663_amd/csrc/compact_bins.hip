@@ -12,7 +12,8 @@
 //   plan  one workgroup per segment: the kept ranges, their first packed row
 //         (block scans over the D + 2 ranges), the segment's length, and for
 //         every chunk of kBinsChunkRows packed rows the range holding its
-//         first row;
+//         first row (a binary search per chunk over the ranges' first rows,
+//         staged in LDS);
 //   scan  one workgroup: offsets from the lengths plus the append room,
 //         with dkv_compact's rule for segments that do not fit below
 //         out_rows (length -1, offset clamped);
@@ -76,8 +77,13 @@ __device__ __forceinline__ bool range_kept(const BinsParams& p, const uint8_t* p
   return kept;
 }
 
+// Kept ranges whose first packed rows the plan stages in LDS to fill the chunk
+// heads cooperatively (16 KiB); segments with more fall back to the serial fill.
+constexpr int kPlanTable = 4096;
+
 __global__ __launch_bounds__(kThreads) void bins_plan_kernel(BinsParams p) {
   __shared__ int64_t red[kThreads / kWave + 1];
+  __shared__ int32_t tbl[kPlanTable];
   const int s = blockIdx.x;
   const int n = s / p.Hkv, g = s - n * p.Hkv;
   const int items = p.D + 2;
@@ -101,15 +107,20 @@ __global__ __launch_bounds__(kThreads) void bins_plan_kernel(BinsParams p) {
   int32_t* ipos = p.item_pos + (int64_t)s * (p.D + 2);
   int32_t* idst = p.item_dst + (int64_t)s * (p.D + 3);
   int32_t* cf = p.chunk_first + (int64_t)s * p.nchunks;
+  const bool staged = cnt_all <= kPlanTable;  // (the same for every lane)
   for (int i = i0; i < i1; ++i) {
     int32_t lo, len;
     range_of(p, i, lo, len);
     if (len > 0 && range_kept(p, prow, i)) {
       ipos[c] = lo;
       idst[c] = (int32_t)r;
-      // chunks whose first packed row lies in this range
-      for (int64_t ch = (r + kBinsChunkRows - 1) / kBinsChunkRows; ch * kBinsChunkRows < r + len; ++ch)
-        cf[ch] = (int32_t)c;
+      if (staged) {
+        tbl[c] = (int32_t)r;
+      } else {
+        // chunks whose first packed row lies in this range, by the range's owner
+        for (int64_t ch = (r + kBinsChunkRows - 1) / kBinsChunkRows; ch * kBinsChunkRows < r + len; ++ch)
+          cf[ch] = (int32_t)c;
+      }
       ++c;
       r += len;
     }
@@ -118,6 +129,23 @@ __global__ __launch_bounds__(kThreads) void bins_plan_kernel(BinsParams p) {
     p.item_cnt[s] = (int32_t)cnt_all;
     p.lens[s] = (int32_t)rows_all;
     idst[cnt_all] = (int32_t)rows_all;  // sentinel: the end of the last range
+  }
+  if (staged) {
+    // every chunk's head: the last kept range whose first packed row is at or
+    // before the chunk's first row (a binary search over the ranges' starts)
+    __syncthreads();
+    const int n = (int)cnt_all;
+    const int64_t nch = (rows_all + kBinsChunkRows - 1) / kBinsChunkRows;
+    for (int64_t ch = threadIdx.x; ch < nch; ch += kThreads) {
+      const int64_t row = ch * kBinsChunkRows;
+      int lo_i = 0, hi_i = n - 1;  // tbl[0] = 0 <= row, so the answer exists
+      while (lo_i < hi_i) {
+        const int mid = (lo_i + hi_i + 1) >> 1;
+        if (tbl[mid] <= row) lo_i = mid;
+        else hi_i = mid - 1;
+      }
+      cf[ch] = lo_i;
+    }
   }
 }
 

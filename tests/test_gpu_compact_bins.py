@@ -158,10 +158,13 @@ def test_compact_bins_one_row_bins(d):
     """Bins one position wide: every kept bin is a range of one row, so a
     copy chunk spans as many ranges as it has rows (the most its range table
     holds), and chunk boundaries fall between and inside the sink and recent
-    ranges; densities from sparse to full, several contexts."""
+    ranges; densities from sparse to full, several contexts, up to more kept
+    ranges per segment (8,986) than the plan pass stages in LDS (4,096)."""
     rng = np.random.default_rng(1)
     N, Hq, Hkv, dim = 2, 4, 2, 128
-    for T, S, R, density in ((2100, 5, 37, 0.5), (2100, 0, 0, 0.9), (4133, 31, 33, 1.0), (700, 64, 64, 0.05)):
+    # (the last case keeps more ranges than the plan stages in LDS: the serial fill)
+    for T, S, R, density in ((2100, 5, 37, 0.5), (2100, 0, 0, 0.9), (4133, 31, 33, 1.0), (700, 64, 64, 0.05),
+                             (9000, 8, 8, 1.0)):
         D = T - S - R
         lay = d.make_layout(N, Hq, Hkv, dim, T, S, R, list(range(D + 1)))
         k, v, pattern = _inputs(rng, N, Hq, Hkv, dim, T, torch.bfloat16, D, density)
