@@ -442,14 +442,15 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
   const int nseg = p.nseg;
   const bool dense = !PAGED && p.seg_len == nullptr;
 
-  // fixed cost of a piece, in rows: about as long as streaming 256 KiB of K
+  // fixed cost of a piece, in rows: about as long as streaming 192 KiB of K
   // and V.  A piece restarts the ring (its first tiles wait out the load
-  // queue: ~8 us under full load, per-workgroup clock stamps) and ends with
-  // the cross-wave fold (1.4-2.3 us); at ~23 KB/us per workgroup that is
-  // ~240 KiB.  (Measured on graph-replayed steps: 256 KiB takes 5-7% off the
-  // ragged 70B-shaped batch and the Qwen-shaped stack against 128 KiB, and
-  // leaves the headline stack, 1-2 pieces per workgroup, unchanged.)
-  constexpr int64_t kSegCost = 262144 / (2 * C::kRowBytes);
+  // queue: ~4 us under full load, per-workgroup clock stamps) and ends with
+  // the cross-wave fold (~1.1 us); at ~25 KB/us per workgroup that is ~125
+  // KiB, and more where a restart also empties the ring.  (Measured on
+  // graph-replayed steps: 192 KiB takes 4-5% off the 70B-shaped batch at 10%
+  // and 1-2% at 20% against 256 KiB; 128 KiB is within noise of 192; the
+  // headline and Qwen-shaped stacks are unchanged from 128 to 384 KiB.)
+  constexpr int64_t kSegCost = 196608 / (2 * C::kRowBytes);
   DKV_STAMP(const unsigned long long stamp_t0 = __builtin_amdgcn_s_memrealtime();)
   build_row_prefix<PAGED>(p, kSegCost, pre, offs, red);
   const int64_t total = uniform64(pre[nseg]);
