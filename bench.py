@@ -1752,13 +1752,41 @@ def main():
             d.dkv_map_pattern(lay_r, pat_rd, km_r, kl_r)
         kept_r = int(kl_r.sum())
         rows_r = kept_r + Br * Hkvr * capr
-        kc_r = torch.empty((rows_r, dim), dtype=torch.bfloat16, device=dev)
-        vc_r = torch.empty_like(kc_r)
+        kc_r = torch.zeros((rows_r, dim), dtype=torch.bfloat16, device=dev)
+        vc_r = torch.zeros_like(kc_r)
         so_r = torch.empty(Br * Hkvr, dtype=torch.int64, device=dev)
         sl_r = torch.empty(Br * Hkvr, dtype=torch.int32, device=dev)
         cws_r = torch.empty(d.dkv_compact_workspace_bytes(lay_r), dtype=torch.uint8, device=dev)
-        d.dkv_compact(lay_r, kr, vr, km_r, capr, kc_r, vc_r, so_r, sl_r, cws_r)
-        del km_r
+        pack_mask = lambda: d.dkv_compact(lay_r, kr, vr, km_r, capr, kc_r, vc_r, so_r, sl_r, cws_r)
+        pack_mask()
+        # the same pack straight from the pattern (the ragged block gather for
+        # the ragged batch), into zeroed buffers of its own, checked against it
+        kb_r, vb_r = torch.zeros_like(kc_r), torch.zeros_like(vc_r)
+        sob_r, slb_r = torch.empty_like(so_r), torch.empty_like(sl_r)
+        bws_r = torch.empty(d.dkv_compact_bins_workspace_bytes(lay_r), dtype=torch.uint8, device=dev)
+        ulen_r = torch.from_numpy(lens_r).to(dev)
+        if mode == "ragged":
+            pack_bins = lambda: d.dkv_compact_bins_ragged(lay_r, ulen_r, kr, vr, pat_rd, capr, kb_r, vb_r, sob_r,
+                                                          slb_r, bws_r)
+        else:
+            pack_bins = lambda: d.dkv_compact_bins(lay_r, kr, vr, pat_rd, capr, kb_r, vb_r, sob_r, slb_r, bws_r)
+        pack_bins()
+        torch.cuda.synchronize()
+        pack_equal = bool(torch.equal(sob_r, so_r) and torch.equal(slb_r, sl_r)
+                          and torch.equal(kb_r.view(torch.int16), kc_r.view(torch.int16))
+                          and torch.equal(vb_r.view(torch.int16), vc_r.view(torch.int16)))
+        pack_us = {}
+        for name_, fn_ in (("compact", pack_mask), ("compact_bins", pack_bins)):
+            t_ = []
+            for _ in range(3):
+                a, b = ev(), ev()
+                a.record(stream)
+                fn_()
+                b.record(stream)
+                torch.cuda.synchronize()
+                t_.append(a.elapsed_time(b) * 1e3)
+            pack_us[name_] = round(min(t_), 1)
+        del km_r, kb_r, vb_r, bws_r
 
         def step_call(s_, shp):
             kn_, vn_ = new_r[s_]
@@ -1787,11 +1815,13 @@ def main():
         r_us = a.elapsed_time(b) * 1e3 / args.steps / wr.decode_steps
         r_bytes = (kept_r + Br * Hkvr * (wr.decode_steps + 1) / 2) * dim * elem * 2 + Br * Hqr * dim * (elem + 4)
         seg = kl_r.view(-1).to(torch.float64)
-        ragged_res[mode] = {"retained_rows": kept_r, "us_per_step": round(r_us, 2),
+        ragged_res[mode] = {"pack_us": pack_us, "packs_equal": pack_equal,
+                            "retained_rows": kept_r, "us_per_step": round(r_us, 2),
                             "gb_per_s": round(r_bytes / (r_us * 1e-6) / 1e9, 1),
                             "segment_rows": {"min": int(seg.min()), "max": int(seg.max()),
                                              "cv": round(float(seg.std() / seg.mean()), 3)}}
-        log(f"{mode} batch: {r_us:.1f} us/step, {ragged_res[mode]['gb_per_s']} GB/s")
+        log(f"{mode} batch: {r_us:.1f} us/step, {ragged_res[mode]['gb_per_s']} GB/s; pack {pack_us}, "
+            f"equal {pack_equal}")
         del kc_r, vc_r, g
         torch.cuda.empty_cache()
     del kr, vr

@@ -13,7 +13,8 @@
  *                     (dkv_map_pattern_ragged: contexts of different lengths)
  *   dkv_compact       dense K/V + keep mask -> packed K/V, offsets, lengths
  *                     (dkv_compact_bins: map and pack from the pattern in one
- *                     call, whole retained bins copied as blocks)
+ *                     call, whole retained bins copied as blocks;
+ *                     dkv_compact_bins_ragged: contexts of different lengths)
  *   dkv_append        new tokens -> free rows after each packed segment
  *   dkv_decode_attn   one decode step of attention over the packed segments
  *   dkv_query_attn    the query block after the context: attention over the
@@ -210,6 +211,27 @@ dkv_status dkv_compact_bins(const dkv_layout *layout, dkv_dtype dtype, const voi
                             void *k_out, void *v_out, int64_t out_rows, int64_t *seg_off,
                             int32_t *seg_len, int32_t *src_pos, int64_t *rows_needed,
                             void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * dkv_compact_bins_ragged -- dkv_compact_bins for a batch of contexts of
+ * different lengths (e.g. sequences of a serving batch).
+ *
+ * unit_len  int32 [N] (device), as for dkv_map_pattern_ragged: unit n's
+ *           context is the first unit_len[n] positions of its dense rows
+ *           (values are clamped to [0, context_len]); its sink, recent window
+ *           and bins count from the end of that context, and positions at or
+ *           past it are not retained.
+ * The outputs equal dkv_compact's for dkv_map_pattern_ragged's kv_mask of the
+ * same layout, lengths and pattern.  The dense rows keep layout->context_len
+ * as their stride.  Everything else, limits and errors included, as
+ * dkv_compact_bins; DKV_ERR_INVALID_ARG also for a null unit_len with N > 0.
+ */
+dkv_status dkv_compact_bins_ragged(const dkv_layout *layout, const int32_t *unit_len,
+                                   dkv_dtype dtype, const void *k, const void *v,
+                                   const uint8_t *pattern, int32_t append_cap, void *k_out,
+                                   void *v_out, int64_t out_rows, int64_t *seg_off,
+                                   int32_t *seg_len, int32_t *src_pos, int64_t *rows_needed,
+                                   void *workspace, size_t workspace_bytes, void *stream);
 
 /*
  * dkv_append -- appended tokens are retained in full (Sec. 3.4).

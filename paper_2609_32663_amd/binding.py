@@ -17,7 +17,7 @@ __all__ = [
     "DKV_ERR_CAPACITY", "DKV_ERR_WORKSPACE", "DKV_ERR_HIP", "DKV_BF16", "DKV_F32",
     "DkvError", "Layout", "make_layout", "library", "library_at", "library_path", "dtype_code",
     "dkv_map_pattern", "dkv_compact_workspace_bytes", "dkv_compact", "dkv_compact_bins_workspace_bytes",
-    "dkv_compact_bins", "dkv_append",
+    "dkv_compact_bins", "dkv_compact_bins_ragged", "dkv_append",
     "dkv_decode_workspace_bytes", "dkv_decode_attn", "dkv_dense_decode_attn",
     "dkv_append_decode_attn", "dkv_append_decode_attn_noalloc", "dkv_dense_append_decode_attn",
     "DKV_NOALLOC_SCRATCH_BYTES",
@@ -124,6 +124,7 @@ def library_at(path):
         "dkv_topk_pattern": (I32, [I32, I32, I32, VP, I64, VP, VP, SZ, VP]),
         "dkv_compact_bins_workspace_bytes": (SZ, [P]),
         "dkv_compact_bins": (I32, [P, I32, VP, VP, VP, I32, VP, VP, I64, VP, VP, VP, VP, VP, SZ, VP]),
+        "dkv_compact_bins_ragged": (I32, [P, VP, I32, VP, VP, VP, I32, VP, VP, I64, VP, VP, VP, VP, VP, SZ, VP]),
     }
     for name, (res, args) in sigs.items():
         f = getattr(lib, name)
@@ -207,6 +208,18 @@ def dkv_compact_bins(layout, k, v, pattern, append_cap, k_out, v_out, seg_off, s
     _check("dkv_compact_bins", library().dkv_compact_bins(
         ctypes.byref(layout), dtype_code(k.dtype), _dev(k, "k"), _dev(v, "v"), _dev(pattern, "pattern"),
         int(append_cap), _dev(k_out, "k_out"), _dev(v_out, "v_out"), k_out.shape[0],
+        _dev(seg_off, "seg_off"), _dev(seg_len, "seg_len"), _dev(src_pos, "src_pos", True),
+        _dev(rows_needed, "rows_needed", True), _dev(workspace, "workspace"),
+        workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def dkv_compact_bins_ragged(layout, unit_len, k, v, pattern, append_cap, k_out, v_out, seg_off, seg_len,
+                            workspace, src_pos=None, rows_needed=None, stream=None):
+    """dkv_compact_bins for contexts of different lengths: unit_len is an
+    int32 device tensor [N] (as for dkv_map_pattern_ragged)."""
+    _check("dkv_compact_bins_ragged", library().dkv_compact_bins_ragged(
+        ctypes.byref(layout), _dev(unit_len, "unit_len"), dtype_code(k.dtype), _dev(k, "k"), _dev(v, "v"),
+        _dev(pattern, "pattern"), int(append_cap), _dev(k_out, "k_out"), _dev(v_out, "v_out"), k_out.shape[0],
         _dev(seg_off, "seg_off"), _dev(seg_len, "seg_len"), _dev(src_pos, "src_pos", True),
         _dev(rows_needed, "rows_needed", True), _dev(workspace, "workspace"),
         workspace.numel() * workspace.element_size(), _stream(stream)))

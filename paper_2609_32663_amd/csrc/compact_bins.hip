@@ -25,7 +25,9 @@
 //         first packed row).  Chunks are short, so each workgroup issues its
 //         loads once and retires.
 // No keep mask is read or written; the outputs are dkv_compact's for
-// dkv_map_pattern's mask.
+// dkv_map_pattern's mask.  In a ragged batch T is each unit's own context
+// length (unit_len), as for dkv_map_pattern_ragged; the dense rows keep the
+// layout's context length as their stride.
 
 #include "dkv_bins.hpp"
 #include "dkv_device.hpp"
@@ -38,10 +40,11 @@ constexpr int kThreads = 256;
 constexpr int kScanThreads = 1024;
 constexpr int kMaxUnroll = 8;  // rows per lane group in flight, at most
 
-// Range i of a segment in token order: 0 = sink, 1 .. D = bin D - i,
-// D + 1 = recent window; [lo, lo + len) of the dense row (len 0: empty).
-__device__ __forceinline__ void range_of(const BinsParams& p, int i, int32_t& lo, int32_t& len) {
-  const int64_t T = p.T, S = p.S, R = p.R;
+// Range i of a segment whose unit's context is the first T positions of its
+// row, in token order: 0 = sink, 1 .. D = bin D - i, D + 1 = recent window;
+// [lo, lo + len) of the dense row (len 0: empty).
+__device__ __forceinline__ void range_of(const BinsParams& p, int64_t T, int i, int32_t& lo, int32_t& len) {
+  const int64_t S = p.S, R = p.R;
   const int64_t U = T - S - R;  // compressible span
   if (U <= 0) {                 // every position is sink or recent
     const int64_t s_end = S < T ? S : T;
@@ -91,11 +94,17 @@ __global__ __launch_bounds__(kThreads) void bins_plan_kernel(BinsParams p) {
   const int i0 = threadIdx.x * per;
   const int i1 = i0 + per < items ? i0 + per : items;
   const uint8_t* prow = p.pattern + ((int64_t)n * p.Hq + (int64_t)g * p.G) * p.D;
+  // this unit's context (a ragged batch: the first unit_len[n] positions)
+  int64_t Tn = p.T;
+  if (p.unit_len != nullptr) {
+    const int32_t u = p.unit_len[n];
+    Tn = u < 0 ? 0 : (u > p.T ? p.T : u);
+  }
   // this thread's ranges (consecutive, so the scans keep token order)
   int64_t cnt = 0, rows = 0;
   for (int i = i0; i < i1; ++i) {
     int32_t lo, len;
-    range_of(p, i, lo, len);
+    range_of(p, Tn, i, lo, len);
     if (len > 0 && range_kept(p, prow, i)) {
       ++cnt;
       rows += len;
@@ -110,7 +119,7 @@ __global__ __launch_bounds__(kThreads) void bins_plan_kernel(BinsParams p) {
   const bool staged = cnt_all <= kPlanTable;  // (the same for every lane)
   for (int i = i0; i < i1; ++i) {
     int32_t lo, len;
-    range_of(p, i, lo, len);
+    range_of(p, Tn, i, lo, len);
     if (len > 0 && range_kept(p, prow, i)) {
       ipos[c] = lo;
       idst[c] = (int32_t)r;

@@ -213,10 +213,12 @@ size_t dkv_compact_bins_workspace_bytes(const dkv_layout* layout) {
   return dkv::bins_workspace_bytes(nseg, layout->num_bins, layout->context_len);
 }
 
-dkv_status dkv_compact_bins(const dkv_layout* layout, dkv_dtype dtype, const void* k, const void* v,
-                            const uint8_t* pattern, int32_t append_cap, void* k_out, void* v_out,
-                            int64_t out_rows, int64_t* seg_off, int32_t* seg_len, int32_t* src_pos,
-                            int64_t* rows_needed, void* workspace, size_t workspace_bytes, void* stream) {
+namespace {
+
+dkv_status compact_bins(const dkv_layout* layout, const int32_t* unit_len, dkv_dtype dtype, const void* k,
+                        const void* v, const uint8_t* pattern, int32_t append_cap, void* k_out, void* v_out,
+                        int64_t out_rows, int64_t* seg_off, int32_t* seg_len, int32_t* src_pos,
+                        int64_t* rows_needed, void* workspace, size_t workspace_bytes, void* stream) {
   dkv_status st = check_shape(layout);
   if (st != DKV_OK) return st;
   const dkv_layout& L = *layout;
@@ -239,6 +241,7 @@ dkv_status dkv_compact_bins(const dkv_layout* layout, dkv_dtype dtype, const voi
   std::memset(&p, 0, sizeof(p));
   const int32_t D = L.num_bins;
   p.pattern = pattern;
+  p.unit_len = unit_len;
   p.k = k;
   p.v = v;
   p.k_out = k_out;
@@ -268,6 +271,26 @@ dkv_status dkv_compact_bins(const dkv_layout* layout, dkv_dtype dtype, const voi
   if (W == 0)
     for (int32_t i = 0; i <= D; ++i) p.edges[i] = L.bin_edges[i];
   return hip_status(dkv::launch_compact_bins(p, (hipStream_t)stream));
+}
+
+}  // namespace
+
+dkv_status dkv_compact_bins(const dkv_layout* layout, dkv_dtype dtype, const void* k, const void* v,
+                            const uint8_t* pattern, int32_t append_cap, void* k_out, void* v_out,
+                            int64_t out_rows, int64_t* seg_off, int32_t* seg_len, int32_t* src_pos,
+                            int64_t* rows_needed, void* workspace, size_t workspace_bytes, void* stream) {
+  return compact_bins(layout, nullptr, dtype, k, v, pattern, append_cap, k_out, v_out, out_rows, seg_off, seg_len,
+                      src_pos, rows_needed, workspace, workspace_bytes, stream);
+}
+
+dkv_status dkv_compact_bins_ragged(const dkv_layout* layout, const int32_t* unit_len, dkv_dtype dtype,
+                                   const void* k, const void* v, const uint8_t* pattern, int32_t append_cap,
+                                   void* k_out, void* v_out, int64_t out_rows, int64_t* seg_off, int32_t* seg_len,
+                                   int32_t* src_pos, int64_t* rows_needed, void* workspace,
+                                   size_t workspace_bytes, void* stream) {
+  if (layout != nullptr && layout->num_units > 0 && unit_len == nullptr) return DKV_ERR_INVALID_ARG;
+  return compact_bins(layout, unit_len, dtype, k, v, pattern, append_cap, k_out, v_out, out_rows, seg_off, seg_len,
+                      src_pos, rows_needed, workspace, workspace_bytes, stream);
 }
 
 dkv_status dkv_append(dkv_dtype dtype, int32_t num_segments, int32_t head_dim, const void* k_new,

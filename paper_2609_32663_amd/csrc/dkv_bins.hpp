@@ -18,6 +18,7 @@ constexpr int kBinsChunkRows = 32;
 
 struct BinsParams {
   const uint8_t* pattern;  // [N][Hq][D]
+  const int32_t* unit_len; // [N] each unit's context length (clamped to [0, T]), or null: every unit T
   const void* k;           // [nseg][T][d]
   const void* v;
   void* k_out;             // [out_rows][d]

@@ -372,6 +372,27 @@ def test_ragged_map_validation():
     assert f(ctypes.byref(_lay(N=0)), NUL, NUL, NUL, NUL, NUL, NUL) == d.DKV_OK
 
 
+def test_ragged_compact_bins_validation():
+    lib = d.library()
+    lay = _lay()
+    ws = d.dkv_compact_bins_workspace_bytes(lay)
+
+    def f(layout, unit_len, **kw):
+        a = dict(dtype=d.DKV_BF16, k=A, v=A, pattern=A, cap=4, k_out=A, v_out=A, out_rows=100, seg_off=A,
+                 seg_len=A, ws=A, ws_bytes=ws)
+        a.update(kw)
+        return lib.dkv_compact_bins_ragged(layout, unit_len, a["dtype"], a["k"], a["v"], a["pattern"], a["cap"],
+                                           a["k_out"], a["v_out"], a["out_rows"], a["seg_off"], a["seg_len"],
+                                           NUL, NUL, a["ws"], a["ws_bytes"], NUL)
+    assert f(ctypes.byref(lay), NUL) == d.DKV_ERR_INVALID_ARG  # unit_len required
+    assert f(NUL, A) == d.DKV_ERR_INVALID_ARG
+    assert f(ctypes.byref(lay), A, k=MIS) == d.DKV_ERR_MISALIGNED
+    assert f(ctypes.byref(lay), A, ws_bytes=ws - 1) == d.DKV_ERR_WORKSPACE
+    assert f(ctypes.byref(lay), A, pattern=NUL) == d.DKV_ERR_INVALID_ARG
+    assert f(ctypes.byref(_lay(dim=96)), A) == d.DKV_ERR_UNSUPPORTED
+    assert f(ctypes.byref(_lay(N=0)), NUL) == d.DKV_OK  # no units: nothing to do
+
+
 def test_budget_and_topk_validation():
     lib = d.library()
     assert d.dkv_budget_entries(0.2, 32, 32, 1013) == 207462

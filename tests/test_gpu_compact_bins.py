@@ -170,3 +170,66 @@ def test_compact_bins_one_row_bins(d):
         k, v, pattern = _inputs(rng, N, Hq, Hkv, dim, T, torch.bfloat16, D, density)
         res, *_ = _both(d, lay, pattern, k, v, 3)
         _assert_same(res)
+
+
+def test_compact_bins_ragged_matches_map_ragged_and_compact(d):
+    """dkv_compact_bins_ragged equals dkv_map_pattern_ragged + dkv_compact in
+    every output, bit for bit: per-unit lengths below zero, zero, shorter than
+    sink + recent, in between, equal to and past the row length (clamped);
+    uniform and irregular edges; and once against the oracle's ragged map and
+    pack."""
+    rng = np.random.default_rng(99)
+    for trial in range(20):
+        G = int(rng.choice([1, 2, 4, 7, 8]))
+        Hkv = int(rng.integers(1, 4))
+        N = int(rng.integers(1, 7))
+        dim = int(rng.choice([64, 128]))
+        S, R = int(rng.integers(0, 40)), int(rng.integers(0, 300))
+        T = int(rng.integers(S + R + 2, 6000))
+        if trial % 2:
+            W = int(rng.integers(1, 150))
+            D = int(rng.integers(1, 50))
+            edges = [W * i for i in range(D + 1)]
+        else:
+            D = int(rng.integers(1, 30))
+            edges = sorted(set([0] + list(rng.integers(1, T + 1, size=D))))
+            D = len(edges) - 1
+            if D < 1:
+                edges, D = [0, 1], 1
+        lay = d.make_layout(N, G * Hkv, Hkv, dim, T, S, R, edges)
+        k, v, pattern = _inputs(rng, N, G * Hkv, Hkv, dim, T, torch.bfloat16, D, float(rng.choice([0.1, 0.5, 1.0])))
+        cands = [-5, 0, max(S + R - 3, 0), S + R, int(rng.integers(0, T + 1)), T, T + 40]
+        ulen = torch.tensor([int(rng.choice(cands)) for _ in range(N)], dtype=torch.int32, device=DEV)
+        cap = int(rng.integers(0, 20))
+        km = torch.empty((N, Hkv, T), dtype=torch.uint8, device=DEV)
+        kl = torch.empty((N, Hkv), dtype=torch.int32, device=DEV)
+        d.dkv_map_pattern_ragged(lay, ulen, pattern, km, kl)
+        need = int((kl.cpu().to(torch.int64) + cap).sum())
+        res = []
+        for route in ("mask", "bins"):
+            k_out = torch.full((max(need, 1), dim), 3.0, dtype=k.dtype, device=DEV)[:need]
+            v_out = torch.full((max(need, 1), dim), -2.0, dtype=k.dtype, device=DEV)[:need]
+            so = torch.full((N * Hkv,), -9, dtype=torch.int64, device=DEV)
+            sl = torch.full((N * Hkv,), -9, dtype=torch.int32, device=DEV)
+            sp = torch.full((max(need, 1),), -7, dtype=torch.int32, device=DEV)[:need]
+            rn = torch.full((1,), -9, dtype=torch.int64, device=DEV)
+            if route == "mask":
+                ws = torch.empty(max(d.dkv_compact_workspace_bytes(lay), 16), dtype=torch.uint8, device=DEV)
+                d.dkv_compact(lay, k, v, km, cap, k_out, v_out, so, sl, ws, src_pos=sp, rows_needed=rn)
+            else:
+                ws = torch.full((max(d.dkv_compact_bins_workspace_bytes(lay), 16),), 0x5A, dtype=torch.uint8,
+                                device=DEV)
+                d.dkv_compact_bins_ragged(lay, ulen, k, v, pattern, cap, k_out, v_out, so, sl, ws, src_pos=sp,
+                                          rows_needed=rn)
+            torch.cuda.synchronize()
+            res.append((k_out, v_out, so, sl, sp, rn))
+        _assert_same(res)
+        if trial == 0:
+            _, okm, okl = o.map_pattern(pattern.cpu().numpy(), T, S, R, edges, Hkv, unit_len=ulen.cpu().numpy())
+            ref = o.compact(bits(k), bits(v), okm, cap)
+            np.testing.assert_array_equal(res[1][3].cpu().numpy(), ref["seg_len"])
+            np.testing.assert_array_equal(res[1][2].cpu().numpy(), ref["seg_off"])
+            ko = bits(res[1][0])
+            for s_ in range(N * Hkv):
+                o0, n0 = int(ref["seg_off"][s_]), int(ref["seg_len"][s_])
+                np.testing.assert_array_equal(ko[o0:o0 + n0], ref["k_c"][o0:o0 + n0])
