@@ -61,6 +61,9 @@ def parse():
                          "host in that section)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 1 GiB device copy (HBM-counter calibration)")
+    ap.add_argument("--no-sustain", action="store_true",
+                    help="skip the untimed load runs before each timed measurement (for runs under a "
+                         "profiler, which serialises every dispatch: the load runs would multiply them)")
     ap.add_argument("--pmc-summary", nargs=3, metavar=("FETCH_CSV", "WRITE_CSV", "BENCH_LOG"),
                     help="summarise two rocprofv3 --pmc runs of this script (FETCH_SIZE, then "
                          "WRITE_SIZE, each with --copy-probe --no-cpu-baseline) and the JSON line one of "
@@ -146,6 +149,7 @@ def log(msg):
 # period or after continuous replays at 1.17-1.19, and a 10 s trace of
 # continuous replays holds 1.170-1.178 from its second 20-step window on.
 SUSTAIN_S = 1.5
+SUSTAIN_ON = True  # cleared by --no-sustain
 
 
 def sustain(replay, seconds=SUSTAIN_S):
@@ -153,6 +157,8 @@ def sustain(replay, seconds=SUSTAIN_S):
     time have passed, synchronising every 16 calls."""
     import time
     import torch
+    if not SUSTAIN_ON:
+        return
     t0 = time.perf_counter()
     while time.perf_counter() - t0 < seconds:
         for _ in range(16):
@@ -1107,7 +1113,9 @@ def phase_budget(args):
 
 
 def main():
+    global SUSTAIN_ON
     args = parse()
+    SUSTAIN_ON = not args.no_sustain
     if args.phase_budget:
         phase_budget(args)
         return
@@ -2100,6 +2108,7 @@ def main():
         "ms_per_step": round(ms, 4),
         "eager_ms_per_step": round(eager_ms, 4),
         "step_ms_spread": timed_spread.get("packed"),
+        "untimed_load_s_before_each_timing": SUSTAIN_S if SUSTAIN_ON else 0,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
