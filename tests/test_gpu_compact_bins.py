@@ -7,7 +7,9 @@ and rows_needed -- and, on a case checked independently, the oracle's map and
 pack.  Layouts: uniform and irregular edges, contexts shorter than sink +
 recent, a farthest bin cut by the compressible span, edges that end before it
 (an uncovered gap), G from 1 to 16, d 64 and 128, bf16 and fp32, and the
-paper's 1,013-bin layout at 130,816 positions.
+paper's 1,013-bin layout at 130,816 positions.  The ragged form
+(dkv_compact_bins_ragged) must equal dkv_map_pattern_ragged + dkv_compact the
+same way.
 """
 
 import numpy as np
