@@ -103,6 +103,32 @@ def test_compact_bins_stays_inside(d, short):
     with out_rows one short of it (some segments marked unpacked)."""
     lay, pattern, k, v, _ = _setup(d)
     pk = _pack(d, lay, pattern, k, v)
+    _bins_guarded(d, lay, pattern, k, v, pk, short)
+
+
+def test_compact_bins_ragged_stays_inside(d):
+    """The ragged block gather (a full and a short context), exactly fitted."""
+    lay, pattern, k, v, _ = _setup(d)
+    unit_len = torch.tensor([T, 613], dtype=torch.int32, device=DEV)
+    km = torch.empty((N, HKV, T), dtype=torch.uint8, device=DEV)
+    kl = torch.empty((N, HKV), dtype=torch.int32, device=DEV)
+    d.dkv_map_pattern_ragged(lay, unit_len, pattern, km, kl)
+    rows = int((kl.cpu().to(torch.int64) + CAP).sum())
+    gb = {
+        "k": Guarded((rows, DIM), torch.bfloat16, 0), "v": Guarded((rows, DIM), torch.bfloat16, 0),
+        "off": Guarded((N * HKV,), torch.int64), "len": Guarded((N * HKV,), torch.int32),
+        "src": Guarded((rows,), torch.int32), "need": Guarded((1,), torch.int64),
+        "ws": _ws(d.dkv_compact_bins_workspace_bytes(lay)),
+    }
+    d.dkv_compact_bins_ragged(lay, unit_len, k, v, pattern, CAP, gb["k"].t, gb["v"].t, gb["off"].t, gb["len"].t,
+                              gb["ws"].t, src_pos=gb["src"].t, rows_needed=gb["need"].t)
+    for name, gbuf in gb.items():
+        assert gbuf.intact(), f"dkv_compact_bins_ragged wrote outside {name}"
+    assert int(gb["need"].t.item()) == rows
+    assert torch.equal(gb["len"].t.cpu().view(N, HKV), kl.cpu())
+
+
+def _bins_guarded(d, lay, pattern, k, v, pk, short):
     rows = pk["rows"] - (1 if short else 0)
     gb = {
         "k": Guarded((rows, DIM), torch.bfloat16, 0), "v": Guarded((rows, DIM), torch.bfloat16, 0),
