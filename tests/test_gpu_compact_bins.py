@@ -235,3 +235,15 @@ def test_compact_bins_ragged_matches_map_ragged_and_compact(d):
             for s_ in range(N * Hkv):
                 o0, n0 = int(ref["seg_off"][s_]), int(ref["seg_len"][s_])
                 np.testing.assert_array_equal(ko[o0:o0 + n0], ref["k_c"][o0:o0 + n0])
+
+
+def test_compact_bins_many_segments(d):
+    """65,520 segments (4,095 units x 16 KV heads), near the 65,535 limit of
+    the segment grid: the plan and copy grids at their largest, and the offset
+    scan over 64 chunks of 1,024 segments; equal to map + compact."""
+    rng = np.random.default_rng(65520)
+    N, Hq, Hkv, dim, T, S, R = 4095, 32, 16, 64, 100, 4, 8
+    lay = d.make_layout(N, Hq, Hkv, dim, T, S, R, [0, 10, 30, 88])
+    k, v, pattern = _inputs(rng, N, Hq, Hkv, dim, T, torch.bfloat16, 3, 0.4)
+    res, *_ = _both(d, lay, pattern, k, v, 2)
+    _assert_same(res)
