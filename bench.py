@@ -74,6 +74,10 @@ def parse():
     ap.add_argument("--phase-budget", action="store_true",
                     help="per-phase time budget of the headline call from the phase-stamp build "
                          "(python paper_2609_32663_amd/build.py --phase-stamps first); writes the profile")
+    ap.add_argument("--power-sample", action="store_true",
+                    help="sample socket power, engine clock and temperature (amd-smi, read only) while the "
+                         "query-block kernel and, for comparison, the decode call run continuously on one "
+                         "layer of the headline stack; writes the query kernel's power profile")
     ap.add_argument("--query-counters", nargs=2, metavar=("SQ_DIR", "BENCH_LOG"),
                     help="summarise a rocprofv3 run of this script with --kernel-trace and --pmc GRBM_GUI_ACTIVE "
                          "SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_BUSY_CYCLES (csv output named "
@@ -402,6 +406,124 @@ def pmc_summary(fetch_csv, write_csv, bench_log, command):
 
 
 QUERY_COUNTERS_FILE = os.path.join(ROOT, "profiles", "query_attn_counters_llama8b_stack_128k.txt")
+POWER_FILE = os.path.join(ROOT, "profiles", "query_attn_power_llama8b_stack_128k.txt")
+
+
+def power_sample(seconds=8.0):
+    """Socket power, engine clocks and hotspot temperature (`amd-smi metric
+    --json`, polled every 0.5 s; read only) while, on layer 0 of the headline
+    stack, the query-block call (256 tokens) and then the decode call run
+    back to back for `seconds` each, with an idle period first."""
+    import ctypes
+    import statistics as st
+    import subprocess
+    import threading
+    import time
+    import torch
+
+    import dkv_inputs as di
+    import paper_2609_32663_amd as d
+    dev = torch.device("cuda:0")
+    P = ctypes.c_void_p
+    w = di.workload(WORKLOAD)
+    T, Hq, Hkv, dim = w.context_len, w.num_q_heads, w.num_kv_heads, w.head_dim
+    nq = QUERY_TOKENS
+    pattern, _ = di.make_pattern(w)
+    k, v = di.kv_unit(w, 0, device=dev)
+    lay = d.make_layout(1, Hq, Hkv, dim, T, w.sink, w.recent, list(w.bin_edges))
+    km = torch.empty((1, Hkv, T), dtype=torch.uint8, device=dev)
+    kl = torch.empty((1, Hkv), dtype=torch.int32, device=dev)
+    d.dkv_map_pattern(lay, torch.from_numpy(pattern[:1]).to(dev), km, kl)
+    lens = kl.cpu().long().reshape(-1)
+    rows = int((lens + nq).sum())
+    k_q = torch.empty((rows, dim), dtype=torch.bfloat16, device=dev)
+    v_q = torch.empty_like(k_q)
+    so = torch.empty(Hkv, dtype=torch.int64, device=dev)
+    sl = torch.empty(Hkv, dtype=torch.int32, device=dev)
+    cws = torch.empty(d.dkv_compact_workspace_bytes(lay), dtype=torch.uint8, device=dev)
+    d.dkv_compact(lay, k[None], v[None], km, nq, k_q, v_q, so, sl, cws)
+    qb, kb, vb = di.query_block(w, 0, nq, device=dev)
+    d.dkv_append(kb.reshape(Hkv, nq, dim).contiguous(), vb.reshape(Hkv, nq, dim).contiguous(), 0, nq, k_q, v_q,
+                 so, sl)
+    qb = qb.contiguous()
+    hint = int(lens.sum()) + Hkv * nq
+    ws = torch.empty(d.dkv_query_workspace_bytes(1, Hq, Hkv, dim, nq, hint), dtype=torch.uint8, device=dev)
+    out = torch.empty((1, nq, Hq, dim), dtype=torch.float32, device=dev)
+    lib = d.library()
+    cs = torch.cuda.Stream()
+    gq = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(gq, stream=cs):
+        for _ in range(8):
+            st_ = lib.dkv_query_attn(d.DKV_BF16, 1, Hq, Hkv, dim, nq, P(qb.data_ptr()), 0, nq, P(k_q.data_ptr()),
+                                     P(v_q.data_ptr()), P(so.data_ptr()), P(sl.data_ptr()), w.sm_scale, hint,
+                                     P(out.data_ptr()), P(ws.data_ptr()), ws.numel(), P(cs.cuda_stream))
+            if st_ != 0:
+                raise d.DkvError("dkv_query_attn", st_)
+    q1 = di.q_step(w, 0, 0, device=dev)
+    dws = torch.zeros(d.dkv_decode_workspace_bytes(1, Hq, Hkv, dim), dtype=torch.uint8, device=dev)
+    o1 = torch.empty((1, Hq, dim), dtype=torch.float32, device=dev)
+    gd = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(gd, stream=cs):
+        for _ in range(64):
+            d.dkv_decode_attn(q1, k_q, v_q, so, sl, 0, w.sm_scale, o1, dws, Hkv, rows_hint=int(lens.sum()),
+                              stream=cs)
+    torch.cuda.synchronize()
+
+    def get(g, path):
+        for p_ in path.split("/"):
+            g = g.get(p_) if isinstance(g, dict) else None
+        return g
+
+    def poll(stop, samples):
+        while not stop.is_set():
+            r = subprocess.run(["amd-smi", "metric", "--json"], capture_output=True, text=True, timeout=20)
+            try:
+                g = json.loads(r.stdout)["gpu_data"][0]
+                clocks = [get(g, f"clock/gfx_{i}/clk/value") for i in range(8)]
+                samples.append((get(g, "power/socket_power/value"),
+                                st.mean(c for c in clocks if isinstance(c, (int, float))),
+                                get(g, "temperature/hotspot/value")))
+            except (ValueError, KeyError, IndexError, TypeError, st.StatisticsError):
+                pass
+            time.sleep(0.5)
+
+    lines = [f"# socket power and engine clock while one call kind runs continuously ({WORKLOAD}, layer 0: "
+             f"{nq} query tokens after the context; decode: the attend-only call over the same packed layer)",
+             "# command: python bench.py --power-sample",
+             "# source: amd-smi metric --json, polled every 0.5 s (read only); the first second of each run "
+             "is left out (the samples while the load ramps up)", ""]
+    for tag, g, per in (("idle", None, 0), ("query", gq, 8), ("decode", gd, 64)):
+        samples, stop = [], threading.Event()
+        th = threading.Thread(target=poll, args=(stop, samples))
+        t0 = time.perf_counter()
+        th.start()
+        n = 0
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        if g is None:
+            time.sleep(seconds / 2)
+        else:
+            a.record()
+            while time.perf_counter() - t0 < seconds:
+                for _ in range(4):
+                    g.replay()
+                torch.cuda.synchronize()
+                n += 4
+            b.record()
+            torch.cuda.synchronize()
+        stop.set()
+        th.join()
+        keep = samples[2:] if len(samples) > 4 else samples
+        pw = [x[0] for x in keep if isinstance(x[0], (int, float))]
+        ck = [x[1] for x in keep]
+        hs = [x[2] for x in keep if isinstance(x[2], (int, float))]
+        call = f"; {a.elapsed_time(b) * 1e3 / (n * per):.1f} us per call over {n * per} calls" if g is not None else ""
+        lines.append(f"{tag:6s}: {len(keep)} samples; socket power median {st.median(pw):.0f} W (min {min(pw):.0f}, "
+                     f"max {max(pw):.0f}); engine clock median {st.median(ck):.0f} MHz (min {min(ck):.0f}, max "
+                     f"{max(ck):.0f}; the part's maximum is 2,400); hotspot {min(hs)}-{max(hs)} C{call}")
+        log(lines[-1])
+    with open(POWER_FILE, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
 
 
 def query_counters(sq_dir, bench_log, command):
@@ -1124,6 +1246,9 @@ def main():
         return
     if args.query_counters:
         query_counters(*args.query_counters, args.pmc_command)
+        return
+    if args.power_sample:
+        power_sample()
         return
     if args.trace_summary:
         trace_summary(*args.trace_summary, args.pmc_command)
