@@ -1,6 +1,6 @@
 """Host logic of bench.py's profile summaries (CPU only): which dispatches a
-counter run attributes to the packed, paged and query-block calls, and how
-the counters are scaled.  Synthetic counter files stand in for rocprofv3's."""
+counter run attributes to the packed, paged and query-block calls and to the
+two packs, and how the counters are scaled.  Synthetic counter files stand in for rocprofv3's."""
 
 import csv
 import importlib.util
@@ -27,6 +27,13 @@ PLAN = "dkv::(anonymous namespace)::query_plan_kernel(dkv::QueryParams)"
 QATT = "void dkv::(anonymous namespace)::query_attn_kernel<128>(dkv::QueryParams)"
 QMRG = "void dkv::(anonymous namespace)::query_merge_kernel<128>(dkv::QueryParams)"
 COPY = "void at::native::elementwise_kernel<128, 2>(int, Lambda)"
+CCOUNT = "dkv::(anonymous namespace)::compact_count_kernel(dkv::CompactParams)"
+CSCAN = "dkv::(anonymous namespace)::compact_scan_kernel(dkv::CompactParams)"
+CGATHER = "void dkv::(anonymous namespace)::compact_gather_kernel<16>(dkv::CompactParams)"
+BPLAN = "dkv::(anonymous namespace)::bins_plan_kernel(dkv::BinsParams)"
+BSCAN = "dkv::(anonymous namespace)::bins_scan_kernel(dkv::BinsParams)"
+BCOPY = "void dkv::(anonymous namespace)::bins_copy_kernel<16>(dkv::BinsParams)"
+PCOPY = "void (anonymous namespace)::copy_kernel<1>(u32x4 const*, u32x4*, long)"
 
 
 def test_helpers(bench):
@@ -54,7 +61,8 @@ def _counter_csv(path, counter, dispatches):
 def test_pmc_summary_attribution(bench, tmp_path, monkeypatch, parity):
     layers, steps, warmup = 2, 2, 1
     line = {"config": {"layers": layers}, "steps": steps, "warmup": warmup, "step_ms_spread": {"median": 1.0},
-            "parity_layer0": {"layers": layers} if parity else None}
+            "parity_layer0": {"layers": layers} if parity else None,
+            "one_time": {"compact_bytes": 2 * 1024 * 1024, "compact_bins_bytes": 1024 * 1024}}
     m = bench.timed_calls_per_mode(line)
     log = tmp_path / "bench.log"
     log.write_text("[bench] noise\n" + json.dumps(line) + "\n")
@@ -62,6 +70,13 @@ def test_pmc_summary_attribution(bench, tmp_path, monkeypatch, parity):
 
     def run(scale):
         d = []
+        # the one-time section: a warm and a timed mask pack, a warm and a timed
+        # block gather (the second of each is counted), then the copy probe
+        d += [(CCOUNT, 9.0), (CSCAN, 9.0), (CGATHER, 9.0)]
+        d += [(CCOUNT, 8.0 * scale), (CSCAN, 2.0 * scale), (CGATHER, 2038.0 * scale)]
+        d += [(BPLAN, 9.0), (BSCAN, 9.0), (BCOPY, 9.0)]
+        d += [(BPLAN, 4.0 * scale), (BSCAN, 1.0 * scale), (BCOPY, 1019.0 * scale)]
+        d += [(PCOPY, 5.0)] * 3
         d += [(PACKED, 999.0), (MERGE, 1.0)] * (layers if parity else 0)  # parity calls: not counted
         d += [(PACKED, 100.0 * scale), (MERGE, 2.0 * scale)] * m             # the packed calls
         d += [(PACKED, 300.0 * scale), (MERGE, 4.0 * scale)] * m             # the dense calls
@@ -88,3 +103,10 @@ def test_pmc_summary_attribution(bench, tmp_path, monkeypatch, parity):
     assert res["query_traffic_bytes_per_call"] == 2 * 551 * 1024
     assert res["kernel_sha256_16"] == bench.kernel_hash()
     assert res["query_kernel_sha256_16"] == bench.kernel_hash(bench.QUERY_SRCS)
+    # the packs: the timed (second) triple of each, scaled like the rest
+    assert res["compact_traffic_bytes"] == 2 * 2048 * 1024
+    assert res["compact_traffic_over_algorithmic"] == pytest.approx(2.0)
+    assert res["compact_bins_traffic_bytes"] == 2 * 1024 * 1024
+    assert res["compact_bins_traffic_over_algorithmic"] == pytest.approx(2.0)
+    assert res["compact_kernel_sha256_16"] == bench.kernel_hash(bench.COMPACT_SRCS)
+    assert res["compact_bins_kernel_sha256_16"] == bench.kernel_hash(bench.BINS_SRCS)
