@@ -38,6 +38,7 @@ PEAK_BF16_TFLOPS = 2500.0  # dense bf16 matrix peak
 QUERY_TOKENS = 256
 MT_TURNS, MT_STEPS = 4, 16  # multi-turn row: query rounds over one pack, tokens generated per round
 PAGE_ROWS = 128  # rows per page of the zero-copy paged variant
+SPREAD_REPS = 50  # single-step replays, at least, behind the median / p10 / p90 of a step
 PMC_FILE = os.path.join(ROOT, "profiles", "decode_attn_llama8b_stack_128k_pmc.json")
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2609_32663_amd", "csrc", f)
                for f in ("decode_attn.hip", "dkv_device.hpp", "dkv_launch.hpp")]
@@ -122,7 +123,7 @@ def timed_calls_per_mode(b):
     """Decode calls one timed mode (packed or dense) issues: a warm step, the
     graph replays, the replays of the per-step spread pass (when the line
     reports one) and the eager steps, one call per layer each."""
-    spread = b["steps"] if b.get("step_ms_spread") else 0
+    spread = b["step_ms_spread"].get("reps", b["steps"]) if b.get("step_ms_spread") else 0
     return b["config"]["layers"] * (1 + 2 * (b["warmup"] + b["steps"]) + spread)
 
 
@@ -364,17 +365,17 @@ def pmc_summary(fetch_csv, write_csv, bench_log, command):
     if len(per_paged) == 2:
         res["paged_traffic_bytes_per_launch"] = int(per_paged["fetch"] + per_paged["write"])
     # the headline's timed one-time compaction: the second count / scan /
-    # gather triple of the run (the first is its warm-up call), against its
-    # algorithmic bytes (retained K and V rows read and written, mask read)
+    # list / copy sequence of the run (the first is its warm-up call), against
+    # its algorithmic bytes (retained K and V rows read and written, mask read)
     res["compact_kernel_sha256_16"] = kernel_hash(COMPACT_SRCS)
+    names = ("compact_count_kernel", "compact_scan_kernel", "compact_list_kernel", "compact_copy_kernel")
     for key, path, counter in (("fetch", fetch_csv, "FETCH_SIZE"), ("write", write_csv, "WRITE_SIZE")):
         rows = pmc_per_dispatch(path, counter)
         calib = res[f"{key}_calibration"]
-        triples = [rows[i][1] + rows[i + 1][1] + rows[i + 2][1] for i in range(len(rows) - 2)
-                   if "compact_count_kernel" in rows[i][0] and "compact_scan_kernel" in rows[i + 1][0]
-                   and "compact_gather_kernel" in rows[i + 2][0]]
-        if len(triples) >= 2:
-            res[f"compact_{key}_bytes"] = int(triples[1] * 1024.0 * calib)
+        packs = [sum(rows[i + j][1] for j in range(4)) for i in range(len(rows) - 3)
+                 if all(names[j] in rows[i + j][0] for j in range(4))]
+        if len(packs) >= 2:
+            res[f"compact_{key}_bytes"] = int(packs[1] * 1024.0 * calib)
     if "compact_fetch_bytes" in res and "compact_write_bytes" in res:
         res["compact_traffic_bytes"] = res["compact_fetch_bytes"] + res["compact_write_bytes"]
         oc = b.get("one_time", {})
@@ -1569,17 +1570,20 @@ def main():
         b.record(stream)
         torch.cuda.synchronize()
         ms = a.elapsed_time(b) / steps
-        # the spread of single steps: the same replays again, one event pair
-        # per step (a pass of its own, so the timed region above is untouched)
-        evs = [ev() for _ in range(steps + 1)]
+        # the spread of single steps: the timed step graphs again, in turn, at
+        # least SPREAD_REPS replays with one event pair each (a pass of its
+        # own, so the timed region above is untouched; a graph replayed again
+        # rewrites its append slot with the same token)
+        reps = max(SPREAD_REPS, steps)
+        evs = [ev() for _ in range(reps + 1)]
         evs[0].record(stream)
-        for i, s in enumerate(range(warmup, warmup + steps)):
-            graphs[s].replay()
+        for i in range(reps):
+            graphs[warmup + i % steps].replay()
             evs[i + 1].record(stream)
         torch.cuda.synchronize()
-        per_step = [evs[i].elapsed_time(evs[i + 1]) for i in range(steps)]
+        per_step = [evs[i].elapsed_time(evs[i + 1]) for i in range(reps)]
         spread = {"median": round(float(np.median(per_step)), 4), "p10": round(float(np.percentile(per_step, 10)), 4),
-                  "p90": round(float(np.percentile(per_step, 90)), 4), "reps": steps}
+                  "p90": round(float(np.percentile(per_step, 90)), 4), "reps": reps}
         plans = [step_args(s, mode, sh) for s in range(warmup + steps)]
         for s in range(warmup):
             run(plans[s])

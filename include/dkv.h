@@ -168,8 +168,12 @@ size_t dkv_compact_workspace_bytes(const dkv_layout *layout);
  * src_pos    out, optional int32 [out_rows]: original position j of every
  *            packed row (free rows untouched).
  * rows_needed out, optional int64 [1]: sum_s (seg_len[s] + append_cap).
- * workspace  at least dkv_compact_workspace_bytes(layout) bytes, no
- *            initial contents required.
+ * workspace  at least dkv_compact_workspace_bytes(layout) bytes (about
+ *            4 * N * Hkv * T: a position list per segment, plus per-tile
+ *            counts), no initial contents required.
+ * DKV_ERR_UNSUPPORTED when N * Hkv > 65535 or T > 268,435,424 (the copy
+ * dispatch, a K and a V workgroup of 256 work-items per 32 packed rows of a
+ * segment's T, must hold fewer than 2^32 work-items).
  * The dense cache may be freed once the stream has executed this call: that
  * is what realises the memory reduction.
  */

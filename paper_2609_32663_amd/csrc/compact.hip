@@ -1,27 +1,26 @@
 // One-time prune and pack of the KV cache (Distance-KV, Sec. 3.4 / Fig. 2(b)),
 // and the append of new tokens.
 //
-// The pack is an order-preserving stream compaction in three passes:
+// The pack is an order-preserving stream compaction in four passes:
 //   count   each (segment, 4096-position tile) counts its retained positions
-//           (16 mask bytes per lane, nonzero-byte popcount, block scan) and
-//           records where each of its kCompactSub-position sub-tiles starts
-//           in the tile's rank order;
+//           (16 mask bytes per lane, nonzero-byte popcount, block scan);
 //   scan    one workgroup turns tile counts into each tile's first rank within
 //           its segment, the segment lengths, and the segment offsets
 //           (running sum of length + append capacity, unit-major);
-//   gather  two workgroups of 256 lanes per sub-tile, one for K and one for
-//           V, each rank the sub-tile's positions with a block scan, list the
-//           retained ones in LDS, and copy the rows: LPR lanes move one row
-//           with 16-byte non-temporal loads and stores (LPR = row bytes / 16),
-//           so a wave moves 64/LPR whole rows per instruction and a lane
-//           group moves at most kCompactSub * LPR / 256 rows.
-// Short workgroups copy fastest.  On the Llama-3.1-8B-shaped 128K stack (35%
-// kept) whole 4096-position tiles per gather workgroup took 2.50-2.55 ms
-// whatever the rows in flight per lane group (1 to 8); sub-tiles of 256, 128,
-// 64 and 32 positions took 2.18, 2.09-2.10, 2.06-2.07 and 2.48-2.50 ms, and
-// on the Qwen-shaped stack 2.78-2.80, 2.65-2.68, 2.81 and 3.72 ms (with 32
-// the launch holds two to four million workgroups).  (One workgroup copying both K
-// and V ran 6% slower: four interleaved streams per workgroup instead of two.)
+//   list    each tile with retained positions ranks them again (block scan),
+//           orders them in LDS and writes them, coalesced, to a per-segment
+//           list at their rank: list[s][r] is the position of packed row r;
+//   copy    a K and a V workgroup per (segment, chunk of kCopyRows packed
+//           rows): LPR lanes move one row with 16-byte non-temporal loads and
+//           stores (LPR = row bytes / 16), the source row being the list's
+//           entry.
+// The copy works on the output side because short workgroups copy fastest on
+// this part and every copy workgroup then has whole rows to move: on the
+// Llama-3.1-8B-shaped 128K stack (35% kept) a gather per 128-position input
+// sub-tile (most of them empty, the others up to 32 KiB) took 2.09-2.15 ms,
+// whole 4096-position tiles 2.50-2.55 ms.  (One workgroup copying both K and
+// V ran 6% slower in the block gather: four interleaved streams per
+// workgroup instead of two.)
 // All row arithmetic is 64-bit: a whole-stack cache has more than 2^31 elements.
 
 #include "dkv_device.hpp"
@@ -44,12 +43,8 @@ __global__ __launch_bounds__(kThreads) void compact_count_kernel(CompactParams p
   const u32x4 w = load_mask16(row, j0, p.T);
   const int64_t c = nonzero_bytes(w[0]) + nonzero_bytes(w[1]) + nonzero_bytes(w[2]) + nonzero_bytes(w[3]);
   int64_t total;
-  const int64_t before = block_exclusive_scan<kThreads>(c, red, &total);
-  const int64_t ti = (int64_t)seg * p.ntiles + tile;
-  if (threadIdx.x == 0) p.tile_cnt[ti] = (int32_t)total;
-  constexpr int kLanesPerSub = kCompactSub / kPerThread;
-  if (threadIdx.x % kLanesPerSub == 0)  // rank of the sub-tile's first position: < 4096
-    p.sub_base[ti * kCompactSubPerTile + threadIdx.x / kLanesPerSub] = (uint16_t)before;
+  block_exclusive_scan<kThreads>(c, red, &total);
+  if (threadIdx.x == 0) p.tile_cnt[(int64_t)seg * p.ntiles + tile] = (int32_t)total;
 }
 
 constexpr int kScanThreads = 1024;
@@ -63,12 +58,19 @@ __global__ __launch_bounds__(kScanThreads) void compact_scan_kernel(CompactParam
     const int64_t s = s0 + threadIdx.x;
     int64_t len = 0;
     if (s < p.nseg) {
+      // the segment's tile counts eight at a time, all eight loads in flight
       int32_t run = 0;
       const int64_t base = s * p.ntiles;
-      for (int t = 0; t < p.ntiles; ++t) {
-        const int32_t c = p.tile_cnt[base + t];
-        p.tile_base[base + t] = run;
-        run += c;
+      for (int t0 = 0; t0 < p.ntiles; t0 += 8) {
+        int32_t c[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) c[e] = p.tile_cnt[base + (t0 + e < p.ntiles ? t0 + e : p.ntiles - 1)];
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (t0 + e < p.ntiles) {
+            p.tile_base[base + t0 + e] = run;
+            run += c[e];
+          }
       }
       len = run;
     }
@@ -93,52 +95,69 @@ __global__ __launch_bounds__(kScanThreads) void compact_scan_kernel(CompactParam
   if (threadIdx.x == 0 && p.rows_needed != nullptr) *p.rows_needed = carry;
 }
 
-constexpr int kGatherThreads = 256;  // lanes < kCompactSub each rank one position
-static_assert(kCompactSub <= kGatherThreads && kCompactSub % 16 == 0, "sub-tile fits the workgroup");
+__global__ __launch_bounds__(kThreads) void compact_list_kernel(CompactParams p) {
+  __shared__ int64_t red[kThreads / kWave + 1];
+  __shared__ int32_t pos[kCompactTile];
+  const int tile = blockIdx.x;
+  const int seg = blockIdx.y;
+  const int64_t ti = (int64_t)seg * p.ntiles + tile;
+  // not packed (it does not fit below out_rows), or nothing kept in this tile
+  if (p.seg_len[seg] < 0 || p.tile_cnt[ti] == 0) return;
+  const int64_t j0 = (int64_t)tile * kCompactTile + threadIdx.x * kPerThread;
+  const u32x4 w = load_mask16(p.mask + (int64_t)seg * p.T, j0, p.T);
+  const int64_t c = nonzero_bytes(w[0]) + nonzero_bytes(w[1]) + nonzero_bytes(w[2]) + nonzero_bytes(w[3]);
+  int64_t total;
+  int r = (int)block_exclusive_scan<kThreads>(c, red, &total);
+  const uint32_t bits = nonzero_byte_bits(w);
+#pragma unroll
+  for (int e = 0; e < kPerThread; ++e)
+    if (bits & (1u << e)) pos[r++] = (int32_t)(j0 + e);
+  __syncthreads();
+  int32_t* dst = p.list + (int64_t)seg * p.T + p.tile_base[ti];
+  for (int i = threadIdx.x; i < total; i += kThreads) dst[i] = pos[i];
+}
 
 template <int LPR>
-__global__ __launch_bounds__(kGatherThreads) void compact_gather_kernel(CompactParams p) {
-  constexpr int kRowsPerPass = kGatherThreads / LPR;
-  constexpr int kPasses = (kCompactSub + kRowsPerPass - 1) / kRowsPerPass;
-  constexpr int kUnroll = kPasses < 8 ? kPasses : 8;  // rows per lane group in flight
-  __shared__ uint16_t list[kCompactSub];
-  __shared__ int64_t red[kGatherThreads / kWave + 1];
-
-  const int sub = blockIdx.x >> 1;
+__global__ __launch_bounds__(kThreads) void compact_copy_kernel(CompactParams p) {
+  constexpr int kRowsPerPass = kThreads / LPR;
+  constexpr int kPasses = (kCopyRows + kRowsPerPass - 1) / kRowsPerPass;  // rows per lane group
+  static_assert(kPasses <= 8, "rows in flight per lane group");
+  const int chunk = blockIdx.x >> 1;
   const int which = blockIdx.x & 1;  // 0: K rows (and source positions), 1: V rows
   const int seg = blockIdx.y;
   const int tid = threadIdx.x;
-  if (p.seg_len[seg] < 0) return;  // not packed: it does not fit below out_rows
-  const int64_t js = (int64_t)sub * kCompactSub;
-  const bool keep = tid < kCompactSub && js + tid < p.T && p.mask[(int64_t)seg * p.T + js + tid] != 0;
-  int64_t kept;
-  const int rank = (int)block_exclusive_scan<kGatherThreads>(keep ? 1 : 0, red, &kept);
-  if (keep) list[rank] = (uint16_t)tid;
-  __syncthreads();
-  if (kept == 0) return;  // (the same for every lane)
-
-  const int tile = sub / kCompactSubPerTile;
-  const int64_t ti = (int64_t)seg * p.ntiles + tile;
-  const int64_t dst0 = p.seg_off[seg] + p.tile_base[ti] + p.sub_base[ti * kCompactSubPerTile + (sub - tile * kCompactSubPerTile)];
-  const int64_t src0 = (int64_t)seg * p.T + js;
   const int lane = tid % LPR;
+  const int64_t r_lo = (int64_t)chunk * kCopyRows;
+  // Most workgroups of the grid lie past their segment's rows: they leave
+  // after one scalar load.
+  const int32_t len = p.seg_len[seg];
+  if (len <= 0 || r_lo >= len) return;  // past the segment's rows, or not packed
+  const int64_t r_hi = r_lo + kCopyRows < len ? r_lo + kCopyRows : len;
+  const int32_t* list = p.list + (int64_t)seg * p.T;
+  int32_t pos[kPasses];
+#pragma unroll
+  for (int u = 0; u < kPasses; ++u) {
+    const int64_t r = r_lo + tid / LPR + (int64_t)u * kRowsPerPass;
+    pos[u] = list[r < r_hi ? r : r_lo];
+  }
+  // Every list entry is waited for at once, then every row load is issued
+  // before any is waited for (rows past the chunk's end load its first
+  // row): waiting per row would also wait for the row loads before it.
+#pragma unroll
+  for (int u = 0; u < kPasses; ++u) asm volatile("" ::"v"(pos[u]));
+  const int64_t dst0 = p.seg_off[seg];
+  const int64_t src0 = (int64_t)seg * p.T;
   const u32x4* src = reinterpret_cast<const u32x4*>(which ? p.v : p.k);
   u32x4* dst = reinterpret_cast<u32x4*>(which ? p.v_out : p.k_out);
-
-  for (int r0 = tid / LPR; r0 < kept; r0 += kRowsPerPass * kUnroll) {
-    u32x4 rb[kUnroll];
+  u32x4 rb[kPasses];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int r = r0 + u * kRowsPerPass;
-      if (r < kept) rb[u] = __builtin_nontemporal_load(&src[(src0 + list[r]) * LPR + lane]);
-    }
+  for (int u = 0; u < kPasses; ++u) rb[u] = __builtin_nontemporal_load(&src[(src0 + pos[u]) * LPR + lane]);
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int r = r0 + u * kRowsPerPass;
-      if (r < kept) {
-        __builtin_nontemporal_store(rb[u], &dst[(dst0 + r) * LPR + lane]);
-        if (which == 0 && lane == 0 && p.src_pos != nullptr) p.src_pos[dst0 + r] = (int32_t)(js + list[r]);
-      }
+  for (int u = 0; u < kPasses; ++u) {
+    const int64_t r = r_lo + tid / LPR + (int64_t)u * kRowsPerPass;
+    if (r < r_hi) {
+      __builtin_nontemporal_store(rb[u], &dst[(dst0 + r) * LPR + lane]);
+      if (which == 0 && lane == 0 && p.src_pos != nullptr) p.src_pos[dst0 + r] = pos[u];
     }
   }
 }
@@ -164,7 +183,7 @@ __global__ __launch_bounds__(kThreads) void append_kernel(AppendParams p) {
 size_t compact_workspace_bytes(int64_t nseg, int64_t T) {
   const int64_t ntiles = (T + kCompactTile - 1) / kCompactTile;
   const int64_t n = nseg * (ntiles > 0 ? ntiles : 1);
-  return (size_t)(2 * n * 4 + n * kCompactSubPerTile * 2 + 256);  // tile counts, tile bases, sub-tile bases
+  return (size_t)(2 * n * 4 + nseg * T * 4 + 256);  // tile counts, tile bases, position lists
 }
 
 hipError_t launch_compact(const CompactParams& p, hipStream_t stream) {
@@ -174,12 +193,12 @@ hipError_t launch_compact(const CompactParams& p, hipStream_t stream) {
   }
   hipLaunchKernelGGL(compact_scan_kernel, dim3(1), dim3(kScanThreads), 0, stream, p);
   if (p.ntiles > 0) {
-    const int64_t nsub = ((int64_t)p.T + kCompactSub - 1) / kCompactSub;
-    const dim3 ggrid((uint32_t)(2 * nsub), p.nseg);  // a K and a V workgroup per sub-tile
+    hipLaunchKernelGGL(compact_list_kernel, grid, dim3(kThreads), 0, stream, p);
+    const dim3 cgrid((uint32_t)(2 * compact_chunks(p.T)), p.nseg);  // a K and a V workgroup per chunk
     switch (p.row_bytes) {
-      case 128: hipLaunchKernelGGL(compact_gather_kernel<8>, ggrid, dim3(kGatherThreads), 0, stream, p); break;
-      case 256: hipLaunchKernelGGL(compact_gather_kernel<16>, ggrid, dim3(kGatherThreads), 0, stream, p); break;
-      case 512: hipLaunchKernelGGL(compact_gather_kernel<32>, ggrid, dim3(kGatherThreads), 0, stream, p); break;
+      case 128: hipLaunchKernelGGL(compact_copy_kernel<8>, cgrid, dim3(kThreads), 0, stream, p); break;
+      case 256: hipLaunchKernelGGL(compact_copy_kernel<16>, cgrid, dim3(kThreads), 0, stream, p); break;
+      case 512: hipLaunchKernelGGL(compact_copy_kernel<32>, cgrid, dim3(kThreads), 0, stream, p); break;
       default: return hipErrorInvalidValue;
     }
   }

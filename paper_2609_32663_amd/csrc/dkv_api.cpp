@@ -171,6 +171,9 @@ dkv_status dkv_compact(const dkv_layout* layout, dkv_dtype dtype, const void* k,
   if (!head_dim_ok(L.head_dim)) return DKV_ERR_UNSUPPORTED;
   const int64_t nseg = (int64_t)L.num_units * L.num_kv_heads;
   if (nseg > 65535) return DKV_ERR_UNSUPPORTED;
+  // the copy dispatch (a K and a V workgroup of 256 per 32-row chunk) must
+  // hold fewer than 2^32 work-items
+  if (2 * dkv::compact_chunks(L.context_len) * 256 > (int64_t)UINT32_MAX) return DKV_ERR_UNSUPPORTED;
   if (nseg == 0) return DKV_OK;
   if (k == nullptr || v == nullptr || kv_mask == nullptr || k_out == nullptr || v_out == nullptr ||
       seg_off == nullptr || seg_len == nullptr)
@@ -190,7 +193,7 @@ dkv_status dkv_compact(const dkv_layout* layout, dkv_dtype dtype, const void* k,
   p.v_out = v_out;
   p.tile_cnt = static_cast<int32_t*>(workspace);
   p.tile_base = p.tile_cnt + nseg * (ntiles > 0 ? ntiles : 1);
-  p.sub_base = reinterpret_cast<uint16_t*>(p.tile_base + nseg * (ntiles > 0 ? ntiles : 1));
+  p.list = p.tile_base + nseg * (ntiles > 0 ? ntiles : 1);
   p.seg_off = seg_off;
   p.seg_len = seg_len;
   p.src_pos = src_pos;
@@ -229,6 +232,9 @@ dkv_status compact_bins(const dkv_layout* layout, const int32_t* unit_len, dkv_d
   if (!head_dim_ok(L.head_dim)) return DKV_ERR_UNSUPPORTED;
   const int64_t nseg = (int64_t)L.num_units * L.num_kv_heads;
   if (nseg > 65535 || nseg * ((int64_t)L.num_bins + 3) > (int64_t(1) << 27)) return DKV_ERR_UNSUPPORTED;
+  // as for dkv_compact: the copy dispatch must hold fewer than 2^32 work-items
+  if (2 * (((int64_t)L.context_len + dkv::kBinsChunkRows - 1) / dkv::kBinsChunkRows) * 256 > (int64_t)UINT32_MAX)
+    return DKV_ERR_UNSUPPORTED;
   if (nseg == 0) return DKV_OK;
   if (k == nullptr || v == nullptr || pattern == nullptr || k_out == nullptr || v_out == nullptr ||
       seg_off == nullptr || seg_len == nullptr)

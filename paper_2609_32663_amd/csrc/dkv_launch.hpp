@@ -33,9 +33,12 @@ int64_t map_blocks(int32_t T, int64_t num_segments);  // workgroups of one launc
 hipError_t launch_map_pattern(const MapParams& p, int num_segments, hipStream_t stream);
 
 // ---------------------------------------------------------------- compaction
-constexpr int kCompactTile = 4096;  // positions per compaction tile (count and scan)
-constexpr int kCompactSub = 128;    // positions per gather workgroup
-constexpr int kCompactSubPerTile = kCompactTile / kCompactSub;
+constexpr int kCompactTile = 4096;  // positions per compaction tile (count, scan and list)
+// Packed rows one copy workgroup moves (8 KiB of K or V at d = 128, bf16):
+// short workgroups copy fastest on this part (the block gather's chunk size).
+constexpr int kCopyRows = 32;
+// Copy chunks per segment: the most rows a segment can keep is T.
+inline int64_t compact_chunks(int64_t T) { return (T + kCopyRows - 1) / kCopyRows; }
 
 struct CompactParams {
   const uint8_t* mask;     // [nseg][T]
@@ -45,7 +48,7 @@ struct CompactParams {
   void* v_out;
   int32_t* tile_cnt;       // [nseg][ntiles] (workspace)
   int32_t* tile_base;      // [nseg][ntiles] (workspace)
-  uint16_t* sub_base;      // [nseg][ntiles][kCompactSubPerTile] rank of a sub-tile's first row in its tile (workspace)
+  int32_t* list;           // [nseg][T] position of each segment's packed row r, r < its length (workspace)
   int64_t* seg_off;        // [nseg]
   int32_t* seg_len;        // [nseg]
   int32_t* src_pos;        // [out_rows] or null

@@ -29,7 +29,8 @@ QMRG = "void dkv::(anonymous namespace)::query_merge_kernel<128>(dkv::QueryParam
 COPY = "void at::native::elementwise_kernel<128, 2>(int, Lambda)"
 CCOUNT = "dkv::(anonymous namespace)::compact_count_kernel(dkv::CompactParams)"
 CSCAN = "dkv::(anonymous namespace)::compact_scan_kernel(dkv::CompactParams)"
-CGATHER = "void dkv::(anonymous namespace)::compact_gather_kernel<16>(dkv::CompactParams)"
+CLIST = "dkv::(anonymous namespace)::compact_list_kernel(dkv::CompactParams)"
+CCOPY = "void dkv::(anonymous namespace)::compact_copy_kernel<16>(dkv::CompactParams)"
 BPLAN = "dkv::(anonymous namespace)::bins_plan_kernel(dkv::BinsParams)"
 BSCAN = "dkv::(anonymous namespace)::bins_scan_kernel(dkv::BinsParams)"
 BCOPY = "void dkv::(anonymous namespace)::bins_copy_kernel<16>(dkv::BinsParams)"
@@ -44,6 +45,8 @@ def test_helpers(bench):
     assert bench.timed_calls_per_mode(line) == 2 * (1 + 2 * 3)
     line["step_ms_spread"] = {"median": 1.0}
     assert bench.timed_calls_per_mode(line) == 2 * (1 + 2 * 3 + 2)
+    line["step_ms_spread"] = {"median": 1.0, "reps": 50}  # the spread pass's own replay count
+    assert bench.timed_calls_per_mode(line) == 2 * (1 + 2 * 3 + 50)
 
 
 def _counter_csv(path, counter, dispatches):
@@ -72,8 +75,8 @@ def test_pmc_summary_attribution(bench, tmp_path, monkeypatch, parity):
         d = []
         # the one-time section: a warm and a timed mask pack, a warm and a timed
         # block gather (the second of each is counted), then the copy probe
-        d += [(CCOUNT, 9.0), (CSCAN, 9.0), (CGATHER, 9.0)]
-        d += [(CCOUNT, 8.0 * scale), (CSCAN, 2.0 * scale), (CGATHER, 2038.0 * scale)]
+        d += [(CCOUNT, 9.0), (CSCAN, 9.0), (CLIST, 9.0), (CCOPY, 9.0)]
+        d += [(CCOUNT, 8.0 * scale), (CSCAN, 2.0 * scale), (CLIST, 30.0 * scale), (CCOPY, 2008.0 * scale)]
         d += [(BPLAN, 9.0), (BSCAN, 9.0), (BCOPY, 9.0)]
         d += [(BPLAN, 4.0 * scale), (BSCAN, 1.0 * scale), (BCOPY, 1019.0 * scale)]
         d += [(PCOPY, 5.0)] * 3
@@ -103,7 +106,7 @@ def test_pmc_summary_attribution(bench, tmp_path, monkeypatch, parity):
     assert res["query_traffic_bytes_per_call"] == 2 * 551 * 1024
     assert res["kernel_sha256_16"] == bench.kernel_hash()
     assert res["query_kernel_sha256_16"] == bench.kernel_hash(bench.QUERY_SRCS)
-    # the packs: the timed (second) triple of each, scaled like the rest
+    # the packs: the timed (second) call of each, scaled like the rest
     assert res["compact_traffic_bytes"] == 2 * 2048 * 1024
     assert res["compact_traffic_over_algorithmic"] == pytest.approx(2.0)
     assert res["compact_bins_traffic_bytes"] == 2 * 1024 * 1024
