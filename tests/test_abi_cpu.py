@@ -86,7 +86,11 @@ def _compact(lay, dtype=d.DKV_BF16, k=A, v=A, mask=A, cap=4, k_out=A, v_out=A, o
 
 
 def test_compact_validation():
-    assert d.dkv_compact_workspace_bytes(_lay()) > 0
+    # per segment (2 of them): a count and a base rank per 4096-position tile, and
+    # the position list (T entries)
+    assert d.dkv_compact_workspace_bytes(_lay()) == 4 * 2 * (1 + 1 + 1024) + 256
+    # the copy dispatch (2 workgroups of 256 per 32 rows of T) must stay below 2^32 work-items
+    assert _compact(_lay(T=268_435_425, edges=(0, 100, 300, 1012))) == d.DKV_ERR_UNSUPPORTED
     assert _compact(_lay(dim=96)) == d.DKV_ERR_UNSUPPORTED
     assert _compact(_lay(), dtype=7) == d.DKV_ERR_INVALID_ARG
     assert _compact(_lay(), cap=-1) == d.DKV_ERR_INVALID_ARG
