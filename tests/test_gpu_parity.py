@@ -177,6 +177,48 @@ def test_compact_all_keep_is_dense(d):
     assert torch.equal(pack.k_c, k.reshape(-1, 128)) and torch.equal(pack.v_c, v.reshape(-1, 128))
 
 
+@pytest.mark.parametrize("dtype,dim,T", [(torch.bfloat16, 128, 4099), (torch.float32, 128, 4096),
+                                         (torch.bfloat16, 64, 8197)])
+def test_compact_chunk_boundaries(d, dtype, dim, T):
+    """Masks with scattered kept positions and kept counts at the copy's
+    32-row chunk edges (0, 1, 31, 32, 33, 63, 64, 65, 4095, T - 33, T - 1, T),
+    straight through dkv_compact: rows, offsets, lengths, source positions
+    and rows_needed equal the oracle's bit for bit."""
+    rng = np.random.default_rng(207)
+    counts = [0, 1, 31, 32, 33, 63, 64, 65, 4095, T - 33, T - 1, T]
+    N, Hkv, cap = 2, len(counts) // 2, 3
+    mask = np.zeros((N, Hkv, T), np.uint8)
+    for s, c in enumerate(counts):
+        pos = rng.choice(T, size=c, replace=False)
+        mask[s // Hkv, s % Hkv, pos] = rng.integers(1, 256, size=c)  # any nonzero byte keeps
+    k = _rand_kv(rng, (N, Hkv, T, dim), dtype)
+    v = _rand_kv(rng, (N, Hkv, T, dim), dtype)
+    ref = o.compact(bits(k), bits(v), mask, cap)
+    rows = ref["rows"]
+    k_c = torch.zeros((rows, dim), dtype=dtype, device=DEV)
+    v_c = torch.zeros_like(k_c)
+    seg_off = torch.empty(N * Hkv, dtype=torch.int64, device=DEV)
+    seg_len = torch.empty(N * Hkv, dtype=torch.int32, device=DEV)
+    src = torch.full((rows,), -7, dtype=torch.int32, device=DEV)
+    rn = torch.empty(1, dtype=torch.int64, device=DEV)
+    lay = _layout(d, N, Hkv, Hkv, dim, T, 0, 0, [0, T])
+    ws = torch.empty(d.dkv_compact_workspace_bytes(lay), dtype=torch.uint8, device=DEV)
+    d.dkv_compact(lay, k, v, torch.from_numpy(mask).to(DEV), cap, k_c, v_c, seg_off, seg_len, ws,
+                  src_pos=src, rows_needed=rn)
+    torch.cuda.synchronize()
+    assert int(rn.item()) == rows
+    np.testing.assert_array_equal(seg_len.cpu().numpy(), ref["seg_len"])
+    np.testing.assert_array_equal(seg_off.cpu().numpy(), ref["seg_off"])
+    kc, vc, sp = bits(k_c), bits(v_c), src.cpu().numpy()
+    for s in range(N * Hkv):
+        lo, ln = int(ref["seg_off"][s]), int(ref["seg_len"][s])
+        np.testing.assert_array_equal(kc[lo:lo + ln], ref["k_c"][lo:lo + ln])
+        np.testing.assert_array_equal(vc[lo:lo + ln], ref["v_c"][lo:lo + ln])
+        np.testing.assert_array_equal(sp[lo:lo + ln], ref["src_pos"][lo:lo + ln])
+        assert (sp[lo + ln:lo + ln + cap] == -7).all()  # free rows untouched
+        assert not kc[lo + ln:lo + ln + cap].any()
+
+
 def test_compact_respects_out_rows(d):
     """Rows at or beyond out_rows are never written; rows_needed reports the need."""
     rng = np.random.default_rng(203)
