@@ -60,6 +60,9 @@ def parse():
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the other configurations' rows (counter runs: rocprofv3 --pmc has crashed on the "
                          "host in that section)")
+    ap.add_argument("--no-full-generation", action="store_true",
+                    help="skip the full-generation row (counter runs: the profiler process has crashed on the "
+                         "host in that section under rocprofv3 --pmc)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 1 GiB device copy (HBM-counter calibration)")
     ap.add_argument("--no-sustain", action="store_true",
@@ -1618,8 +1621,6 @@ def main():
     dms, deager_ms, dbytes = timed("dense", args.steps, args.warmup)
     # the whole generation of the workload: every one of its decode steps
     # (tails 0 .. decode_steps - 1), one graph per step, replayed in order
-    log("timing the full generation")
-
     def full_generation(mode):
         graphs = []
         for s_ in range(w.decode_steps):
@@ -1645,14 +1646,17 @@ def main():
         n_bytes = sum(decode_bytes(s_, mode) for s_ in range(w.decode_steps))
         return a_.elapsed_time(b_) / w.decode_steps, n_bytes / w.decode_steps
 
-    fg_ms, fg_bytes = full_generation("packed")
-    fgd_ms, fgd_bytes = full_generation("dense")
-    full_gen = {"steps": w.decode_steps, "ms_per_step": round(fg_ms, 4),
-                "gb_per_s": round(fg_bytes / (fg_ms * 1e-3) / 1e9, 2),
-                "dense_ms_per_step": round(fgd_ms, 4), "speedup_vs_dense": round(fgd_ms / fg_ms, 3),
-                "step": f"all {w.decode_steps} steps of the generation (tails 0-{w.decode_steps - 1}), one graph per "
-                        "step, replayed once in order"}
-    log(f"full generation: {fg_ms:.4f} ms/step packed, {fgd_ms:.4f} dense")
+    full_gen = None
+    if not args.no_full_generation:
+        log("timing the full generation")
+        fg_ms, fg_bytes = full_generation("packed")
+        fgd_ms, fgd_bytes = full_generation("dense")
+        full_gen = {"steps": w.decode_steps, "ms_per_step": round(fg_ms, 4),
+                    "gb_per_s": round(fg_bytes / (fg_ms * 1e-3) / 1e9, 2),
+                    "dense_ms_per_step": round(fgd_ms, 4), "speedup_vs_dense": round(fgd_ms / fg_ms, 3),
+                    "step": f"all {w.decode_steps} steps of the generation (tails 0-{w.decode_steps - 1}), one "
+                            "graph per step, replayed once in order"}
+        log(f"full generation: {fg_ms:.4f} ms/step packed, {fgd_ms:.4f} dense")
     # A step is exactly one attention call per layer on one stream, so the
     # average duration of a call (split + combine kernel, with the gaps
     # between them) is the timed region's event interval over L calls.
