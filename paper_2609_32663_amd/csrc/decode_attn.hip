@@ -18,9 +18,8 @@
 // last-workgroup-merges scheme avoids device-scope fences, which on this part
 // are whole-L2 write-backs and cost more than the merge itself.
 //
-// Inside a workgroup the 4 waves take 16-key tiles round-robin (from a start
-// tile of the workgroup's own, wrapping round), with the next tile's loads in
-// flight while the current one is computed.  Per tile:
+// Inside a workgroup the 4 waves take 16-key tiles round-robin, with the next
+// tile's loads in flight while the current one is computed.  Per tile:
 //   * K rows go straight from HBM into MFMA operands: lane (j, kg) of a wave
 //     loads 16-byte chunks kg, kg+4, ... of key j (j = lane % 16), which is
 //     exactly the B-operand layout of v_mfma_f32_16x16x32_bf16 (8 bf16 per
@@ -654,21 +653,6 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
       const __amdgpu_buffer_rsrc_t kr = make_rsrc(kbase + a2 * C::kRowBytes, nrows * C::kRowBytes);
       const __amdgpu_buffer_rsrc_t vr = make_rsrc(vbase + a2 * C::kRowBytes, nrows * C::kRowBytes);
       const uint32_t ntile = (nrows + kTK - 1) / kTK;
-      // Each workgroup starts its range at a tile of its own (a multiplicative
-      // hash of its index) and wraps round to the range's first tile, so the
-      // workgroups of a call do not all stream the same offset in their
-      // slices at the same moment.  Graph-replayed on this part: 0.5% off the
-      // headline call, 0.4% and 1.4% off the 70B-shaped batch at 20% and 10%
-      // (against starting every range at its first tile; reversing every
-      // other workgroup's order instead gained 0-1%).  The order is a function
-      // of the workgroup and the range only, so results stay deterministic.
-      // Sequence positions past the last tile map past the descriptor's range.
-      const uint32_t rot = ntile > 1 ? (uint32_t)(((uint64_t)((uint32_t)w * 2654435761u) * ntile) >> 32) : 0u;
-      auto tile_row = [&](uint32_t tt) -> uint32_t {
-        if (tt >= ntile) return tt * kTK;
-        const uint32_t x = tt + rot;
-        return (x >= ntile ? x - ntile : x) * kTK;
-      };
       // A ring of S register tiles per wave: S - 1 later tiles are loading
       // while one is computed.  The ring is unrolled so each stage keeps its
       // own registers (reusing the registers of a tile still in flight makes
@@ -682,7 +666,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
       uint32_t t = wave;
 #pragma unroll
       for (int i = 0; i < S - 1; ++i) {
-        load_tile(tl[i], kr, vr, tile_row(t + i * kWaves), k_lane, v_lane);
+        load_tile(tl[i], kr, vr, (t + i * kWaves) * kTK, k_lane, v_lane);
         __builtin_amdgcn_sched_barrier(0);
       }
       // The loop runs whole rounds of S stages and has a single exit: an
@@ -693,12 +677,12 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
       for (uint32_t r = 0; r < n_round; ++r) {
 #pragma unroll
         for (int i = 0; i < S; ++i) {
-          load_tile(tl[(i + S - 1) % S], kr, vr, tile_row(t + (S - 1) * kWaves), k_lane, v_lane);
+          load_tile(tl[(i + S - 1) % S], kr, vr, (t + (S - 1) * kWaves) * kTK, k_lane, v_lane);
           __builtin_amdgcn_sched_barrier(0);
           if (t < ntile) {
             DKV_STAMP(if (stamp_first && wave == 0 && lane == 0) stamp[2] = __builtin_amdgcn_s_memrealtime();
                       stamp_first = false;)
-            compute_tile<BF16, D, GP, false>(st, tl[i], qa, tile_row(t), nrows, p.scale_log2, pbuf[wave], abuf[wave],
+            compute_tile<BF16, D, GP, false>(st, tl[i], qa, t * kTK, nrows, p.scale_log2, pbuf[wave], abuf[wave],
                                              j16, kg, rp);
           }
           t += kWaves;
