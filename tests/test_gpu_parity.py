@@ -219,6 +219,52 @@ def test_compact_chunk_boundaries(d, dtype, dim, T):
         assert not kc[lo + ln:lo + ln + cap].any()
 
 
+def test_compact_long_context(d):
+    """Two segments of a 2^20 + 1-token context (the list and the copy index
+    past 2^20 rows of a segment; the copy grid holds 65,538 chunks per
+    segment): rows, lengths, offsets and source positions bit-exact."""
+    rng = np.random.default_rng(208)
+    N, Hkv, T, dim, cap = 1, 2, (1 << 20) + 1, 128, 5
+    # runs of kept positions (lengths 1-2,000) with scattered single positions between
+    mask = np.zeros((N, Hkv, T), np.uint8)
+    for g in range(Hkv):
+        j = 0
+        while j < T:
+            j += int(rng.integers(0, 4000))
+            n = int(rng.integers(1, 2000))
+            mask[0, g, j:j + n] = 1
+            j += n
+        mask[0, g, rng.integers(0, T, size=5000)] = 1
+    mask[0, 1, T - 1] = 1  # the last position
+    gen = torch.Generator(device=DEV).manual_seed(208)
+    k = torch.randn((N, Hkv, T, dim), generator=gen, device=DEV).to(torch.bfloat16)
+    v = torch.randn((N, Hkv, T, dim), generator=gen, device=DEV).to(torch.bfloat16)
+    ref = o.compact(bits(k), bits(v), mask, cap)
+    rows = ref["rows"]
+    k_c = torch.zeros((rows, dim), dtype=torch.bfloat16, device=DEV)
+    v_c = torch.zeros_like(k_c)
+    seg_off = torch.empty(N * Hkv, dtype=torch.int64, device=DEV)
+    seg_len = torch.empty(N * Hkv, dtype=torch.int32, device=DEV)
+    src = torch.full((rows,), -7, dtype=torch.int32, device=DEV)
+    rn = torch.empty(1, dtype=torch.int64, device=DEV)
+    lay = _layout(d, N, Hkv, Hkv, dim, T, 0, 0, [0, T])
+    ws = torch.empty(d.dkv_compact_workspace_bytes(lay), dtype=torch.uint8, device=DEV)
+    d.dkv_compact(lay, k, v, torch.from_numpy(mask).to(DEV), cap, k_c, v_c, seg_off, seg_len, ws,
+                  src_pos=src, rows_needed=rn)
+    torch.cuda.synchronize()
+    assert int(rn.item()) == rows
+    np.testing.assert_array_equal(seg_len.cpu().numpy(), ref["seg_len"])
+    np.testing.assert_array_equal(seg_off.cpu().numpy(), ref["seg_off"])
+    assert ref["seg_len"].max() > (1 << 18)
+    np.testing.assert_array_equal(bits(k_c), ref["k_c"])
+    np.testing.assert_array_equal(bits(v_c), ref["v_c"])
+    sp = src.cpu().numpy()
+    for s_ in range(N * Hkv):
+        lo, ln = int(ref["seg_off"][s_]), int(ref["seg_len"][s_])
+        np.testing.assert_array_equal(sp[lo:lo + ln], ref["src_pos"][lo:lo + ln])
+        assert (sp[lo + ln:lo + ln + cap] == -7).all()
+
+
 def test_compact_respects_out_rows(d):
     """Rows at or beyond out_rows are never written; rows_needed reports the need."""
     rng = np.random.default_rng(203)
