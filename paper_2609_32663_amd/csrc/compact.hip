@@ -16,9 +16,10 @@
 //           entry.
 // The copy works on the output side because short workgroups copy fastest on
 // this part and every copy workgroup then has whole rows to move: on the
-// Llama-3.1-8B-shaped 128K stack (35% kept) a gather per 128-position input
-// sub-tile (most of them empty, the others up to 32 KiB) took 2.09-2.15 ms,
-// whole 4096-position tiles 2.50-2.55 ms.  (One workgroup copying both K and
+// Llama-3.1-8B-shaped 128K stack (35% kept) the pack takes 1.91-1.97 ms this
+// way, against 2.09-2.15 ms for a gather per 128-position input sub-tile (most
+// of them empty, the others up to 32 KiB) and 2.50-2.55 ms for one per
+// 4096-position tile.  (One workgroup copying both K and
 // V ran 6% slower in the block gather: four interleaved streams per
 // workgroup instead of two.)
 // All row arithmetic is 64-bit: a whole-stack cache has more than 2^31 elements.
