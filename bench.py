@@ -88,7 +88,10 @@ def parse():
                          "run_*) into the query kernel's clock and matrix-unit profile")
     ap.add_argument("--pmc-command", default="",
                     help="command line recorded by --pmc-summary / --trace-summary")
-    return ap.parse_args()
+    args = ap.parse_args()
+    if args.steps < 1 or args.warmup < 0:
+        ap.error("--steps must be at least 1 and --warmup at least 0")
+    return args
 
 
 def host_info():
