@@ -290,6 +290,52 @@ def test_compact_respects_out_rows(d):
                                   ref["k_c"][:ref["seg_len"][0]])
 
 
+@pytest.mark.parametrize("short", [0, 1])
+def test_compact_out_rows_exact_edge(d, short):
+    """out_rows equal to the need packs every segment; one row fewer leaves
+    exactly the last segment unpacked (length -1, offset clamped to
+    out_rows), and nothing is written at or past out_rows."""
+    rng = np.random.default_rng(209)
+    N, Hkv, T, dim, cap = 2, 3, 3000, 128, 7
+    mask = (rng.uniform(size=(N, Hkv, T)) < 0.4).astype(np.uint8)
+    k = _rand_kv(rng, (N, Hkv, T, dim), torch.bfloat16)
+    v = _rand_kv(rng, (N, Hkv, T, dim), torch.bfloat16)
+    ref = o.compact(bits(k), bits(v), mask, cap)
+    need = ref["rows"]
+    out_rows = need - short
+    big_k = torch.full((need + 64, dim), 3.0, dtype=torch.bfloat16, device=DEV)
+    big_v = torch.full((need + 64, dim), 3.0, dtype=torch.bfloat16, device=DEV)
+    src = torch.full((need + 64,), -7, dtype=torch.int32, device=DEV)
+    seg_off = torch.empty(N * Hkv, dtype=torch.int64, device=DEV)
+    seg_len = torch.empty(N * Hkv, dtype=torch.int32, device=DEV)
+    rn = torch.empty(1, dtype=torch.int64, device=DEV)
+    lay = _layout(d, N, Hkv, Hkv, dim, T, 0, 0, [0, T])
+    ws = torch.empty(d.dkv_compact_workspace_bytes(lay), dtype=torch.uint8, device=DEV)
+    d.dkv_compact(lay, k, v, torch.from_numpy(mask).to(DEV), cap, big_k[:out_rows], big_v[:out_rows], seg_off,
+                  seg_len, ws, src_pos=src[:out_rows], rows_needed=rn)
+    torch.cuda.synchronize()
+    assert int(rn.item()) == need
+    want_len = ref["seg_len"].copy()
+    want_off = ref["seg_off"].copy()
+    if short:
+        want_len[-1] = -1
+        want_off[-1] = min(int(want_off[-1]), out_rows)
+    np.testing.assert_array_equal(seg_len.cpu().numpy(), want_len)
+    np.testing.assert_array_equal(seg_off.cpu().numpy(), want_off)
+    kc, vc, sp = bits(big_k), bits(big_v), src.cpu().numpy()
+    for s_ in range(N * Hkv):
+        if want_len[s_] < 0:
+            continue
+        lo, ln = int(want_off[s_]), int(want_len[s_])
+        np.testing.assert_array_equal(kc[lo:lo + ln], ref["k_c"][lo:lo + ln])
+        np.testing.assert_array_equal(vc[lo:lo + ln], ref["v_c"][lo:lo + ln])
+        np.testing.assert_array_equal(sp[lo:lo + ln], ref["src_pos"][lo:lo + ln])
+    # nothing at or past out_rows, and nothing of the unpacked last segment
+    last_lo = int(ref["seg_off"][-1]) if short else out_rows
+    assert (big_k[last_lo:].float() == 3.0).all() and (big_v[last_lo:].float() == 3.0).all()
+    assert (src[last_lo:] == -7).all()
+
+
 def test_truncated_compaction_is_safe_downstream(d):
     """A pack that does not fit out_rows: segments that fit are packed whole,
     the others get seg_len -1 and an offset clamped to out_rows; append,
