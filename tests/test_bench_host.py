@@ -113,3 +113,15 @@ def test_pmc_summary_attribution(bench, tmp_path, monkeypatch, parity):
     assert res["compact_bins_traffic_over_algorithmic"] == pytest.approx(2.0)
     assert res["compact_kernel_sha256_16"] == bench.kernel_hash(bench.COMPACT_SRCS)
     assert res["compact_bins_kernel_sha256_16"] == bench.kernel_hash(bench.BINS_SRCS)
+
+
+@pytest.mark.parametrize("argv,text", [(["--gpus", "2"], "one GPU only"), (["--steps", "0"], "--steps")])
+def test_refusals_exit_before_any_gpu_work(argv, text):
+    """More than one GPU, or no timed step, is refused with exit status 2
+    before torch or the library is loaded."""
+    import subprocess
+    import sys
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), *argv], capture_output=True, text=True,
+                       timeout=120)
+    assert r.returncode == 2
+    assert text in r.stderr and r.stdout == ""
